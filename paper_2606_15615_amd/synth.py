@@ -1,0 +1,181 @@
+"""Seeded synthetic inputs for the branch-cached MoE layer step.
+
+This module only draws random numbers and stores them in the layouts the
+library and the oracle take.  It holds none of the method's arithmetic
+(no routing, scoring, selection, expert FFN or combine).  Both the GPU path
+(tests, bench) and the CPU oracle (tests) read their inputs from here.
+
+Workloads (paper Sec. 5.1: DiT-MoE / DSMoE at 256x256 px, 250 steps; the
+latent is 32x32 with patch 2 -> 256 tokens, or 64x64 -> 1024 tokens):
+
+* weights   ~ N(0, 1/d), router bias optional (log of a Zipf prior for the
+  skewed stress layer);
+* x_0       ~ N(0, 1);
+* x_t       = sqrt(1 - a_i) * x_{t-1} + sqrt(a_i) * xi_t, with a per-token
+  drift rate a_i (log-uniform in [1e-3, 1e-1], or bimodal);
+* attn_in_t follows the same drift model from an independent stream.
+
+The trained checkpoints and datasets the paper measures on are not
+available; these inputs stand in for them with the same shapes.
+
+bf16 tensors are returned as numpy ``uint16`` arrays holding the bf16 bit
+patterns (round-to-nearest-even from the fp32 draw); fp32 tensors as
+``float32``.
+"""
+from __future__ import annotations
+
+import dataclasses
+import math
+
+import numpy as np
+
+BF16 = "bf16"
+FP32 = "fp32"
+
+
+def fp32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
+    """Round an fp32 array to bf16 (nearest, ties to even); return the bits."""
+    a = np.ascontiguousarray(a, dtype=np.float32)
+    u = a.view(np.uint32).astype(np.uint64)
+    nan = np.isnan(a)
+    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
+    r[nan] = 0x7FC0
+    return r
+
+
+def bf16_bits_to_fp32(b: np.ndarray) -> np.ndarray:
+    """Widen bf16 bit patterns to fp32 (exact)."""
+    return (np.asarray(b, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+@dataclasses.dataclass(frozen=True)
+class LayerShape:
+    """Shape of one routed MoE layer and of the token batch it serves."""
+    d: int          # model width
+    E: int          # routed experts
+    k: int          # experts per token (top-k)
+    d_ff: int       # expert hidden width
+    B: int          # samples in the batch
+    N: int          # tokens per sample
+    dtype: str = BF16
+
+    @property
+    def tokens(self) -> int:
+        return self.B * self.N
+
+    @property
+    def branches(self) -> int:
+        return self.B * self.N * self.k
+
+
+# Named workloads.  "xl256" and "xl1024" are the DiT-MoE-XL-like layer at a
+# 32x32 and a 64x64 latent; "tiny" is the small fp32 parity layer; "skewed"
+# is the Zipf-biased stress layer.
+WORKLOADS = {
+    "tiny": LayerShape(d=384, E=8, k=2, d_ff=1536, B=1, N=256, dtype=FP32),
+    "xl256": LayerShape(d=1152, E=16, k=2, d_ff=4608, B=8, N=256, dtype=BF16),
+    "xl1024": LayerShape(d=1152, E=16, k=2, d_ff=4608, B=8, N=1024, dtype=BF16),
+    "skewed": LayerShape(d=3072, E=32, k=2, d_ff=8192, B=2, N=4096, dtype=BF16),
+}
+
+
+def _store(a32: np.ndarray, dtype: str) -> np.ndarray:
+    if dtype == BF16:
+        return fp32_to_bf16_bits(a32)
+    if dtype == FP32:
+        return np.ascontiguousarray(a32, dtype=np.float32)
+    raise ValueError(dtype)
+
+
+class Synth:
+    """Independent seeded streams for weights, trajectory, drift and attention."""
+
+    def __init__(self, shape: LayerShape, seed: int = 0):
+        self.shape = shape
+        ss = np.random.SeedSequence(seed)
+        kids = ss.spawn(6)
+        self._rng_w = np.random.Generator(np.random.PCG64(kids[0]))
+        self._rng_x0 = np.random.Generator(np.random.PCG64(kids[1]))
+        self._rng_a = np.random.Generator(np.random.PCG64(kids[2]))
+        self._rng_xi = np.random.Generator(np.random.PCG64(kids[3]))
+        self._rng_attn = np.random.Generator(np.random.PCG64(kids[4]))
+        self._rng_misc = np.random.Generator(np.random.PCG64(kids[5]))
+        self._drift = {}
+
+    # ---- weights -------------------------------------------------------
+    def weights(self, router_bias: str | None = None, zipf_s: float = 1.2):
+        """Router and expert weights, ``out x in`` row-major, ~N(0, 1/d).
+
+        Returns ``(W_r[E][d], b_r[E] or None, W_up[E][d_ff][d],
+        W_down[E][d][d_ff])``; ``b_r`` is fp32.  ``router_bias="zipf"`` gives
+        ``b_e = -s * ln(e + 1)`` (the log of a Zipf(s) prior over expert rank,
+        rank = expert id).
+        """
+        s = self.shape
+        std = 1.0 / math.sqrt(s.d)
+        g = self._rng_w
+        W_r = g.standard_normal((s.E, s.d), dtype=np.float32) * np.float32(std)
+        W_up = g.standard_normal((s.E, s.d_ff, s.d), dtype=np.float32) * np.float32(std)
+        W_down = g.standard_normal((s.E, s.d, s.d_ff), dtype=np.float32) * np.float32(std)
+        b_r = None
+        if router_bias == "zipf":
+            b_r = (-zipf_s * np.log(np.arange(s.E, dtype=np.float64) + 1.0)).astype(np.float32)
+        elif router_bias is not None:
+            raise ValueError(router_bias)
+        return (_store(W_r, s.dtype), b_r, _store(W_up, s.dtype), _store(W_down, s.dtype))
+
+    # ---- trajectory ----------------------------------------------------
+    def drift_rates(self, kind: str = "loguniform") -> np.ndarray:
+        """Per-token drift rate a_i, shape (B, N), float64."""
+        if kind in self._drift:
+            return self._drift[kind]
+        s = self.shape
+        g = self._rng_a
+        if kind == "loguniform":
+            lo, hi = math.log(1e-3), math.log(1e-1)
+            a = np.exp(g.uniform(lo, hi, size=(s.B, s.N)))
+        elif kind == "bimodal":
+            fast = g.random(size=(s.B, s.N)) < 0.1
+            a = np.where(fast, 0.2, 1e-3)
+        else:
+            raise ValueError(kind)
+        self._drift[kind] = a
+        return a
+
+    def trajectory(self, T: int, drift: str = "loguniform"):
+        """Yield ``T`` layer inputs x_t, shape (B, N, d), in the layer dtype."""
+        s = self.shape
+        a = self.drift_rates(drift)[..., None].astype(np.float32)
+        keep = np.sqrt(1.0 - a).astype(np.float32)
+        mix = np.sqrt(a).astype(np.float32)
+        x = self._rng_x0.standard_normal((s.B, s.N, s.d), dtype=np.float32)
+        for t in range(T):
+            if t > 0:
+                xi = self._rng_xi.standard_normal((s.B, s.N, s.d), dtype=np.float32)
+                x = keep * x + mix * xi
+            yield _store(x, s.dtype)
+
+    def attention_trajectory(self, T: int, drift: str = "loguniform"):
+        """Yield ``T`` attention-path features, shape (B, N, d), layer dtype."""
+        s = self.shape
+        a = self.drift_rates(drift)[..., None].astype(np.float32)
+        keep = np.sqrt(1.0 - a).astype(np.float32)
+        mix = np.sqrt(a).astype(np.float32)
+        g = self._rng_attn
+        x = g.standard_normal((s.B, s.N, s.d), dtype=np.float32)
+        for t in range(T):
+            if t > 0:
+                x = keep * x + mix * g.standard_normal((s.B, s.N, s.d), dtype=np.float32)
+            yield _store(x, s.dtype)
+
+    # ---- arbitrary cached rows ----------------------------------------
+    def rows(self, shape, scale: float = 1.0) -> np.ndarray:
+        """Random rows in the layer dtype (used to fill a cache directly)."""
+        a = self._rng_misc.standard_normal(shape, dtype=np.float32) * np.float32(scale)
+        return _store(a, self.shape.dtype)
+
+    def integers(self, low, high, size) -> np.ndarray:
+        return self._rng_misc.integers(low, high, size=size)
+
+    def uniform(self, low, high, size) -> np.ndarray:
+        return self._rng_misc.uniform(low, high, size=size)
