@@ -1,0 +1,231 @@
+"""Benchmark: cached MoE-layer step on one MI355X.
+
+A step is one pass of the whole branch-cached layer (router, statistic and
+thresholds, matching and scores, selection, expert lists, grouped expert
+FFN, combine with cache and attention write) over one batch of synthetic
+input already resident in HBM.  The timed steps are cache steps at a 30%
+per-sample branch budget; the full-recompute comparator (the uncached layer
+through the same kernels) is timed on the same inputs.
+
+    python bench.py [--steps K] [--warmup W] [--workload xl1024] [--no-cpu]
+
+Prints one JSON line.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "cached MoE-layer ms/step + MFMA TFLOP/s on recomputed branches, 30% refresh"
+PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 MFMA
+PEAK_FP32_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+
+
+def log(msg):
+    print(msg, file=sys.stderr, flush=True)
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=20)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default="xl1024")
+    ap.add_argument("--ratio", type=float, default=0.3)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--copy-mib", type=int, default=0,
+                    help="also run a plain device copy of this many MiB (counter calibration)")
+    return ap.parse_args()
+
+
+def cpu_baseline(shape, ratio, seed):
+    """The oracle, as it stands, on one sample of the batch: a refresh step
+    and then a timed cache step (median of 3), scaled to the whole batch."""
+    from oracle import moeca_oracle as O
+    from paper_2606_15615_amd.synth import LayerShape, Synth
+    try:
+        from threadpoolctl import threadpool_info
+        cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        cores = 1
+    one = LayerShape(shape.d, shape.E, shape.k, shape.d_ff, 1, shape.N, shape.dtype)
+    sy = Synth(one, seed)
+    W = sy.weights()
+    dims = O.Dims(one.d, one.E, one.k, one.d_ff, 1, one.N, one.dtype)
+    Wo = O.Weights(dims, *W)
+    xs = list(sy.trajectory(5))
+    pol = O.Policy(mode=O.MODE_RATIO, ratio=ratio, refresh_cycle=0)
+    st = O.State(dims)
+    _, st, _ = O.step(dims, pol, Wo, st, xs[0], 0)
+    times = []
+    for t in range(1, 4):
+        t0 = time.perf_counter()
+        _, st2, _ = O.step(dims, pol, Wo, st, xs[t], t)
+        times.append(time.perf_counter() - t0)
+        st = st2
+    ms = float(np.median(times)) * 1e3 * shape.B
+    return {"value": round(ms, 3), "unit": "ms/step", "cores": int(cores), "kind": "oracle",
+            "sample": f"1 of {shape.B} samples ({shape.N} tokens), cache step at ratio {ratio}, "
+                      f"median of 3, scaled x{shape.B}"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
+              "this build has no multi-GPU path", file=sys.stderr)
+        sys.exit(2)
+    import torch
+    from paper_2606_15615_amd import _lib
+    from paper_2606_15615_amd.layer import MoecaLayer, np_to_device
+    from paper_2606_15615_amd.synth import WORKLOADS, Synth
+
+    _lib.load()  # fails loudly when the library is not built
+    shape = WORKLOADS[args.workload]
+    dev = torch.device("cuda:0")
+    K, Wm = args.steps, args.warmup
+    T = Wm + K
+    log(f"[bench] workload {args.workload} {shape}; generating inputs")
+    sy = Synth(shape, args.seed)
+    W = sy.weights()
+    dW = [np_to_device(W[0], dev), None, np_to_device(W[2], dev), np_to_device(W[3], dev)]
+    xs = [np_to_device(x, dev) for x in sy.trajectory(T)]
+    attn = np_to_device(next(sy.attention_trajectory(1)), dev)
+    attn_cache = torch.zeros_like(attn)
+    out = torch.empty_like(xs[0])
+    torch.cuda.synchronize()
+
+    def make(mode):
+        L = MoecaLayer(shape.d, shape.E, shape.k, shape.d_ff, batch=shape.B, tokens=shape.N,
+                       mode=mode, ratio=args.ratio, refresh_cycle=0, dtype=shape.dtype)
+        L.set_weights(*dW)
+        L.bind_attention(attn, attn_cache)
+        L.reset()
+        return L
+
+    cached = make(_lib.MOECA_MODE_RATIO)
+    full = make(_lib.MOECA_MODE_FULL)
+    stream = torch.cuda.current_stream()
+
+    def run(L, t0, t1):
+        for t in range(t0, t1):
+            L.step(xs[t], t, out)
+
+    # ---- headline: K cache steps ------------------------------------------
+    log("[bench] warmup")
+    run(cached, 0, Wm)                 # step 0 is the refresh step
+    torch.cuda.synchronize()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    log("[bench] timing cache steps")
+    torch.cuda.synchronize()
+    e0.record(stream)
+    run(cached, Wm, T)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_cached = e0.elapsed_time(e1) / K
+
+    # ---- comparator: K full-recompute steps on the same inputs --------------
+    log("[bench] timing full recompute")
+    run(full, 0, min(Wm, 3))
+    torch.cuda.synchronize()
+    e0.record(stream)
+    run(full, Wm, T)
+    e1.record(stream)
+    torch.cuda.synchronize()
+    ms_full = e0.elapsed_time(e1) / K
+
+    # ---- per-stage times and refresh counts (replay with stage events) -----
+    log("[bench] stage breakdown")
+    cached.reset()
+    run(cached, 0, Wm)
+    torch.cuda.synchronize()
+    cached.set_timing(True)
+    recompute = []
+    for t in range(Wm, T):
+        cached.step(xs[t], t, out)
+        recompute.append(cached.stats().n_recompute)
+    stage_ms, nsteps = cached.timing()
+    cached.set_timing(False)
+    stage_ms = {k: v / nsteps for k, v in stage_ms.items()}
+    full.set_timing(True)
+    for t in range(Wm, T):
+        full.step(xs[t], t, out)
+    fstage, fsteps = full.timing()
+    full.set_timing(False)
+    fstage = {k: v / fsteps for k, v in fstage.items()}
+
+    if args.copy_mib:
+        n = args.copy_mib * (1 << 20)
+        a = torch.empty(n, dtype=torch.uint8, device=dev)
+        b = torch.empty_like(a)
+        b.copy_(a)
+        torch.cuda.synchronize()
+
+    branches = shape.B * shape.N * shape.k
+    flop_per_branch = 4.0 * shape.d * shape.d_ff
+    mean_rec = float(np.mean(recompute))
+    ffn_ms = stage_ms["ffn_up"] + stage_ms["ffn_down"]
+    tflops = mean_rec * flop_per_branch / (ffn_ms * 1e-3) / 1e12
+    peak = PEAK_BF16_TFLOPS if shape.dtype == "bf16" else PEAK_FP32_TFLOPS
+    act = 2 if shape.dtype == "bf16" else 4
+    # algorithmic HBM bytes of a cache step: expert weights (touched experts
+    # only is <= all), inputs, reused cached rows, recomputed rows written,
+    # outputs; the attention refresh is excluded
+    wbytes = shape.E * 2 * shape.d * shape.d_ff * act
+    step_bytes = (wbytes + shape.tokens * shape.d * act * 2
+                  + branches * shape.d * act)
+    res = {
+        "metric": METRIC,
+        "value": round(ms_cached, 4),
+        "unit": "ms/step",
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": round(ms_cached, 4),
+        "higher_is_better": False,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": shape.dtype,
+        "data": "synthetic",
+        "config": {"workload": f"{args.workload}: MoE layer d={shape.d}, E={shape.E}, "
+                               f"top-{shape.k}, d_ff={shape.d_ff} GELU, {shape.N} tokens x "
+                               f"batch {shape.B}, ratio mode rho={args.ratio}",
+                   "batch": shape.B, "tokens": shape.N},
+        "tflops_recomputed": round(tflops, 2),
+        "full_ms_per_step": round(ms_full, 4),
+        "cached_over_full": round(ms_cached / ms_full, 4),
+        "speedup_vs_full": round(ms_full / ms_cached, 3),
+        "refresh_ratio_actual": round(mean_rec / branches, 4),
+        "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
+        "full_stage_ms": {k: round(v, 4) for k, v in fstage.items()},
+        "step_hbm_frac": round(step_bytes / (ms_cached * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+        "roofline": {
+            "bound": "mfma",
+            "kernel": "grouped expert FFN (up + down launches)",
+            "achieved": round(tflops, 2),
+            "peak": peak,
+            "unit": "TFLOP/s",
+            "frac": round(tflops / peak, 4),
+            "traffic": None,
+        },
+    }
+    if not args.no_cpu:
+        log("[bench] cpu baseline (oracle)")
+        res["cpu_baseline"] = cpu_baseline(shape, args.ratio, args.seed)
+    cached.close()
+    full.close()
+    print(json.dumps(res), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,222 @@
+/*
+ * moeca.h - branch-cached DiT-MoE layer step on AMD Instinct MI355X (gfx950).
+ *
+ * MoECa (Sec. 4) caches, per token i, the outputs of its k routed expert
+ * branches C_i = {(e_q, w_q, h_q)} and the token's attention-path feature
+ * a_i (Sec. 4.1).  At every denoising step the router runs (Sec. 4.1); the
+ * current branches are matched to the cached ones and scored (Sec. 4.2);
+ * only the branches in the recomputation set R_i go through their expert
+ * FFN; the layer output combines recomputed and cached features with the
+ * current gate weights (Sec. 4.1, output eq.); the cache and, for tokens with
+ * a recomputed branch, the attention feature are refreshed in the same step
+ * (Sec. 4.1, synchronised update).  Thresholds adapt per expert from an EMA
+ * of its spatial activation and that statistic's entropy (Sec. 4.3).
+ *
+ * Conventions for every call below
+ *  - Pointers named "device" point to memory on the current HIP device; the
+ *    caller allocates and frees them and keeps them alive while the layer
+ *    uses them.  The library never allocates device memory.
+ *  - Activations and weights are bf16 (IEEE binary16-brain, stored as
+ *    uint16) or fp32, as the policy's dtype says; gate weights, scores and
+ *    statistics are fp32.  All arrays are dense, row-major, no padding.
+ *  - "stream" is a hipStream_t passed as void* (NULL = the null stream).
+ *  - Functions return MOECA_OK (0) or a negative error code and never throw;
+ *    moeca_last_error() then describes the failure (thread-local string).
+ *  - One host thread at a time per handle.  Handles are independent.
+ */
+#ifndef MOECA_H
+#define MOECA_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* ---- error codes ------------------------------------------------------- */
+#define MOECA_OK 0
+#define MOECA_E_INVAL (-1) /* bad argument: NULL, size, range                */
+#define MOECA_E_STATE (-2) /* weights or workspace not bound yet             */
+#define MOECA_E_HIP (-3)   /* a HIP launch or copy reported an error         */
+
+/* ---- policy ------------------------------------------------------------ */
+enum {
+  MOECA_MODE_FULL = 0,      /* uncached routed MoE layer (Sec. 2.3 MoE eq.);
+                               the full-recompute comparator; no cache state */
+  MOECA_MODE_THRESHOLD = 1, /* Sec. 4.2: recompute iff unmatched or s > tau  */
+  MOECA_MODE_RATIO = 2      /* per sample: all unmatched branches plus the
+                               best matched ones by margin s - tau, up to
+                               K_b = floor(ratio * N * k + 0.5) branches     */
+};
+enum { MOECA_DTYPE_BF16 = 0, MOECA_DTYPE_FP32 = 1 };
+enum { MOECA_ACT_GELU_TANH = 0, MOECA_ACT_GELU_ERF = 1 };
+
+typedef struct moeca_policy {
+  int32_t mode;          /* MOECA_MODE_*                                      */
+  float ratio;           /* refresh ratio rho in [0, 1] (RATIO mode)          */
+  float tau0;            /* base threshold tau_0 (Sec. 4.3), > 0; 0.80        */
+  float alpha;           /* adaptation strength alpha in [0, 1); 0.6          */
+  float beta;            /* EMA decay beta in [0, 1); 0.65                     */
+  float lambda1;         /* weight of the drift term Delta (Sec. 4.2); 1.0    */
+  float lambda2;         /* weight of the contribution term o (Sec. 4.2); 1.0 */
+  int32_t refresh_cycle; /* forced full step when t % cycle == 0; 0 = never;
+                            4 (Sec. 5.1)                                      */
+  int32_t norm_topk;     /* 1: gate = softmax renormalised over the top-k     */
+  int32_t act;           /* MOECA_ACT_*                                       */
+  int32_t dtype;         /* MOECA_DTYPE_*                                     */
+  int32_t batch;         /* B, samples per step, >= 1                         */
+  int32_t tokens;        /* N, tokens per sample, >= 1                         */
+} moeca_policy;
+
+/* Fill *p with the paper's settings: THRESHOLD mode, tau0 0.80, alpha 0.6,
+ * beta 0.65 (Sec. 5.4, Tab. 4), refresh cycle 4 (Sec. 5.1), lambda1 =
+ * lambda2 = 1 (not reported by the paper), ratio 0.3, bf16, tanh GELU,
+ * renormalised top-k, batch 1, tokens 1.  NULL is ignored. */
+void moeca_policy_default(moeca_policy* p);
+
+/* ---- layer handle ------------------------------------------------------ */
+typedef struct moeca_layer moeca_layer;
+
+/* Create a layer of width d, E routed experts, top-k routing and expert
+ * hidden width d_ff (FFN_e(x) = W_down[e] act(W_up[e] x), Sec. 2.3).
+ * Host only; the policy is copied.  Limits: 1 <= k <= min(E, 8), E <= 64,
+ * d and d_ff multiples of 64, d <= 16384, d_ff <= 65536, B*N*k < 2^31.
+ * Returns NULL on a bad argument (moeca_last_error() says which). */
+moeca_layer* moeca_layer_create(int d, int E, int k, int d_ff, const moeca_policy* policy);
+
+/* Release the handle.  Never frees caller memory.  NULL is a no-op. */
+void moeca_layer_destroy(moeca_layer* layer);
+
+/* Description of the last error on this thread ("" if none). */
+const char* moeca_last_error(void);
+
+/* Bind the weights (device, policy dtype, not copied):
+ *   W_r    [E][d]        router (Sec. 4.1: B_i^t is its top-k)
+ *   b_r    [E] fp32      optional router bias added to the logits, or NULL
+ *   W_up   [E][d_ff][d]  expert up-projections  (out x in)
+ *   W_down [E][d][d_ff]  expert down-projections (out x in)
+ * Host only.  MOECA_E_INVAL if a required pointer is NULL or a weight
+ * pointer is not 16-byte aligned (the bias 4-byte). */
+int moeca_layer_set_weights(moeca_layer* layer, const void* W_r, const float* b_r,
+                            const void* W_up, const void* W_down);
+
+/* Bytes of device workspace the layer needs: the branch cache (ids, gate
+ * weights, norms and rows of B*N*k branches), the EMA statistic [B][E][N],
+ * and per-step scratch (routing, scores, masks, expert lists, the FFN
+ * intermediate).  0 if layer is NULL. */
+size_t moeca_workspace_bytes(const moeca_layer* layer);
+
+/* Bind caller-owned device memory of at least moeca_workspace_bytes() bytes,
+ * 256-byte aligned.  Binding invalidates the cache: the next step is a full
+ * step, and the statistic must be cleared with moeca_cache_reset() before
+ * it (an unreset workspace holds undefined values).  MOECA_E_INVAL on NULL,
+ * misalignment or a short buffer. */
+int moeca_bind_workspace(moeca_layer* layer, void* dev, size_t bytes);
+
+/* Optional attention path (Sec. 4.1, synchronised update).  attn_in and
+ * attn_cache are device [B][N][d] in the policy dtype.  After each step,
+ * attn_cache row i equals attn_in row i if token i had at least one
+ * recomputed branch (every token on full steps), and is unchanged
+ * otherwise.  attn_in is read when the step runs, so the caller may write
+ * each step's features into the same buffer.  Both NULL unbinds; one NULL,
+ * or a pointer that is not 16-byte aligned, is MOECA_E_INVAL. */
+int moeca_bind_attention(moeca_layer* layer, const void* attn_in, void* attn_cache);
+
+/* One layer step at sampling step t (0-based).
+ *   x_t [B][N][d]  device, policy dtype: the MoE layer input u of Sec. 2.3
+ *   out [B][N][d]  device, policy dtype: y_i of Sec. 4.1 (the routed sum,
+ *                  without the residual, which the caller adds)
+ * The step is a full step when the cache is invalid, in FULL mode, or when
+ * refresh_cycle > 0 and t % refresh_cycle == 0 (Sec. 4.1 / Sec. 5.1);
+ * otherwise a cache step.  Enqueues work on the stream and returns without
+ * waiting; it neither allocates nor synchronises.  Kernel faults surface at
+ * the caller's next synchronisation.  x_t and out must not overlap the
+ * workspace; both must be 16-byte aligned (else MOECA_E_INVAL).
+ * MOECA_E_STATE if weights or workspace are unbound. */
+int moeca_step(moeca_layer* layer, const void* x_t, int t, void* out, void* stream);
+
+/* Enqueue a cache reset on the stream: every cached branch becomes empty,
+ * the EMA statistic becomes zero, and the next step is a full step. */
+int moeca_cache_reset(moeca_layer* layer, void* stream);
+
+/* ---- statistics of the last step -------------------------------------- */
+typedef struct moeca_stats {
+  int64_t n_branches;      /* B * N * k                                        */
+  int64_t n_recompute;     /* |R| summed over tokens                           */
+  int64_t n_unmatched;     /* branches whose expert was not cached (0 on full) */
+  int64_t n_matched;       /* branches matched to a cached slot (0 on full)    */
+  int64_t n_reused;        /* matched and not recomputed                       */
+  int64_t n_sync;          /* tokens whose attention feature was refreshed     */
+  int32_t full_step;       /* 1 if the last step was a full step               */
+  int32_t nonfinite;       /* 1 if a router logit was NaN or infinite          */
+  double reuse_over_match; /* n_reused / n_matched (Sec. 5.4, Fig. 8); 0 if none */
+  int32_t expert_count[64];/* recomputed branches per expert                  */
+} moeca_stats;
+
+/* Copy the last step's statistics to *out.  Synchronises the stream. */
+int moeca_get_stats(moeca_layer* layer, moeca_stats* out, void* stream);
+
+/* ---- inspection (tests and benchmarks) --------------------------------- */
+enum {
+  MOECA_BUF_E_C = 0,    /* int32 [B*N*k]    cached expert id, -1 = empty      */
+  MOECA_BUF_W_C = 1,    /* fp32  [B*N*k]    cached gate weight w^{t0}         */
+  MOECA_BUF_N_C = 2,    /* fp32  [B*N*k]    norm of the cached row ||h^{t0}|| */
+  MOECA_BUF_H_C = 3,    /* act   [B*N*k][d] cached branch outputs h^{t0}      */
+  MOECA_BUF_STAT = 4,   /* fp32  [B][E][N]  EMA statistic C_{e,i}             */
+  MOECA_BUF_LOGITS = 5, /* fp32  [B*N][E]   router logits of the last step    */
+  MOECA_BUF_E_T = 6,    /* int32 [B*N*k]    current experts e_{i,p}           */
+  MOECA_BUF_W_T = 7,    /* fp32  [B*N*k]    current gate weights w_{i,p}      */
+  MOECA_BUF_HBAR = 8,   /* fp32  [B][E]     normalised entropy                */
+  MOECA_BUF_TAU = 9,    /* fp32  [B][E]     thresholds tau_e                  */
+  MOECA_BUF_MARGIN = 10,/* fp32  [B*N*k]    s - tau_e (+inf if unmatched)     */
+  MOECA_BUF_Q = 11,     /* int32 [B*N*k]    matched slot q(p), -1 unmatched   */
+  MOECA_BUF_MASK = 12,  /* uint8 [B*N*k]    1 = recomputed (p in R_i)         */
+  MOECA_BUF_SIGMA = 13, /* int32 [B*N*k]    cache slot of branch p after step */
+  MOECA_BUF_SYNC = 14,  /* uint8 [B*N]      S_i = [R_i non-empty]             */
+  MOECA_BUF_OFF = 15,   /* int32 [E+1]      per-expert offsets into LIST      */
+  MOECA_BUF_LIST = 16,  /* int32 [B*N*k]    recomputed flat branch ids
+                           f = (b*N + i)*k + p, grouped by expert, ascending  */
+  MOECA_BUF_POS = 17,   /* int32 [B*N*k]    index of f in LIST, -1 if reused  */
+  MOECA_BUF_COUNT = 18
+};
+
+/* Byte offset and size of an internal buffer inside the bound workspace, for
+ * tests that read or overwrite layer state between steps (all prior work on
+ * the stream must be complete).  Buffers 5-17 hold the last step's
+ * decisions; their contents are unspecified before the first step.
+ * MOECA_E_INVAL for an unknown id. */
+int moeca_debug_buffer(const moeca_layer* layer, int which, size_t* offset, size_t* bytes);
+
+/* Declare the cache valid (1) or invalid (0) after a test has written the
+ * state buffers 0-4 directly.  Host only. */
+int moeca_debug_set_valid(moeca_layer* layer, int valid);
+
+/* ---- per-stage timing --------------------------------------------------- */
+enum {
+  MOECA_STAGE_ROUTER = 0,  /* router logits, top-k, gate                       */
+  MOECA_STAGE_STAT = 1,    /* EMA statistic, entropy, thresholds                */
+  MOECA_STAGE_SCORE = 2,   /* matching and branch scores                       */
+  MOECA_STAGE_SELECT = 3,  /* recomputation set, slots, sync mask              */
+  MOECA_STAGE_LISTS = 4,   /* per-expert compaction                            */
+  MOECA_STAGE_FFN_UP = 5,  /* gathered up-projection + activation              */
+  MOECA_STAGE_FFN_DOWN = 6,/* down-projection into the cache rows              */
+  MOECA_STAGE_COMBINE = 7, /* combine, norms, cache metadata, attention path   */
+  MOECA_STAGE_COUNT = 8
+};
+
+/* Enable (1) or disable (0) HIP-event timing of each stage of each step on
+ * the step's stream (at most 512 steps are kept).  Enabling creates the
+ * events, disabling destroys them. */
+int moeca_set_timing(moeca_layer* layer, int enable);
+
+/* Sum of the per-stage times, in ms, over the steps recorded since timing
+ * was enabled or last read, into ms[0..n-1] (n <= MOECA_STAGE_COUNT); a
+ * stage skipped on a step contributes 0.  *steps receives the number of
+ * steps.  Synchronises the recorded events and clears the record. */
+int moeca_get_timing(moeca_layer* layer, double* ms, int n, int* steps);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* MOECA_H */

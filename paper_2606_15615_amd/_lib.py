@@ -1,0 +1,175 @@
+"""ctypes binding of libmoeca.so (include/moeca.h): same names, argument
+marshalling only.  Every step of the layer runs in the library's HIP
+kernels; if the library is missing this module raises instead of falling
+back to anything else."""
+from __future__ import annotations
+
+import ctypes
+import os
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmoeca.so")
+
+MOECA_OK = 0
+MOECA_E_INVAL = -1
+MOECA_E_STATE = -2
+MOECA_E_HIP = -3
+
+MOECA_MODE_FULL, MOECA_MODE_THRESHOLD, MOECA_MODE_RATIO = 0, 1, 2
+MOECA_DTYPE_BF16, MOECA_DTYPE_FP32 = 0, 1
+MOECA_ACT_GELU_TANH, MOECA_ACT_GELU_ERF = 0, 1
+
+BUF = {
+    "e_c": 0, "w_c": 1, "n_c": 2, "h_c": 3, "stat": 4, "logits": 5, "e_t": 6, "w_t": 7,
+    "hbar": 8, "tau": 9, "margin": 10, "q": 11, "mask": 12, "sigma": 13, "sync": 14,
+    "off": 15, "list": 16, "pos": 17,
+}
+STAGES = ["router", "stat", "score", "select", "lists", "ffn_up", "ffn_down", "combine"]
+
+
+class moeca_policy(ctypes.Structure):
+    _fields_ = [
+        ("mode", ctypes.c_int32), ("ratio", ctypes.c_float), ("tau0", ctypes.c_float),
+        ("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("lambda1", ctypes.c_float),
+        ("lambda2", ctypes.c_float), ("refresh_cycle", ctypes.c_int32),
+        ("norm_topk", ctypes.c_int32), ("act", ctypes.c_int32), ("dtype", ctypes.c_int32),
+        ("batch", ctypes.c_int32), ("tokens", ctypes.c_int32),
+    ]
+
+
+class moeca_stats(ctypes.Structure):
+    _fields_ = [
+        ("n_branches", ctypes.c_int64), ("n_recompute", ctypes.c_int64),
+        ("n_unmatched", ctypes.c_int64), ("n_matched", ctypes.c_int64),
+        ("n_reused", ctypes.c_int64), ("n_sync", ctypes.c_int64),
+        ("full_step", ctypes.c_int32), ("nonfinite", ctypes.c_int32),
+        ("reuse_over_match", ctypes.c_double), ("expert_count", ctypes.c_int32 * 64),
+    ]
+
+
+_SIGS = {
+    "moeca_policy_default": (None, [ctypes.POINTER(moeca_policy)]),
+    "moeca_layer_create": (ctypes.c_void_p, [ctypes.c_int, ctypes.c_int, ctypes.c_int,
+                                             ctypes.c_int, ctypes.POINTER(moeca_policy)]),
+    "moeca_layer_destroy": (None, [ctypes.c_void_p]),
+    "moeca_last_error": (ctypes.c_char_p, []),
+    "moeca_layer_set_weights": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
+                                               ctypes.c_void_p, ctypes.c_void_p]),
+    "moeca_workspace_bytes": (ctypes.c_size_t, [ctypes.c_void_p]),
+    "moeca_bind_workspace": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t]),
+    "moeca_bind_attention": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
+    "moeca_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                  ctypes.c_void_p, ctypes.c_void_p]),
+    "moeca_cache_reset": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
+    "moeca_get_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(moeca_stats),
+                                       ctypes.c_void_p]),
+    "moeca_debug_buffer": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int,
+                                          ctypes.POINTER(ctypes.c_size_t),
+                                          ctypes.POINTER(ctypes.c_size_t)]),
+    "moeca_debug_set_valid": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
+    "moeca_set_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
+    "moeca_get_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_double),
+                                        ctypes.c_int, ctypes.POINTER(ctypes.c_int)]),
+}
+EXPORTED = tuple(_SIGS)
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libmoeca.so (built by ``__graft_entry__.build()``)."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+        lib = ctypes.CDLL(LIB_PATH)
+        for name, (res, args) in _SIGS.items():
+            fn = getattr(lib, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = lib
+    return _lib
+
+
+class MoecaError(RuntimeError):
+    def __init__(self, code: int, msg: str):
+        super().__init__(f"{msg} (code {code})")
+        self.code = code
+
+
+def _check(code: int) -> int:
+    if code != MOECA_OK:
+        raise MoecaError(code, load().moeca_last_error().decode())
+    return code
+
+
+def moeca_policy_default() -> moeca_policy:
+    p = moeca_policy()
+    load().moeca_policy_default(ctypes.byref(p))
+    return p
+
+
+def moeca_layer_create(d: int, E: int, k: int, d_ff: int, policy: moeca_policy) -> int:
+    h = load().moeca_layer_create(d, E, k, d_ff, ctypes.byref(policy))
+    if not h:
+        raise MoecaError(MOECA_E_INVAL, load().moeca_last_error().decode())
+    return h
+
+
+def moeca_layer_destroy(h: int) -> None:
+    load().moeca_layer_destroy(h)
+
+
+def moeca_last_error() -> str:
+    return load().moeca_last_error().decode()
+
+
+def moeca_layer_set_weights(h, W_r, b_r, W_up, W_down) -> int:
+    return _check(load().moeca_layer_set_weights(h, W_r, b_r, W_up, W_down))
+
+
+def moeca_workspace_bytes(h) -> int:
+    return load().moeca_workspace_bytes(h)
+
+
+def moeca_bind_workspace(h, dev, nbytes) -> int:
+    return _check(load().moeca_bind_workspace(h, dev, nbytes))
+
+
+def moeca_bind_attention(h, attn_in, attn_cache) -> int:
+    return _check(load().moeca_bind_attention(h, attn_in, attn_cache))
+
+
+def moeca_step(h, x_t, t, out, stream) -> int:
+    return _check(load().moeca_step(h, x_t, t, out, stream))
+
+
+def moeca_cache_reset(h, stream) -> int:
+    return _check(load().moeca_cache_reset(h, stream))
+
+
+def moeca_get_stats(h, stream) -> moeca_stats:
+    s = moeca_stats()
+    _check(load().moeca_get_stats(h, ctypes.byref(s), stream))
+    return s
+
+
+def moeca_debug_buffer(h, which: int) -> tuple[int, int]:
+    off, nb = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(load().moeca_debug_buffer(h, which, ctypes.byref(off), ctypes.byref(nb)))
+    return off.value, nb.value
+
+
+def moeca_debug_set_valid(h, valid: int) -> int:
+    return _check(load().moeca_debug_set_valid(h, valid))
+
+
+def moeca_set_timing(h, enable: int) -> int:
+    return _check(load().moeca_set_timing(h, enable))
+
+
+def moeca_get_timing(h, n: int = 8) -> tuple[list[float], int]:
+    arr = (ctypes.c_double * n)()
+    steps = ctypes.c_int()
+    _check(load().moeca_get_timing(h, arr, n, ctypes.byref(steps)))
+    return list(arr), steps.value

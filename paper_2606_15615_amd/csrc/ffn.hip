@@ -1,0 +1,337 @@
+// Grouped expert FFN on the recomputed branches (Sec. 4.1: only R_i goes
+// through FFN_e; Sec. 2.3: FFN_e(x) = W_down[e] act(W_up[e] x)).
+//
+// The per-expert lists (ascending flat branch ids, grouped by expert) define
+// a grouped GEMM with a device-side row count per expert.  The grid is sized
+// on the host for the worst case and every block derives its tile from the
+// per-expert offsets, so no count ever travels to the host.
+//
+//   up   : mid[r]  = act(x[token(r)] . W_up[e]^T)     gathered rows -> rows
+//   down : h_c[slot(r)] = mid[r] . W_down[e]^T        rows -> cache rows
+//
+// The down projection writes each recomputed branch straight into the cache
+// slot it will occupy: reused slots are never touched, so the combine reads
+// every branch feature from the cache.
+//
+// bf16 path: v_mfma_f32_32x32x16_bf16 with fp32 accumulation; 256 threads
+// as 2x2 waves, block tile TM x TN, k-tile 64, LDS double buffered with
+// padded rows; the activation is applied to the fp32 accumulator and the
+// result rounded to bf16.  Tile order: expert-major, then N tile, then M tile,
+// and consecutive logical tiles sit on the same XCD, so the M tiles sharing a
+// weight slice run together and the expert's gathered rows stay in that
+// XCD's L2.
+#include "common.h"
+#include "internal.h"
+
+namespace moeca {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(16))) float f32x16_t;
+
+enum { kUp = 0, kDown = 1 };
+constexpr int kXcds = 8;
+
+__device__ __forceinline__ float act_fn(float z, int act) {
+  if (act == 0) {
+    // tanh GELU: 0.5 z (1 + tanh(u)) = z / (1 + exp(-2u)),
+    // u = sqrt(2/pi) (z + 0.044715 z^3)
+    const float u = 0.7978845608028654f * (z + 0.044715f * z * z * z);
+    return z * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * u));
+  }
+  return 0.5f * z * (1.0f + erff(z * 0.7071067811865476f));
+}
+
+struct Tile {
+  int e, r0, rows, n0;
+};
+
+// Logical tile L -> (expert, first row, row count, first column); e = -1 if
+// this block has no tile.  Tiles per expert: ceil(cnt_e / TM) * NT.
+template <int TM>
+__device__ Tile decode_tile(const int32_t* __restrict__ off, int E, int NT) {
+  int total = 0;
+  for (int e = 0; e < E; ++e) total += ((off[e + 1] - off[e] + TM - 1) / TM) * NT;
+  const int per = (total + kXcds - 1) / kXcds;
+  const int xcd = blockIdx.x % kXcds;
+  const int slot = blockIdx.x / kXcds;
+  const int L = xcd * per + slot;
+  Tile t{-1, 0, 0, 0};
+  if (slot >= per || L >= total) return t;
+  int acc = 0;
+  for (int e = 0; e < E; ++e) {
+    const int cnt = off[e + 1] - off[e];
+    const int mt = (cnt + TM - 1) / TM;
+    const int tiles = mt * NT;
+    if (L < acc + tiles) {
+      const int local = L - acc;
+      const int m = local % mt;
+      t.e = e;
+      t.r0 = off[e] + m * TM;
+      t.rows = min(TM, cnt - m * TM);
+      t.n0 = (local / mt);
+      return t;
+    }
+    acc += tiles;
+  }
+  return t;
+}
+
+// ---------------------------------------------------------------------------
+// bf16 MFMA grouped GEMM
+// ---------------------------------------------------------------------------
+constexpr int kTK = 64;
+constexpr int kLdsRow = kTK + 8;  // padded row (bf16 elements): 144 bytes
+
+template <int TM, int TN, int KIND>
+__global__ __launch_bounds__(256) void gemm_bf16_kernel(
+    const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
+    const int32_t* __restrict__ off, const int32_t* __restrict__ list,
+    const int32_t* __restrict__ sigma, int E, int k, int K, int Nout, int act,
+    uint16_t* __restrict__ dst) {
+  constexpr int WM = TM / 2, WN = TN / 2;  // wave tile
+  constexpr int FM = WM / 32, FN = WN / 32;
+  constexpr int LA = TM / 32, LB = TN / 32;  // 16-byte loads per thread per k-tile
+  __shared__ __attribute__((aligned(16))) uint16_t As[2][TM * kLdsRow];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][TN * kLdsRow];
+  __shared__ int s_src[TM];
+  __shared__ int s_dst[TM];
+  __shared__ int s_tile[4];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = tid >> 6;
+  const int wm = wv >> 1, wn = wv & 1;
+
+  if (tid == 0) {
+    const Tile t = decode_tile<TM>(off, E, Nout / TN);
+    s_tile[0] = t.e;
+    s_tile[1] = t.r0;
+    s_tile[2] = t.rows;
+    s_tile[3] = t.n0 * TN;
+  }
+  __syncthreads();
+  const int e = s_tile[0];
+  if (e < 0) return;
+  const int r0 = s_tile[1], rows = s_tile[2], n0 = s_tile[3];
+
+  for (int r = tid; r < TM; r += 256) {
+    const int rr = r < rows ? r : 0;  // padding rows re-read row 0 and are never stored
+    const int f = list[r0 + rr];
+    if (KIND == kUp) {
+      s_src[r] = f / k;
+      s_dst[r] = r < rows ? r0 + r : -1;
+    } else {
+      s_src[r] = r0 + rr;
+      s_dst[r] = r < rows ? (f / k) * k + sigma[f] : -1;
+    }
+  }
+  __syncthreads();
+
+  const int lrow = tid >> 3;        // 0..31
+  const int lcol = (tid & 7) * 8;   // element offset of this thread's 16 bytes
+  const uint16_t* a_ptr[LA];
+  const uint16_t* b_ptr[LB];
+#pragma unroll
+  for (int i = 0; i < LA; ++i) a_ptr[i] = A + int64_t(s_src[lrow + 32 * i]) * K + lcol;
+#pragma unroll
+  for (int i = 0; i < LB; ++i)
+    b_ptr[i] = W + (int64_t(e) * Nout + n0 + lrow + 32 * i) * K + lcol;
+
+  uint4 ra[LA], rb[LB];
+  f32x16_t acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+  auto gload = [&](int kt) {
+#pragma unroll
+    for (int i = 0; i < LA; ++i) ra[i] = *reinterpret_cast<const uint4*>(a_ptr[i] + kt * kTK);
+#pragma unroll
+    for (int i = 0; i < LB; ++i) rb[i] = *reinterpret_cast<const uint4*>(b_ptr[i] + kt * kTK);
+  };
+  auto lstore = [&](int buf) {
+#pragma unroll
+    for (int i = 0; i < LA; ++i)
+      *reinterpret_cast<uint4*>(&As[buf][(lrow + 32 * i) * kLdsRow + lcol]) = ra[i];
+#pragma unroll
+    for (int i = 0; i < LB; ++i)
+      *reinterpret_cast<uint4*>(&Bs[buf][(lrow + 32 * i) * kLdsRow + lcol]) = rb[i];
+  };
+
+  const int KT = K / kTK;
+  gload(0);
+  lstore(0);
+  __syncthreads();
+  const int frow = lane & 31;
+  const int fk = (lane >> 5) * 8;
+  for (int kt = 0; kt < KT; ++kt) {
+    const int cur = kt & 1;
+    if (kt + 1 < KT) gload(kt + 1);
+#pragma unroll
+    for (int ks = 0; ks < kTK / 16; ++ks) {
+      bf16x8_t fa[FM], fb[FN];
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        fa[i] = *reinterpret_cast<const bf16x8_t*>(
+            &As[cur][(wm * WM + i * 32 + frow) * kLdsRow + ks * 16 + fk]);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        fb[j] = *reinterpret_cast<const bf16x8_t*>(
+            &Bs[cur][(wn * WN + j * 32 + frow) * kLdsRow + ks * 16 + fk]);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j)
+          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+    }
+    if (kt + 1 < KT) lstore(cur ^ 1);
+    __syncthreads();
+  }
+
+  // D layout of a 32x32 MFMA tile: lane holds column (lane & 31) and rows
+  // 8*(r/4) + 4*(lane/32) + (r%4) for r = 0..15.
+#pragma unroll
+  for (int i = 0; i < FM; ++i) {
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int m = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+      const int drow = s_dst[m];
+      if (drow < 0) continue;
+      uint16_t* out = dst + int64_t(drow) * Nout + n0 + wn * WN + (lane & 31);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        float v = acc[i][j][r];
+        if (KIND == kUp) v = act_fn(v, act);
+        out[j * 32] = f32_to_bf16(v);
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// fp32 grouped GEMM (fp32 layers): 64x64 block tile, 4x4 per thread, FMA.
+// ---------------------------------------------------------------------------
+constexpr int kF32T = 64;
+constexpr int kF32K = 16;
+
+template <int KIND>
+__global__ __launch_bounds__(256) void gemm_f32_kernel(
+    const float* __restrict__ A, const float* __restrict__ W, const int32_t* __restrict__ off,
+    const int32_t* __restrict__ list, const int32_t* __restrict__ sigma, int E, int k, int K,
+    int Nout, int act, float* __restrict__ dst) {
+  __shared__ float As[kF32K][kF32T + 4];
+  __shared__ float Bs[kF32K][kF32T + 4];
+  __shared__ int s_src[kF32T];
+  __shared__ int s_dst[kF32T];
+  __shared__ int s_tile[4];
+  const int tid = threadIdx.x;
+  if (tid == 0) {
+    const Tile t = decode_tile<kF32T>(off, E, Nout / kF32T);
+    s_tile[0] = t.e;
+    s_tile[1] = t.r0;
+    s_tile[2] = t.rows;
+    s_tile[3] = t.n0 * kF32T;
+  }
+  __syncthreads();
+  const int e = s_tile[0];
+  if (e < 0) return;
+  const int r0 = s_tile[1], rows = s_tile[2], n0 = s_tile[3];
+  if (tid < kF32T) {
+    const int r = tid;
+    const int rr = r < rows ? r : 0;
+    const int f = list[r0 + rr];
+    if (KIND == kUp) {
+      s_src[r] = f / k;
+      s_dst[r] = r < rows ? r0 + r : -1;
+    } else {
+      s_src[r] = r0 + rr;
+      s_dst[r] = r < rows ? (f / k) * k + sigma[f] : -1;
+    }
+  }
+  __syncthreads();
+  const int lr = tid >> 2, lk = (tid & 3) * 4;
+  const float* ap = A + int64_t(s_src[lr]) * K + lk;
+  const float* bp = W + (int64_t(e) * Nout + n0 + lr) * K + lk;
+  const int tx = tid & 15, ty = tid >> 4;
+  float acc[4][4] = {};
+  for (int k0 = 0; k0 < K; k0 += kF32K) {
+    const float4 va = *reinterpret_cast<const float4*>(ap + k0);
+    const float4 vb = *reinterpret_cast<const float4*>(bp + k0);
+    As[lk + 0][lr] = va.x;
+    As[lk + 1][lr] = va.y;
+    As[lk + 2][lr] = va.z;
+    As[lk + 3][lr] = va.w;
+    Bs[lk + 0][lr] = vb.x;
+    Bs[lk + 1][lr] = vb.y;
+    Bs[lk + 2][lr] = vb.z;
+    Bs[lk + 3][lr] = vb.w;
+    __syncthreads();
+#pragma unroll
+    for (int kk = 0; kk < kF32K; ++kk) {
+      float a[4], b[4];
+#pragma unroll
+      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
+    }
+    __syncthreads();
+  }
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int drow = s_dst[ty * 4 + i];
+    if (drow < 0) continue;
+    float* out = dst + int64_t(drow) * Nout + n0 + tx * 4;
+#pragma unroll
+    for (int j = 0; j < 4; ++j) out[j] = (KIND == kUp) ? act_fn(acc[i][j], act) : acc[i][j];
+  }
+}
+
+int max_tiles(const Shape& s, int TM, int NT) {
+  const int64_t mt = (s.branches() + TM - 1) / TM + s.E;
+  const int64_t g = mt * NT;
+  return static_cast<int>((g + kXcds - 1) / kXcds * kXcds);
+}
+
+template <int KIND>
+hipError_t launch_gemm(const Shape& s, const void* A, const void* W, int K, int Nout, int act,
+                       const Buffers& b, void* dst, hipStream_t st) {
+  if (s.bf16) {
+    const auto* a = static_cast<const uint16_t*>(A);
+    const auto* w = static_cast<const uint16_t*>(W);
+    auto* o = static_cast<uint16_t*>(dst);
+    if (Nout % 128 == 0 && KIND == kUp) {
+      gemm_bf16_kernel<128, 128, KIND><<<max_tiles(s, 128, Nout / 128), 256, 0, st>>>(
+          a, w, b.off, b.list, b.sigma, s.E, s.k, K, Nout, act, o);
+    } else {
+      gemm_bf16_kernel<128, 64, KIND><<<max_tiles(s, 128, Nout / 64), 256, 0, st>>>(
+          a, w, b.off, b.list, b.sigma, s.E, s.k, K, Nout, act, o);
+    }
+  } else {
+    gemm_f32_kernel<KIND><<<max_tiles(s, kF32T, Nout / kF32T), 256, 0, st>>>(
+        static_cast<const float*>(A), static_cast<const float*>(W), b.off, b.list, b.sigma, s.E,
+        s.k, K, Nout, act, static_cast<float*>(dst));
+  }
+  return hipGetLastError();
+}
+
+}  // namespace
+
+hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, int act,
+                         const Buffers& b, hipStream_t st) {
+  return launch_gemm<kUp>(s, x, W_up, s.d, s.d_ff, act, b, b.mid, st);
+}
+
+hipError_t launch_ffn_down(const Shape& s, const void* W_down, const Buffers& b,
+                           hipStream_t st) {
+  return launch_gemm<kDown>(s, b.mid, W_down, s.d_ff, s.d, 0, b, b.h_c, st);
+}
+
+}  // namespace moeca

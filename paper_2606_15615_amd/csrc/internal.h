@@ -1,0 +1,66 @@
+// Internal interface between the host orchestration (moeca.cpp) and the
+// kernel launchers (*.hip).  Not part of the public C ABI.
+#pragma once
+#include <hip/hip_runtime.h>
+#include <cstddef>
+#include <cstdint>
+
+namespace moeca {
+
+struct Shape {
+  int d, E, k, d_ff, B, N;
+  bool bf16;
+  int64_t tokens() const { return int64_t(B) * N; }
+  int64_t branches() const { return int64_t(B) * N * k; }
+  size_t act_bytes() const { return bf16 ? 2 : 4; }
+};
+
+// Device views of the workspace regions (see moeca_debug_buffer for the
+// meaning of the public ones).
+struct Buffers {
+  int32_t* e_c;
+  float* w_c;
+  float* n_c;
+  void* h_c;
+  float* stat;      // [B][E][N]
+  float* logits;    // [B*N][E]
+  int32_t* e_t;
+  float* w_t;
+  float* hbar;      // [B][E]
+  float* tau;       // [B][E]
+  float* margin;
+  int32_t* q;
+  uint8_t* mask;
+  int32_t* sigma;
+  uint8_t* sync;    // [B*N]
+  int32_t* off;     // [E+1]
+  int32_t* list;
+  int32_t* pos;
+  int32_t* cnt_bs;  // [B][E] recomputed branches per sample and expert
+  int32_t* stats_bs;// [B][4] recompute, unmatched, matched, sync per sample
+  int32_t* rflags;  // router: one non-finite flag per block
+  void* mid;        // [B*N*k][d_ff] FFN activation of listed rows
+};
+
+enum SelectMode { kSelFull = 0, kSelThreshold = 1, kSelRatio = 2 };
+
+int router_blocks(const Shape& s);
+
+hipError_t launch_router(const Shape& s, const void* x, const void* W_r, const float* b_r,
+                         int norm_topk, const Buffers& b, hipStream_t st);
+hipError_t launch_stat(const Shape& s, float beta, float tau0, float alpha, const Buffers& b,
+                       hipStream_t st);
+hipError_t launch_score(const Shape& s, float lambda1, float lambda2, const Buffers& b,
+                        hipStream_t st);
+hipError_t launch_select(const Shape& s, int sel_mode, int budget, const Buffers& b,
+                         hipStream_t st);
+hipError_t launch_lists(const Shape& s, const Buffers& b, hipStream_t st);
+hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, int act,
+                         const Buffers& b, hipStream_t st);
+hipError_t launch_ffn_down(const Shape& s, const void* W_down, const Buffers& b,
+                           hipStream_t st);
+hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void* attn_in,
+                          void* attn_cache, const Buffers& b, hipStream_t st);
+hipError_t launch_reset(const Shape& s, const Buffers& b, hipStream_t st);
+
+}  // namespace moeca

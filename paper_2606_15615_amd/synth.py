@@ -36,11 +36,15 @@ FP32 = "fp32"
 def fp32_to_bf16_bits(a: np.ndarray) -> np.ndarray:
     """Round an fp32 array to bf16 (nearest, ties to even); return the bits."""
     a = np.ascontiguousarray(a, dtype=np.float32)
-    u = a.view(np.uint32).astype(np.uint64)
-    nan = np.isnan(a)
-    r = ((u + 0x7FFF + ((u >> 16) & 1)) >> 16).astype(np.uint16)
-    r[nan] = 0x7FC0
-    return r
+    u = a.view(np.uint32)
+    # no uint32 overflow: the largest non-NaN pattern is 0xFF800000 (-inf)
+    r = (u >> 16) & np.uint32(1)
+    r += u
+    r += np.uint32(0x7FFF)
+    r >>= 16
+    out = r.astype(np.uint16)
+    out[np.isnan(a)] = 0x7FC0
+    return out
 
 
 def bf16_bits_to_fp32(b: np.ndarray) -> np.ndarray:

@@ -1,0 +1,193 @@
+"""GPU parity of the branch-cached MoE layer step against the CPU oracle.
+
+Every test drives the HIP library through its C ABI (paper_2606_15615_amd
+._lib via MoecaLayer) on seeded synthetic inputs and compares with the
+oracle as described in tests/gpu_harness.py: decisions (logits, experts,
+gate weights, statistic, thresholds, matching, margins, masks, slots, sync
+mask, expert lists) bit for bit; rows and outputs within 2e-2 (bf16) or
+1e-4 (fp32) max relative error.
+"""
+import numpy as np
+import pytest
+
+pytestmark = pytest.mark.gpu
+
+from oracle import moeca_oracle as O
+from paper_2606_15615_amd.synth import LayerShape, WORKLOADS
+
+from gpu_harness import Setup, check_step, run_forced, say, rel_err
+
+
+@pytest.fixture(scope="module", autouse=True)
+def _gpu():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_15615_amd import _lib
+    _lib.load()   # fails loudly if the library is missing
+
+
+# ---------------------------------------------------------------------------
+# tiny fp32 layer (d=384, 8 experts, top-2, 1536 hidden, 256 tokens, 5 steps)
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("mode,ratio", [("ratio", 0.0), ("ratio", 0.3), ("ratio", 1.0),
+                                        ("threshold", 0.3)])
+def test_tiny_fp32_trajectory(mode, ratio):
+    S = Setup(WORKLOADS["tiny"], mode=mode, seed=1, T=5, ratio=ratio)
+    infos = run_forced(S, 5, label=f"tiny {mode} {ratio}")
+    say(f"  tiny {mode} {ratio}: {infos}")
+
+
+# ---------------------------------------------------------------------------
+# small bf16 layers with ragged token counts and a 64-multiple hidden width
+# ---------------------------------------------------------------------------
+RAGGED = LayerShape(d=256, E=6, k=2, d_ff=320, B=3, N=77, dtype="bf16")
+
+
+@pytest.mark.parametrize("mode,ratio", [("threshold", 0.3), ("ratio", 0.3), ("ratio", 0.05)])
+def test_ragged_bf16_trajectory(mode, ratio):
+    S = Setup(RAGGED, mode=mode, seed=2, T=6, ratio=ratio)
+    run_forced(S, 6, label=f"ragged {mode} {ratio}")
+
+
+@pytest.mark.parametrize("shape", [
+    LayerShape(d=128, E=4, k=4, d_ff=128, B=2, N=33, dtype="bf16"),    # k == E
+    LayerShape(d=192, E=5, k=1, d_ff=256, B=2, N=40, dtype="bf16"),    # top-1
+    LayerShape(d=64, E=3, k=2, d_ff=64, B=4, N=1, dtype="bf16"),       # one token per sample
+    LayerShape(d=128, E=64, k=8, d_ff=128, B=1, N=50, dtype="fp32"),   # many experts, k = 8
+])
+def test_edge_shapes(shape):
+    S = Setup(shape, mode="ratio", seed=3, T=5, ratio=0.4, refresh_cycle=3)
+    run_forced(S, 5, label=f"edge {shape}")
+
+
+def test_unnormalised_gate_erf_gelu_and_bias():
+    shape = LayerShape(d=128, E=8, k=2, d_ff=192, B=2, N=64, dtype="fp32")
+    S = Setup(shape, mode="threshold", seed=4, T=4, norm_topk=False, act="gelu_erf",
+              bias="zipf", lambda1=0.5, lambda2=2.0, tau0=0.9, alpha=0.3, beta=0.5)
+    run_forced(S, 4, label="variants")
+
+
+# ---------------------------------------------------------------------------
+# uncached comparator, empty recomputation set, ratio 0 bit-exact combine
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("shape", [WORKLOADS["tiny"], RAGGED])
+def test_uncached_mode(shape):
+    S = Setup(shape, mode="full", seed=5, T=3)
+    run_forced(S, 3, label="uncached")
+    assert S.layer.stats().full_step == 1
+
+
+@pytest.mark.parametrize("mode", ["ratio", "threshold"])
+def test_nothing_recomputed_is_bit_exact(mode):
+    """Same input as the refresh step: ratio 0 (or a huge threshold) reuses
+    every branch; the output is then the combine of cached rows, which the
+    GPU must reproduce bit for bit."""
+    S = Setup(RAGGED, mode=mode, seed=6, T=1, ratio=0.0, tau0=1e6, refresh_cycle=0)
+    st0 = O.State(S.dims, attention=True)
+    out0, st1, _ = O.step(S.dims, S.pol, S.W, st0, S.xs[0], 0, attn_in=S.attn[0])
+    S.import_state(st1)
+    out_g = S.gpu_step(S.xs[0], 1, S.attn[0])
+    out_o, st2, rec = O.step(S.dims, S.pol, S.W, st1, S.xs[0], 1, attn_in=S.attn[0])
+    assert rec["mask"].sum() == 0
+    check_step(S, 1, rec, out_o, st1, st2, out_g, label="reuse-all")
+    assert np.array_equal(out_g, out_o)
+    assert np.array_equal(out_o, out0)
+
+
+def test_reset_mid_trajectory():
+    S = Setup(RAGGED, mode="ratio", seed=7, T=4, ratio=0.3, refresh_cycle=0)
+    for t in range(3):
+        S.gpu_step(S.xs[t], t, S.attn[t])
+    assert S.layer.stats().full_step == 0
+    S.layer.reset()
+    out_g = S.gpu_step(S.xs[3], 3, S.attn[3])
+    out_o, st_new, rec = O.step(S.dims, S.pol, S.W, O.State(S.dims, True), S.xs[3], 3,
+                                attn_in=S.attn[3])
+    assert rec["full"] and S.layer.stats().full_step == 1
+    check_step(S, 3, rec, out_o, O.State(S.dims, True), st_new, out_g, label="after reset")
+
+
+def test_determinism():
+    S = Setup(RAGGED, mode="ratio", seed=8, T=3, ratio=0.3, refresh_cycle=0)
+    st = O.State(S.dims, attention=True)
+    for t in range(2):
+        _, st, _ = O.step(S.dims, S.pol, S.W, st, S.xs[t], t, attn_in=S.attn[t])
+    outs = []
+    for _ in range(2):
+        S.import_state(st)
+        outs.append((S.gpu_step(S.xs[2], 2, S.attn[2]), S.layer.read("h_c"),
+                     S.layer.read("mask"), S.layer.read("list")))
+    for a, b in zip(*outs):
+        assert np.array_equal(a, b)
+
+
+def test_nonfinite_input_is_flagged():
+    S = Setup(RAGGED, mode="ratio", seed=9, T=1, ratio=0.3)
+    x = S.xs[0].copy()
+    x[1, 5, 7] = 0x7FC0            # bf16 NaN
+    S.gpu_step(x, 0, S.attn[0])
+    assert S.layer.stats().nonfinite == 1
+    S.gpu_step(S.xs[0], 1, S.attn[0])
+    assert S.layer.stats().nonfinite == 0
+
+
+# ---------------------------------------------------------------------------
+# DiT-MoE-XL-like layer (d=1152, 16 experts, top-2, 4608 hidden), 256 tokens x 8
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("mode", ["ratio", "threshold"])
+def test_xl256_trajectory(mode):
+    S = Setup(WORKLOADS["xl256"], mode=mode, seed=10, T=5, ratio=0.3)
+    infos = run_forced(S, 5, label=f"xl256 {mode}")
+    say(f"  xl256 {mode}: {infos}")
+
+
+# ---------------------------------------------------------------------------
+# The same layer at 1024 tokens x 8 (the benchmarked shape): decisions over
+# the whole batch, outputs and rows on sampled tokens.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("mode", ["ratio", "threshold"])
+def test_xl1024_sampled(mode):
+    shape = WORKLOADS["xl1024"]
+    S = Setup(shape, mode=mode, seed=11, T=3, ratio=0.3, refresh_cycle=0)
+    dims = S.dims
+    rng = np.random.default_rng(12)
+    sample = np.sort(rng.choice(shape.tokens, size=48, replace=False))
+    ev = np.zeros(shape.tokens, bool)
+    ev[sample] = True
+    ev = ev.reshape(shape.B, shape.N)
+    # a valid cache: routing and statistic from the oracle's first two steps,
+    # rows of unsampled tokens filled with synthetic values and their norms
+    st = O.State(dims, attention=True)
+    for t in range(2):
+        _, st, _ = O.step(dims, S.pol, S.W, st, S.xs[t], t, attn_in=S.attn[t], tokens=sample)
+        fill = ~ev
+        rows = S.sy.rows((int(fill.sum()), shape.k, shape.d), scale=0.05)
+        st.h_c[fill] = rows
+        st.n_c[fill] = O.row_norms(rows, shape.dtype)
+    S.import_state(st)
+    out_g = S.gpu_step(S.xs[2], 2, S.attn[2])
+    out_o, st_new, rec = O.step(dims, S.pol, S.W, st, S.xs[2], 2, attn_in=S.attn[2],
+                                tokens=sample)
+    info = check_step(S, 2, rec, out_o, st, st_new, out_g, evaluated=ev, label=f"xl1024 {mode}")
+    say(f"  xl1024 {mode}: {info}")
+
+
+def test_free_running_agreement():
+    """Both sides run freely from a reset.  Stored rows legitimately differ
+    in their last bf16 bits, so masks may drift apart over time; report the
+    agreement and require the outputs to stay within tolerance while the
+    masks agree."""
+    S = Setup(WORKLOADS["xl256"], mode="ratio", seed=13, T=6, ratio=0.3)
+    st = O.State(S.dims, attention=True)
+    agree = []
+    for t in range(6):
+        out_g = S.gpu_step(S.xs[t], t, S.attn[t])
+        out_o, st, rec = O.step(S.dims, S.pol, S.W, st, S.xs[t], t, attn_in=S.attn[t])
+        mask = S.layer.read("mask").reshape(rec["mask"].shape).astype(bool)
+        a = float((mask == rec["mask"]).mean())
+        agree.append(a)
+        if a == 1.0:
+            assert rel_err(out_g, out_o, "bf16") <= 2e-2
+    say(f"  free-running mask agreement per step: {agree}")
+    assert min(agree) >= 0.99
