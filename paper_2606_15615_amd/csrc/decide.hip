@@ -309,7 +309,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kSelThreads) void lists_kernel(
     const uint8_t* __restrict__ mask, const int32_t* __restrict__ e_t,
-    const int32_t* __restrict__ cnt_bs, int B, int N, int E, int k, int32_t* __restrict__ off,
+    const int32_t* __restrict__ cnt_bs, int B, int N, int E, int k, int tm, int nt_up,
+    int nt_down, int32_t* __restrict__ off, int32_t* __restrict__ tiles,
     int32_t* __restrict__ list, int32_t* __restrict__ pos) {
   __shared__ int s_base[64];
   __shared__ int s_run[64];
@@ -321,21 +322,39 @@ __global__ __launch_bounds__(kSelThreads) void lists_kernel(
   const int lane = tid & (kWave - 1);
   const int wv = tid / kWave;
 
-  if (tid == 0) {
-    int acc = 0;
-    for (int e = 0; e < E; ++e) {
-      int tot = 0, below = 0;
-      for (int b2 = 0; b2 < B; ++b2) {
-        const int c = cnt_bs[b2 * E + e];
-        tot += c;
-        if (b2 < b) below += c;
-      }
-      s_base[e] = acc + below;
-      s_run[e] = 0;
-      if (b == 0) off[e] = acc;
-      acc += tot;
+  // per expert: total count and count in samples before this one
+  if (tid < E) {
+    int tot = 0, below = 0;
+    for (int b2 = 0; b2 < B; ++b2) {
+      const int c = cnt_bs[b2 * E + tid];
+      tot += c;
+      if (b2 < b) below += c;
     }
-    if (b == 0) off[E] = acc;
+    s_base[tid] = below;
+    s_run[tid] = tot;
+  }
+  __syncthreads();
+  if (tid == 0) {
+    int acc = 0, tu = 0, td = 0;
+    for (int e = 0; e < E; ++e) {
+      const int tot = s_run[e];
+      if (b == 0) {
+        off[e] = acc;
+        tiles[e] = tu;
+        tiles[E + 1 + e] = td;
+      }
+      s_base[e] += acc;
+      s_run[e] = 0;
+      acc += tot;
+      const int mt = (tot + tm - 1) / tm;
+      tu += mt * nt_up;
+      td += mt * nt_down;
+    }
+    if (b == 0) {
+      off[E] = acc;
+      tiles[E] = tu;
+      tiles[2 * E + 1] = td;
+    }
   }
   __syncthreads();
 
@@ -413,9 +432,10 @@ hipError_t launch_select(const Shape& s, int sel_mode, int budget, const Buffers
   return hipGetLastError();
 }
 
-hipError_t launch_lists(const Shape& s, const Buffers& b, hipStream_t st) {
-  lists_kernel<<<dim3(s.B), dim3(kSelThreads), 0, st>>>(b.mask, b.e_t, b.cnt_bs, s.B, s.N, s.E,
-                                                        s.k, b.off, b.list, b.pos);
+hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st) {
+  lists_kernel<<<dim3(s.B), dim3(kSelThreads), 0, st>>>(
+      b.mask, b.e_t, b.cnt_bs, s.B, s.N, s.E, s.k, plan.tm, s.d_ff / plan.tn_up,
+      s.d / plan.tn_down, b.off, b.tiles, b.list, b.pos);
   return hipGetLastError();
 }
 

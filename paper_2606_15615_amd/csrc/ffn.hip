@@ -28,6 +28,7 @@ namespace {
 
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;  // 16 bytes, a native vector
 
 enum { kUp = 0, kDown = 1 };
 constexpr int kXcds = 8;
@@ -78,137 +79,201 @@ __device__ Tile decode_tile(const int32_t* __restrict__ off, int E, int NT) {
 }
 
 // ---------------------------------------------------------------------------
-// bf16 MFMA grouped GEMM
+// bf16 MFMA grouped GEMM, persistent.
+//
+// The grid holds a fixed number of blocks per CU.  Logical tiles (expert-
+// major, then N tile, then M tile; prefix per expert in `tile_off`) are split
+// into eight contiguous ranges, one per XCD (block b runs on XCD b % 8), and
+// the blocks of an XCD walk their range with a stride.  A block finds the
+// expert of a tile with one ballot over the per-expert prefixes.
+//
+// Main loop: k-tile 64, two LDS buffers, global loads issued two k-tiles
+// ahead into two register sets, one barrier per k-tile.  Epilogue: the tile
+// goes through LDS and leaves as 16-byte row segments.
 // ---------------------------------------------------------------------------
 constexpr int kTK = 64;
 constexpr int kLdsRow = kTK + 8;  // padded row (bf16 elements): 144 bytes
+constexpr int kGemmThreads = 256;
+
+// Global -> registers: LA rows of A and LB rows of W, 16 bytes each.
+template <int LA, int LB>
+__device__ __forceinline__ void gload(u32x4_t (&R)[LA + LB], const uint16_t* const (&ap)[LA],
+                                      const uint16_t* const (&bp)[LB], int koff) {
+#pragma unroll
+  for (int i = 0; i < LA; ++i) R[i] = *reinterpret_cast<const u32x4_t*>(ap[i] + koff);
+#pragma unroll
+  for (int i = 0; i < LB; ++i) R[LA + i] = *reinterpret_cast<const u32x4_t*>(bp[i] + koff);
+}
+
+// Registers -> one LDS buffer (row r of the tile at r * kLdsRow).
+template <int LA, int LB>
+__device__ __forceinline__ void lstore(const u32x4_t (&R)[LA + LB], uint16_t* as, uint16_t* bs,
+                                       int lrow, int lcol) {
+#pragma unroll
+  for (int i = 0; i < LA; ++i)
+    *reinterpret_cast<u32x4_t*>(&as[(lrow + 32 * i) * kLdsRow + lcol]) = R[i];
+#pragma unroll
+  for (int i = 0; i < LB; ++i)
+    *reinterpret_cast<u32x4_t*>(&bs[(lrow + 32 * i) * kLdsRow + lcol]) = R[LA + i];
+}
+
+// One k-tile of MFMAs on an LDS buffer: the wave's FM x FN 32x32 tiles.
+template <int FM, int FN>
+__device__ __forceinline__ void mfma_ktile(f32x16_t (&acc)[FM][FN], const uint16_t* as,
+                                           const uint16_t* bs, int arow0, int brow0, int frow,
+                                           int fk) {
+#pragma unroll
+  for (int ks = 0; ks < kTK / 16; ++ks) {
+    bf16x8_t fa[FM], fb[FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+      fa[i] = *reinterpret_cast<const bf16x8_t*>(
+          &as[(arow0 + i * 32 + frow) * kLdsRow + ks * 16 + fk]);
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+      fb[j] = *reinterpret_cast<const bf16x8_t*>(
+          &bs[(brow0 + j * 32 + frow) * kLdsRow + ks * 16 + fk]);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
+  }
+}
 
 template <int TM, int TN, int KIND>
-__global__ __launch_bounds__(256) void gemm_bf16_kernel(
+__global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
-    const int32_t* __restrict__ off, const int32_t* __restrict__ list,
-    const int32_t* __restrict__ sigma, int E, int k, int K, int Nout, int act,
-    uint16_t* __restrict__ dst) {
-  constexpr int WM = TM / 2, WN = TN / 2;  // wave tile
+    const int32_t* __restrict__ off, const int32_t* __restrict__ tile_off,
+    const int32_t* __restrict__ list, const int32_t* __restrict__ sigma, int E, int k, int K,
+    int Nout, int act, uint16_t* __restrict__ dst) {
+  constexpr int WM = TM / 2, WN = TN / 2;  // wave tile (2 x 2 waves)
   constexpr int FM = WM / 32, FN = WN / 32;
   constexpr int LA = TM / 32, LB = TN / 32;  // 16-byte loads per thread per k-tile
-  __shared__ __attribute__((aligned(16))) uint16_t As[2][TM * kLdsRow];
-  __shared__ __attribute__((aligned(16))) uint16_t Bs[2][TN * kLdsRow];
+  constexpr int CROW = TN + 8;               // epilogue LDS row (bf16 elements)
+  static_assert(TM * CROW <= 2 * TM * kLdsRow, "epilogue tile must fit in As");
+  __shared__ __attribute__((aligned(16))) uint16_t As[2 * TM * kLdsRow];
+  __shared__ __attribute__((aligned(16))) uint16_t Bs[2 * TN * kLdsRow];
   __shared__ int s_src[TM];
   __shared__ int s_dst[TM];
-  __shared__ int s_tile[4];
 
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = tid >> 6;
   const int wm = wv >> 1, wn = wv & 1;
+  const int NT = Nout / TN;
+  const int total = tile_off[E];
+  const int per = (total + kXcds - 1) / kXcds;
+  const int lo = (blockIdx.x % kXcds) * per;
+  const int hi = min(total, lo + per);
+  const int stride = gridDim.x / kXcds;
+  const int my_toff = lane < E ? tile_off[lane] : 0x7fffffff;
 
-  if (tid == 0) {
-    const Tile t = decode_tile<TM>(off, E, Nout / TN);
-    s_tile[0] = t.e;
-    s_tile[1] = t.r0;
-    s_tile[2] = t.rows;
-    s_tile[3] = t.n0 * TN;
-  }
-  __syncthreads();
-  const int e = s_tile[0];
-  if (e < 0) return;
-  const int r0 = s_tile[1], rows = s_tile[2], n0 = s_tile[3];
-
-  for (int r = tid; r < TM; r += 256) {
-    const int rr = r < rows ? r : 0;  // padding rows re-read row 0 and are never stored
-    const int f = list[r0 + rr];
-    if (KIND == kUp) {
-      s_src[r] = f / k;
-      s_dst[r] = r < rows ? r0 + r : -1;
-    } else {
-      s_src[r] = r0 + rr;
-      s_dst[r] = r < rows ? (f / k) * k + sigma[f] : -1;
-    }
-  }
-  __syncthreads();
-
-  const int lrow = tid >> 3;        // 0..31
-  const int lcol = (tid & 7) * 8;   // element offset of this thread's 16 bytes
-  const uint16_t* a_ptr[LA];
-  const uint16_t* b_ptr[LB];
-#pragma unroll
-  for (int i = 0; i < LA; ++i) a_ptr[i] = A + int64_t(s_src[lrow + 32 * i]) * K + lcol;
-#pragma unroll
-  for (int i = 0; i < LB; ++i)
-    b_ptr[i] = W + (int64_t(e) * Nout + n0 + lrow + 32 * i) * K + lcol;
-
-  uint4 ra[LA], rb[LB];
-  f32x16_t acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
-
-  auto gload = [&](int kt) {
-#pragma unroll
-    for (int i = 0; i < LA; ++i) ra[i] = *reinterpret_cast<const uint4*>(a_ptr[i] + kt * kTK);
-#pragma unroll
-    for (int i = 0; i < LB; ++i) rb[i] = *reinterpret_cast<const uint4*>(b_ptr[i] + kt * kTK);
-  };
-  auto lstore = [&](int buf) {
-#pragma unroll
-    for (int i = 0; i < LA; ++i)
-      *reinterpret_cast<uint4*>(&As[buf][(lrow + 32 * i) * kLdsRow + lcol]) = ra[i];
-#pragma unroll
-    for (int i = 0; i < LB; ++i)
-      *reinterpret_cast<uint4*>(&Bs[buf][(lrow + 32 * i) * kLdsRow + lcol]) = rb[i];
-  };
-
-  const int KT = K / kTK;
-  gload(0);
-  lstore(0);
-  __syncthreads();
+  const int lrow = tid >> 3;       // 0..31
+  const int lcol = (tid & 7) * 8;  // element offset of this thread's 16 bytes
   const int frow = lane & 31;
   const int fk = (lane >> 5) * 8;
-  for (int kt = 0; kt < KT; ++kt) {
-    const int cur = kt & 1;
-    if (kt + 1 < KT) gload(kt + 1);
-#pragma unroll
-    for (int ks = 0; ks < kTK / 16; ++ks) {
-      bf16x8_t fa[FM], fb[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-        fa[i] = *reinterpret_cast<const bf16x8_t*>(
-            &As[cur][(wm * WM + i * 32 + frow) * kLdsRow + ks * 16 + fk]);
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        fb[j] = *reinterpret_cast<const bf16x8_t*>(
-            &Bs[cur][(wn * WN + j * 32 + frow) * kLdsRow + ks * 16 + fk]);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(fa[i], fb[j], acc[i][j], 0, 0, 0);
-    }
-    if (kt + 1 < KT) lstore(cur ^ 1);
-    __syncthreads();
-  }
+  const int KT = K / kTK;
 
-  // D layout of a 32x32 MFMA tile: lane holds column (lane & 31) and rows
-  // 8*(r/4) + 4*(lane/32) + (r%4) for r = 0..15.
-#pragma unroll
-  for (int i = 0; i < FM; ++i) {
-#pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int m = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
-      const int drow = s_dst[m];
-      if (drow < 0) continue;
-      uint16_t* out = dst + int64_t(drow) * Nout + n0 + wn * WN + (lane & 31);
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        float v = acc[i][j][r];
-        if (KIND == kUp) v = act_fn(v, act);
-        out[j * 32] = f32_to_bf16(v);
+  for (int L = lo + static_cast<int>(blockIdx.x) / kXcds; L < hi; L += stride) {
+    const int e = __popcll(__ballot(my_toff <= L)) - 1;
+    const int e_base = __shfl(my_toff, e, 64);
+    const int o0 = off[e];
+    const int cnt = off[e + 1] - o0;
+    const int mt = (cnt + TM - 1) / TM;
+    const int local = L - e_base;
+    const int m = local % mt;
+    const int r0 = o0 + m * TM;
+    const int rows = min(TM, cnt - m * TM);
+    const int n0 = (local / mt) * TN;
+    (void)NT;
+
+    for (int r = tid; r < TM; r += kGemmThreads) {
+      const int rr = r < rows ? r : 0;  // padding rows re-read row 0, never stored
+      const int f = list[r0 + rr];
+      if (KIND == kUp) {
+        s_src[r] = f / k;
+        s_dst[r] = r < rows ? r0 + r : -1;
+      } else {
+        s_src[r] = r0 + rr;
+        s_dst[r] = r < rows ? (f / k) * k + sigma[f] : -1;
       }
     }
+    __syncthreads();
+
+    const uint16_t* a_ptr[LA];
+    const uint16_t* b_ptr[LB];
+#pragma unroll
+    for (int i = 0; i < LA; ++i) a_ptr[i] = A + int64_t(s_src[lrow + 32 * i]) * K + lcol;
+#pragma unroll
+    for (int i = 0; i < LB; ++i)
+      b_ptr[i] = W + (int64_t(e) * Nout + n0 + lrow + 32 * i) * K + lcol;
+
+    f32x16_t acc[FM][FN];
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    u32x4_t R0[LA + LB], R1[LA + LB];
+    uint16_t* const as0 = As;
+    uint16_t* const as1 = As + TM * kLdsRow;
+    uint16_t* const bs0 = Bs;
+    uint16_t* const bs1 = Bs + TN * kLdsRow;
+    const int arow0 = wm * WM, brow0 = wn * WN;
+
+    // prologue: tile 0 in LDS buffer 0, tile 1 in R1, tile 2 in R0
+    gload<LA, LB>(R0, a_ptr, b_ptr, 0);
+    if (KT > 1) gload<LA, LB>(R1, a_ptr, b_ptr, kTK);
+    lstore<LA, LB>(R0, as0, bs0, lrow, lcol);
+    if (KT > 2) gload<LA, LB>(R0, a_ptr, b_ptr, 2 * kTK);
+    __syncthreads();
+    for (int kt = 0; kt < KT; kt += 2) {
+      mfma_ktile<FM, FN>(acc, as0, bs0, arow0, brow0, frow, fk);          // tile kt
+      if (kt + 1 < KT) {
+        lstore<LA, LB>(R1, as1, bs1, lrow, lcol);                          // tile kt+1
+        if (kt + 3 < KT) gload<LA, LB>(R1, a_ptr, b_ptr, (kt + 3) * kTK);
+      }
+      __syncthreads();
+      if (kt + 1 < KT) {
+        mfma_ktile<FM, FN>(acc, as1, bs1, arow0, brow0, frow, fk);        // tile kt+1
+        if (kt + 2 < KT) {
+          lstore<LA, LB>(R0, as0, bs0, lrow, lcol);                        // tile kt+2
+          if (kt + 4 < KT) gload<LA, LB>(R0, a_ptr, b_ptr, (kt + 4) * kTK);
+        }
+        __syncthreads();
+      }
+    }
+
+    // epilogue: activation, bf16, through LDS (reusing As), 16-byte stores.
+    // D layout of a 32x32 MFMA tile: lane holds column (lane & 31) and rows
+    // 8*(r/4) + 4*(lane/32) + (r%4) for r = 0..15.
+    uint16_t* cs = As;
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) {
+          const int mr = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
+          const int nc = wn * WN + j * 32 + (lane & 31);
+          float v = acc[i][j][r];
+          if (KIND == kUp) v = act_fn(v, act);
+          cs[mr * CROW + nc] = f32_to_bf16(v);
+        }
+    __syncthreads();
+    constexpr int CPR = TN / 8;  // 16-byte chunks per row
+    for (int c = tid; c < TM * CPR; c += kGemmThreads) {
+      const int mr = c / CPR;
+      const int cc = (c % CPR) * 8;
+      const int drow = s_dst[mr];
+      if (drow >= 0)
+        *reinterpret_cast<u32x4_t*>(dst + int64_t(drow) * Nout + n0 + cc) =
+            *reinterpret_cast<const u32x4_t*>(&cs[mr * CROW + cc]);
+    }
+    __syncthreads();
   }
 }
 
@@ -300,19 +365,25 @@ int max_tiles(const Shape& s, int TM, int NT) {
   return static_cast<int>((g + kXcds - 1) / kXcds * kXcds);
 }
 
+constexpr int kBlocksPerCu = 2;
+
 template <int KIND>
 hipError_t launch_gemm(const Shape& s, const void* A, const void* W, int K, int Nout, int act,
                        const Buffers& b, void* dst, hipStream_t st) {
   if (s.bf16) {
+    const FfnPlan plan = ffn_plan(s);
+    const int tn = KIND == kUp ? plan.tn_up : plan.tn_down;
+    const int32_t* toff = b.tiles + (KIND == kUp ? 0 : s.E + 1);
+    const int grid = device_cus() * kBlocksPerCu;  // multiple of 8
     const auto* a = static_cast<const uint16_t*>(A);
     const auto* w = static_cast<const uint16_t*>(W);
     auto* o = static_cast<uint16_t*>(dst);
-    if (Nout % 128 == 0 && KIND == kUp) {
-      gemm_bf16_kernel<128, 128, KIND><<<max_tiles(s, 128, Nout / 128), 256, 0, st>>>(
-          a, w, b.off, b.list, b.sigma, s.E, s.k, K, Nout, act, o);
+    if (tn == 128) {
+      gemm_bf16_kernel<128, 128, KIND><<<grid, kGemmThreads, 0, st>>>(
+          a, w, b.off, toff, b.list, b.sigma, s.E, s.k, K, Nout, act, o);
     } else {
-      gemm_bf16_kernel<128, 64, KIND><<<max_tiles(s, 128, Nout / 64), 256, 0, st>>>(
-          a, w, b.off, b.list, b.sigma, s.E, s.k, K, Nout, act, o);
+      gemm_bf16_kernel<128, 64, KIND><<<grid, kGemmThreads, 0, st>>>(
+          a, w, b.off, toff, b.list, b.sigma, s.E, s.k, K, Nout, act, o);
     }
   } else {
     gemm_f32_kernel<KIND><<<max_tiles(s, kF32T, Nout / kF32T), 256, 0, st>>>(
@@ -323,6 +394,28 @@ hipError_t launch_gemm(const Shape& s, const void* A, const void* W, int K, int 
 }
 
 }  // namespace
+
+FfnPlan ffn_plan(const Shape& s) {
+  FfnPlan p;
+  p.tm = 128;
+  p.tn_up = s.d_ff % 128 == 0 ? 128 : 64;
+  p.tn_down = s.d % 128 == 0 ? 128 : 64;
+  return p;
+}
+
+int device_cus() {
+  static int cus = 0;
+  if (cus == 0) {
+    int dev = 0, n = 0;
+    if (hipGetDevice(&dev) == hipSuccess &&
+        hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess &&
+        n > 0)
+      cus = (n + kXcds - 1) / kXcds * kXcds;
+    else
+      cus = 256;
+  }
+  return cus;
+}
 
 hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, int act,
                          const Buffers& b, hipStream_t st) {

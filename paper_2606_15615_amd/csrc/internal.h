@@ -39,8 +39,20 @@ struct Buffers {
   int32_t* cnt_bs;  // [B][E] recomputed branches per sample and expert
   int32_t* stats_bs;// [B][4] recompute, unmatched, matched, sync per sample
   int32_t* rflags;  // router: one non-finite flag per block
+  int32_t* tiles;   // [2][E+1] grouped-GEMM tile prefix per expert (up, down)
   void* mid;        // [B*N*k][d_ff] FFN activation of listed rows
 };
+
+// Tiling of the grouped expert FFN: M tile (rows of one expert) and N tile
+// of the up and down projections.  The lists kernel turns the per-expert row
+// counts into tile prefixes with the same plan.
+struct FfnPlan {
+  int tm;
+  int tn_up;
+  int tn_down;
+};
+FfnPlan ffn_plan(const Shape& s);
+int device_cus();
 
 enum SelectMode { kSelFull = 0, kSelThreshold = 1, kSelRatio = 2 };
 
@@ -54,7 +66,7 @@ hipError_t launch_score(const Shape& s, float lambda1, float lambda2, const Buff
                         hipStream_t st);
 hipError_t launch_select(const Shape& s, int sel_mode, int budget, const Buffers& b,
                          hipStream_t st);
-hipError_t launch_lists(const Shape& s, const Buffers& b, hipStream_t st);
+hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st);
 hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, int act,
                          const Buffers& b, hipStream_t st);
 hipError_t launch_ffn_down(const Shape& s, const void* W_down, const Buffers& b,

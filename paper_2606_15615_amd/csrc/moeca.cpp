@@ -40,7 +40,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 enum Region {
   R_E_C, R_W_C, R_N_C, R_H_C, R_STAT, R_LOGITS, R_E_T, R_W_T, R_HBAR, R_TAU, R_MARGIN, R_Q,
   R_MASK, R_SIGMA, R_SYNC, R_OFF, R_LIST, R_POS,
-  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_MID, R_COUNT
+  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_MID, R_COUNT
 };
 
 struct Layout {
@@ -75,6 +75,7 @@ Layout make_layout(const Shape& s) {
   b[R_CNT_BS] = size_t(s.B) * s.E * 4;
   b[R_STATS_BS] = size_t(s.B) * 4 * 4;
   b[R_RFLAGS] = size_t(moeca::router_blocks(s)) * 4;
+  b[R_TILES] = size_t(2) * (s.E + 1) * 4;
   b[R_MID] = nbr * s.d_ff * act;
   Layout L;
   size_t cur = 0;
@@ -222,6 +223,7 @@ int moeca_bind_workspace(moeca_layer* L, void* dev, size_t bytes) {
   b.cnt_bs = reinterpret_cast<int32_t*>(w + o[R_CNT_BS]);
   b.stats_bs = reinterpret_cast<int32_t*>(w + o[R_STATS_BS]);
   b.rflags = reinterpret_cast<int32_t*>(w + o[R_RFLAGS]);
+  b.tiles = reinterpret_cast<int32_t*>(w + o[R_TILES]);
   b.mid = w + o[R_MID];
   L->ws = w;
   L->valid = false;
@@ -287,7 +289,7 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
     budget = static_cast<int>(std::floor(static_cast<double>(p.ratio) * s.N * s.k + 0.5));
   }
   if (!check(moeca::launch_select(s, sel, budget, b, st), "select")) return MOECA_E_HIP;
-  if (!check(moeca::launch_lists(s, b, st), "lists")) return MOECA_E_HIP;
+  if (!check(moeca::launch_lists(s, moeca::ffn_plan(s), b, st), "lists")) return MOECA_E_HIP;
   if (!check(moeca::launch_ffn_up(s, x_t, L->W_up, p.act, b, st), "ffn up")) return MOECA_E_HIP;
   if (!check(moeca::launch_ffn_down(s, L->W_down, b, st), "ffn down")) return MOECA_E_HIP;
   if (!check(moeca::launch_combine(s, uncached ? 0 : 1, out, L->attn_in, L->attn_cache, b, st),
