@@ -5,7 +5,9 @@ thresholds, matching and scores, selection, expert lists, grouped expert
 FFN, combine with cache and attention write) over one batch of synthetic
 input already resident in HBM.  The timed steps are cache steps at a 30%
 per-sample branch budget; the full-recompute comparator (the uncached layer
-through the same kernels) is timed on the same inputs.
+through the same kernels) is timed on the same inputs.  The K timed steps
+are captured in one HIP graph and replayed (eager launch timings are
+reported beside them).
 
     python bench.py [--steps K] [--warmup W] [--workload xl1024] [--no-cpu]
 
@@ -43,6 +45,8 @@ def parse():
     ap.add_argument("--ratio", type=float, default=0.3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--no-graph", action="store_true",
+                    help="time eager launches only (no HIP graph replay)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -121,28 +125,51 @@ def main():
         for t in range(t0, t1):
             L.step(xs[t], t, out)
 
-    # ---- headline: K cache steps ------------------------------------------
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+
+    def timed(L, t0, t1):
+        torch.cuda.synchronize()
+        e0.record(stream)
+        run(L, t0, t1)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / (t1 - t0)
+
+    def graph_timed(L):
+        """Capture the K steps in one HIP graph, replay it once, time it."""
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            run(L, Wm, T)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        g.replay()
+        e1.record(stream)
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / K
+
+    # ---- eager: K cache steps, then K full-recompute steps ------------------
     log("[bench] warmup")
     run(cached, 0, Wm)                 # step 0 is the refresh step
-    torch.cuda.synchronize()
-    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-    log("[bench] timing cache steps")
-    torch.cuda.synchronize()
-    e0.record(stream)
-    run(cached, Wm, T)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms_cached = e0.elapsed_time(e1) / K
-
-    # ---- comparator: K full-recompute steps on the same inputs --------------
-    log("[bench] timing full recompute")
+    log("[bench] timing cache steps (eager)")
+    ms_cached_eager = timed(cached, Wm, T)
+    log("[bench] timing full recompute (eager)")
     run(full, 0, min(Wm, 3))
-    torch.cuda.synchronize()
-    e0.record(stream)
-    run(full, Wm, T)
-    e1.record(stream)
-    torch.cuda.synchronize()
-    ms_full = e0.elapsed_time(e1) / K
+    ms_full_eager = timed(full, Wm, T)
+
+    # ---- headline: the same K steps replayed from a HIP graph ---------------
+    ms_cached, ms_full, graphed = ms_cached_eager, ms_full_eager, False
+    if not args.no_graph:
+        try:
+            log("[bench] timing cache steps (graph)")
+            cached.reset()
+            run(cached, 0, Wm)
+            ms_cached = graph_timed(cached)
+            log("[bench] timing full recompute (graph)")
+            ms_full = graph_timed(full)
+            graphed = True
+        except Exception as exc:  # capture unsupported: report the eager numbers
+            log(f"[bench] graph capture failed ({exc}); reporting eager timings")
+            ms_cached, ms_full = ms_cached_eager, ms_full_eager
 
     # ---- per-stage times and refresh counts (replay with stage events) -----
     log("[bench] stage breakdown")
@@ -201,6 +228,9 @@ def main():
                                f"top-{shape.k}, d_ff={shape.d_ff} GELU, {shape.N} tokens x "
                                f"batch {shape.B}, ratio mode rho={args.ratio}",
                    "batch": shape.B, "tokens": shape.N},
+        "launch": "hip_graph" if graphed else "eager",
+        "eager_ms_per_step": round(ms_cached_eager, 4),
+        "eager_full_ms_per_step": round(ms_full_eager, 4),
         "tflops_recomputed": round(tflops, 2),
         "full_ms_per_step": round(ms_full, 4),
         "cached_over_full": round(ms_cached / ms_full, 4),

@@ -194,15 +194,15 @@ int moeca_debug_set_valid(moeca_layer* layer, int valid);
 
 /* ---- per-stage timing --------------------------------------------------- */
 enum {
-  MOECA_STAGE_ROUTER = 0,  /* router logits, top-k, gate                       */
-  MOECA_STAGE_STAT = 1,    /* EMA statistic, entropy, thresholds                */
-  MOECA_STAGE_SCORE = 2,   /* matching and branch scores                       */
-  MOECA_STAGE_SELECT = 3,  /* recomputation set, slots, sync mask              */
-  MOECA_STAGE_LISTS = 4,   /* per-expert compaction                            */
-  MOECA_STAGE_FFN_UP = 5,  /* gathered up-projection + activation              */
-  MOECA_STAGE_FFN_DOWN = 6,/* down-projection into the cache rows              */
-  MOECA_STAGE_COMBINE = 7, /* combine, norms, cache metadata, attention path   */
-  MOECA_STAGE_COUNT = 8
+  MOECA_STAGE_ROUTER = 0,  /* router logits, top-k, gate; EMA statistic update */
+  MOECA_STAGE_STAT = 1,    /* entropy of the statistic, thresholds            */
+  MOECA_STAGE_SELECT = 2,  /* matching, branch scores, recomputation set,
+                              slots, sync mask                                */
+  MOECA_STAGE_LISTS = 3,   /* per-expert compaction                            */
+  MOECA_STAGE_FFN_UP = 4,  /* gathered up-projection + activation              */
+  MOECA_STAGE_FFN_DOWN = 5,/* down-projection into the cache rows              */
+  MOECA_STAGE_COMBINE = 6, /* combine, norms, cache metadata, attention path   */
+  MOECA_STAGE_COUNT = 7
 };
 
 /* Enable (1) or disable (0) HIP-event timing of each stage of each step on

@@ -24,7 +24,7 @@ BUF = {
     "hbar": 8, "tau": 9, "margin": 10, "q": 11, "mask": 12, "sigma": 13, "sync": 14,
     "off": 15, "list": 16, "pos": 17,
 }
-STAGES = ["router", "stat", "score", "select", "lists", "ffn_up", "ffn_down", "combine"]
+STAGES = ["router", "stat", "select", "lists", "ffn_up", "ffn_down", "combine"]
 
 
 class moeca_policy(ctypes.Structure):
@@ -168,7 +168,7 @@ def moeca_set_timing(h, enable: int) -> int:
     return _check(load().moeca_set_timing(h, enable))
 
 
-def moeca_get_timing(h, n: int = 8) -> tuple[list[float], int]:
+def moeca_get_timing(h, n: int = 7) -> tuple[list[float], int]:
     arr = (ctypes.c_double * n)()
     steps = ctypes.c_int()
     _check(load().moeca_get_timing(h, arr, n, ctypes.byref(steps)))

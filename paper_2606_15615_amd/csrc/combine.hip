@@ -127,17 +127,17 @@ hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void
                           void* attn_cache, const Buffers& b, hipStream_t st) {
   const dim3 grid(static_cast<unsigned>((s.tokens() + kCombWaves - 1) / kCombWaves));
   const dim3 block(kCombWaves * kWave);
+#define MOECA_COMBINE(KER, TT)                                                                 \
+  KER<<<grid, block, 0, st>>>(b.w_t, b.e_t, b.sigma, b.mask, b.sync, static_cast<TT*>(b.h_c),  \
+                              b.e_c, b.w_c, b.n_c, static_cast<TT*>(out),                     \
+                              static_cast<const TT*>(attn_in), static_cast<TT*>(attn_cache),  \
+                              s.tokens(), s.d, s.k, write_cache)
   if (s.bf16) {
-    combine_kernel<uint16_t><<<grid, block, 0, st>>>(
-        b.w_t, b.e_t, b.sigma, b.mask, b.sync, static_cast<uint16_t*>(b.h_c), b.e_c, b.w_c,
-        b.n_c, static_cast<uint16_t*>(out), static_cast<const uint16_t*>(attn_in),
-        static_cast<uint16_t*>(attn_cache), s.tokens(), s.d, s.k, write_cache);
+    MOECA_COMBINE(combine_kernel<uint16_t>, uint16_t);
   } else {
-    combine_kernel<float><<<grid, block, 0, st>>>(
-        b.w_t, b.e_t, b.sigma, b.mask, b.sync, static_cast<float*>(b.h_c), b.e_c, b.w_c, b.n_c,
-        static_cast<float*>(out), static_cast<const float*>(attn_in),
-        static_cast<float*>(attn_cache), s.tokens(), s.d, s.k, write_cache);
+    MOECA_COMBINE(combine_kernel<float>, float);
   }
+#undef MOECA_COMBINE
   return hipGetLastError();
 }
 

@@ -1,4 +1,4 @@
-// Decision path of a cache step: expert statistic and thresholds (Sec. 4.3),
+// Decision path of a cache step: entropy-based thresholds (Sec. 4.3),
 // branch matching and score (Sec. 4.2), the recomputation set (Sec. 4.2),
 // slot assignment and the sync mask (Sec. 4.1), and the per-expert lists of
 // recomputed branches that drive the grouped expert FFN.
@@ -17,33 +17,23 @@ namespace moeca {
 namespace {
 
 // ---------------------------------------------------------------------------
-// EMA statistic, normalised entropy and per-expert threshold, one block per
-// (sample, expert).
-//   C_{e,i} <- f32(f32(beta*C) + f32(1-beta)*[e in B_i])     (Sec. 4.3 EMA eq.)
+// Normalised entropy and per-expert threshold, one block per (sample,
+// expert).  The statistic C was advanced by the router in this step.
 //   P(i) = C_i / sum C,  H = -sum P log P,  Hbar = clamp(H / log N, 0, 1)
 //   tau_e = tau0 * (1 + alpha * (2*Hbar - 1))                 (Sec. 4.3)
 // ---------------------------------------------------------------------------
 constexpr int kStatThreads = 256;
 
-__global__ __launch_bounds__(kStatThreads) void stat_kernel(
-    const int32_t* __restrict__ e_t, float* __restrict__ C, int N, int E, int k, float beta,
-    float tau0, float alpha, float* __restrict__ hbar, float* __restrict__ tau) {
+__global__ __launch_bounds__(kStatThreads) void entropy_kernel(
+    const float* __restrict__ C, int N, int E, float tau0, float alpha,
+    float* __restrict__ hbar, float* __restrict__ tau) {
   __shared__ double s_red[kStatThreads / kWave];
   const int b = blockIdx.x / E;
   const int e = blockIdx.x % E;
-  float* Cr = C + (int64_t(b) * E + e) * N;
-  const int32_t* eb = e_t + int64_t(b) * N * k;
-  const float c1 = __fsub_rn(1.0f, beta);
+  const float* Cr = C + (int64_t(b) * E + e) * N;
 
   double part = 0.0;
-  for (int i = threadIdx.x; i < N; i += kStatThreads) {
-    bool hit = false;
-    for (int p = 0; p < k; ++p) hit |= (eb[int64_t(i) * k + p] == e);
-    float c = __fmul_rn(beta, Cr[i]);
-    if (hit) c = __fadd_rn(c, c1);
-    Cr[i] = c;
-    part += static_cast<double>(c);
-  }
+  for (int i = threadIdx.x; i < N; i += kStatThreads) part += static_cast<double>(Cr[i]);
   const double S = block_sum_f64<kStatThreads / kWave>(part, s_red);
 
   double hpart = 0.0;
@@ -73,51 +63,12 @@ __global__ __launch_bounds__(kStatThreads) void stat_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// Matching and branch score, one thread per branch (cache steps only).
+// Matching, branch scores, recomputation set, slots, sync mask and
+// per-expert counts; one block per sample, each thread holding up to R of
+// the sample's branches (j = tid + 1024 r) in registers.
 //   q(p): cached slot with the same expert, or -1           (Sec. 4.2)
 //   Delta = |w_p - w_c[q]|,  o = n_c[q] / f32(sum_j n_c[j]),
 //   s = (w_p + lambda1*Delta) + lambda2*o,  m = s - tau_{b,e_p}
-// ---------------------------------------------------------------------------
-constexpr int kScoreThreads = 256;
-
-__global__ __launch_bounds__(kScoreThreads) void score_kernel(
-    const int32_t* __restrict__ e_t, const float* __restrict__ w_t,
-    const int32_t* __restrict__ e_c, const float* __restrict__ w_c,
-    const float* __restrict__ n_c, const float* __restrict__ tau, int64_t nbr, int N, int E,
-    int k, float lambda1, float lambda2, int32_t* __restrict__ q_out,
-    float* __restrict__ margin) {
-  const int64_t f = int64_t(blockIdx.x) * kScoreThreads + threadIdx.x;
-  if (f >= nbr) return;
-  const int64_t tok = f / k;
-  const int b = static_cast<int>(tok / N);
-  const int e = e_t[f];
-  const float w = w_t[f];
-  const int32_t* ec = e_c + tok * k;
-  const float* wc = w_c + tok * k;
-  const float* nc = n_c + tok * k;
-  int q = -1;
-  double den = 0.0;
-  for (int j = 0; j < k; ++j) {
-    const int ej = ec[j];
-    if (ej >= 0) den += static_cast<double>(nc[j]);
-    if (q < 0 && ej >= 0 && ej == e) q = j;
-  }
-  float m = __int_as_float(0x7f800000);  // +inf: unmatched, always recomputed
-  if (q >= 0) {
-    const float denf = static_cast<float>(den);
-    const float delta = fabsf(__fsub_rn(w, wc[q]));
-    const float o = denf > 0.0f ? __fdiv_rn(nc[q], denf) : 0.0f;
-    float s = __fadd_rn(w, __fmul_rn(lambda1, delta));
-    s = __fadd_rn(s, __fmul_rn(lambda2, o));
-    m = __fsub_rn(s, tau[b * E + e]);
-  }
-  q_out[f] = q;
-  margin[f] = m;
-}
-
-// ---------------------------------------------------------------------------
-// Recomputation set, slots, sync mask and per-expert counts; one block per
-// sample.
 //   full step : R = all, sigma(p) = p
 //   threshold : R = unmatched U {m > 0}                    (Sec. 4.2)
 //   ratio     : R = unmatched U the first max(0, K_b - |U|) matched branches
@@ -134,15 +85,21 @@ __device__ __forceinline__ uint64_t branch_key(float m, int j) {
   return (static_cast<uint64_t>(f32_order_key(m)) << 32) | static_cast<uint32_t>(~j);
 }
 
-__global__ __launch_bounds__(kSelThreads) void select_kernel(
-    const int32_t* __restrict__ q, const float* __restrict__ margin,
-    const int32_t* __restrict__ e_t, int N, int E, int k, int mode, int budget,
-    uint8_t* __restrict__ mask, int32_t* __restrict__ sigma, uint8_t* __restrict__ sync,
-    int32_t* __restrict__ cnt_bs, int32_t* __restrict__ stats_bs) {
+template <int R>
+__global__ __launch_bounds__(kSelThreads) void decide_kernel(
+    const int32_t* __restrict__ e_t, const float* __restrict__ w_t,
+    const int32_t* __restrict__ e_c, const float* __restrict__ w_c,
+    const float* __restrict__ n_c, const float* __restrict__ tau, int N, int E, int k, int mode,
+    int budget, float lambda1, float lambda2, int32_t* __restrict__ q_out,
+    float* __restrict__ margin, uint8_t* __restrict__ mask, int32_t* __restrict__ sigma,
+    uint8_t* __restrict__ sync, int32_t* __restrict__ cnt_bs, int32_t* __restrict__ stats_bs) {
+  extern __shared__ __attribute__((aligned(16))) unsigned char s_dyn[];
+  int8_t* s_q = reinterpret_cast<int8_t*>(s_dyn);            // [N*k] matched slot or -1
+  uint8_t* s_mask = reinterpret_cast<uint8_t*>(s_dyn) + N * k; // [N*k]
   __shared__ int s_hist[256];
   __shared__ int s_wtot[kSelWaves];
   __shared__ int s_cnt[64];
-  __shared__ int s_unmatched, s_matched, s_recompute, s_sync;
+  __shared__ int s_unmatched, s_recompute, s_sync;
   __shared__ unsigned long long s_prefix;
   __shared__ int s_remaining;
 
@@ -156,34 +113,74 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   if (tid < 64) s_cnt[tid] = 0;
   if (tid == 0) {
     s_unmatched = 0;
-    s_matched = 0;
     s_recompute = 0;
     s_sync = 0;
     s_prefix = 0ull;
   }
   __syncthreads();
 
-  // 1. count unmatched / matched branches of the sample
-  if (mode != kSelFull) {
-    int u = 0;
-    for (int j = tid; j < nb; j += kSelThreads) u += (q[base + j] < 0) ? 1 : 0;
-    u = wave_sum_i32(u);
-    if (lane == 0) atomicAdd(&s_unmatched, u);
-    __syncthreads();
-    if (tid == 0) s_matched = nb - s_unmatched;
-    __syncthreads();
+  // 1. matching and scores (cache steps)
+  int qv[R];
+  float mv[R];
+  int ev[R];
+  int unmatched = 0;
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int j = tid + kSelThreads * r;
+    qv[r] = -1;
+    mv[r] = __int_as_float(0x7f800000);  // +inf: unmatched, always recomputed
+    ev[r] = 0;
+    if (j < nb) {
+      const int64_t f = base + j;
+      const int e = e_t[f];
+      ev[r] = e;
+      if (mode != kSelFull) {
+        const int64_t tok = f / k;
+        const float w = w_t[f];
+        int q = -1;
+        double den = 0.0;
+        for (int jj = 0; jj < k; ++jj) {
+          const int ej = e_c[tok * k + jj];
+          if (ej >= 0) den += static_cast<double>(n_c[tok * k + jj]);
+          if (q < 0 && ej >= 0 && ej == e) q = jj;
+        }
+        if (q >= 0) {
+          const float denf = static_cast<float>(den);
+          const float delta = fabsf(__fsub_rn(w, w_c[tok * k + q]));
+          const float o = denf > 0.0f ? __fdiv_rn(n_c[tok * k + q], denf) : 0.0f;
+          float sc = __fadd_rn(w, __fmul_rn(lambda1, delta));
+          sc = __fadd_rn(sc, __fmul_rn(lambda2, o));
+          mv[r] = __fsub_rn(sc, tau[b * E + e]);
+        } else {
+          ++unmatched;
+        }
+        qv[r] = q;
+        q_out[f] = q;
+        margin[f] = mv[r];
+      }
+    }
   }
+  if (mode != kSelFull) {
+    unmatched = wave_sum_i32(unmatched);
+    if (lane == 0) atomicAdd(&s_unmatched, unmatched);
+  }
+  __syncthreads();
+  const int n_unmatched = s_unmatched;
+  const int n_matched = mode == kSelFull ? 0 : nb - n_unmatched;
 
-  // 2. ratio mode: find the key of the need-th best matched branch
+  // 2. ratio mode: key of the need-th best matched branch
   int need = 0;
   bool take_all_matched = false;
   if (mode == kSelRatio) {
-    need = budget - s_unmatched;
+    need = budget - n_unmatched;
     if (need < 0) need = 0;
-    if (need >= s_matched) take_all_matched = true;
+    if (need >= n_matched) take_all_matched = true;
     if (need > 0 && !take_all_matched) {
       if (tid == 0) s_remaining = need;
       __syncthreads();
+      uint64_t key[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) key[r] = branch_key(mv[r], tid + kSelThreads * r);
       for (int shift = 56; shift >= 0; shift -= 8) {
         // prefix and remaining are read here and written only after the two
         // barriers below, so every thread sees this pass's values.
@@ -192,18 +189,16 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
         if (tid < 256) s_hist[tid] = 0;
         __syncthreads();
         const uint64_t hi_mask = (shift == 56) ? 0ull : (~0ull << (shift + 8));
-        for (int j = tid; j < nb; j += kSelThreads) {
-          if (q[base + j] < 0) continue;
-          const uint64_t key = branch_key(margin[base + j], j);
-          if (((key ^ prefix) & hi_mask) == 0ull)
-            atomicAdd(&s_hist[(key >> shift) & 255ull], 1);
+#pragma unroll
+        for (int r = 0; r < R; ++r) {
+          if (qv[r] >= 0 && ((key[r] ^ prefix) & hi_mask) == 0ull)
+            atomicAdd(&s_hist[(key[r] >> shift) & 255ull], 1);
         }
         __syncthreads();
         // suffix sums over the 256 bins (bin 255 first) by the first 4 waves
         int h = 0, incl = 0;
         if (tid < 256) {
-          const int bin = 255 - tid;  // tid 0 holds the top bin
-          h = s_hist[bin];
+          h = s_hist[255 - tid];
           incl = h;
 #pragma unroll
           for (int o = 1; o < kWave; o <<= 1) {
@@ -227,51 +222,50 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   }
   const uint64_t thr = s_prefix;
 
-  // 3. mask
-  for (int j = tid; j < nb; j += kSelThreads) {
-    bool r;
-    if (mode == kSelFull) {
-      r = true;
+  // 3. mask and per-expert counts
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int j = tid + kSelThreads * r;
+    if (j >= nb) continue;
+    bool rc;
+    if (mode == kSelFull || qv[r] < 0) {
+      rc = true;
+    } else if (mode == kSelThreshold) {
+      rc = mv[r] > 0.0f;
+    } else if (take_all_matched) {
+      rc = true;
+    } else if (need == 0) {
+      rc = false;
     } else {
-      const bool matched = q[base + j] >= 0;
-      if (!matched) {
-        r = true;
-      } else if (mode == kSelThreshold) {
-        r = margin[base + j] > 0.0f;
-      } else if (take_all_matched) {
-        r = true;
-      } else if (need == 0) {
-        r = false;
-      } else {
-        r = branch_key(margin[base + j], j) >= thr;
-      }
+      rc = branch_key(mv[r], j) >= thr;
     }
-    mask[base + j] = r ? 1 : 0;
-    if (r) atomicAdd(&s_cnt[e_t[base + j]], 1);
+    mask[base + j] = rc ? 1 : 0;
+    s_mask[j] = rc ? 1 : 0;
+    s_q[j] = static_cast<int8_t>(qv[r]);
+    if (rc) atomicAdd(&s_cnt[ev[r]], 1);
   }
   __syncthreads();
 
   // 4. per token: sync flag and slots
   int rec = 0, syn = 0;
   for (int i = tid; i < N; i += kSelThreads) {
-    const int64_t t0 = base + int64_t(i) * k;
     bool any = false;
     uint32_t taken = 0;
     if (mode != kSelFull) {
       for (int p = 0; p < k; ++p) {
-        const int qp = q[t0 + p];
+        const int qp = s_q[i * k + p];
         if (qp >= 0) taken |= 1u << qp;
       }
     }
     for (int p = 0; p < k; ++p) {
-      const bool r = mask[t0 + p] != 0;
-      any |= r;
-      rec += r ? 1 : 0;
+      const bool rc = s_mask[i * k + p] != 0;
+      any |= rc;
+      rec += rc ? 1 : 0;
       int sg;
       if (mode == kSelFull) {
         sg = p;
       } else {
-        const int qp = q[t0 + p];
+        const int qp = s_q[i * k + p];
         if (qp >= 0) {
           sg = qp;
         } else {
@@ -280,7 +274,7 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
           taken |= 1u << sg;
         }
       }
-      sigma[t0 + p] = sg;
+      sigma[base + int64_t(i) * k + p] = sg;
     }
     sync[int64_t(b) * N + i] = any ? 1 : 0;
     syn += any ? 1 : 0;
@@ -295,8 +289,8 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
   if (tid < E) cnt_bs[b * E + tid] = s_cnt[tid];
   if (tid == 0) {
     stats_bs[b * 4 + 0] = s_recompute;
-    stats_bs[b * 4 + 1] = (mode == kSelFull) ? 0 : s_unmatched;
-    stats_bs[b * 4 + 2] = (mode == kSelFull) ? 0 : s_matched;
+    stats_bs[b * 4 + 1] = mode == kSelFull ? 0 : n_unmatched;
+    stats_bs[b * 4 + 2] = n_matched;
     stats_bs[b * 4 + 3] = s_sync;
   }
 }
@@ -310,8 +304,9 @@ __global__ __launch_bounds__(kSelThreads) void select_kernel(
 __global__ __launch_bounds__(kSelThreads) void lists_kernel(
     const uint8_t* __restrict__ mask, const int32_t* __restrict__ e_t,
     const int32_t* __restrict__ cnt_bs, int B, int N, int E, int k, int tm, int nt_up,
-    int nt_down, int32_t* __restrict__ off, int32_t* __restrict__ tiles,
-    int32_t* __restrict__ list, int32_t* __restrict__ pos) {
+    int nt_down, const int32_t* __restrict__ sigma, int32_t* __restrict__ off,
+    int32_t* __restrict__ tiles, int32_t* __restrict__ list, int32_t* __restrict__ pos,
+    int32_t* __restrict__ row_dst) {
   __shared__ int s_base[64];
   __shared__ int s_run[64];
   __shared__ int s_wcnt[kSelWaves][64];
@@ -374,8 +369,10 @@ __global__ __launch_bounds__(kSelThreads) void lists_kernel(
       int before = 0;
       for (int w2 = 0; w2 < wv; ++w2) before += s_wcnt[w2][e];
       const int idx = s_base[e] + s_run[e] + before + rank;
-      list[idx] = static_cast<int32_t>(base + j);
-      pos[base + j] = idx;
+      const int64_t f = base + j;
+      list[idx] = static_cast<int32_t>(f);
+      pos[f] = idx;
+      row_dst[idx] = static_cast<int32_t>((f / k) * k + sigma[f]);
     } else if (in) {
       pos[base + j] = -1;
     }
@@ -407,35 +404,40 @@ __global__ void reset_kernel(int32_t* __restrict__ e_c, float* __restrict__ w_c,
 
 }  // namespace
 
-hipError_t launch_stat(const Shape& s, float beta, float tau0, float alpha, const Buffers& b,
-                       hipStream_t st) {
-  stat_kernel<<<dim3(s.B * s.E), dim3(kStatThreads), 0, st>>>(b.e_t, b.stat, s.N, s.E, s.k,
-                                                                beta, tau0, alpha, b.hbar, b.tau);
+hipError_t launch_entropy(const Shape& s, float tau0, float alpha, const Buffers& b,
+                          hipStream_t st) {
+  entropy_kernel<<<dim3(s.B * s.E), dim3(kStatThreads), 0, st>>>(b.stat, s.N, s.E, tau0, alpha,
+                                                                   b.hbar, b.tau);
   return hipGetLastError();
 }
 
-hipError_t launch_score(const Shape& s, float lambda1, float lambda2, const Buffers& b,
-                        hipStream_t st) {
-  const int64_t n = s.branches();
-  const dim3 grid(static_cast<unsigned>((n + kScoreThreads - 1) / kScoreThreads));
-  score_kernel<<<grid, dim3(kScoreThreads), 0, st>>>(b.e_t, b.w_t, b.e_c, b.w_c, b.n_c, b.tau,
-                                                      n, s.N, s.E, s.k, lambda1, lambda2, b.q,
-                                                      b.margin);
-  return hipGetLastError();
-}
-
-hipError_t launch_select(const Shape& s, int sel_mode, int budget, const Buffers& b,
-                         hipStream_t st) {
-  select_kernel<<<dim3(s.B), dim3(kSelThreads), 0, st>>>(b.q, b.margin, b.e_t, s.N, s.E, s.k,
-                                                         sel_mode, budget, b.mask, b.sigma,
-                                                         b.sync, b.cnt_bs, b.stats_bs);
+hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1, float lambda2,
+                         const Buffers& b, hipStream_t st) {
+  const int nb = s.N * s.k;
+  const size_t lds = size_t(2) * nb;
+  if (lds > 64 * 1024) return hipErrorInvalidValue;
+#define MOECA_DECIDE(RR)                                                                      \
+  decide_kernel<RR><<<dim3(s.B), dim3(kSelThreads), lds, st>>>(                               \
+      b.e_t, b.w_t, b.e_c, b.w_c, b.n_c, b.tau, s.N, s.E, s.k, sel_mode, budget, lambda1,     \
+      lambda2, b.q, b.margin, b.mask, b.sigma, b.sync, b.cnt_bs, b.stats_bs)
+  if (nb <= 2 * kSelThreads) {
+    MOECA_DECIDE(2);
+  } else if (nb <= 8 * kSelThreads) {
+    MOECA_DECIDE(8);
+  } else if (nb <= 32 * kSelThreads) {
+    MOECA_DECIDE(32);
+  } else {
+    return hipErrorInvalidValue;
+  }
+#undef MOECA_DECIDE
   return hipGetLastError();
 }
 
 hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st) {
   lists_kernel<<<dim3(s.B), dim3(kSelThreads), 0, st>>>(
-      b.mask, b.e_t, b.cnt_bs, s.B, s.N, s.E, s.k, plan.tm, s.d_ff / plan.tn_up,
-      s.d / plan.tn_down, b.off, b.tiles, b.list, b.pos);
+      b.mask, b.e_t, b.cnt_bs, s.B, s.N, s.E, s.k, plan.tm,
+      (s.d_ff + plan.tn_up - 1) / plan.tn_up, (s.d + plan.tn_down - 1) / plan.tn_down, b.sigma,
+      b.off, b.tiles, b.list, b.pos, b.row_dst);
   return hipGetLastError();
 }
 

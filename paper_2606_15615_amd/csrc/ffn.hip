@@ -29,18 +29,27 @@ namespace {
 typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
 typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;  // 16 bytes, a native vector
+typedef __attribute__((ext_vector_type(2))) unsigned int u32x2_t;
 
 enum { kUp = 0, kDown = 1 };
 constexpr int kXcds = 8;
 
-__device__ __forceinline__ float act_fn(float z, int act) {
-  if (act == 0) {
-    // tanh GELU: 0.5 z (1 + tanh(u)) = z / (1 + exp(-2u)),
-    // u = sqrt(2/pi) (z + 0.044715 z^3)
+// Activation of the up projection.  tanh GELU:
+//   0.5 z (1 + tanh(u)) = z / (1 + exp(-2u)),  u = sqrt(2/pi) (z + 0.044715 z^3),
+// with exp(-2u) = 2^(-2u log2 e) from the hardware exp2 (about 1 ulp) and a
+// hardware reciprocal; the erf form uses erff.
+enum { kActGeluTanh = 0, kActGeluErf = 1, kActNone = 2 };
+
+template <int ACT>
+__device__ __forceinline__ float act_fn(float z) {
+  if constexpr (ACT == kActGeluTanh) {
     const float u = 0.7978845608028654f * (z + 0.044715f * z * z * z);
-    return z * __builtin_amdgcn_rcpf(1.0f + __expf(-2.0f * u));
+    return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-2.8853900817779268f * u));
+  } else if constexpr (ACT == kActGeluErf) {
+    return 0.5f * z * (1.0f + erff(z * 0.7071067811865476f));
+  } else {
+    return z;
   }
-  return 0.5f * z * (1.0f + erff(z * 0.7071067811865476f));
 }
 
 struct Tile {
@@ -141,12 +150,12 @@ __device__ __forceinline__ void mfma_ktile(f32x16_t (&acc)[FM][FN], const uint16
   }
 }
 
-template <int TM, int TN, int KIND>
+template <int TM, int TN, int KIND, int ACT>
 __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
     const int32_t* __restrict__ off, const int32_t* __restrict__ tile_off,
     const int32_t* __restrict__ list, const int32_t* __restrict__ sigma, int E, int k, int K,
-    int Nout, int act, uint16_t* __restrict__ dst) {
+    int Nout, uint16_t* __restrict__ dst) {
   constexpr int WM = TM / 2, WN = TN / 2;  // wave tile (2 x 2 waves)
   constexpr int FM = WM / 32, FN = WN / 32;
   constexpr int LA = TM / 32, LB = TN / 32;  // 16-byte loads per thread per k-tile
@@ -260,7 +269,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(
           const int mr = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
           const int nc = wn * WN + j * 32 + (lane & 31);
           float v = acc[i][j][r];
-          if (KIND == kUp) v = act_fn(v, act);
+          v = act_fn<ACT>(v);
           cs[mr * CROW + nc] = f32_to_bf16(v);
         }
     __syncthreads();
@@ -278,16 +287,270 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// bf16 MFMA grouped GEMM, large tile: 128 x 256 per block, 8 waves (two per
+// SIMD) of 64 x 64 (four MFMA tiles each, accumulators in AGPRs), k-tile 64, a
+// three-stage LDS ring filled by direct global -> LDS loads
+// (global_load_lds_dwordx4: a wave's 64 x 16 bytes land contiguously at a
+// wave-uniform LDS address), one barrier per k-tile.  Within a k-tile each
+// wave reads the next 16-wide k-step's fragments while the current step's
+// MFMAs run.  The epilogue applies the activation and writes packed bf16
+// straight from the accumulators.  Each 128-byte tile row keeps its eight
+// 16-byte chunks XOR-swizzled by ((row >> 1) & 7): a ds_read_b128 is served
+// 16 lanes (256 bytes) at a time, and with this swizzle the 16 rows of a
+// group land on distinct 16-byte bank groups.  N need not be a multiple of
+// 256: weight rows past N are clamped and their columns dropped.  Used when
+// the output width is at least 512.
+// ---------------------------------------------------------------------------
+constexpr int kBigTM = 128;
+constexpr int kBigTN = 256;
+constexpr int kBigWaves = 8;
+constexpr int kBigThreads = kBigWaves * kWave;
+constexpr int kStages = 3;
+constexpr int kTileA = kBigTM * kTK;          // bf16 elements of one A stage (16 KB)
+constexpr int kTileB = kBigTN * kTK;          // 32 KB
+constexpr int kStageElems = kTileA + kTileB;  // 48 KB
+constexpr int kLoadsA = kBigTM / 8 / kBigWaves;  // DMA instructions per wave per stage (A)
+constexpr int kLoadsB = kBigTN / 8 / kBigWaves;  // (B)
+constexpr int kLoadsPerStage = kLoadsA + kLoadsB;
+
+__device__ __forceinline__ void s_waitcnt_vm(int n) {
+  // gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14
+  if (n == 0) __builtin_amdgcn_s_waitcnt(0x0F70);
+  else __builtin_amdgcn_s_waitcnt(0x0F70 | kLoadsPerStage);
+}
+
+// 16 bytes per lane, global -> LDS at the wave-uniform LDS byte address
+// `lds` (lane l lands at lds + 16 l).  Issued as inline assembly so that the
+// compiler does not treat it as an LDS store: it would otherwise wait for
+// every outstanding DMA before each LDS read.  The kernel orders the
+// accesses itself with s_waitcnt vmcnt and s_barrier (loads complete in
+// order, so the compiler's own vmcnt waits stay conservative).
+__device__ __forceinline__ void dma16(const uint16_t* g, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off"
+      :
+      : "s"(lds), "v"(g)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)p));
+}
+
+// MFMA operand fragments of one 16-wide k-step: weights are the A operand
+// (32 output columns x 16 k), token rows the B operand (16 k x 32 rows), so
+// a lane's accumulator holds four consecutive output columns of one row.
+template <int FN, int FM>
+struct Frags {
+  bf16x8_t w[FN];
+  bf16x8_t x[FM];
+};
+
+template <int FN, int FM>
+__device__ __forceinline__ void read_frags(Frags<FN, FM>& f, const uint16_t* xs,
+                                           const uint16_t* ws, int xrow0, int wrow0, int ks,
+                                           int lane) {
+  const int rr = lane & 31;
+  // swizzled chunk: ((row >> 1) & 7) == ((lane >> 1) & 7) for rows 32-aligned + (lane & 31)
+  const int pos = (2 * ks + (lane >> 5)) ^ ((lane >> 1) & 7);
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+    f.w[i] = *reinterpret_cast<const bf16x8_t*>(ws + ((wrow0 + i * 32 + rr) * 8 + pos) * 8);
+#pragma unroll
+  for (int j = 0; j < FM; ++j)
+    f.x[j] = *reinterpret_cast<const bf16x8_t*>(xs + ((xrow0 + j * 32 + rr) * 8 + pos) * 8);
+}
+
+template <int FN, int FM>
+__device__ __forceinline__ void mfma_step(f32x16_t (&acc)[FN][FM], const Frags<FN, FM>& f) {
+#pragma unroll
+  for (int i = 0; i < FN; ++i)
+#pragma unroll
+    for (int j = 0; j < FM; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.w[i], f.x[j], acc[i][j], 0, 0, 0);
+}
+
+// One k-tile (four k-steps) on a swizzled stage, the next step's fragment
+// reads interleaved with the current step's MFMAs.
+template <int FN, int FM>
+__device__ __forceinline__ void mfma_ktile_pipe(f32x16_t (&acc)[FN][FM], const uint16_t* xs,
+                                                const uint16_t* ws, int xrow0, int wrow0,
+                                                int lane) {
+  constexpr int KS = kTK / 16;
+  Frags<FN, FM> cur, nxt;
+  read_frags(cur, xs, ws, xrow0, wrow0, 0, lane);
+#pragma unroll
+  for (int ks = 0; ks < KS; ++ks) {
+    if (ks + 1 < KS) read_frags(nxt, xs, ws, xrow0, wrow0, ks + 1, lane);
+    mfma_step(acc, cur);
+    if (ks + 1 < KS) cur = nxt;
+  }
+  // schedule: first step's reads, then per step one MFMA per read of the
+  // next step, the step's remaining MFMAs, and the last step's MFMAs
+  __builtin_amdgcn_sched_group_barrier(0x100, FN + FM, 0);
+#pragma unroll
+  for (int ks = 0; ks + 1 < KS; ++ks) {
+#pragma unroll
+    for (int r = 0; r < FN + FM; ++r) {
+      __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+      __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+    }
+    __builtin_amdgcn_sched_group_barrier(0x008, FN * FM - (FN + FM), 0);
+  }
+  __builtin_amdgcn_sched_group_barrier(0x008, FN * FM, 0);
+}
+
+typedef __attribute__((ext_vector_type(2))) float f32x2_t;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+
+// Four fp32 -> four bf16 (hardware round to nearest even), packed in 8 bytes.
+__device__ __forceinline__ u32x2_t pack4_bf16(float a, float b, float c, float d) {
+  const bf16x2_t lo = __builtin_convertvector(f32x2_t{a, b}, bf16x2_t);
+  const bf16x2_t hi = __builtin_convertvector(f32x2_t{c, d}, bf16x2_t);
+  return u32x2_t{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
+}
+
+template <int KIND, int ACT>
+__global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
+    const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
+    const int32_t* __restrict__ off, const int32_t* __restrict__ tile_off,
+    const int32_t* __restrict__ list, const int32_t* __restrict__ row_dst, int E, int k, int K,
+    int Nout, uint16_t* __restrict__ dst) {
+  constexpr int TM = kBigTM, TN = kBigTN;
+  constexpr int FM = 2, FN = 2;  // wave tile: 64 rows x 64 columns
+  constexpr int WN = TN / (FN * 32);  // waves along N
+  static_assert(kBigWaves == (TM / (FM * 32)) * WN, "wave grid must cover the tile");
+  __shared__ __attribute__((aligned(16))) uint16_t lds[kStages * kStageElems];
+  __shared__ int s_src[TM];
+  __shared__ int s_dst[TM];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = tid >> 6;
+  const int wm = wv / WN, wn = wv % WN;
+  const int total = tile_off[E];
+  const int per = (total + kXcds - 1) / kXcds;
+  const int lo = (blockIdx.x % kXcds) * per;
+  const int hi = min(total, lo + per);
+  const int stride = gridDim.x / kXcds;
+  const int my_toff = lane < E ? tile_off[lane] : 0x7fffffff;
+  const int KT = K / kTK;
+  // Logical chunk this lane fetches.  DMA instruction i covers rows 8i..8i+7
+  // (lane l: row 8i + l/8, stored position l & 7); the stored position is
+  // chunk ^ ((row >> 1) & 7) = chunk ^ (4 (i & 1) + l / 16), and
+  // i = wv + kBigWaves u has the parity of wv.
+  const int chunk = (lane & 7) ^ (4 * (wv & 1) + (lane >> 4));
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(lds) + wv * 1024);
+
+  for (int L = lo + static_cast<int>(blockIdx.x) / kXcds; L < hi; L += stride) {
+    const int e = __popcll(__ballot(my_toff <= L)) - 1;
+    const int e_base = __shfl(my_toff, e, 64);
+    const int o0 = off[e];
+    const int cnt = off[e + 1] - o0;
+    const int mt = (cnt + TM - 1) / TM;
+    const int local = L - e_base;
+    const int m = local % mt;
+    const int r0 = o0 + m * TM;
+    const int rows = min(TM, cnt - m * TM);
+    const int n0 = (local / mt) * TN;
+
+    for (int r = tid; r < TM; r += kBigThreads) {
+      const int rr = r < rows ? r : 0;  // padding rows re-read row 0, never stored
+      if (KIND == kUp) {
+        s_src[r] = list[r0 + rr] / k;
+        s_dst[r] = r < rows ? r0 + r : -1;
+      } else {
+        s_src[r] = r0 + rr;
+        s_dst[r] = r < rows ? row_dst[r0 + r] : -1;
+      }
+    }
+    __syncthreads();
+
+    // per-lane sources: wave wv issues DMA instructions i = wv + kBigWaves u,
+    // each covering tile rows 8i .. 8i+7 (lane l: row 8i + l/8)
+    const uint16_t* ga[kLoadsA];
+    const uint16_t* gb[kLoadsB];
+#pragma unroll
+    for (int u = 0; u < kLoadsA; ++u) {
+      const int r = 8 * (wv + kBigWaves * u) + (lane >> 3);
+      ga[u] = A + int64_t(s_src[r]) * K + chunk * 8;
+    }
+#pragma unroll
+    for (int u = 0; u < kLoadsB; ++u) {
+      const int r = 8 * (wv + kBigWaves * u) + (lane >> 3);
+      const int n = min(n0 + r, Nout - 1);
+      gb[u] = W + (int64_t(e) * Nout + n) * K + chunk * 8;
+    }
+    auto issue = [&](int kt, int st) __attribute__((always_inline)) {
+      const uint32_t base = lds0 + st * (kStageElems * 2);
+#pragma unroll
+      for (int u = 0; u < kLoadsA; ++u) dma16(ga[u] + kt * kTK, base + u * kBigWaves * 1024);
+#pragma unroll
+      for (int u = 0; u < kLoadsB; ++u)
+        dma16(gb[u] + kt * kTK, base + kTileA * 2 + u * kBigWaves * 1024);
+    };
+
+    f32x16_t acc[FN][FM];
+#pragma unroll
+    for (int i = 0; i < FN; ++i)
+#pragma unroll
+      for (int j = 0; j < FM; ++j)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
+
+    issue(0, 0);
+    if (KT > 1) issue(1, 1);
+    int st = 0;
+    for (int kt = 0; kt < KT; ++kt) {
+      // this wave's loads of tile kt have landed once at most one later
+      // tile's loads are outstanding; the barrier then publishes every
+      // wave's loads and retires all reads of the stage refilled next
+      if (kt + 1 < KT) s_waitcnt_vm(kLoadsPerStage);
+      else s_waitcnt_vm(0);
+      __builtin_amdgcn_s_barrier();
+      if (kt + 2 < KT) issue(kt + 2, st == 0 ? 2 : st - 1);
+      const uint16_t* base = lds + st * kStageElems;
+      mfma_ktile_pipe<FN, FM>(acc, base, base + kTileA, wm * FM * 32, wn * FN * 32, lane);
+      st = st == 2 ? 0 : st + 1;
+    }
+
+    // epilogue: lane holds columns 8*(r/4) + 4*(lane/32) + (r%4) of row
+    // (lane & 31) in each 32 x 32 tile; activation, bf16, 8-byte stores
+#pragma unroll
+    for (int j = 0; j < FM; ++j) {
+      const int drow = s_dst[wm * FM * 32 + j * 32 + (lane & 31)];
+      if (drow < 0) continue;
+      const int c0 = n0 + wn * FN * 32 + 4 * (lane >> 5);
+      uint16_t* orow = dst + int64_t(drow) * Nout + c0;
+#pragma unroll
+      for (int i = 0; i < FN; ++i)
+#pragma unroll
+        for (int g = 0; g < 4; ++g) {
+          if (c0 + i * 32 + 8 * g >= Nout) continue;
+          const f32x16_t& a = acc[i][j];
+          *reinterpret_cast<u32x2_t*>(orow + i * 32 + 8 * g) =
+              pack4_bf16(act_fn<ACT>(a[4 * g]), act_fn<ACT>(a[4 * g + 1]),
+                         act_fn<ACT>(a[4 * g + 2]), act_fn<ACT>(a[4 * g + 3]));
+        }
+    }
+    __syncthreads();
+  }
+}
+
+// ---------------------------------------------------------------------------
 // fp32 grouped GEMM (fp32 layers): 64x64 block tile, 4x4 per thread, FMA.
 // ---------------------------------------------------------------------------
 constexpr int kF32T = 64;
 constexpr int kF32K = 16;
 
-template <int KIND>
+template <int KIND, int ACT>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(
     const float* __restrict__ A, const float* __restrict__ W, const int32_t* __restrict__ off,
     const int32_t* __restrict__ list, const int32_t* __restrict__ sigma, int E, int k, int K,
-    int Nout, int act, float* __restrict__ dst) {
+    int Nout, float* __restrict__ dst) {
   __shared__ float As[kF32K][kF32T + 4];
   __shared__ float Bs[kF32K][kF32T + 4];
   __shared__ int s_src[kF32T];
@@ -355,7 +618,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(
     if (drow < 0) continue;
     float* out = dst + int64_t(drow) * Nout + n0 + tx * 4;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) out[j] = (KIND == kUp) ? act_fn(acc[i][j], act) : acc[i][j];
+    for (int j = 0; j < 4; ++j) out[j] = act_fn<ACT>(acc[i][j]);
   }
 }
 
@@ -367,8 +630,8 @@ int max_tiles(const Shape& s, int TM, int NT) {
 
 constexpr int kBlocksPerCu = 2;
 
-template <int KIND>
-hipError_t launch_gemm(const Shape& s, const void* A, const void* W, int K, int Nout, int act,
+template <int KIND, int ACT>
+hipError_t launch_gemm(const Shape& s, const void* A, const void* W, int K, int Nout,
                        const Buffers& b, void* dst, hipStream_t st) {
   if (s.bf16) {
     const FfnPlan plan = ffn_plan(s);
@@ -378,28 +641,34 @@ hipError_t launch_gemm(const Shape& s, const void* A, const void* W, int K, int 
     const auto* a = static_cast<const uint16_t*>(A);
     const auto* w = static_cast<const uint16_t*>(W);
     auto* o = static_cast<uint16_t*>(dst);
-    if (tn == 128) {
-      gemm_bf16_kernel<128, 128, KIND><<<grid, kGemmThreads, 0, st>>>(
-          a, w, b.off, toff, b.list, b.sigma, s.E, s.k, K, Nout, act, o);
+    if (tn == kBigTN) {
+      gemm_bf16_big_kernel<KIND, ACT><<<device_cus(), kBigThreads, 0, st>>>(
+          a, w, b.off, toff, b.list, b.row_dst, s.E, s.k, K, Nout, o);
+    } else if (tn == 128) {
+      gemm_bf16_kernel<128, 128, KIND, ACT><<<grid, kGemmThreads, 0, st>>>(
+          a, w, b.off, toff, b.list, b.sigma, s.E, s.k, K, Nout, o);
     } else {
-      gemm_bf16_kernel<128, 64, KIND><<<grid, kGemmThreads, 0, st>>>(
-          a, w, b.off, toff, b.list, b.sigma, s.E, s.k, K, Nout, act, o);
+      gemm_bf16_kernel<128, 64, KIND, ACT><<<grid, kGemmThreads, 0, st>>>(
+          a, w, b.off, toff, b.list, b.sigma, s.E, s.k, K, Nout, o);
     }
   } else {
-    gemm_f32_kernel<KIND><<<max_tiles(s, kF32T, Nout / kF32T), 256, 0, st>>>(
+    gemm_f32_kernel<KIND, ACT><<<max_tiles(s, kF32T, Nout / kF32T), 256, 0, st>>>(
         static_cast<const float*>(A), static_cast<const float*>(W), b.off, b.list, b.sigma, s.E,
-        s.k, K, Nout, act, static_cast<float*>(dst));
+        s.k, K, Nout, static_cast<float*>(dst));
   }
   return hipGetLastError();
 }
 
 }  // namespace
 
+// Output widths of at least 512 take the large 128 x 256 tile (a partial
+// last N tile is masked); smaller ones the 128 x 128 / 128 x 64 tiles.
 FfnPlan ffn_plan(const Shape& s) {
+  auto tn = [](int n) { return n >= 512 ? kBigTN : (n % 128 == 0 ? 128 : 64); };
   FfnPlan p;
   p.tm = 128;
-  p.tn_up = s.d_ff % 128 == 0 ? 128 : 64;
-  p.tn_down = s.d % 128 == 0 ? 128 : 64;
+  p.tn_up = tn(s.d_ff);
+  p.tn_down = tn(s.d);
   return p;
 }
 
@@ -419,12 +688,14 @@ int device_cus() {
 
 hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, int act,
                          const Buffers& b, hipStream_t st) {
-  return launch_gemm<kUp>(s, x, W_up, s.d, s.d_ff, act, b, b.mid, st);
+  if (act == kActGeluErf)
+    return launch_gemm<kUp, kActGeluErf>(s, x, W_up, s.d, s.d_ff, b, b.mid, st);
+  return launch_gemm<kUp, kActGeluTanh>(s, x, W_up, s.d, s.d_ff, b, b.mid, st);
 }
 
 hipError_t launch_ffn_down(const Shape& s, const void* W_down, const Buffers& b,
                            hipStream_t st) {
-  return launch_gemm<kDown>(s, b.mid, W_down, s.d_ff, s.d, 0, b, b.h_c, st);
+  return launch_gemm<kDown, kActNone>(s, b.mid, W_down, s.d_ff, s.d, b, b.h_c, st);
 }
 
 }  // namespace moeca

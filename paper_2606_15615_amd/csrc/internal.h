@@ -40,6 +40,7 @@ struct Buffers {
   int32_t* stats_bs;// [B][4] recompute, unmatched, matched, sync per sample
   int32_t* rflags;  // router: one non-finite flag per block
   int32_t* tiles;   // [2][E+1] grouped-GEMM tile prefix per expert (up, down)
+  int32_t* row_dst; // [B*N*k] cache row of each listed branch: (f/k)*k + sigma(f)
   void* mid;        // [B*N*k][d_ff] FFN activation of listed rows
 };
 
@@ -59,13 +60,12 @@ enum SelectMode { kSelFull = 0, kSelThreshold = 1, kSelRatio = 2 };
 int router_blocks(const Shape& s);
 
 hipError_t launch_router(const Shape& s, const void* x, const void* W_r, const float* b_r,
-                         int norm_topk, const Buffers& b, hipStream_t st);
-hipError_t launch_stat(const Shape& s, float beta, float tau0, float alpha, const Buffers& b,
-                       hipStream_t st);
-hipError_t launch_score(const Shape& s, float lambda1, float lambda2, const Buffers& b,
-                        hipStream_t st);
-hipError_t launch_select(const Shape& s, int sel_mode, int budget, const Buffers& b,
+                         int norm_topk, float beta, bool update_stat, const Buffers& b,
                          hipStream_t st);
+hipError_t launch_entropy(const Shape& s, float tau0, float alpha, const Buffers& b,
+                          hipStream_t st);
+hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1, float lambda2,
+                         const Buffers& b, hipStream_t st);
 hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st);
 hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, int act,
                          const Buffers& b, hipStream_t st);

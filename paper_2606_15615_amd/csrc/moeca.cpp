@@ -40,7 +40,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 enum Region {
   R_E_C, R_W_C, R_N_C, R_H_C, R_STAT, R_LOGITS, R_E_T, R_W_T, R_HBAR, R_TAU, R_MARGIN, R_Q,
   R_MASK, R_SIGMA, R_SYNC, R_OFF, R_LIST, R_POS,
-  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_MID, R_COUNT
+  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_MID, R_COUNT
 };
 
 struct Layout {
@@ -76,6 +76,7 @@ Layout make_layout(const Shape& s) {
   b[R_STATS_BS] = size_t(s.B) * 4 * 4;
   b[R_RFLAGS] = size_t(moeca::router_blocks(s)) * 4;
   b[R_TILES] = size_t(2) * (s.E + 1) * 4;
+  b[R_ROW_DST] = nbr * 4;
   b[R_MID] = nbr * s.d_ff * act;
   Layout L;
   size_t cur = 0;
@@ -224,6 +225,7 @@ int moeca_bind_workspace(moeca_layer* L, void* dev, size_t bytes) {
   b.stats_bs = reinterpret_cast<int32_t*>(w + o[R_STATS_BS]);
   b.rflags = reinterpret_cast<int32_t*>(w + o[R_RFLAGS]);
   b.tiles = reinterpret_cast<int32_t*>(w + o[R_TILES]);
+  b.row_dst = reinterpret_cast<int32_t*>(w + o[R_ROW_DST]);
   b.mid = w + o[R_MID];
   L->ws = w;
   L->valid = false;
@@ -274,13 +276,11 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
   if (err != hipSuccess) return fail(MOECA_E_HIP, hipGetErrorString(err));
 
   const Buffers& b = L->buf;
-  if (!check(moeca::launch_router(s, x_t, L->W_r, L->b_r, p.norm_topk, b, st), "router"))
+  if (!check(moeca::launch_router(s, x_t, L->W_r, L->b_r, p.norm_topk, p.beta, !uncached, b, st),
+             "router"))
     return MOECA_E_HIP;
-  if (!check(uncached ? hipSuccess
-                      : moeca::launch_stat(s, p.beta, p.tau0, p.alpha, b, st),
-             "statistic"))
-    return MOECA_E_HIP;
-  if (!check(full ? hipSuccess : moeca::launch_score(s, p.lambda1, p.lambda2, b, st), "score"))
+  if (!check(uncached ? hipSuccess : moeca::launch_entropy(s, p.tau0, p.alpha, b, st),
+             "entropy"))
     return MOECA_E_HIP;
   int sel = moeca::kSelFull;
   int budget = 0;
@@ -288,7 +288,8 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
     sel = p.mode == MOECA_MODE_THRESHOLD ? moeca::kSelThreshold : moeca::kSelRatio;
     budget = static_cast<int>(std::floor(static_cast<double>(p.ratio) * s.N * s.k + 0.5));
   }
-  if (!check(moeca::launch_select(s, sel, budget, b, st), "select")) return MOECA_E_HIP;
+  if (!check(moeca::launch_decide(s, sel, budget, p.lambda1, p.lambda2, b, st), "decide"))
+    return MOECA_E_HIP;
   if (!check(moeca::launch_lists(s, moeca::ffn_plan(s), b, st), "lists")) return MOECA_E_HIP;
   if (!check(moeca::launch_ffn_up(s, x_t, L->W_up, p.act, b, st), "ffn up")) return MOECA_E_HIP;
   if (!check(moeca::launch_ffn_down(s, L->W_down, b, st), "ffn down")) return MOECA_E_HIP;
