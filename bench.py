@@ -5,11 +5,15 @@ thresholds, matching and scores, selection, expert lists, grouped expert
 FFN, combine with cache and attention write) over one batch of synthetic
 input already resident in HBM.  The timed steps are cache steps at a 30%
 per-sample branch budget; the full-recompute comparator (the uncached layer
-through the same kernels) is timed on the same inputs.  The K timed steps
-are captured in one HIP graph and replayed (eager launch timings are
-reported beside them).
+through the same kernels) is timed on the same inputs.  Each phase runs
+its K steps eagerly with HIP events between kernels (per-kernel times), then
+replays the same K steps from one HIP graph (the headline time).  The
+roofline object is for the FFN up-projection launch; its HBM traffic comes
+from the committed rocprofv3 counter summary, and is null when the kernel
+source no longer matches the one the counters were taken on.
 
-    python bench.py [--steps K] [--warmup W] [--workload xl1024] [--no-cpu]
+    python bench.py [--steps K] [--warmup W] [--workload xl1024]
+                    [--phase both|cached|full] [--no-cpu] [--no-graph]
 
 Prints one JSON line.
 """
@@ -45,6 +49,8 @@ def parse():
     ap.add_argument("--ratio", type=float, default=0.3)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
+    ap.add_argument("--phase", choices=("both", "cached", "full"), default="both",
+                    help="time the cache steps, the full-recompute comparator, or both")
     ap.add_argument("--no-graph", action="store_true",
                     help="time eager launches only (no HIP graph replay)")
     ap.add_argument("--copy-mib", type=int, default=0,
@@ -83,6 +89,28 @@ def cpu_baseline(shape, ratio, seed):
                       f"median of 3, scaled x{shape.B}"}
 
 
+def kernel_traffic(kernel_src: str, summary: str):
+    """HBM bytes per launch of the FFN-up kernel from the committed counter
+    summary (FETCH_SIZE and WRITE_SIZE, scaled by the copy-kernel factors;
+    keys ``ffn_up.kernel_source_sha256`` and ``ffn_up.hbm_bytes_per_launch``),
+    or None when the kernel source changed since the counters were taken."""
+    import hashlib
+    try:
+        vals = {}
+        with open(summary) as f:
+            for line in f:
+                if "=" in line and not line.lstrip().startswith("#"):
+                    k, v = line.split("=", 1)
+                    vals[k.strip()] = v.strip()
+        with open(kernel_src, "rb") as f:
+            digest = hashlib.sha256(f.read()).hexdigest()
+        if vals.get("ffn_up.kernel_source_sha256") != digest:
+            return None
+        return float(vals["ffn_up.hbm_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -99,7 +127,9 @@ def main():
     dev = torch.device("cuda:0")
     K, Wm = args.steps, args.warmup
     T = Wm + K
-    log(f"[bench] workload {args.workload} {shape}; generating inputs")
+    do_cached = args.phase in ("both", "cached")
+    do_full = args.phase in ("both", "full")
+    log(f"[bench] workload {args.workload} {shape}; phase {args.phase}; generating inputs")
     sy = Synth(shape, args.seed)
     W = sy.weights()
     dW = [np_to_device(W[0], dev), None, np_to_device(W[2], dev), np_to_device(W[3], dev)]
@@ -117,8 +147,6 @@ def main():
         L.reset()
         return L
 
-    cached = make(_lib.MOECA_MODE_RATIO)
-    full = make(_lib.MOECA_MODE_FULL)
     stream = torch.cuda.current_stream()
 
     def run(L, t0, t1):
@@ -147,49 +175,48 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / K
 
-    # ---- eager: K cache steps, then K full-recompute steps ------------------
-    log("[bench] warmup")
-    run(cached, 0, Wm)                 # step 0 is the refresh step
-    log("[bench] timing cache steps (eager)")
-    ms_cached_eager = timed(cached, Wm, T)
-    log("[bench] timing full recompute (eager)")
-    run(full, 0, min(Wm, 3))
-    ms_full_eager = timed(full, Wm, T)
+    def phase(L, warm):
+        """Eager timed region with per-kernel events (the library records
+        them on the launch stream between kernels), then the same K steps
+        replayed from a HIP graph, then an untimed replay for the counts."""
+        L.reset()
+        run(L, 0, warm)                      # step 0 is the refresh step
+        L.set_timing(True)
+        ms_eager = timed(L, Wm, T)
+        stage, n = L.timing()
+        L.set_timing(False)
+        stage = {k: v / n for k, v in stage.items()}
+        ms_graph, graphed = ms_eager, False
+        if not args.no_graph:
+            try:
+                L.reset()
+                run(L, 0, warm)
+                ms_graph = graph_timed(L)
+                graphed = True
+            except Exception as exc:  # capture unsupported: report the eager numbers
+                log(f"[bench] graph capture failed ({exc}); reporting eager timings")
+        L.reset()
+        run(L, 0, warm)
+        torch.cuda.synchronize()
+        rec, syn = [], []
+        for t in range(Wm, T):
+            L.step(xs[t], t, out)
+            st = L.stats()
+            rec.append(st.n_recompute)
+            syn.append(st.n_sync)
+        return ms_eager, ms_graph, graphed, stage, (rec, syn)
 
-    # ---- headline: the same K steps replayed from a HIP graph ---------------
-    ms_cached, ms_full, graphed = ms_cached_eager, ms_full_eager, False
-    if not args.no_graph:
-        try:
-            log("[bench] timing cache steps (graph)")
-            cached.reset()
-            run(cached, 0, Wm)
-            ms_cached = graph_timed(cached)
-            log("[bench] timing full recompute (graph)")
-            ms_full = graph_timed(full)
-            graphed = True
-        except Exception as exc:  # capture unsupported: report the eager numbers
-            log(f"[bench] graph capture failed ({exc}); reporting eager timings")
-            ms_cached, ms_full = ms_cached_eager, ms_full_eager
-
-    # ---- per-stage times and refresh counts (replay with stage events) -----
-    log("[bench] stage breakdown")
-    cached.reset()
-    run(cached, 0, Wm)
-    torch.cuda.synchronize()
-    cached.set_timing(True)
-    recompute = []
-    for t in range(Wm, T):
-        cached.step(xs[t], t, out)
-        recompute.append(cached.stats().n_recompute)
-    stage_ms, nsteps = cached.timing()
-    cached.set_timing(False)
-    stage_ms = {k: v / nsteps for k, v in stage_ms.items()}
-    full.set_timing(True)
-    for t in range(Wm, T):
-        full.step(xs[t], t, out)
-    fstage, fsteps = full.timing()
-    full.set_timing(False)
-    fstage = {k: v / fsteps for k, v in fstage.items()}
+    res_c = res_f = None
+    if do_cached:
+        log("[bench] cache steps")
+        cached = make(_lib.MOECA_MODE_RATIO)
+        res_c = phase(cached, Wm)
+        cached.close()
+    if do_full:
+        log("[bench] full recompute")
+        full = make(_lib.MOECA_MODE_FULL)
+        res_f = phase(full, min(Wm, 3))
+        full.close()
 
     if args.copy_mib:
         n = args.copy_mib * (1 << 20)
@@ -199,61 +226,67 @@ def main():
         torch.cuda.synchronize()
 
     branches = shape.B * shape.N * shape.k
-    flop_per_branch = 4.0 * shape.d * shape.d_ff
-    mean_rec = float(np.mean(recompute))
-    ffn_ms = stage_ms["ffn_up"] + stage_ms["ffn_down"]
-    tflops = mean_rec * flop_per_branch / (ffn_ms * 1e-3) / 1e12
+    up_flop = 2.0 * shape.d * shape.d_ff       # per recomputed branch, each projection
     peak = PEAK_BF16_TFLOPS if shape.dtype == "bf16" else PEAK_FP32_TFLOPS
     act = 2 if shape.dtype == "bf16" else 4
-    # algorithmic HBM bytes of a cache step: expert weights (touched experts
-    # only is <= all), inputs, reused cached rows, recomputed rows written,
-    # outputs; the attention refresh is excluded
-    wbytes = shape.E * 2 * shape.d * shape.d_ff * act
-    step_bytes = (wbytes + shape.tokens * shape.d * act * 2
-                  + branches * shape.d * act)
-    res = {
-        "metric": METRIC,
-        "value": round(ms_cached, 4),
-        "unit": "ms/step",
-        "n_gpus": 1,
-        "steps": K,
-        "warmup": Wm,
-        "ms_per_step": round(ms_cached, 4),
-        "higher_is_better": False,
-        "scaling": "weak",
-        "vs_baseline": None,
-        "dtype": shape.dtype,
-        "data": "synthetic",
-        "config": {"workload": f"{args.workload}: MoE layer d={shape.d}, E={shape.E}, "
-                               f"top-{shape.k}, d_ff={shape.d_ff} GELU, {shape.N} tokens x "
-                               f"batch {shape.B}, ratio mode rho={args.ratio}",
-                   "batch": shape.B, "tokens": shape.N},
-        "launch": "hip_graph" if graphed else "eager",
-        "eager_ms_per_step": round(ms_cached_eager, 4),
-        "eager_full_ms_per_step": round(ms_full_eager, 4),
-        "tflops_recomputed": round(tflops, 2),
-        "full_ms_per_step": round(ms_full, 4),
-        "cached_over_full": round(ms_cached / ms_full, 4),
-        "speedup_vs_full": round(ms_full / ms_cached, 3),
-        "refresh_ratio_actual": round(mean_rec / branches, 4),
-        "stage_ms": {k: round(v, 4) for k, v in stage_ms.items()},
-        "full_stage_ms": {k: round(v, 4) for k, v in fstage.items()},
-        "step_hbm_frac": round(step_bytes / (ms_cached * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-        "roofline": {
-            "bound": "mfma",
-            "kernel": "grouped expert FFN (up + down launches)",
-            "achieved": round(tflops, 2),
-            "peak": peak,
-            "unit": "TFLOP/s",
-            "frac": round(tflops / peak, 4),
-            "traffic": None,
-        },
-    }
-    if not args.no_cpu:
+    wl = (f"{args.workload}: MoE layer d={shape.d}, E={shape.E}, top-{shape.k}, "
+          f"d_ff={shape.d_ff} GELU, {shape.N} tokens x batch {shape.B}, ratio mode rho={args.ratio}")
+    res = {"metric": METRIC, "unit": "ms/step", "n_gpus": 1, "steps": K, "warmup": Wm,
+           "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
+           "dtype": shape.dtype, "data": "synthetic",
+           "config": {"workload": wl, "batch": shape.B, "tokens": shape.N, "phase": args.phase}}
+    if res_c is not None:
+        ms_eager, ms_graph, graphed, stage, (rec, syn) = res_c
+        mean_rec = float(np.mean(rec))
+        up_ms = stage["ffn_up"]
+        ffn_ms = stage["ffn_up"] + stage["ffn_down"]
+        up_tf = mean_rec * up_flop / (up_ms * 1e-3) / 1e12
+        ffn_tf = mean_rec * 2 * up_flop / (ffn_ms * 1e-3) / 1e12
+        # algorithmic HBM bytes of a cache step: expert weights, inputs,
+        # reused cached rows, recomputed rows written, outputs (the
+        # attention refresh excluded)
+        wbytes = shape.E * 2 * shape.d * shape.d_ff * act
+        step_bytes = wbytes + shape.tokens * shape.d * act * 2 + branches * shape.d * act
+        traffic = kernel_traffic(os.path.join(ROOT, "paper_2606_15615_amd", "csrc", "ffn.hip"),
+                                 os.path.join(ROOT, "profiles", "xl1024_cached_counters.txt"))
+        if args.workload != "xl1024":
+            traffic = None
+        res.update({
+            "value": round(ms_graph, 4),
+            "ms_per_step": round(ms_graph, 4),
+            "launch": "hip_graph" if graphed else "eager",
+            "eager_ms_per_step": round(ms_eager, 4),
+            "tflops_recomputed": round(ffn_tf, 2),
+            "refresh_ratio_actual": round(mean_rec / branches, 4),
+            "recomputed_branches": round(mean_rec, 1),
+            "synchronized_tokens": round(float(np.mean(syn)), 1),
+            "stage_ms": {k: round(v, 4) for k, v in stage.items()},
+            "step_hbm_frac": round(step_bytes / (ms_graph * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
+            "roofline": {
+                "bound": "mfma",
+                "kernel": "gemm_bf16_big_kernel<0,0> (expert FFN up-projection + GELU)",
+                "achieved": round(up_tf, 2),
+                "peak": peak,
+                "unit": "TFLOP/s",
+                "frac": round(up_tf / peak, 4),
+                "traffic": None if traffic is None else int(traffic),
+                "launch_ms": round(up_ms, 4),
+                "flop_per_launch": mean_rec * up_flop,
+            },
+        })
+    if res_f is not None:
+        ms_eager_f, ms_graph_f, _, stage_f, _ = res_f
+        res.update({"full_ms_per_step": round(ms_graph_f, 4),
+                    "eager_full_ms_per_step": round(ms_eager_f, 4),
+                    "full_stage_ms": {k: round(v, 4) for k, v in stage_f.items()}})
+        if res_c is None:
+            res.update({"value": round(ms_graph_f, 4), "ms_per_step": round(ms_graph_f, 4)})
+    if res_c is not None and res_f is not None:
+        res["cached_over_full"] = round(res_c[1] / res_f[1], 4)
+        res["speedup_vs_full"] = round(res_f[1] / res_c[1], 3)
+    if not args.no_cpu and res_c is not None:
         log("[bench] cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(shape, args.ratio, args.seed)
-    cached.close()
-    full.close()
     print(json.dumps(res), flush=True)
 
 

@@ -35,7 +35,7 @@ The expert FFN runs in fp64 (library matmul) and its stored results are
 rounded to the layer's activation dtype (bf16 or fp32), as is the GELU
 intermediate.
 
-Readings where the paper is silent or ambiguous (also listed in the design doc):
+Readings where the paper is silent or ambiguous:
 R-1 gate = softmax over all experts, top-k, renormalised over the top-k
 (``norm_topk``; the unnormalised form is a flag); R-2 entropy normalised by
 log N; R-3 C is kept per sample; R-4 EMA updated every step (full steps

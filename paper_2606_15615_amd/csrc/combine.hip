@@ -128,10 +128,10 @@ hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void
   const dim3 grid(static_cast<unsigned>((s.tokens() + kCombWaves - 1) / kCombWaves));
   const dim3 block(kCombWaves * kWave);
 #define MOECA_COMBINE(KER, TT)                                                                 \
-  KER<<<grid, block, 0, st>>>(b.w_t, b.e_t, b.sigma, b.mask, b.sync, static_cast<TT*>(b.h_c),  \
-                              b.e_c, b.w_c, b.n_c, static_cast<TT*>(out),                     \
-                              static_cast<const TT*>(attn_in), static_cast<TT*>(attn_cache),  \
-                              s.tokens(), s.d, s.k, write_cache)
+  launch_kernel(&KER, grid, block, 0, st, b.w_t, b.e_t, b.sigma, b.mask, b.sync,               \
+                static_cast<TT*>(b.h_c), b.e_c, b.w_c, b.n_c, static_cast<TT*>(out),           \
+                static_cast<const TT*>(attn_in), static_cast<TT*>(attn_cache), s.tokens(), s.d,  \
+                s.k, write_cache)
   if (s.bf16) {
     MOECA_COMBINE(combine_kernel<uint16_t>, uint16_t);
   } else {

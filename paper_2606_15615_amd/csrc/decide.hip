@@ -406,8 +406,8 @@ __global__ void reset_kernel(int32_t* __restrict__ e_c, float* __restrict__ w_c,
 
 hipError_t launch_entropy(const Shape& s, float tau0, float alpha, const Buffers& b,
                           hipStream_t st) {
-  entropy_kernel<<<dim3(s.B * s.E), dim3(kStatThreads), 0, st>>>(b.stat, s.N, s.E, tau0, alpha,
-                                                                   b.hbar, b.tau);
+  launch_kernel(&entropy_kernel, dim3(s.B * s.E), dim3(kStatThreads), 0, st, b.stat, s.N, s.E,
+                tau0, alpha, b.hbar, b.tau);
   return hipGetLastError();
 }
 
@@ -417,9 +417,9 @@ hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1
   const size_t lds = size_t(2) * nb;
   if (lds > 64 * 1024) return hipErrorInvalidValue;
 #define MOECA_DECIDE(RR)                                                                      \
-  decide_kernel<RR><<<dim3(s.B), dim3(kSelThreads), lds, st>>>(                               \
-      b.e_t, b.w_t, b.e_c, b.w_c, b.n_c, b.tau, s.N, s.E, s.k, sel_mode, budget, lambda1,     \
-      lambda2, b.q, b.margin, b.mask, b.sigma, b.sync, b.cnt_bs, b.stats_bs)
+  launch_kernel(&decide_kernel<RR>, dim3(s.B), dim3(kSelThreads), uint32_t(lds), st, b.e_t,   \
+                b.w_t, b.e_c, b.w_c, b.n_c, b.tau, s.N, s.E, s.k, sel_mode, budget, lambda1,  \
+                lambda2, b.q, b.margin, b.mask, b.sigma, b.sync, b.cnt_bs, b.stats_bs)
   if (nb <= 2 * kSelThreads) {
     MOECA_DECIDE(2);
   } else if (nb <= 8 * kSelThreads) {
@@ -434,16 +434,17 @@ hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1
 }
 
 hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st) {
-  lists_kernel<<<dim3(s.B), dim3(kSelThreads), 0, st>>>(
-      b.mask, b.e_t, b.cnt_bs, s.B, s.N, s.E, s.k, plan.tm,
+  launch_kernel(
+      &lists_kernel, dim3(s.B), dim3(kSelThreads), 0, st, b.mask, b.e_t, b.cnt_bs, s.B, s.N, s.E,
+      s.k, plan.tm,
       (s.d_ff + plan.tn_up - 1) / plan.tn_up, (s.d + plan.tn_down - 1) / plan.tn_down, b.sigma,
       b.off, b.tiles, b.list, b.pos, b.row_dst);
   return hipGetLastError();
 }
 
 hipError_t launch_reset(const Shape& s, const Buffers& b, hipStream_t st) {
-  reset_kernel<<<dim3(256), dim3(256), 0, st>>>(b.e_c, b.w_c, b.n_c, s.branches(), b.stat,
-                                                 int64_t(s.B) * s.E * s.N);
+  launch_kernel(&reset_kernel, dim3(256), dim3(256), 0, st, b.e_c, b.w_c, b.n_c, s.branches(),
+                b.stat, int64_t(s.B) * s.E * s.N);
   return hipGetLastError();
 }
 

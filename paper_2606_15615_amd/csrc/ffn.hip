@@ -642,18 +642,18 @@ hipError_t launch_gemm(const Shape& s, const void* A, const void* W, int K, int 
     const auto* w = static_cast<const uint16_t*>(W);
     auto* o = static_cast<uint16_t*>(dst);
     if (tn == kBigTN) {
-      gemm_bf16_big_kernel<KIND, ACT><<<device_cus(), kBigThreads, 0, st>>>(
+      launch_kernel(&gemm_bf16_big_kernel<KIND, ACT>, dim3(device_cus()), dim3(kBigThreads), 0, st,
           a, w, b.off, toff, b.list, b.row_dst, s.E, s.k, K, Nout, o);
     } else if (tn == 128) {
-      gemm_bf16_kernel<128, 128, KIND, ACT><<<grid, kGemmThreads, 0, st>>>(
+      launch_kernel(&gemm_bf16_kernel<128, 128, KIND, ACT>, dim3(grid), dim3(kGemmThreads), 0, st,
           a, w, b.off, toff, b.list, b.sigma, s.E, s.k, K, Nout, o);
     } else {
-      gemm_bf16_kernel<128, 64, KIND, ACT><<<grid, kGemmThreads, 0, st>>>(
+      launch_kernel(&gemm_bf16_kernel<128, 64, KIND, ACT>, dim3(grid), dim3(kGemmThreads), 0, st,
           a, w, b.off, toff, b.list, b.sigma, s.E, s.k, K, Nout, o);
     }
   } else {
-    gemm_f32_kernel<KIND, ACT><<<max_tiles(s, kF32T, Nout / kF32T), 256, 0, st>>>(
-        static_cast<const float*>(A), static_cast<const float*>(W), b.off, b.list, b.sigma, s.E,
+    launch_kernel(&gemm_f32_kernel<KIND, ACT>, dim3(max_tiles(s, kF32T, Nout / kF32T)), dim3(256),
+        0, st, static_cast<const float*>(A), static_cast<const float*>(W), b.off, b.list, b.sigma, s.E,
         s.k, K, Nout, static_cast<float*>(dst));
   }
   return hipGetLastError();

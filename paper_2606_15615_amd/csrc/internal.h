@@ -2,10 +2,34 @@
 // kernel launchers (*.hip).  Not part of the public C ABI.
 #pragma once
 #include <hip/hip_runtime.h>
+#include <hip/hip_ext.h>
 #include <cstddef>
 #include <cstdint>
 
 namespace moeca {
+
+// Launch timing.  When `start` is set, the next kernel launched through
+// launch_kernel records the two events as part of its own dispatch (its
+// start and completion timestamps, with no marker packets in between), and
+// the slot is cleared.  Per host thread.
+struct LaunchEvents {
+  hipEvent_t start = nullptr;
+  hipEvent_t stop = nullptr;
+};
+LaunchEvents& launch_events();
+
+template <typename... P, typename... A>
+inline void launch_kernel(void (*kernel)(P...), dim3 grid, dim3 block, uint32_t shmem,
+                          hipStream_t st, A... args) {
+  LaunchEvents& ev = launch_events();
+  if (ev.start != nullptr) {
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, st, ev.start, ev.stop, 0u,
+                          static_cast<P>(args)...);
+    ev = LaunchEvents{};
+  } else {
+    kernel<<<grid, block, shmem, st>>>(static_cast<P>(args)...);
+  }
+}
 
 struct Shape {
   int d, E, k, d_ff, B, N;

@@ -18,6 +18,13 @@
 using moeca::Buffers;
 using moeca::Shape;
 
+namespace moeca {
+LaunchEvents& launch_events() {
+  thread_local LaunchEvents ev;
+  return ev;
+}
+}  // namespace moeca
+
 namespace {
 
 thread_local std::string g_error;
@@ -32,7 +39,7 @@ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 constexpr size_t kAlign = 256;
 constexpr int kMaxTimedSteps = 512;
-constexpr int kEventsPerStep = MOECA_STAGE_COUNT + 1;
+constexpr int kEventsPerStep = 2 * MOECA_STAGE_COUNT;
 
 size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 
@@ -260,25 +267,38 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
 
   const bool timed = L->timing && L->timed_steps < kMaxTimedSteps;
   hipEvent_t* ev = timed ? &L->events[size_t(L->timed_steps) * kEventsPerStep] : nullptr;
+  // Each stage's kernel records its start and completion events with its
+  // own dispatch (launch_kernel).  A stage that launches nothing records
+  // both events back to back.
   int stage = 0;
-  auto mark = [&]() -> hipError_t {
-    return ev ? hipEventRecord(ev[stage++], st) : hipSuccess;
+  auto arm = [&]() {
+    if (ev) {
+      moeca::launch_events() = {ev[2 * stage], ev[2 * stage + 1]};
+    }
   };
-  hipError_t err = mark();
   auto check = [&](hipError_t e, const char* what) -> bool {
-    if (e == hipSuccess) e = mark();
+    if (ev) {
+      moeca::LaunchEvents& le = moeca::launch_events();
+      if (le.start != nullptr) {
+        le = moeca::LaunchEvents{};
+        if (e == hipSuccess) e = hipEventRecord(ev[2 * stage], st);
+        if (e == hipSuccess) e = hipEventRecord(ev[2 * stage + 1], st);
+      }
+      ++stage;
+    }
     if (e != hipSuccess) {
       fail(MOECA_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
       return false;
     }
     return true;
   };
-  if (err != hipSuccess) return fail(MOECA_E_HIP, hipGetErrorString(err));
 
   const Buffers& b = L->buf;
+  arm();
   if (!check(moeca::launch_router(s, x_t, L->W_r, L->b_r, p.norm_topk, p.beta, !uncached, b, st),
              "router"))
     return MOECA_E_HIP;
+  arm();
   if (!check(uncached ? hipSuccess : moeca::launch_entropy(s, p.tau0, p.alpha, b, st),
              "entropy"))
     return MOECA_E_HIP;
@@ -288,11 +308,16 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
     sel = p.mode == MOECA_MODE_THRESHOLD ? moeca::kSelThreshold : moeca::kSelRatio;
     budget = static_cast<int>(std::floor(static_cast<double>(p.ratio) * s.N * s.k + 0.5));
   }
+  arm();
   if (!check(moeca::launch_decide(s, sel, budget, p.lambda1, p.lambda2, b, st), "decide"))
     return MOECA_E_HIP;
+  arm();
   if (!check(moeca::launch_lists(s, moeca::ffn_plan(s), b, st), "lists")) return MOECA_E_HIP;
+  arm();
   if (!check(moeca::launch_ffn_up(s, x_t, L->W_up, p.act, b, st), "ffn up")) return MOECA_E_HIP;
+  arm();
   if (!check(moeca::launch_ffn_down(s, L->W_down, b, st), "ffn down")) return MOECA_E_HIP;
+  arm();
   if (!check(moeca::launch_combine(s, uncached ? 0 : 1, out, L->attn_in, L->attn_cache, b, st),
              "combine"))
     return MOECA_E_HIP;
@@ -367,7 +392,9 @@ int moeca_set_timing(moeca_layer* L, int enable) {
   if (!enable) return MOECA_OK;
   L->events.resize(size_t(kMaxTimedSteps) * kEventsPerStep);
   for (auto& e : L->events) {
-    const hipError_t r = hipEventCreate(&e);
+    // timing-only events: no system-scope fence (cache writeback) at each
+    // record, which would stretch the measured kernel intervals
+    const hipError_t r = hipEventCreateWithFlags(&e, hipEventDisableSystemFence);
     if (r != hipSuccess) {
       e = nullptr;
       return fail(MOECA_E_HIP, std::string("event create: ") + hipGetErrorString(r));
@@ -391,7 +418,7 @@ int moeca_get_timing(moeca_layer* L, double* ms, int n, int* steps) {
     hipEvent_t* ev = &L->events[size_t(sidx) * kEventsPerStep];
     for (int i = 0; i < n; ++i) {
       float v = 0.0f;
-      const hipError_t r = hipEventElapsedTime(&v, ev[i], ev[i + 1]);
+      const hipError_t r = hipEventElapsedTime(&v, ev[2 * i], ev[2 * i + 1]);
       if (r != hipSuccess)
         return fail(MOECA_E_HIP, std::string("elapsed: ") + hipGetErrorString(r));
       ms[i] += v;

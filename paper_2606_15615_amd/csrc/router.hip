@@ -225,12 +225,12 @@ hipError_t launch_typed(const Shape& s, const void* x, const void* W_r, const fl
   const dim3 grid(router_blocks(s)), block(kRouterWaves * kWave);
   const size_t wbytes = size_t(s.E) * s.d * sizeof(T);
   if (wbytes <= kLdsWBytes) {
-    router_kernel<T, true><<<grid, block, wbytes, st>>>(
-        static_cast<const T*>(x), static_cast<const T*>(W_r), b_r, s.tokens(), s.d, s.E, s.k,
+    launch_kernel(
+        &router_kernel<T, true>, grid, block, uint32_t(wbytes), st, static_cast<const T*>(x), static_cast<const T*>(W_r), b_r, s.tokens(), s.d, s.E, s.k,
         norm_topk, b.logits, b.e_t, b.w_t, b.rflags, C, s.N, beta);
   } else {
-    router_kernel<T, false><<<grid, block, 0, st>>>(
-        static_cast<const T*>(x), static_cast<const T*>(W_r), b_r, s.tokens(), s.d, s.E, s.k,
+    launch_kernel(
+        &router_kernel<T, false>, grid, block, 0, st, static_cast<const T*>(x), static_cast<const T*>(W_r), b_r, s.tokens(), s.d, s.E, s.k,
         norm_topk, b.logits, b.e_t, b.w_t, b.rflags, C, s.N, beta);
   }
   return hipGetLastError();
