@@ -121,6 +121,137 @@ __global__ __launch_bounds__(kCombWaves * kWave) void combine_kernel(
   }
 }
 
+// Fast path for k <= 2 and d <= 512 GI: the token index is wave-uniform, so
+// the branch metadata comes in by scalar loads; then every row load of the
+// token (its k cache rows and, when synchronised, its attention row) is
+// issued before any is used, so a token costs two dependent memory round
+// trips.  Same arithmetic as above.
+template <typename T> struct Raw8;
+template <> struct Raw8<uint16_t> {
+  typedef __attribute__((ext_vector_type(4))) unsigned int v;
+  static __device__ __forceinline__ v load(const uint16_t* p) {
+    return *reinterpret_cast<const v*>(p);
+  }
+  static __device__ __forceinline__ void store(uint16_t* p, v x) { *reinterpret_cast<v*>(p) = x; }
+  static __device__ __forceinline__ void widen(v x, float* f) {
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      f[2 * u] = __uint_as_float(x[u] << 16);
+      f[2 * u + 1] = __uint_as_float(x[u] & 0xffff0000u);
+    }
+  }
+  static __device__ __forceinline__ v narrow(const float* f) {
+    v x;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      x[u] = f32_to_bf16(f[2 * u]) | (uint32_t(f32_to_bf16(f[2 * u + 1])) << 16);
+    return x;
+  }
+};
+template <> struct Raw8<float> {
+  typedef __attribute__((ext_vector_type(8))) float v;
+  static __device__ __forceinline__ v load(const float* p) {
+    return *reinterpret_cast<const v*>(p);
+  }
+  static __device__ __forceinline__ void store(float* p, v x) { *reinterpret_cast<v*>(p) = x; }
+  static __device__ __forceinline__ void widen(v x, float* f) {
+#pragma unroll
+    for (int u = 0; u < 8; ++u) f[u] = x[u];
+  }
+  static __device__ __forceinline__ v narrow(const float* f) {
+    v x;
+#pragma unroll
+    for (int u = 0; u < 8; ++u) x[u] = f[u];
+    return x;
+  }
+};
+
+template <typename T, int K, int GI>
+__global__ __launch_bounds__(kCombWaves * kWave) void combine_fast_kernel(
+    const float* __restrict__ w_t, const int32_t* __restrict__ e_t,
+    const int32_t* __restrict__ sigma, const uint8_t* __restrict__ mask,
+    const uint8_t* __restrict__ sync, T* __restrict__ h_c, int32_t* __restrict__ e_c,
+    float* __restrict__ w_c, float* __restrict__ n_c, T* __restrict__ out,
+    const T* __restrict__ attn_in, T* __restrict__ attn_cache, int64_t T_tokens, int d, int k,
+    int write_cache) {
+  typedef typename Raw8<T>::v raw;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int t = __builtin_amdgcn_readfirstlane(
+      static_cast<int>(blockIdx.x) * kCombWaves + static_cast<int>(threadIdx.x) / kWave);
+  if (t >= T_tokens) return;
+  const int groups = d / 8;
+
+  float wp[K];
+  int slot[K];
+  bool rec[K];
+#pragma unroll
+  for (int p = 0; p < K; ++p) {
+    const int64_t f = int64_t(t) * K + p;
+    wp[p] = w_t[f];
+    slot[p] = sigma[f];
+    rec[p] = mask[f] != 0;
+  }
+  const bool syn = write_cache && attn_in != nullptr && sync[t] != 0;
+
+  raw h[K][GI];
+  raw a[GI];
+#pragma unroll
+  for (int p = 0; p < K; ++p) {
+    const T* row = h_c + (int64_t(t) * K + slot[p]) * d;
+#pragma unroll
+    for (int gi = 0; gi < GI; ++gi) {
+      const int g = lane + kWave * gi;
+      if (g < groups) h[p][gi] = Raw8<T>::load(row + g * 8);
+    }
+  }
+  if (syn) {
+#pragma unroll
+    for (int gi = 0; gi < GI; ++gi) {
+      const int g = lane + kWave * gi;
+      if (g < groups) a[gi] = Raw8<T>::load(attn_in + int64_t(t) * d + g * 8);
+    }
+  }
+
+  double ss[K];
+#pragma unroll
+  for (int p = 0; p < K; ++p) ss[p] = 0.0;
+#pragma unroll
+  for (int gi = 0; gi < GI; ++gi) {
+    const int g = lane + kWave * gi;
+    if (g >= groups) continue;
+    float acc[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc[u] = 0.0f;
+#pragma unroll
+    for (int p = 0; p < K; ++p) {
+      float hv[8];
+      Raw8<T>::widen(h[p][gi], hv);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc[u] = __fadd_rn(acc[u], __fmul_rn(wp[p], hv[u]));
+      if (rec[p]) {
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          ss[p] += static_cast<double>(hv[u]) * static_cast<double>(hv[u]);
+      }
+    }
+    Raw8<T>::store(out + int64_t(t) * d + g * 8, Raw8<T>::narrow(acc));
+    if (syn) Raw8<T>::store(attn_cache + int64_t(t) * d + g * 8, a[gi]);
+  }
+
+  if (!write_cache) return;
+#pragma unroll
+  for (int p = 0; p < K; ++p) {
+    if (!rec[p]) continue;  // uniform across the wave (one token per wave)
+    const double sq = wave_sum_f64(ss[p]);
+    if (lane == 0) {
+      const int64_t c = int64_t(t) * K + slot[p];
+      n_c[c] = static_cast<float>(sqrt(sq));
+      e_c[c] = e_t[int64_t(t) * K + p];
+      w_c[c] = wp[p];
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void* attn_in,
@@ -132,11 +263,25 @@ hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void
                 static_cast<TT*>(b.h_c), b.e_c, b.w_c, b.n_c, static_cast<TT*>(out),           \
                 static_cast<const TT*>(attn_in), static_cast<TT*>(attn_cache), s.tokens(), s.d,  \
                 s.k, write_cache)
-  if (s.bf16) {
+  const int gi = (s.d / 8 + kWave - 1) / kWave;  // 8-element groups per lane
+  const bool fast = s.k <= 2 && gi <= 4 && s.tokens() < (int64_t(1) << 31);
+#define MOECA_FAST(TT, KK)                                                           \
+  switch (gi) {                                                                      \
+    case 1: MOECA_COMBINE((combine_fast_kernel<TT, KK, 1>), TT); break;              \
+    case 2: MOECA_COMBINE((combine_fast_kernel<TT, KK, 2>), TT); break;              \
+    case 3: MOECA_COMBINE((combine_fast_kernel<TT, KK, 3>), TT); break;              \
+    default: MOECA_COMBINE((combine_fast_kernel<TT, KK, 4>), TT); break;             \
+  }
+  if (fast && s.bf16) {
+    if (s.k == 1) { MOECA_FAST(uint16_t, 1) } else { MOECA_FAST(uint16_t, 2) }
+  } else if (fast) {
+    if (s.k == 1) { MOECA_FAST(float, 1) } else { MOECA_FAST(float, 2) }
+  } else if (s.bf16) {
     MOECA_COMBINE(combine_kernel<uint16_t>, uint16_t);
   } else {
     MOECA_COMBINE(combine_kernel<float>, float);
   }
+#undef MOECA_FAST
 #undef MOECA_COMBINE
   return hipGetLastError();
 }

@@ -72,18 +72,14 @@ __global__ __launch_bounds__(kStatThreads) void entropy_kernel(
 //   full step : R = all, sigma(p) = p
 //   threshold : R = unmatched U {m > 0}                    (Sec. 4.2)
 //   ratio     : R = unmatched U the first max(0, K_b - |U|) matched branches
-//               by (m desc, flat id asc), found with an MSB-first radix select
-//               on the 64-bit key (order(m) << 32 | ~id): keys are unique, so
-//               exactly that many keys are >= the selected one.
+//               by (m desc, flat id asc): an MSB-first radix select on the
+//               order-preserving 32-bit key of m, then the lowest flat ids
+//               among the keys equal to the selected one.
 //   slots     : matched p keep q(p); unmatched p (ascending) take the free
 //               slots in ascending order
 // ---------------------------------------------------------------------------
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
-
-__device__ __forceinline__ uint64_t branch_key(float m, int j) {
-  return (static_cast<uint64_t>(f32_order_key(m)) << 32) | static_cast<uint32_t>(~j);
-}
 
 template <int R>
 __global__ __launch_bounds__(kSelThreads) void decide_kernel(
@@ -96,11 +92,12 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   extern __shared__ __attribute__((aligned(16))) unsigned char s_dyn[];
   int8_t* s_q = reinterpret_cast<int8_t*>(s_dyn);            // [N*k] matched slot or -1
   uint8_t* s_mask = reinterpret_cast<uint8_t*>(s_dyn) + N * k; // [N*k]
-  __shared__ int s_hist[256];
-  __shared__ int s_wtot[kSelWaves];
+  __shared__ int s_hist[2][256];
   __shared__ int s_cnt[64];
+  __shared__ float s_tau[64];
+  __shared__ int s_tcnt[R][kSelWaves];
   __shared__ int s_unmatched, s_recompute, s_sync;
-  __shared__ unsigned long long s_prefix;
+  __shared__ unsigned s_bin;
   __shared__ int s_remaining;
 
   const int b = blockIdx.x;
@@ -110,16 +107,20 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   const int lane = tid & (kWave - 1);
   const int wv = tid / kWave;
 
-  if (tid < 64) s_cnt[tid] = 0;
+  if (tid < 64) {
+    s_cnt[tid] = 0;
+    if (tid < E) s_tau[tid] = tau[b * E + tid];
+  }
+  if (tid < 256) s_hist[0][tid] = 0;
   if (tid == 0) {
     s_unmatched = 0;
     s_recompute = 0;
     s_sync = 0;
-    s_prefix = 0ull;
   }
   __syncthreads();
 
-  // 1. matching and scores (cache steps)
+  // 1. matching and scores (cache steps); every operand of a branch is
+  // loaded before any is used
   int qv[R];
   float mv[R];
   int ev[R];
@@ -135,22 +136,39 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
       const int e = e_t[f];
       ev[r] = e;
       if (mode != kSelFull) {
-        const int64_t tok = f / k;
+        const int64_t c0 = base + (j / k) * k;  // the token's first slot
         const float w = w_t[f];
+        int ejs[8];
+        float ncs[8], wcs[8];
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          if (jj < k) {
+            ejs[jj] = e_c[c0 + jj];
+            ncs[jj] = n_c[c0 + jj];
+            wcs[jj] = w_c[c0 + jj];
+          }
+        }
         int q = -1;
         double den = 0.0;
-        for (int jj = 0; jj < k; ++jj) {
-          const int ej = e_c[tok * k + jj];
-          if (ej >= 0) den += static_cast<double>(n_c[tok * k + jj]);
-          if (q < 0 && ej >= 0 && ej == e) q = jj;
+        float ncq = 0.0f, wcq = 0.0f;
+#pragma unroll
+        for (int jj = 0; jj < 8; ++jj) {
+          if (jj < k) {
+            if (ejs[jj] >= 0) den += static_cast<double>(ncs[jj]);
+            if (q < 0 && ejs[jj] >= 0 && ejs[jj] == e) {
+              q = jj;
+              ncq = ncs[jj];
+              wcq = wcs[jj];
+            }
+          }
         }
         if (q >= 0) {
           const float denf = static_cast<float>(den);
-          const float delta = fabsf(__fsub_rn(w, w_c[tok * k + q]));
-          const float o = denf > 0.0f ? __fdiv_rn(n_c[tok * k + q], denf) : 0.0f;
+          const float delta = fabsf(__fsub_rn(w, wcq));
+          const float o = denf > 0.0f ? __fdiv_rn(ncq, denf) : 0.0f;
           float sc = __fadd_rn(w, __fmul_rn(lambda1, delta));
           sc = __fadd_rn(sc, __fmul_rn(lambda2, o));
-          mv[r] = __fsub_rn(sc, tau[b * E + e]);
+          mv[r] = __fsub_rn(sc, s_tau[e]);
         } else {
           ++unmatched;
         }
@@ -168,81 +186,131 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   const int n_unmatched = s_unmatched;
   const int n_matched = mode == kSelFull ? 0 : nb - n_unmatched;
 
-  // 2. ratio mode: key of the need-th best matched branch
+  // 2. ratio mode: the need-th best matched branch.  Four 8-bit radix
+  // passes (most significant first) find the margin key T with fewer than
+  // `need` matched keys above it and at least `need` at or above it; of the
+  // keys equal to T the lowest flat ids are taken (rank by ballots).
   int need = 0;
   bool take_all_matched = false;
+  uint32_t thr = 0;
+  int tie_rem = 0;
+  bool tie_take[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) tie_take[r] = false;
   if (mode == kSelRatio) {
     need = budget - n_unmatched;
     if (need < 0) need = 0;
     if (need >= n_matched) take_all_matched = true;
     if (need > 0 && !take_all_matched) {
-      if (tid == 0) s_remaining = need;
-      __syncthreads();
-      uint64_t key[R];
+      uint32_t mk[R];
 #pragma unroll
-      for (int r = 0; r < R; ++r) key[r] = branch_key(mv[r], tid + kSelThreads * r);
-      for (int shift = 56; shift >= 0; shift -= 8) {
-        // prefix and remaining are read here and written only after the two
-        // barriers below, so every thread sees this pass's values.
-        const uint64_t prefix = s_prefix;
-        const int rem = s_remaining;
-        if (tid < 256) s_hist[tid] = 0;
-        __syncthreads();
-        const uint64_t hi_mask = (shift == 56) ? 0ull : (~0ull << (shift + 8));
+      for (int r = 0; r < R; ++r) mk[r] = f32_order_key(mv[r]);
+      uint32_t prefix = 0;
+      int rem = need;
+#pragma unroll
+      for (int pass = 0; pass < 4; ++pass) {
+        const int shift = 24 - 8 * pass;
+        int* hist = s_hist[pass & 1];
+        const uint32_t hi_mask = pass == 0 ? 0u : (~0u << (shift + 8));
+        // histogram of this digit over the matched keys that share the
+        // prefix: the (at most two) most frequent bins of a wave are added
+        // once by one lane, the remaining lanes add their own
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-          if (qv[r] >= 0 && ((key[r] ^ prefix) & hi_mask) == 0ull)
-            atomicAdd(&s_hist[(key[r] >> shift) & 255ull], 1);
+          bool part = qv[r] >= 0 && ((mk[r] ^ prefix) & hi_mask) == 0u;
+          const int bin = static_cast<int>((mk[r] >> shift) & 255u);
+#pragma unroll
+          for (int it = 0; it < 2; ++it) {
+            const uint64_t todo = __ballot(part);
+            if (todo == 0ull) break;
+            const int leader = __builtin_ctzll(todo);
+            const int lb = __builtin_amdgcn_readlane(bin, leader);
+            const uint64_t same = __ballot(part && bin == lb);
+            if (lane == leader) atomicAdd(&hist[lb], __popcll(same));
+            if (bin == lb) part = false;
+          }
+          if (part) atomicAdd(&hist[bin], 1);
         }
         __syncthreads();
-        // suffix sums over the 256 bins (bin 255 first) by the first 4 waves
-        int h = 0, incl = 0;
-        if (tid < 256) {
-          h = s_hist[255 - tid];
-          incl = h;
+        if (wv == 0) {
+          // lane l holds bins 255 - 4l .. 252 - 4l (descending)
+          int c[4];
+#pragma unroll
+          for (int u = 0; u < 4; ++u) c[u] = hist[255 - 4 * lane - u];
+          const int tot = c[0] + c[1] + c[2] + c[3];
+          int incl = tot;
 #pragma unroll
           for (int o = 1; o < kWave; o <<= 1) {
             const int v = __shfl_up(incl, o, kWave);
             if (lane >= o) incl += v;
           }
-          if (lane == kWave - 1) s_wtot[wv] = incl;
-        }
-        __syncthreads();
-        if (tid < 256) {
-          for (int w2 = 0; w2 < wv; ++w2) incl += s_wtot[w2];
-          const int excl = incl - h;
-          if (h > 0 && excl < rem && rem <= incl) {
-            s_prefix = prefix | (static_cast<uint64_t>(255 - tid) << shift);
-            s_remaining = rem - excl;
+          int run = incl - tot;
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            if (c[u] > 0 && run < rem && rem <= run + c[u]) {
+              s_bin = static_cast<unsigned>(255 - 4 * lane - u);
+              s_remaining = rem - run;
+            }
+            run += c[u];
           }
+        } else if (wv == 1) {
+#pragma unroll
+          for (int u = 0; u < 4; ++u) s_hist[(pass + 1) & 1][4 * lane + u] = 0;
         }
         __syncthreads();
+        prefix |= static_cast<uint32_t>(s_bin) << shift;
+        rem = s_remaining;
+      }
+      thr = prefix;
+      tie_rem = rem;
+      // keys equal to T: take the tie_rem lowest flat ids (j = tid + 1024 r,
+      // so the order is r-major, then wave, then lane)
+      uint64_t tb[R];
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        tb[r] = __ballot(qv[r] >= 0 && mk[r] == thr);
+        if (lane == 0) s_tcnt[r][wv] = __popcll(tb[r]);
+      }
+      __syncthreads();
+      int before = 0;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        int in_r = 0, below = 0;
+        for (int w2 = 0; w2 < kSelWaves; ++w2) {
+          const int c = s_tcnt[r][w2];
+          in_r += c;
+          if (w2 < wv) below += c;
+        }
+        const bool flag = ((tb[r] >> lane) & 1ull) != 0;
+        tie_take[r] = flag && before + below + lane_rank(tb[r]) < tie_rem;
+        before += in_r;
       }
     }
   }
-  const uint64_t thr = s_prefix;
 
   // 3. mask and per-expert counts
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int j = tid + kSelThreads * r;
-    if (j >= nb) continue;
-    bool rc;
-    if (mode == kSelFull || qv[r] < 0) {
-      rc = true;
-    } else if (mode == kSelThreshold) {
-      rc = mv[r] > 0.0f;
-    } else if (take_all_matched) {
-      rc = true;
-    } else if (need == 0) {
-      rc = false;
-    } else {
-      rc = branch_key(mv[r], j) >= thr;
+    bool rc = false;
+    if (j < nb) {
+      if (mode == kSelFull || qv[r] < 0) {
+        rc = true;
+      } else if (mode == kSelThreshold) {
+        rc = mv[r] > 0.0f;
+      } else if (take_all_matched) {
+        rc = true;
+      } else if (need == 0) {
+        rc = false;
+      } else {
+        const uint32_t mk = f32_order_key(mv[r]);
+        rc = mk > thr || tie_take[r];
+      }
+      mask[base + j] = rc ? 1 : 0;
+      s_mask[j] = rc ? 1 : 0;
+      s_q[j] = static_cast<int8_t>(qv[r]);
+      if (rc) atomicAdd(&s_cnt[ev[r]], 1);
     }
-    mask[base + j] = rc ? 1 : 0;
-    s_mask[j] = rc ? 1 : 0;
-    s_q[j] = static_cast<int8_t>(qv[r]);
-    if (rc) atomicAdd(&s_cnt[ev[r]], 1);
   }
   __syncthreads();
 
@@ -297,11 +365,122 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
 
 // ---------------------------------------------------------------------------
 // Per-expert lists of recomputed branches, ascending flat id within each
-// expert; one block per sample.  Each block derives its write base per
+// expert; one block per sample, each thread holding up to R of the sample's
+// branches (j = tid + 1024 r).  All inputs are loaded first.  Wave 0 turns the
+// [B][E] count table into this sample's write base per expert (and, in block
+// 0, the expert offsets and the GEMM tile tables); each wave counts and ranks
+// its selected branches per expert with ballots; after one barrier every
+// branch knows its place: branches of earlier r, then of earlier waves, then
+// of lower lanes come first (stable, no atomics).
+// ---------------------------------------------------------------------------
+template <int R>
+__global__ __launch_bounds__(kSelThreads) void lists_kernel(
+    const uint8_t* __restrict__ mask, const int32_t* __restrict__ e_t,
+    const int32_t* __restrict__ cnt_bs, int B, int N, int E, int k, int tm, int nt_up,
+    int nt_down, const int32_t* __restrict__ sigma, int32_t* __restrict__ off,
+    int32_t* __restrict__ tiles, int32_t* __restrict__ list, int32_t* __restrict__ pos,
+    int32_t* __restrict__ row_dst) {
+  __shared__ int s_base[64];
+  __shared__ int s_wcnt[R][kSelWaves][64];
+  const int b = blockIdx.x;
+  const int nb = N * k;
+  const int64_t base = int64_t(b) * nb;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wv = tid / kWave;
+
+  int ev[R], sg[R];
+  bool sel[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int j = tid + kSelThreads * r;
+    sel[r] = false;
+    ev[r] = -1;
+    sg[r] = 0;
+    if (j < nb) {
+      sel[r] = mask[base + j] != 0;
+      ev[r] = e_t[base + j];
+      sg[r] = sigma[base + j];
+    }
+  }
+  if (wv == 0) {
+    // lane e: expert e's total over all samples and over the samples before b
+    int tot = 0, below = 0;
+    if (lane < E) {
+      for (int b2 = 0; b2 < B; ++b2) {
+        const int c = cnt_bs[b2 * E + lane];
+        tot += c;
+        if (b2 < b) below += c;
+      }
+    }
+    const int mt = (tot + tm - 1) / tm;
+    int o = tot, tu = mt * nt_up, td = mt * nt_down;  // inclusive scans over experts
+#pragma unroll
+    for (int dd = 1; dd < kWave; dd <<= 1) {
+      const int vo = __shfl_up(o, dd, kWave);
+      const int vu = __shfl_up(tu, dd, kWave);
+      const int vd = __shfl_up(td, dd, kWave);
+      if (lane >= dd) {
+        o += vo;
+        tu += vu;
+        td += vd;
+      }
+    }
+    if (lane < E) s_base[lane] = o - tot + below;
+    if (b == 0 && lane < E) {
+      // exclusive prefixes per expert; the last expert also writes the totals
+      off[lane] = o - tot;
+      tiles[lane] = tu - mt * nt_up;
+      tiles[E + 1 + lane] = td - mt * nt_down;
+      if (lane == E - 1) {
+        off[E] = o;
+        tiles[E] = tu;
+        tiles[2 * E + 1] = td;
+      }
+    }
+  }
+  int rk[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    rk[r] = 0;
+    for (int ee = 0; ee < E; ++ee) {
+      const bool mine = sel[r] && ev[r] == ee;
+      const uint64_t bal = __ballot(mine);
+      if (lane == ee) s_wcnt[r][wv][ee] = __popcll(bal);
+      if (mine) rk[r] = lane_rank(bal);
+    }
+  }
+  __syncthreads();
+
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    const int j = tid + kSelThreads * r;
+    if (j >= nb) continue;
+    const int64_t f = base + j;
+    if (!sel[r]) {
+      pos[f] = -1;
+      continue;
+    }
+    const int e = ev[r];
+    int before = 0;
+    for (int r2 = 0; r2 < r; ++r2)
+      for (int w2 = 0; w2 < kSelWaves; ++w2) before += s_wcnt[r2][w2][e];
+    for (int w2 = 0; w2 < wv; ++w2) before += s_wcnt[r][w2][e];
+    const int idx = s_base[e] + before + rk[r];
+    list[idx] = static_cast<int32_t>(f);
+    pos[f] = idx;
+    row_dst[idx] = static_cast<int32_t>((f / k) * k + sg[r]);
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Per-expert lists for samples of more than 8192 branches (the register
+// version below would not fit its count table in LDS): ascending flat id
+// within each expert; one block per sample.  Each block derives its write base per
 // expert from the [B][E] count table, then walks its branches in flat order
 // in chunks of 1024 and ranks them with wave ballots (stable, no atomics).
 // ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kSelThreads) void lists_kernel(
+__global__ __launch_bounds__(kSelThreads) void lists_chunked_kernel(
     const uint8_t* __restrict__ mask, const int32_t* __restrict__ e_t,
     const int32_t* __restrict__ cnt_bs, int B, int N, int E, int k, int tm, int nt_up,
     int nt_down, const int32_t* __restrict__ sigma, int32_t* __restrict__ off,
@@ -434,11 +613,21 @@ hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1
 }
 
 hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st) {
-  launch_kernel(
-      &lists_kernel, dim3(s.B), dim3(kSelThreads), 0, st, b.mask, b.e_t, b.cnt_bs, s.B, s.N, s.E,
-      s.k, plan.tm,
-      (s.d_ff + plan.tn_up - 1) / plan.tn_up, (s.d + plan.tn_down - 1) / plan.tn_down, b.sigma,
-      b.off, b.tiles, b.list, b.pos, b.row_dst);
+  const int nb = s.N * s.k;
+  const int nt_up = (s.d_ff + plan.tn_up - 1) / plan.tn_up;
+  const int nt_down = (s.d + plan.tn_down - 1) / plan.tn_down;
+#define MOECA_LISTS(KER)                                                                       \
+  launch_kernel(&KER, dim3(s.B), dim3(kSelThreads), 0, st, b.mask, b.e_t, b.cnt_bs, s.B, s.N, \
+                s.E, s.k, plan.tm, nt_up, nt_down, b.sigma, b.off, b.tiles, b.list, b.pos,    \
+                b.row_dst)
+  if (nb <= 2 * kSelThreads) {
+    MOECA_LISTS(lists_kernel<2>);
+  } else if (nb <= 8 * kSelThreads) {
+    MOECA_LISTS(lists_kernel<8>);
+  } else {
+    MOECA_LISTS(lists_chunked_kernel);
+  }
+#undef MOECA_LISTS
   return hipGetLastError();
 }
 
