@@ -413,6 +413,44 @@ __device__ __forceinline__ u32x2_t pack4_bf16(float a, float b, float c, float d
   return u32x2_t{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
 }
 
+// One tile of the persistent walk: expert, first list row, rows, first
+// output column.
+struct BigTile {
+  int e, r0, rows, n0;
+};
+
+__device__ __forceinline__ BigTile big_tile(int L, int my_toff, const int32_t* __restrict__ off) {
+  BigTile t;
+  t.e = __popcll(__ballot(my_toff <= L)) - 1;
+  const int e_base = __shfl(my_toff, t.e, 64);
+  const int o0 = off[t.e];
+  const int cnt = off[t.e + 1] - o0;
+  const int mt = (cnt + kBigTM - 1) / kBigTM;
+  const int local = L - e_base;
+  const int m = local % mt;
+  t.r0 = o0 + m * kBigTM;
+  t.rows = min(kBigTM, cnt - m * kBigTM);
+  t.n0 = (local / mt) * kBigTN;
+  return t;
+}
+
+// Row table entry r of a tile: the source row of the A operand and the
+// destination row of the output (-1: padding, never stored).
+template <int KIND>
+__device__ __forceinline__ void big_rows(const BigTile& t, int r, int k,
+                                         const int32_t* __restrict__ list,
+                                         const int32_t* __restrict__ row_dst, int& src,
+                                         int& dst) {
+  const int rr = r < t.rows ? r : 0;  // padding rows re-read row 0
+  if (KIND == kUp) {
+    src = list[t.r0 + rr] / k;
+    dst = r < t.rows ? t.r0 + r : -1;
+  } else {
+    src = t.r0 + rr;
+    dst = r < t.rows ? row_dst[t.r0 + r] : -1;
+  }
+}
+
 template <int KIND, int ACT>
 __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
@@ -445,34 +483,15 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
   const int chunk = (lane & 7) ^ (4 * (wv & 1) + (lane >> 4));
   const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(lds) + wv * 1024);
 
-  for (int L = lo + static_cast<int>(blockIdx.x) / kXcds; L < hi; L += stride) {
-    const int e = __popcll(__ballot(my_toff <= L)) - 1;
-    const int e_base = __shfl(my_toff, e, 64);
-    const int o0 = off[e];
-    const int cnt = off[e + 1] - o0;
-    const int mt = (cnt + TM - 1) / TM;
-    const int local = L - e_base;
-    const int m = local % mt;
-    const int r0 = o0 + m * TM;
-    const int rows = min(TM, cnt - m * TM);
-    const int n0 = (local / mt) * TN;
-
-    for (int r = tid; r < TM; r += kBigThreads) {
-      const int rr = r < rows ? r : 0;  // padding rows re-read row 0, never stored
-      if (KIND == kUp) {
-        s_src[r] = list[r0 + rr] / k;
-        s_dst[r] = r < rows ? r0 + r : -1;
-      } else {
-        s_src[r] = r0 + rr;
-        s_dst[r] = r < rows ? row_dst[r0 + r] : -1;
-      }
+  const uint16_t* ga[kLoadsA];
+  const uint16_t* gb[kLoadsB];
+  // publish a tile's row table, then point this lane's loads at it
+  auto start_tile = [&](const BigTile& t, int src, int dstr) __attribute__((always_inline)) {
+    if (tid < TM) {
+      s_src[tid] = src;
+      s_dst[tid] = dstr;
     }
     __syncthreads();
-
-    // per-lane sources: wave wv issues DMA instructions i = wv + kBigWaves u,
-    // each covering tile rows 8i .. 8i+7 (lane l: row 8i + l/8)
-    const uint16_t* ga[kLoadsA];
-    const uint16_t* gb[kLoadsB];
 #pragma unroll
     for (int u = 0; u < kLoadsA; ++u) {
       const int r = 8 * (wv + kBigWaves * u) + (lane >> 3);
@@ -481,17 +500,41 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
 #pragma unroll
     for (int u = 0; u < kLoadsB; ++u) {
       const int r = 8 * (wv + kBigWaves * u) + (lane >> 3);
-      const int n = min(n0 + r, Nout - 1);
-      gb[u] = W + (int64_t(e) * Nout + n) * K + chunk * 8;
+      const int n = min(t.n0 + r, Nout - 1);
+      gb[u] = W + (int64_t(t.e) * Nout + n) * K + chunk * 8;
     }
-    auto issue = [&](int kt, int st) __attribute__((always_inline)) {
-      const uint32_t base = lds0 + st * (kStageElems * 2);
+  };
+  auto issue = [&](int kt, int st) __attribute__((always_inline)) {
+    const uint32_t base = lds0 + st * (kStageElems * 2);
 #pragma unroll
-      for (int u = 0; u < kLoadsA; ++u) dma16(ga[u] + kt * kTK, base + u * kBigWaves * 1024);
+    for (int u = 0; u < kLoadsA; ++u) dma16(ga[u] + kt * kTK, base + u * kBigWaves * 1024);
 #pragma unroll
-      for (int u = 0; u < kLoadsB; ++u)
-        dma16(gb[u] + kt * kTK, base + kTileA * 2 + u * kBigWaves * 1024);
-    };
+    for (int u = 0; u < kLoadsB; ++u)
+      dma16(gb[u] + kt * kTK, base + kTileA * 2 + u * kBigWaves * 1024);
+  };
+
+  int L = lo + static_cast<int>(blockIdx.x) / kXcds;
+  if (L >= hi) return;
+  BigTile cur = big_tile(L, my_toff, off);
+  {
+    int src = 0, dstr = -1;
+    if (tid < TM) big_rows<KIND>(cur, tid, k, list, row_dst, src, dstr);
+    start_tile(cur, src, dstr);
+  }
+  issue(0, 0);
+  if (KT > 1) issue(1, 1);
+
+  for (;;) {
+    // the next tile's metadata and row table entries, loaded now and used
+    // only after this tile's k-loop (which ends with every load complete)
+    const int Ln = L + stride;
+    const bool has_next = Ln < hi;
+    BigTile nxt = cur;
+    int nsrc = 0, ndst = -1;
+    if (has_next) {
+      nxt = big_tile(Ln, my_toff, off);
+      if (tid < TM) big_rows<KIND>(nxt, tid, k, list, row_dst, nsrc, ndst);
+    }
 
     f32x16_t acc[FN][FM];
 #pragma unroll
@@ -501,8 +544,9 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
 #pragma unroll
         for (int r = 0; r < 16; ++r) acc[i][j][r] = 0.0f;
 
-    issue(0, 0);
-    if (KT > 1) issue(1, 1);
+    // a wave whose 64 x 64 sub-tile lies wholly past the tile's rows or the
+    // output width skips its MFMAs (it still loads its share and syncs)
+    const bool active = wm * FM * 32 < cur.rows && cur.n0 + wn * FN * 32 < Nout;
     int st = 0;
     for (int kt = 0; kt < KT; ++kt) {
       // this wave's loads of tile kt have landed once at most one later
@@ -513,18 +557,30 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
       __builtin_amdgcn_s_barrier();
       if (kt + 2 < KT) issue(kt + 2, st == 0 ? 2 : st - 1);
       const uint16_t* base = lds + st * kStageElems;
-      mfma_ktile_pipe<FN, FM>(acc, base, base + kTileA, wm * FM * 32, wn * FN * 32, lane);
+      if (active)
+        mfma_ktile_pipe<FN, FM>(acc, base, base + kTileA, wm * FM * 32, wn * FN * 32, lane);
       st = st == 2 ? 0 : st + 1;
+    }
+
+    // destination rows of this wave's accumulators, then hand the LDS over
+    // to the next tile and start its loads before this tile's epilogue
+    int drow[FM];
+#pragma unroll
+    for (int j = 0; j < FM; ++j) drow[j] = s_dst[wm * FM * 32 + j * 32 + (lane & 31)];
+    __syncthreads();
+    if (has_next) {
+      start_tile(nxt, nsrc, ndst);
+      issue(0, 0);
+      if (KT > 1) issue(1, 1);
     }
 
     // epilogue: lane holds columns 8*(r/4) + 4*(lane/32) + (r%4) of row
     // (lane & 31) in each 32 x 32 tile; activation, bf16, 8-byte stores
+    const int c0 = cur.n0 + wn * FN * 32 + 4 * (lane >> 5);
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
-      const int drow = s_dst[wm * FM * 32 + j * 32 + (lane & 31)];
-      if (drow < 0) continue;
-      const int c0 = n0 + wn * FN * 32 + 4 * (lane >> 5);
-      uint16_t* orow = dst + int64_t(drow) * Nout + c0;
+      if (drow[j] < 0) continue;
+      uint16_t* orow = dst + int64_t(drow[j]) * Nout + c0;
 #pragma unroll
       for (int i = 0; i < FN; ++i)
 #pragma unroll
@@ -536,7 +592,9 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
                          act_fn<ACT>(a[4 * g + 2]), act_fn<ACT>(a[4 * g + 3]));
         }
     }
-    __syncthreads();
+    if (!has_next) break;
+    L = Ln;
+    cur = nxt;
   }
 }
 
