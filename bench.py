@@ -14,6 +14,7 @@ source no longer matches the one the counters were taken on.
 
     python bench.py [--steps K] [--warmup W] [--workload xl1024]
                     [--phase both|cached|full] [--no-cpu] [--no-graph]
+                    [--sweep 0,0.1,...]   (extra cache-step timings per refresh ratio)
 
 Prints one JSON line.
 """
@@ -53,6 +54,8 @@ def parse():
                     help="time the cache steps, the full-recompute comparator, or both")
     ap.add_argument("--no-graph", action="store_true",
                     help="time eager launches only (no HIP graph replay)")
+    ap.add_argument("--sweep", default="",
+                    help="comma-separated refresh ratios: also time cache steps at each one")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -130,18 +133,22 @@ def main():
     do_cached = args.phase in ("both", "cached")
     do_full = args.phase in ("both", "full")
     log(f"[bench] workload {args.workload} {shape}; phase {args.phase}; generating inputs")
+    # the skewed-routing layer: Zipf(1.2) router prior, bimodal token drift
+    bias, drift = ("zipf", "bimodal") if args.workload == "skewed" else (None, "loguniform")
     sy = Synth(shape, args.seed)
-    W = sy.weights()
-    dW = [np_to_device(W[0], dev), None, np_to_device(W[2], dev), np_to_device(W[3], dev)]
-    xs = [np_to_device(x, dev) for x in sy.trajectory(T)]
-    attn = np_to_device(next(sy.attention_trajectory(1)), dev)
+    W = sy.weights(bias)
+    dW = [np_to_device(W[0], dev), None if W[1] is None else np_to_device(W[1], dev),
+          np_to_device(W[2], dev), np_to_device(W[3], dev)]
+    del W
+    xs = [np_to_device(x, dev) for x in sy.trajectory(T, drift)]
+    attn = np_to_device(next(sy.attention_trajectory(1, drift)), dev)
     attn_cache = torch.zeros_like(attn)
     out = torch.empty_like(xs[0])
     torch.cuda.synchronize()
 
-    def make(mode):
+    def make(mode, ratio=args.ratio):
         L = MoecaLayer(shape.d, shape.E, shape.k, shape.d_ff, batch=shape.B, tokens=shape.N,
-                       mode=mode, ratio=args.ratio, refresh_cycle=0, dtype=shape.dtype)
+                       mode=mode, ratio=ratio, refresh_cycle=0, dtype=shape.dtype)
         L.set_weights(*dW)
         L.bind_attention(attn, attn_cache)
         L.reset()
@@ -218,6 +225,16 @@ def main():
         res_f = phase(full, min(Wm, 3))
         full.close()
 
+    sweep = []
+    for rho in [float(v) for v in args.sweep.split(",") if v.strip()]:
+        log(f"[bench] sweep: cache steps at ratio {rho}")
+        Ls = make(_lib.MOECA_MODE_RATIO, ratio=rho)
+        ms_e, ms_g, graphed_s, stage_s, (rec_s, _) = phase(Ls, Wm)
+        Ls.close()
+        sweep.append({"ratio": rho, "ms_per_step": round(ms_g, 4),
+                      "refresh_ratio_actual": round(float(np.mean(rec_s)) / (shape.tokens * shape.k), 4),
+                      "ffn_ms": round(stage_s["ffn_up"] + stage_s["ffn_down"], 4)})
+
     if args.copy_mib:
         n = args.copy_mib * (1 << 20)
         a = torch.empty(n, dtype=torch.uint8, device=dev)
@@ -230,7 +247,8 @@ def main():
     peak = PEAK_BF16_TFLOPS if shape.dtype == "bf16" else PEAK_FP32_TFLOPS
     act = 2 if shape.dtype == "bf16" else 4
     wl = (f"{args.workload}: MoE layer d={shape.d}, E={shape.E}, top-{shape.k}, "
-          f"d_ff={shape.d_ff} GELU, {shape.N} tokens x batch {shape.B}, ratio mode rho={args.ratio}")
+          f"d_ff={shape.d_ff} GELU, {shape.N} tokens x batch {shape.B}, ratio mode rho={args.ratio}"
+          + (", Zipf(1.2) router prior, bimodal drift" if bias else ""))
     res = {"metric": METRIC, "unit": "ms/step", "n_gpus": 1, "steps": K, "warmup": Wm,
            "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
            "dtype": shape.dtype, "data": "synthetic",
@@ -284,6 +302,8 @@ def main():
     if res_c is not None and res_f is not None:
         res["cached_over_full"] = round(res_c[1] / res_f[1], 4)
         res["speedup_vs_full"] = round(res_f[1] / res_c[1], 3)
+    if sweep:
+        res["ratio_sweep"] = sweep
     if not args.no_cpu and res_c is not None:
         log("[bench] cpu baseline (oracle)")
         res["cpu_baseline"] = cpu_baseline(shape, args.ratio, args.seed)

@@ -173,6 +173,30 @@ def test_xl1024_sampled(mode):
     say(f"  xl1024 {mode}: {info}")
 
 
+# ---------------------------------------------------------------------------
+# Skewed routing: 32 experts with a Zipf(1.2) router prior, bimodal token
+# drift (90 % slow, 10 % fast), swept over refresh ratios.  Width reduced
+# (d = 512, d_ff = 1024) so the oracle evaluates every branch; the same
+# kernels run at the full width in the benchmark's ratio sweep.
+# ---------------------------------------------------------------------------
+SKEWED_SMALL = LayerShape(d=512, E=32, k=2, d_ff=1024, B=2, N=1024, dtype="bf16")
+
+
+@pytest.mark.parametrize("ratio", [0.1, 0.5, 0.9])
+def test_skewed_ratio_sweep(ratio):
+    S = Setup(SKEWED_SMALL, mode="ratio", seed=14, T=4, ratio=ratio, refresh_cycle=0,
+              bias="zipf", drift="bimodal")
+    infos = run_forced(S, 4, label=f"skewed rho={ratio}")
+    say(f"  skewed rho={ratio}: {infos}")
+
+
+def test_skewed_threshold():
+    S = Setup(SKEWED_SMALL, mode="threshold", seed=15, T=4, refresh_cycle=0, bias="zipf",
+              drift="bimodal")
+    infos = run_forced(S, 4, label="skewed threshold")
+    say(f"  skewed threshold: {infos}")
+
+
 def test_free_running_agreement():
     """Both sides run freely from a reset.  Stored rows legitimately differ
     in their last bf16 bits, so masks may drift apart over time; report the
