@@ -56,6 +56,8 @@ def parse():
                     help="time eager launches only (no HIP graph replay)")
     ap.add_argument("--sweep", default="",
                     help="comma-separated refresh ratios: also time cache steps at each one")
+    ap.add_argument("--flush-mib", type=int, default=512,
+                    help="MALL-flushed timing: write this many MiB between single timed steps (0: off)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
     return ap.parse_args()
@@ -202,17 +204,30 @@ def main():
                 graphed = True
             except Exception as exc:  # capture unsupported: report the eager numbers
                 log(f"[bench] graph capture failed ({exc}); reporting eager timings")
+        # the same steps once more, one at a time: counts, and (optionally)
+        # each step timed alone after a write of flush_mib MiB, which leaves
+        # none of the weights in the 256 MB MALL
         L.reset()
         run(L, 0, warm)
         torch.cuda.synchronize()
-        rec, syn = [], []
+        rec, syn, flushed = [], [], []
         for t in range(Wm, T):
+            if flush is not None:
+                flush.fill_(t & 0xff)
+                e0.record(stream)
             L.step(xs[t], t, out)
-            st = L.stats()
+            if flush is not None:
+                e1.record(stream)
+            st = L.stats()  # synchronises
+            if flush is not None:
+                flushed.append(e0.elapsed_time(e1))
             rec.append(st.n_recompute)
             syn.append(st.n_sync)
-        return ms_eager, ms_graph, graphed, stage, (rec, syn)
+        ms_flushed = float(np.mean(flushed)) if flushed else None
+        return ms_eager, ms_graph, graphed, stage, (rec, syn, ms_flushed)
 
+    flush = (torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev)
+             if args.flush_mib > 0 else None)
     res_c = res_f = None
     if do_cached:
         log("[bench] cache steps")
@@ -229,7 +244,7 @@ def main():
     for rho in [float(v) for v in args.sweep.split(",") if v.strip()]:
         log(f"[bench] sweep: cache steps at ratio {rho}")
         Ls = make(_lib.MOECA_MODE_RATIO, ratio=rho)
-        ms_e, ms_g, graphed_s, stage_s, (rec_s, _) = phase(Ls, Wm)
+        ms_e, ms_g, graphed_s, stage_s, (rec_s, _, _) = phase(Ls, Wm)
         Ls.close()
         sweep.append({"ratio": rho, "ms_per_step": round(ms_g, 4),
                       "refresh_ratio_actual": round(float(np.mean(rec_s)) / (shape.tokens * shape.k), 4),
@@ -254,7 +269,7 @@ def main():
            "dtype": shape.dtype, "data": "synthetic",
            "config": {"workload": wl, "batch": shape.B, "tokens": shape.N, "phase": args.phase}}
     if res_c is not None:
-        ms_eager, ms_graph, graphed, stage, (rec, syn) = res_c
+        ms_eager, ms_graph, graphed, stage, (rec, syn, ms_flushed) = res_c
         mean_rec = float(np.mean(rec))
         up_ms = stage["ffn_up"]
         ffn_ms = stage["ffn_up"] + stage["ffn_down"]
@@ -274,6 +289,7 @@ def main():
             "ms_per_step": round(ms_graph, 4),
             "launch": "hip_graph" if graphed else "eager",
             "eager_ms_per_step": round(ms_eager, 4),
+            "flushed_ms_per_step": None if ms_flushed is None else round(ms_flushed, 4),
             "tflops_recomputed": round(ffn_tf, 2),
             "refresh_ratio_actual": round(mean_rec / branches, 4),
             "recomputed_branches": round(mean_rec, 1),
@@ -293,8 +309,9 @@ def main():
             },
         })
     if res_f is not None:
-        ms_eager_f, ms_graph_f, _, stage_f, _ = res_f
+        ms_eager_f, ms_graph_f, _, stage_f, (_, _, ms_flushed_f) = res_f
         res.update({"full_ms_per_step": round(ms_graph_f, 4),
+                    "full_flushed_ms_per_step": None if ms_flushed_f is None else round(ms_flushed_f, 4),
                     "eager_full_ms_per_step": round(ms_eager_f, 4),
                     "full_stage_ms": {k: round(v, 4) for k, v in stage_f.items()}})
         if res_c is None:

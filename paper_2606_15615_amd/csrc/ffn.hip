@@ -324,7 +324,10 @@ __device__ __forceinline__ void s_waitcnt_vm(int n) {
 // compiler does not treat it as an LDS store: it would otherwise wait for
 // every outstanding DMA before each LDS read.  The kernel orders the
 // accesses itself with s_waitcnt vmcnt and s_barrier (loads complete in
-// order, so the compiler's own vmcnt waits stay conservative).
+// order, so the compiler's own vmcnt waits stay conservative).  m0 is
+// reserved by the compiler, which may not preserve it around the statement:
+// this is safe because no kernel here has other m0 uses (the generated code
+// contains no m0 access besides these statements).
 __device__ __forceinline__ void dma16(const uint16_t* g, uint32_t lds) {
   asm volatile(
       "s_mov_b32 m0, %0\n\t"
