@@ -51,7 +51,13 @@ unmatched plus the best matched by (margin desc, flat id asc) up to
 K_b = floor(rho*N*k + 0.5) per sample; R-16 ties toward the lower expert id
 and the lower flat id; R-17 tanh GELU; R-18 the layer returns y (the caller
 adds the residual); R-20 round to nearest even; full steps place branch p
-in slot p.
+in slot p; R-24 shared experts (Sec. 2.3, shared-expert MoE eq.) are
+ungated, evaluated for every token on every step and never cached; the
+combine adds their outputs first (in expert order), then the routed
+branches, in fp32; R-25 the gated (SwiGLU) expert FFN is
+W_down (silu(W_gate x) * (W_up x)), silu(z) = z / (1 + exp(-z)), with the
+gate and up rows interleaved in one up-projection matrix (row 2j gate j,
+row 2j+1 up j) and the product rounded once to the stored dtype.
 
 Pins: every function here is checked by ``tests/test_oracle_pins.py``
 against closed forms, special cases that reduce to a library routine, a
@@ -153,17 +159,20 @@ class Dims:
     B: int
     N: int
     dtype: str = BF16
+    n_shared: int = 0
 
 
 class Weights:
     """Router and expert weights, ``out x in`` row-major, stored dtype."""
 
-    def __init__(self, dims: Dims, W_r, b_r, W_up, W_down):
+    def __init__(self, dims: Dims, W_r, b_r, W_up, W_down, W_sh_up=None, W_sh_down=None):
         self.dims = dims
         self.W_r = W_r
         self.b_r = None if b_r is None else np.asarray(b_r, dtype=F32)
         self.W_up = W_up
         self.W_down = W_down
+        self.W_sh_up = W_sh_up      # (S, up rows, d) shared experts, or None
+        self.W_sh_down = W_sh_down  # (S, d, d_ff)
         self._up64 = {}
         self._down64 = {}
         self.W_r64 = to_f64(W_r, dims.dtype)
@@ -177,6 +186,12 @@ class Weights:
         if e not in self._down64:
             self._down64[e] = to_f64(self.W_down[e], self.dims.dtype)
         return self._down64[e]
+
+    def shared_up64(self, s: int) -> np.ndarray:
+        return to_f64(self.W_sh_up[s], self.dims.dtype)
+
+    def shared_down64(self, s: int) -> np.ndarray:
+        return to_f64(self.W_sh_down[s], self.dims.dtype)
 
 
 class State:
@@ -425,7 +440,7 @@ def expert_lists(mask: np.ndarray, e_t: np.ndarray, E: int):
 
 
 # ---------------------------------------------------------------------------
-# 9. expert FFN (Sec. 2.3: FFN_e; GELU activation)
+# 9. expert FFN (Sec. 2.3: FFN_e; GELU, or the gated SwiGLU form)
 # ---------------------------------------------------------------------------
 _SQRT_2_OVER_PI = math.sqrt(2.0 / math.pi)
 
@@ -441,12 +456,23 @@ def gelu(z: np.ndarray, kind: str) -> np.ndarray:
     raise ValueError(kind)
 
 
+def silu(z: np.ndarray) -> np.ndarray:
+    """z * sigmoid(z) = z / (1 + exp(-z)) in fp64."""
+    return z / (1.0 + np.exp(-z))
+
+
 def expert_ffn(x_rows64: np.ndarray, Wup64: np.ndarray, Wdown64: np.ndarray,
                act: str, dtype: str) -> np.ndarray:
     """h = W_down . g(W_up . x): fp64 contractions, the activation and the
-    output each rounded to the stored dtype.  Rows in, rows out."""
+    output each rounded to the stored dtype.  Rows in, rows out.  For the
+    gated form (``act == "swiglu"``) W_up holds 2 d_ff rows, gate and up
+    interleaved, and g = silu(gate) * up."""
     z = x_rows64 @ Wup64.T
-    g = to_f64(round_act(gelu(z, act), dtype), dtype)
+    if act == "swiglu":
+        g = silu(z[:, 0::2]) * z[:, 1::2]
+    else:
+        g = gelu(z, act)
+    g = to_f64(round_act(g, dtype), dtype)
     return round_act(g @ Wdown64.T, dtype)
 
 
@@ -459,11 +485,15 @@ def row_norms(h: np.ndarray, dtype: str) -> np.ndarray:
 # ---------------------------------------------------------------------------
 # 10. combine (Sec. 4.1 output eq.)
 # ---------------------------------------------------------------------------
-def combine(w_t: np.ndarray, hhat: np.ndarray, dtype: str) -> np.ndarray:
-    """y = sum_p f32(w_p * hhat_p), accumulated in fp32 in branch order, then
-    rounded to the stored dtype.  w_t: (T, k); hhat: (T, k, d) stored."""
+def combine(w_t: np.ndarray, hhat: np.ndarray, dtype: str, shared=()) -> np.ndarray:
+    """y = sum_s h_s + sum_p f32(w_p * hhat_p), accumulated in fp32 (shared
+    experts first, in order, then the branches in order), then rounded to
+    the stored dtype.  w_t: (T, k); hhat: (T, k, d) stored; shared: stored
+    (T, d) outputs of the shared experts."""
     T, k = w_t.shape
     y = np.zeros((T, hhat.shape[-1]), dtype=F32)
+    for hs in shared:
+        y = (y + to_f32(hs, dtype)).astype(F32)
     for p in range(k):
         prod = (w_t[:, p, None] * to_f32(hhat[:, p, :], dtype)).astype(F32)
         y = (y + prod).astype(F32)
@@ -550,12 +580,17 @@ def step(dims: Dims, policy: Policy, W: Weights, state: State, x_t: np.ndarray,
     h_new = h_new.reshape(B, N, k, d)
     rec["h_new"] = h_new
 
+    # shared experts (Sec. 2.3 shared-expert eq.): every evaluated token
+    ev = evaluated
+    shared = [expert_ffn(x64[ev], W.shared_up64(s_), W.shared_down64(s_), policy.act, dt)
+              for s_ in range(dims.n_shared)]
+    rec["h_shared"] = shared
+
     # 10. combine: recomputed -> new feature, reused -> cached feature q(p)
     hc_q = np.take_along_axis(state.h_c, np.where(matched, q, 0)[..., None], axis=2)
     hhat = np.where(mask[..., None], h_new, hc_q)
-    ev = evaluated
     out = np.zeros((T, d), dtype=act_t)
-    out[ev] = combine(w_t.reshape(T, k)[ev], hhat.reshape(T, k, d)[ev], dt)
+    out[ev] = combine(w_t.reshape(T, k)[ev], hhat.reshape(T, k, d)[ev], dt, shared)
     out = out.reshape(B, N, d)
 
     # 11. cache write (not for the uncached comparator)
@@ -588,8 +623,8 @@ def step(dims: Dims, policy: Policy, W: Weights, state: State, x_t: np.ndarray,
 
 def uncached_layer(dims: Dims, W: Weights, x_t: np.ndarray, norm_topk: bool = True,
                    act: str = "gelu_tanh") -> np.ndarray:
-    """The plain routed MoE layer output sum_p w_p FFN_{e_p}(x) (Sec. 2.3),
-    i.e. a step in the uncached comparator mode."""
+    """The plain MoE layer output sum_s FFN_s(x) + sum_p w_p FFN_{e_p}(x)
+    (Sec. 2.3), i.e. a step in the uncached comparator mode."""
     pol = Policy(mode=MODE_FULL, norm_topk=norm_topk, act=act)
     out, _, _ = step(dims, pol, W, State(dims), x_t, 0)
     return out

@@ -62,6 +62,12 @@ class LayerShape:
     B: int          # samples in the batch
     N: int          # tokens per sample
     dtype: str = BF16
+    ffn: str = "gelu"   # "gelu" or "swiglu" (gated: 2 d_ff up-projection rows)
+    n_shared: int = 0   # always-on shared experts (same width as the routed ones)
+
+    @property
+    def up_rows(self) -> int:
+        return 2 * self.d_ff if self.ffn == "swiglu" else self.d_ff
 
     @property
     def tokens(self) -> int:
@@ -74,12 +80,16 @@ class LayerShape:
 
 # Named workloads.  "xl256" and "xl1024" are the DiT-MoE-XL-like layer at a
 # 32x32 and a 64x64 latent; "tiny" is the small fp32 parity layer; "skewed"
-# is the Zipf-biased stress layer.
+# is the Zipf-biased stress layer; "fine" the fine-grained layer with shared
+# experts.
 WORKLOADS = {
     "tiny": LayerShape(d=384, E=8, k=2, d_ff=1536, B=1, N=256, dtype=FP32),
     "xl256": LayerShape(d=1152, E=16, k=2, d_ff=4608, B=8, N=256, dtype=BF16),
     "xl1024": LayerShape(d=1152, E=16, k=2, d_ff=4608, B=8, N=1024, dtype=BF16),
     "skewed": LayerShape(d=3072, E=32, k=2, d_ff=8192, B=2, N=4096, dtype=BF16),
+    # fine-grained layer: 64 small SwiGLU experts, top-8, two shared experts
+    "fine": LayerShape(d=2048, E=64, k=8, d_ff=1408, B=4, N=4096, dtype=BF16, ffn="swiglu",
+                       n_shared=2),
 }
 
 
@@ -96,6 +106,7 @@ class Synth:
 
     def __init__(self, shape: LayerShape, seed: int = 0):
         self.shape = shape
+        self.seed = seed
         ss = np.random.SeedSequence(seed)
         kids = ss.spawn(6)
         self._rng_w = np.random.Generator(np.random.PCG64(kids[0]))
@@ -119,7 +130,7 @@ class Synth:
         std = 1.0 / math.sqrt(s.d)
         g = self._rng_w
         W_r = g.standard_normal((s.E, s.d), dtype=np.float32) * np.float32(std)
-        W_up = g.standard_normal((s.E, s.d_ff, s.d), dtype=np.float32) * np.float32(std)
+        W_up = g.standard_normal((s.E, s.up_rows, s.d), dtype=np.float32) * np.float32(std)
         W_down = g.standard_normal((s.E, s.d, s.d_ff), dtype=np.float32) * np.float32(std)
         b_r = None
         if router_bias == "zipf":
@@ -127,6 +138,19 @@ class Synth:
         elif router_bias is not None:
             raise ValueError(router_bias)
         return (_store(W_r, s.dtype), b_r, _store(W_up, s.dtype), _store(W_down, s.dtype))
+
+    def shared_weights(self):
+        """Shared-expert weights ``(W_up[S][up_rows][d], W_down[S][d][d_ff])``
+        ~N(0, 1/d) from their own stream, or None without shared experts.
+        With a gated FFN the up-projection rows alternate gate / up."""
+        s = self.shape
+        if s.n_shared == 0:
+            return None
+        g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([self.seed, 7919])))
+        std = np.float32(1.0 / math.sqrt(s.d))
+        up = g.standard_normal((s.n_shared, s.up_rows, s.d), dtype=np.float32) * std
+        down = g.standard_normal((s.n_shared, s.d, s.d_ff), dtype=np.float32) * std
+        return _store(up, s.dtype), _store(down, s.dtype)
 
     # ---- trajectory ----------------------------------------------------
     def drift_rates(self, kind: str = "loguniform") -> np.ndarray:

@@ -32,8 +32,10 @@ F32 = np.float32
 def build(shape: LayerShape, seed=0, bias=None):
     sy = Synth(shape, seed)
     W_r, b_r, W_up, W_down = sy.weights(bias)
-    dims = O.Dims(shape.d, shape.E, shape.k, shape.d_ff, shape.B, shape.N, shape.dtype)
-    return sy, dims, O.Weights(dims, W_r, b_r, W_up, W_down)
+    dims = O.Dims(shape.d, shape.E, shape.k, shape.d_ff, shape.B, shape.N, shape.dtype,
+                  shape.n_shared)
+    sh = sy.shared_weights() or (None, None)
+    return sy, dims, O.Weights(dims, W_r, b_r, W_up, W_down, *sh)
 
 
 def run_traj(dims, pol, W, xs, attn=None, t0=0):
@@ -50,6 +52,9 @@ def run_traj(dims, pol, W, xs, attn=None, t0=0):
 
 SMALL32 = LayerShape(d=64, E=4, k=2, d_ff=128, B=2, N=16, dtype="fp32")
 SMALL16 = LayerShape(d=64, E=6, k=2, d_ff=128, B=2, N=24, dtype="bf16")
+# fine-grained layers: gated (SwiGLU) experts plus ungated shared experts
+FINE32 = LayerShape(d=64, E=8, k=4, d_ff=48, B=2, N=16, dtype="fp32", ffn="swiglu", n_shared=2)
+FINE16 = LayerShape(d=64, E=8, k=4, d_ff=48, B=2, N=24, dtype="bf16", ffn="swiglu", n_shared=1)
 
 
 # ---------------------------------------------------------------------------
@@ -98,7 +103,17 @@ def test_default_policy_matches_paper_hyperparameters():
 # ---------------------------------------------------------------------------
 # uncached layer == library evaluation (Sec. 2.3 MoE eq.)
 # ---------------------------------------------------------------------------
-def _torch_moe(dims, W, x, norm_topk=True):
+def _torch_expert(X, up, dn, act):
+    F = torch.nn.functional
+    if act == "swiglu":
+        # the up-projection rows alternate gate / up
+        hid = F.silu(F.linear(X, up[0::2])) * F.linear(X, up[1::2])
+    else:
+        hid = F.gelu(F.linear(X, up), approximate="tanh")
+    return F.linear(hid, dn)
+
+
+def _torch_moe(dims, W, x, norm_topk=True, act="gelu_tanh"):
     dt = dims.dtype
     X = torch.from_numpy(O.to_f64(x, dt).reshape(-1, dims.d))
     Wr = torch.from_numpy(O.to_f64(W.W_r, dt))
@@ -114,10 +129,13 @@ def _torch_moe(dims, W, x, norm_topk=True):
     for e in range(dims.E):
         up = torch.from_numpy(O.to_f64(W.W_up[e], dt))
         dn = torch.from_numpy(O.to_f64(W.W_down[e], dt))
-        he = torch.nn.functional.linear(
-            torch.nn.functional.gelu(torch.nn.functional.linear(X, up), approximate="tanh"), dn)
+        he = _torch_expert(X, up, dn, act)
         ge = (g * (topi == e)).sum(dim=-1, keepdim=True)
         out = out + ge * he
+    for s_ in range(dims.n_shared):          # shared experts: no gate
+        up = torch.from_numpy(O.to_f64(W.W_sh_up[s_], dt))
+        dn = torch.from_numpy(O.to_f64(W.W_sh_down[s_], dt))
+        out = out + _torch_expert(X, up, dn, act)
     return out.numpy(), topi.numpy(), g.numpy()
 
 
@@ -142,6 +160,52 @@ def test_uncached_layer_bf16_close_to_unrounded_fp64():
     assert np.abs(out - ref).max() / np.abs(ref).max() < 2e-2
 
 
+def test_silu_closed_forms():
+    z = np.concatenate([np.linspace(-30, 30, 601), [0.0, 1e-300, -1e-300, 700.0, -700.0]])
+    got = O.silu(z)
+    assert np.allclose(got, torch.nn.functional.silu(torch.from_numpy(z)).numpy(),
+                       rtol=1e-15, atol=1e-300)
+    assert O.silu(np.array([0.0]))[0] == 0.0
+    # silu(-z) = silu(z) - z (sigmoid(-z) = 1 - sigmoid(z)); silu(z) -> z, -> 0
+    zz = np.linspace(-8, 8, 161)
+    assert np.allclose(O.silu(-zz), O.silu(zz) - zz, rtol=0, atol=1e-14)
+    assert abs(O.silu(np.array([50.0]))[0] - 50.0) < 1e-18 * 50 + 1e-12
+    assert abs(O.silu(np.array([-50.0]))[0]) < 1e-19
+
+
+@pytest.mark.parametrize("norm_topk", [True, False])
+def test_fine_layer_matches_torch_fp64(norm_topk):
+    """Gated experts and ungated shared experts (Sec. 2.3 shared-expert eq.)."""
+    sy, dims, W = build(FINE32, seed=31)
+    x = next(sy.trajectory(1))
+    out = O.uncached_layer(dims, W, x, norm_topk=norm_topk, act="swiglu")
+    ref, topi, _ = _torch_moe(dims, W, x, norm_topk, act="swiglu")
+    err = np.abs(out.reshape(-1, dims.d).astype(np.float64) - ref).max() / np.abs(ref).max()
+    assert err < 1e-6
+    # the shared experts carry weight: dropping them moves the output
+    d0 = O.Dims(dims.d, dims.E, dims.k, dims.d_ff, dims.B, dims.N, dims.dtype, 0)
+    routed = O.uncached_layer(d0, O.Weights(d0, W.W_r, W.b_r, W.W_up, W.W_down), x,
+                              norm_topk=norm_topk, act="swiglu")
+    assert np.abs(routed.reshape(-1, dims.d) - ref).max() > 100 * err * np.abs(ref).max()
+
+
+def test_shared_experts_with_gelu_match_torch_fp64():
+    shape = LayerShape(d=64, E=4, k=2, d_ff=96, B=1, N=24, dtype="fp32", n_shared=3)
+    sy, dims, W = build(shape, seed=32)
+    x = next(sy.trajectory(1))
+    out = O.uncached_layer(dims, W, x)
+    ref, _, _ = _torch_moe(dims, W, x)
+    assert np.abs(out.reshape(-1, dims.d) - ref).max() / np.abs(ref).max() < 1e-6
+
+
+def test_fine_layer_bf16_close_to_unrounded_fp64():
+    sy, dims, W = build(FINE16, seed=33)
+    x = next(sy.trajectory(1))
+    out = O.to_f64(O.uncached_layer(dims, W, x, act="swiglu"), "bf16").reshape(-1, dims.d)
+    ref, _, _ = _torch_moe(dims, W, x, act="swiglu")
+    assert np.abs(out - ref).max() / np.abs(ref).max() < 2e-2
+
+
 def test_router_bias_shifts_logits():
     shape = LayerShape(d=64, E=8, k=2, d_ff=64, B=1, N=32, dtype="fp32")
     sy, dims, W = build(shape, seed=5, bias="zipf")
@@ -155,23 +219,27 @@ def test_router_bias_shifts_logits():
 # ---------------------------------------------------------------------------
 # refresh ratio 100% == uncached; 0% == cached outputs
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("shape", [SMALL32, SMALL16])
+def _act(shape):
+    return "swiglu" if shape.ffn == "swiglu" else "gelu_tanh"
+
+
+@pytest.mark.parametrize("shape", [SMALL32, SMALL16, FINE32, FINE16])
 def test_ratio_one_reduces_to_uncached_layer(shape):
     sy, dims, W = build(shape, seed=6)
     xs = list(sy.trajectory(4))
-    pol = O.Policy(mode=O.MODE_RATIO, ratio=1.0, refresh_cycle=0)
+    pol = O.Policy(mode=O.MODE_RATIO, ratio=1.0, refresh_cycle=0, act=_act(shape))
     outs, recs, _, _ = run_traj(dims, pol, W, xs)
     for j in range(1, 4):
         assert not recs[j]["full"]
         assert recs[j]["mask"].all()
-        assert np.array_equal(outs[j], O.uncached_layer(dims, W, xs[j]))
+        assert np.array_equal(outs[j], O.uncached_layer(dims, W, xs[j], act=_act(shape)))
 
 
-@pytest.mark.parametrize("shape", [SMALL32, SMALL16])
+@pytest.mark.parametrize("shape", [SMALL32, SMALL16, FINE32, FINE16])
 def test_ratio_zero_returns_cached_outputs(shape):
     sy, dims, W = build(shape, seed=7)
     x0, x1 = list(sy.trajectory(2))
-    pol = O.Policy(mode=O.MODE_RATIO, ratio=0.0, refresh_cycle=0)
+    pol = O.Policy(mode=O.MODE_RATIO, ratio=0.0, refresh_cycle=0, act=_act(shape))
     st = O.State(dims)
     out0, st1, _ = O.step(dims, pol, W, st, x0, 0)
     # identical input: every branch matches, nothing is recomputed, output identical
@@ -508,9 +576,17 @@ def _bf_gelu(v):
     return 0.5 * v * (1.0 + math.tanh(math.sqrt(2.0 / math.pi) * (v + 0.044715 * v ** 3)))
 
 
-def _bf_ffn(xrow, Wu, Wd):
-    hid = [float(F32(_bf_gelu(math.fsum(float(a) * float(b) for a, b in zip(xrow, Wu[j])))))
-           for j in range(Wu.shape[0])]
+def _bf_silu(v):
+    return v / (1.0 + math.exp(-v))
+
+
+def _bf_ffn(xrow, Wu, Wd, act="gelu_tanh"):
+    dot = lambda w: math.fsum(float(a) * float(b) for a, b in zip(xrow, w))
+    if act == "swiglu":
+        hid = [float(F32(_bf_silu(dot(Wu[2 * j])) * dot(Wu[2 * j + 1])))
+               for j in range(Wu.shape[0] // 2)]
+    else:
+        hid = [float(F32(_bf_gelu(dot(Wu[j])))) for j in range(Wu.shape[0])]
     return [F32(math.fsum(a * float(b) for a, b in zip(hid, Wd[r]))) for r in range(Wd.shape[0])]
 
 
@@ -581,10 +657,13 @@ def _bf_step(dims, pol, W, st, x, t):
     for b in range(B):
         for i in range(N):
             acc = np.zeros(dims.d, F32)
+            for s_ in range(dims.n_shared):     # shared experts first, ungated
+                h = np.array(_bf_ffn(x[b, i], W.W_sh_up[s_], W.W_sh_down[s_], pol.act), F32)
+                acc = (acc + h).astype(F32)
             for p in range(k):
                 if mask[b, i, p]:
                     e = e_t[b, i, p]
-                    h = np.array(_bf_ffn(x[b, i], W.W_up[e], W.W_down[e]), F32)
+                    h = np.array(_bf_ffn(x[b, i], W.W_up[e], W.W_down[e], pol.act), F32)
                 else:
                     h = st.h_c[b, i, q[b, i, p]]
                 acc = (acc + (w_t[b, i, p] * h).astype(F32)).astype(F32)
@@ -592,12 +671,16 @@ def _bf_step(dims, pol, W, st, x, t):
     return dict(e_t=e_t, w_t=w_t, C=C, tau=tau, matched=matched, m=m, mask=mask, out=out)
 
 
-@pytest.mark.parametrize("mode", [O.MODE_THRESHOLD, O.MODE_RATIO])
-def test_brute_force_tiny(mode):
-    shape = LayerShape(d=8, E=4, k=2, d_ff=16, B=2, N=6, dtype="fp32")
+@pytest.mark.parametrize("mode,fine", [(O.MODE_THRESHOLD, False), (O.MODE_RATIO, False),
+                                       (O.MODE_THRESHOLD, True), (O.MODE_RATIO, True)])
+def test_brute_force_tiny(mode, fine):
+    if fine:
+        shape = LayerShape(d=8, E=5, k=3, d_ff=6, B=2, N=5, dtype="fp32", ffn="swiglu", n_shared=2)
+    else:
+        shape = LayerShape(d=8, E=4, k=2, d_ff=16, B=2, N=6, dtype="fp32")
     sy, dims, W = build(shape, seed=20)
     xs = list(sy.trajectory(4))
-    pol = O.Policy(mode=mode, ratio=0.3, tau0=0.8, refresh_cycle=0)
+    pol = O.Policy(mode=mode, ratio=0.3, tau0=0.8, refresh_cycle=0, act=_act(shape))
     st = O.State(dims)
     for t, x in enumerate(xs):
         before = st
@@ -638,6 +721,53 @@ def test_expert_ffn_bf16_brute_force_bit_exact():
         for c in range(16):
             v = math.fsum(a * b for a, b in zip(hid, Wd[c]))
             assert O.round_act(np.array([v]), "bf16")[0] == got[r, c]
+
+
+def test_swiglu_expert_bf16_brute_force_bit_exact():
+    """Gated expert: silu(gate) * up rounded once to bf16, gate and up rows
+    interleaved in the up-projection (Sec. 2.3 FFN_e, gated form)."""
+    shape = LayerShape(d=16, E=2, k=1, d_ff=12, B=1, N=6, dtype="bf16", ffn="swiglu")
+    sy, dims, W = build(shape, seed=25)
+    x = next(sy.trajectory(1)).reshape(-1, 16)
+    x64 = O.to_f64(x, "bf16")
+    Wu, Wd = O.to_f64(W.W_up[0], "bf16"), O.to_f64(W.W_down[0], "bf16")
+    assert Wu.shape == (24, 16)
+    got = O.expert_ffn(x64, W.up64(0), W.down64(0), "swiglu", "bf16")
+    for r in range(x.shape[0]):
+        hid = []
+        for j in range(12):
+            gt = math.fsum(x64[r] * Wu[2 * j])
+            up = math.fsum(x64[r] * Wu[2 * j + 1])
+            hid.append(O.to_f64(O.round_act(np.array([_bf_silu(gt) * up]), "bf16"), "bf16")[0])
+        for c in range(16):
+            v = math.fsum(a * b for a, b in zip(hid, Wd[c]))
+            assert O.round_act(np.array([v]), "bf16")[0] == got[r, c]
+
+
+def test_shared_experts_are_not_cached():
+    """A cache step with nothing recomputed still evaluates the shared
+    experts on the current input (they are never cached)."""
+    sy, dims, W = build(FINE32, seed=34)
+    x0, x1 = list(sy.trajectory(2))
+    pol = O.Policy(mode=O.MODE_RATIO, ratio=0.0, refresh_cycle=0, act="swiglu")
+    _, st1, _ = O.step(dims, pol, W, O.State(dims), x0, 0)
+    # expected: the shared rows of x1 first, then the (cached or new) routed rows
+    out, _, rec = O.step(dims, pol, W, st1, x1, 1)
+    T = dims.B * dims.N
+    x64 = O.to_f64(x1, "fp32").reshape(T, dims.d)
+    sh = [O.expert_ffn(x64, W.shared_up64(s_), W.shared_down64(s_), "swiglu", "fp32")
+          for s_ in range(dims.n_shared)]
+    for s_ in range(dims.n_shared):
+        assert np.array_equal(rec["h_shared"][s_], sh[s_])
+    q = np.where(rec["matched"], rec["q"], 0)
+    hc = np.take_along_axis(st1.h_c, q[..., None], axis=2)
+    hhat = np.where(rec["mask"][..., None], rec["h_new"], hc).reshape(T, dims.k, dims.d)
+    y = np.zeros((T, dims.d), F32)
+    for s_ in range(dims.n_shared):
+        y = y + sh[s_]
+    for p in range(dims.k):
+        y = y + (rec["w_t"].reshape(T, dims.k)[:, p, None] * hhat[:, p]).astype(F32)
+    assert np.array_equal(out.reshape(T, dims.d), y)
 
 
 def test_brute_force_cache_norms():
