@@ -50,7 +50,15 @@ enum {
                                K_b = floor(ratio * N * k + 0.5) branches     */
 };
 enum { MOECA_DTYPE_BF16 = 0, MOECA_DTYPE_FP32 = 1 };
-enum { MOECA_ACT_GELU_TANH = 0, MOECA_ACT_GELU_ERF = 1 };
+enum {
+  MOECA_ACT_GELU_TANH = 0, /* act(z) = 0.5 z (1 + tanh(sqrt(2/pi)(z + 0.044715 z^3)))   */
+  MOECA_ACT_GELU_ERF = 1,  /* act(z) = 0.5 z (1 + erf(z / sqrt 2))                      */
+  MOECA_ACT_SWIGLU = 2     /* gated expert: W_up has 2 d_ff rows, gate and up
+                              interleaved (row 2j is gate j, row 2j+1 up j), and
+                              the hidden value j is silu(gate_j) * up_j with
+                              silu(z) = z / (1 + exp(-z)); the product is rounded
+                              once to the activation dtype                     */
+};
 
 typedef struct moeca_policy {
   int32_t mode;          /* MOECA_MODE_*                                      */
@@ -67,12 +75,17 @@ typedef struct moeca_policy {
   int32_t dtype;         /* MOECA_DTYPE_*                                     */
   int32_t batch;         /* B, samples per step, >= 1                         */
   int32_t tokens;        /* N, tokens per sample, >= 1                         */
+  int32_t n_shared;      /* S, always-on shared experts (Sec. 2.3, shared-expert
+                            MoE eq.), 0..8; they have the routed experts' shape
+                            and activation, no gate, run on every token at
+                            every step and are never cached                   */
 } moeca_policy;
 
 /* Fill *p with the paper's settings: THRESHOLD mode, tau0 0.80, alpha 0.6,
  * beta 0.65 (Sec. 5.4, Tab. 4), refresh cycle 4 (Sec. 5.1), lambda1 =
  * lambda2 = 1 (not reported by the paper), ratio 0.3, bf16, tanh GELU,
- * renormalised top-k, batch 1, tokens 1.  NULL is ignored. */
+ * renormalised top-k, batch 1, tokens 1, no shared experts.  NULL is
+ * ignored. */
 void moeca_policy_default(moeca_policy* p);
 
 /* ---- layer handle ------------------------------------------------------ */
@@ -81,7 +94,8 @@ typedef struct moeca_layer moeca_layer;
 /* Create a layer of width d, E routed experts, top-k routing and expert
  * hidden width d_ff (FFN_e(x) = W_down[e] act(W_up[e] x), Sec. 2.3).
  * Host only; the policy is copied.  Limits: 1 <= k <= min(E, 8), E <= 64,
- * d and d_ff multiples of 64, d <= 16384, d_ff <= 65536, B*N*k < 2^31.
+ * 0 <= n_shared <= 8, d and d_ff multiples of 64, d <= 16384, d_ff <= 65536
+ * (32768 with MOECA_ACT_SWIGLU), B*N*(k + n_shared) < 2^31.
  * Returns NULL on a bad argument (moeca_last_error() says which). */
 moeca_layer* moeca_layer_create(int d, int E, int k, int d_ff, const moeca_policy* policy);
 
@@ -94,17 +108,27 @@ const char* moeca_last_error(void);
 /* Bind the weights (device, policy dtype, not copied):
  *   W_r    [E][d]        router (Sec. 4.1: B_i^t is its top-k)
  *   b_r    [E] fp32      optional router bias added to the logits, or NULL
- *   W_up   [E][d_ff][d]  expert up-projections  (out x in)
+ *   W_up   [E][U][d]     expert up-projections (out x in); U = d_ff, or
+ *                        2 d_ff with MOECA_ACT_SWIGLU (gate/up interleaved)
  *   W_down [E][d][d_ff]  expert down-projections (out x in)
  * Host only.  MOECA_E_INVAL if a required pointer is NULL or a weight
  * pointer is not 16-byte aligned (the bias 4-byte). */
 int moeca_layer_set_weights(moeca_layer* layer, const void* W_r, const float* b_r,
                             const void* W_up, const void* W_down);
 
+/* Bind the shared experts' weights (Sec. 2.3, shared-expert MoE eq.;
+ * device, policy dtype, not copied), required when n_shared > 0:
+ *   W_up_s   [S][U][d]     up-projections, U as for W_up
+ *   W_down_s [S][d][d_ff]  down-projections
+ * Their outputs are added to every token's output without a gate.  Host
+ * only.  MOECA_E_INVAL if the layer has no shared experts, a pointer is
+ * NULL or not 16-byte aligned. */
+int moeca_layer_set_shared(moeca_layer* layer, const void* W_up_s, const void* W_down_s);
+
 /* Bytes of device workspace the layer needs: the branch cache (ids, gate
  * weights, norms and rows of B*N*k branches), the EMA statistic [B][E][N],
  * and per-step scratch (routing, scores, masks, expert lists, the FFN
- * intermediate).  0 if layer is NULL. */
+ * intermediate, the shared experts' outputs).  0 if layer is NULL. */
 size_t moeca_workspace_bytes(const moeca_layer* layer);
 
 /* Bind caller-owned device memory of at least moeca_workspace_bytes() bytes,
@@ -126,6 +150,7 @@ int moeca_bind_attention(moeca_layer* layer, const void* attn_in, void* attn_cac
 /* One layer step at sampling step t (0-based).
  *   x_t [B][N][d]  device, policy dtype: the MoE layer input u of Sec. 2.3
  *   out [B][N][d]  device, policy dtype: y_i of Sec. 4.1 (the routed sum,
+ *                  plus the shared experts' outputs when n_shared > 0,
  *                  without the residual, which the caller adds)
  * The step is a full step when the cache is invalid, in FULL mode, or when
  * refresh_cycle > 0 and t % refresh_cycle == 0 (Sec. 4.1 / Sec. 5.1);
@@ -133,7 +158,8 @@ int moeca_bind_attention(moeca_layer* layer, const void* attn_in, void* attn_cac
  * waiting; it neither allocates nor synchronises.  Kernel faults surface at
  * the caller's next synchronisation.  x_t and out must not overlap the
  * workspace; both must be 16-byte aligned (else MOECA_E_INVAL).
- * MOECA_E_STATE if weights or workspace are unbound. */
+ * MOECA_E_STATE if the weights, the workspace or (n_shared > 0) the shared
+ * weights are unbound. */
 int moeca_step(moeca_layer* layer, const void* x_t, int t, void* out, void* stream);
 
 /* Enqueue a cache reset on the stream: every cached branch becomes empty,
@@ -174,7 +200,9 @@ enum {
   MOECA_BUF_MASK = 12,  /* uint8 [B*N*k]    1 = recomputed (p in R_i)         */
   MOECA_BUF_SIGMA = 13, /* int32 [B*N*k]    cache slot of branch p after step */
   MOECA_BUF_SYNC = 14,  /* uint8 [B*N]      S_i = [R_i non-empty]             */
-  MOECA_BUF_OFF = 15,   /* int32 [E+1]      per-expert offsets into LIST      */
+  MOECA_BUF_OFF = 15,   /* int32 [E+1]      per-expert offsets into LIST (the
+                           workspace keeps S more entries after it: the shared
+                           experts' row ranges in the FFN intermediate)      */
   MOECA_BUF_LIST = 16,  /* int32 [B*N*k]    recomputed flat branch ids
                            f = (b*N + i)*k + p, grouped by expert, ascending  */
   MOECA_BUF_POS = 17,   /* int32 [B*N*k]    index of f in LIST, -1 if reused  */
@@ -199,8 +227,10 @@ enum {
   MOECA_STAGE_SELECT = 2,  /* matching, branch scores, recomputation set,
                               slots, sync mask                                */
   MOECA_STAGE_LISTS = 3,   /* per-expert compaction                            */
-  MOECA_STAGE_FFN_UP = 4,  /* gathered up-projection + activation              */
-  MOECA_STAGE_FFN_DOWN = 5,/* down-projection into the cache rows              */
+  MOECA_STAGE_FFN_UP = 4,  /* gathered up-projection + activation (routed and
+                              shared experts in one grouped launch)           */
+  MOECA_STAGE_FFN_DOWN = 5,/* down-projection into the cache rows (shared
+                              experts: into their own output rows)            */
   MOECA_STAGE_COMBINE = 6, /* combine, norms, cache metadata, attention path   */
   MOECA_STAGE_COUNT = 7
 };

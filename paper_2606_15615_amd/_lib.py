@@ -17,7 +17,7 @@ MOECA_E_HIP = -3
 
 MOECA_MODE_FULL, MOECA_MODE_THRESHOLD, MOECA_MODE_RATIO = 0, 1, 2
 MOECA_DTYPE_BF16, MOECA_DTYPE_FP32 = 0, 1
-MOECA_ACT_GELU_TANH, MOECA_ACT_GELU_ERF = 0, 1
+MOECA_ACT_GELU_TANH, MOECA_ACT_GELU_ERF, MOECA_ACT_SWIGLU = 0, 1, 2
 
 BUF = {
     "e_c": 0, "w_c": 1, "n_c": 2, "h_c": 3, "stat": 4, "logits": 5, "e_t": 6, "w_t": 7,
@@ -33,7 +33,7 @@ class moeca_policy(ctypes.Structure):
         ("alpha", ctypes.c_float), ("beta", ctypes.c_float), ("lambda1", ctypes.c_float),
         ("lambda2", ctypes.c_float), ("refresh_cycle", ctypes.c_int32),
         ("norm_topk", ctypes.c_int32), ("act", ctypes.c_int32), ("dtype", ctypes.c_int32),
-        ("batch", ctypes.c_int32), ("tokens", ctypes.c_int32),
+        ("batch", ctypes.c_int32), ("tokens", ctypes.c_int32), ("n_shared", ctypes.c_int32),
     ]
 
 
@@ -55,6 +55,8 @@ _SIGS = {
     "moeca_last_error": (ctypes.c_char_p, []),
     "moeca_layer_set_weights": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p,
                                                ctypes.c_void_p, ctypes.c_void_p]),
+    "moeca_layer_set_shared": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p,
+                                              ctypes.c_void_p]),
     "moeca_workspace_bytes": (ctypes.c_size_t, [ctypes.c_void_p]),
     "moeca_bind_workspace": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_size_t]),
     "moeca_bind_attention": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
@@ -126,6 +128,10 @@ def moeca_last_error() -> str:
 
 def moeca_layer_set_weights(h, W_r, b_r, W_up, W_down) -> int:
     return _check(load().moeca_layer_set_weights(h, W_r, b_r, W_up, W_down))
+
+
+def moeca_layer_set_shared(h, W_up_s, W_down_s) -> int:
+    return _check(load().moeca_layer_set_shared(h, W_up_s, W_down_s))
 
 
 def moeca_workspace_bytes(h) -> int:

@@ -1,9 +1,11 @@
 // Combine, cache metadata and attention-path refresh (Sec. 4.1).
 //
-//   y_i = sum_p f32(w_p * hhat_p), accumulated in fp32 in branch order, where
-//   hhat_p is the cache row in slot sigma(p): the row the down projection
-//   just wrote for a recomputed branch, the untouched cached row h_{q(p)} for
-//   a reused one (reused branches use the current gate weight).
+//   y_i = sum_s h_s + sum_p f32(w_p * hhat_p), accumulated in fp32, shared
+//   experts first (Sec. 2.3, shared-expert MoE eq.; no gate), then the
+//   branches in order, where hhat_p is the cache row in slot sigma(p): the
+//   row the down projection just wrote for a recomputed branch, the
+//   untouched cached row h_{q(p)} for a reused one (reused branches use the
+//   current gate weight).
 //   For each recomputed branch the slot's metadata becomes (e_p, w_p,
 //   ||h||), the norm an fp64 sum of squares of the stored row rounded once.
 //   Tokens with a recomputed branch copy their attention-path feature into
@@ -68,8 +70,8 @@ __global__ __launch_bounds__(kCombWaves * kWave) void combine_kernel(
     const int32_t* __restrict__ sigma, const uint8_t* __restrict__ mask,
     const uint8_t* __restrict__ sync, T* __restrict__ h_c, int32_t* __restrict__ e_c,
     float* __restrict__ w_c, float* __restrict__ n_c, T* __restrict__ out,
-    const T* __restrict__ attn_in, T* __restrict__ attn_cache, int64_t T_tokens, int d, int k,
-    int write_cache) {
+    const T* __restrict__ attn_in, T* __restrict__ attn_cache, const T* __restrict__ h_sh,
+    int S, int64_t T_tokens, int d, int k, int write_cache) {
   const int lane = threadIdx.x & (kWave - 1);
   const int64_t t = int64_t(blockIdx.x) * kCombWaves + threadIdx.x / kWave;
   if (t >= T_tokens) return;
@@ -91,6 +93,12 @@ __global__ __launch_bounds__(kCombWaves * kWave) void combine_kernel(
     float acc[8];
 #pragma unroll
     for (int u = 0; u < 8; ++u) acc[u] = 0.0f;
+    for (int sh = 0; sh < S; ++sh) {
+      float h[8];
+      Vec8<T>::load(h_sh + (sh * T_tokens + t) * d + g * 8, h);
+#pragma unroll
+      for (int u = 0; u < 8; ++u) acc[u] = __fadd_rn(acc[u], h[u]);
+    }
     for (int p = 0; p < k; ++p) {
       float h[8];
       Vec8<T>::load(h_c + (t * k + slot[p]) * d + g * 8, h);
@@ -121,11 +129,12 @@ __global__ __launch_bounds__(kCombWaves * kWave) void combine_kernel(
   }
 }
 
-// Fast path for k <= 2 and d <= 512 GI: the token index is wave-uniform, so
-// the branch metadata comes in by scalar loads; then every row load of the
-// token (its k cache rows and, when synchronised, its attention row) is
-// issued before any is used, so a token costs two dependent memory round
-// trips.  Same arithmetic as above.
+// Fast path for k <= 2, d <= 512 GI and no shared experts (h_sh and S are
+// not read): the token index is wave-uniform, so the branch metadata comes
+// in by scalar loads; then every row load of the token (its k cache rows
+// and, when synchronised, its attention row) is issued before any is used,
+// so a token costs two dependent memory round trips.  Same arithmetic as
+// above.
 template <typename T> struct Raw8;
 template <> struct Raw8<uint16_t> {
   typedef __attribute__((ext_vector_type(4))) unsigned int v;
@@ -172,8 +181,8 @@ __global__ __launch_bounds__(kCombWaves * kWave) void combine_fast_kernel(
     const int32_t* __restrict__ sigma, const uint8_t* __restrict__ mask,
     const uint8_t* __restrict__ sync, T* __restrict__ h_c, int32_t* __restrict__ e_c,
     float* __restrict__ w_c, float* __restrict__ n_c, T* __restrict__ out,
-    const T* __restrict__ attn_in, T* __restrict__ attn_cache, int64_t T_tokens, int d, int k,
-    int write_cache) {
+    const T* __restrict__ attn_in, T* __restrict__ attn_cache, const T* __restrict__ h_sh,
+    int S, int64_t T_tokens, int d, int k, int write_cache) {
   typedef typename Raw8<T>::v raw;
   const int lane = threadIdx.x & (kWave - 1);
   const int t = __builtin_amdgcn_readfirstlane(
@@ -261,10 +270,10 @@ hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void
 #define MOECA_COMBINE(KER, TT)                                                                 \
   launch_kernel(&KER, grid, block, 0, st, b.w_t, b.e_t, b.sigma, b.mask, b.sync,               \
                 static_cast<TT*>(b.h_c), b.e_c, b.w_c, b.n_c, static_cast<TT*>(out),           \
-                static_cast<const TT*>(attn_in), static_cast<TT*>(attn_cache), s.tokens(), s.d,  \
-                s.k, write_cache)
+                static_cast<const TT*>(attn_in), static_cast<TT*>(attn_cache),                 \
+                static_cast<const TT*>(b.h_sh), s.S, s.tokens(), s.d, s.k, write_cache)
   const int gi = (s.d / 8 + kWave - 1) / kWave;  // 8-element groups per lane
-  const bool fast = s.k <= 2 && gi <= 4 && s.tokens() < (int64_t(1) << 31);
+  const bool fast = s.k <= 2 && gi <= 4 && s.S == 0 && s.tokens() < (int64_t(1) << 31);
 #define MOECA_FAST(TT, KK)                                                           \
   switch (gi) {                                                                      \
     case 1: MOECA_COMBINE((combine_fast_kernel<TT, KK, 1>), TT); break;              \

@@ -373,10 +373,27 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
 // branch knows its place: branches of earlier r, then of earlier waves, then
 // of lower lanes come first (stable, no atomics).
 // ---------------------------------------------------------------------------
+// Group table entries E..E+S: the shared experts (Sec. 2.3, shared-expert
+// MoE eq.) follow the routed ones in the FFN's grouped GEMM, T rows each (every
+// token, in token order), so their offsets and tile prefixes continue the
+// routed totals (o rows, tu / td tiles).  Tile tables: up at [0, E+S],
+// down at [E+S+1, 2(E+S)+1].
+__device__ __forceinline__ void write_shared_groups(int32_t* __restrict__ off,
+                                                    int32_t* __restrict__ tiles, int E, int S,
+                                                    int T, int tm, int nt_up, int nt_down, int o,
+                                                    int tu, int td) {
+  const int mts = (T + tm - 1) / tm;
+  for (int s2 = 0; s2 <= S; ++s2) {
+    off[E + s2] = o + s2 * T;
+    tiles[E + s2] = tu + s2 * mts * nt_up;
+    tiles[E + S + 1 + E + s2] = td + s2 * mts * nt_down;
+  }
+}
+
 template <int R>
 __global__ __launch_bounds__(kSelThreads) void lists_kernel(
     const uint8_t* __restrict__ mask, const int32_t* __restrict__ e_t,
-    const int32_t* __restrict__ cnt_bs, int B, int N, int E, int k, int tm, int nt_up,
+    const int32_t* __restrict__ cnt_bs, int B, int N, int E, int S, int k, int tm, int nt_up,
     int nt_down, const int32_t* __restrict__ sigma, int32_t* __restrict__ off,
     int32_t* __restrict__ tiles, int32_t* __restrict__ list, int32_t* __restrict__ pos,
     int32_t* __restrict__ row_dst) {
@@ -428,15 +445,12 @@ __global__ __launch_bounds__(kSelThreads) void lists_kernel(
     }
     if (lane < E) s_base[lane] = o - tot + below;
     if (b == 0 && lane < E) {
-      // exclusive prefixes per expert; the last expert also writes the totals
+      // exclusive prefixes per expert; the last expert also writes the
+      // prefixes of the shared experts and the totals
       off[lane] = o - tot;
       tiles[lane] = tu - mt * nt_up;
-      tiles[E + 1 + lane] = td - mt * nt_down;
-      if (lane == E - 1) {
-        off[E] = o;
-        tiles[E] = tu;
-        tiles[2 * E + 1] = td;
-      }
+      tiles[E + S + 1 + lane] = td - mt * nt_down;
+      if (lane == E - 1) write_shared_groups(off, tiles, E, S, B * N, tm, nt_up, nt_down, o, tu, td);
     }
   }
   int rk[R];
@@ -482,7 +496,7 @@ __global__ __launch_bounds__(kSelThreads) void lists_kernel(
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kSelThreads) void lists_chunked_kernel(
     const uint8_t* __restrict__ mask, const int32_t* __restrict__ e_t,
-    const int32_t* __restrict__ cnt_bs, int B, int N, int E, int k, int tm, int nt_up,
+    const int32_t* __restrict__ cnt_bs, int B, int N, int E, int S, int k, int tm, int nt_up,
     int nt_down, const int32_t* __restrict__ sigma, int32_t* __restrict__ off,
     int32_t* __restrict__ tiles, int32_t* __restrict__ list, int32_t* __restrict__ pos,
     int32_t* __restrict__ row_dst) {
@@ -515,7 +529,7 @@ __global__ __launch_bounds__(kSelThreads) void lists_chunked_kernel(
       if (b == 0) {
         off[e] = acc;
         tiles[e] = tu;
-        tiles[E + 1 + e] = td;
+        tiles[E + S + 1 + e] = td;
       }
       s_base[e] += acc;
       s_run[e] = 0;
@@ -524,11 +538,7 @@ __global__ __launch_bounds__(kSelThreads) void lists_chunked_kernel(
       tu += mt * nt_up;
       td += mt * nt_down;
     }
-    if (b == 0) {
-      off[E] = acc;
-      tiles[E] = tu;
-      tiles[2 * E + 1] = td;
-    }
+    if (b == 0) write_shared_groups(off, tiles, E, S, B * N, tm, nt_up, nt_down, acc, tu, td);
   }
   __syncthreads();
 
@@ -614,12 +624,12 @@ hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1
 
 hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st) {
   const int nb = s.N * s.k;
-  const int nt_up = (s.d_ff + plan.tn_up - 1) / plan.tn_up;
+  const int nt_up = (s.up_rows() + plan.tn_up - 1) / plan.tn_up;
   const int nt_down = (s.d + plan.tn_down - 1) / plan.tn_down;
 #define MOECA_LISTS(KER)                                                                       \
   launch_kernel(&KER, dim3(s.B), dim3(kSelThreads), 0, st, b.mask, b.e_t, b.cnt_bs, s.B, s.N, \
-                s.E, s.k, plan.tm, nt_up, nt_down, b.sigma, b.off, b.tiles, b.list, b.pos,    \
-                b.row_dst)
+                s.E, s.S, s.k, plan.tm, nt_up, nt_down, b.sigma, b.off, b.tiles, b.list,      \
+                b.pos, b.row_dst)
   if (nb <= 2 * kSelThreads) {
     MOECA_LISTS(lists_kernel<2>);
   } else if (nb <= 8 * kSelThreads) {

@@ -13,6 +13,14 @@
 // slot it will occupy: reused slots are never touched, so the combine reads
 // every branch feature from the cache.
 //
+// Shared experts (Sec. 2.3, shared-expert MoE eq.) are S more groups of the
+// same grouped GEMM, after the E routed ones: group E+s has every token as
+// its rows (in token order), its own weights, and its down projection writes
+// h_sh[s][token].  With the gated activation (SwiGLU) the up-projection rows
+// alternate gate / up, so a lane's four consecutive accumulator columns hold
+// two (gate, up) pairs and the epilogue emits silu(gate) * up for both:
+// the intermediate is d_ff wide for either activation.
+//
 // bf16 path: v_mfma_f32_32x32x16_bf16 with fp32 accumulation; 256 threads
 // as 2x2 waves, block tile TM x TN, k-tile 64, LDS double buffered with
 // padded rows; the activation is applied to the fp32 accumulator and the
@@ -22,6 +30,7 @@
 // XCD's L2.
 #include "common.h"
 #include "internal.h"
+#include "moeca.h"
 
 namespace moeca {
 namespace {
@@ -37,8 +46,14 @@ constexpr int kXcds = 8;
 // Activation of the up projection.  tanh GELU:
 //   0.5 z (1 + tanh(u)) = z / (1 + exp(-2u)),  u = sqrt(2/pi) (z + 0.044715 z^3),
 // with exp(-2u) = 2^(-2u log2 e) from the hardware exp2 (about 1 ulp) and a
-// hardware reciprocal; the erf form uses erff.
-enum { kActGeluTanh = 0, kActGeluErf = 1, kActNone = 2 };
+// hardware reciprocal; the erf form uses erff.  kActSwiglu marks the gated
+// epilogue (silu below), which pairs columns instead of mapping each one.
+enum { kActGeluTanh = 0, kActGeluErf = 1, kActNone = 2, kActSwiglu = 3 };
+
+// silu(z) = z / (1 + exp(-z)), exp(-z) = 2^(-z log2 e) by the hardware exp2.
+__device__ __forceinline__ float silu_f(float z) {
+  return z * __builtin_amdgcn_rcpf(1.0f + __builtin_amdgcn_exp2f(-1.4426950408889634f * z));
+}
 
 template <int ACT>
 __device__ __forceinline__ float act_fn(float z) {
@@ -56,12 +71,12 @@ struct Tile {
   int e, r0, rows, n0;
 };
 
-// Logical tile L -> (expert, first row, row count, first column); e = -1 if
-// this block has no tile.  Tiles per expert: ceil(cnt_e / TM) * NT.
+// Logical tile L -> (group, first row, row count, first column); e = -1 if
+// this block has no tile.  Tiles per group: ceil(cnt_e / TM) * NT.
 template <int TM>
-__device__ Tile decode_tile(const int32_t* __restrict__ off, int E, int NT) {
+__device__ Tile decode_tile(const int32_t* __restrict__ off, int G, int NT) {
   int total = 0;
-  for (int e = 0; e < E; ++e) total += ((off[e + 1] - off[e] + TM - 1) / TM) * NT;
+  for (int e = 0; e < G; ++e) total += ((off[e + 1] - off[e] + TM - 1) / TM) * NT;
   const int per = (total + kXcds - 1) / kXcds;
   const int xcd = blockIdx.x % kXcds;
   const int slot = blockIdx.x / kXcds;
@@ -69,7 +84,7 @@ __device__ Tile decode_tile(const int32_t* __restrict__ off, int E, int NT) {
   Tile t{-1, 0, 0, 0};
   if (slot >= per || L >= total) return t;
   int acc = 0;
-  for (int e = 0; e < E; ++e) {
+  for (int e = 0; e < G; ++e) {
     const int cnt = off[e + 1] - off[e];
     const int mt = (cnt + TM - 1) / TM;
     const int tiles = mt * NT;
@@ -85,6 +100,51 @@ __device__ Tile decode_tile(const int32_t* __restrict__ off, int E, int NT) {
     acc += tiles;
   }
   return t;
+}
+
+// Group of logical tile L: the number of group tile prefixes <= L, minus
+// one, from two ballots (groups 0-63 in toff0, 64-127 in toff1: lane l holds
+// the prefixes of groups l and 64 + l, INT_MAX past the last group); also
+// returns the group's first tile.
+__device__ __forceinline__ int tile_group(int L, int toff0, int toff1, int& first) {
+  const int n0 = __popcll(__ballot(toff0 <= L));
+  const int n1 = __popcll(__ballot(toff1 <= L));
+  const int e = n0 + n1 - 1;
+  first = e < 64 ? __shfl(toff0, e, 64) : __shfl(toff1, e - 64, 64);
+  return e;
+}
+
+// Row table entry r of a tile of group e (first list row r0, `rows` rows):
+// the A-operand source row and the output row (-1: padding, never stored;
+// padding rows re-read the tile's first row).  Routed groups (e < E): up
+// reads token list[r]/k and writes intermediate row r; down reads
+// intermediate row r and writes cache row row_dst[r].  Shared groups: up
+// reads token r - off[e] and writes intermediate row r; down reads
+// intermediate row r and writes shared-output row r - off[E].
+template <int KIND>
+__device__ __forceinline__ void group_row(int e, int E, int r0, int rows, int r, int k,
+                                          const int32_t* __restrict__ off,
+                                          const int32_t* __restrict__ list,
+                                          const int32_t* __restrict__ row_dst, int& src,
+                                          int& dst) {
+  const int rr = r < rows ? r : 0;
+  if (e < E) {
+    if (KIND == kUp) {
+      src = list[r0 + rr] / k;
+      dst = r < rows ? r0 + r : -1;
+    } else {
+      src = r0 + rr;
+      dst = r < rows ? row_dst[r0 + r] : -1;
+    }
+  } else {
+    if (KIND == kUp) {
+      src = r0 + rr - off[e];
+      dst = r < rows ? r0 + r : -1;
+    } else {
+      src = r0 + rr;
+      dst = r < rows ? r0 + r - off[E] : -1;
+    }
+  }
 }
 
 // ---------------------------------------------------------------------------
@@ -153,13 +213,16 @@ __device__ __forceinline__ void mfma_ktile(f32x16_t (&acc)[FM][FN], const uint16
 template <int TM, int TN, int KIND, int ACT>
 __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
-    const int32_t* __restrict__ off, const int32_t* __restrict__ tile_off,
-    const int32_t* __restrict__ list, const int32_t* __restrict__ sigma, int E, int k, int K,
-    int Nout, uint16_t* __restrict__ dst) {
+    const uint16_t* __restrict__ Wsh, const int32_t* __restrict__ off,
+    const int32_t* __restrict__ tile_off, const int32_t* __restrict__ list,
+    const int32_t* __restrict__ row_dst, int E, int G, int k, int K, int Nout,
+    uint16_t* __restrict__ dst, uint16_t* __restrict__ dst_sh) {
   constexpr int WM = TM / 2, WN = TN / 2;  // wave tile (2 x 2 waves)
   constexpr int FM = WM / 32, FN = WN / 32;
   constexpr int LA = TM / 32, LB = TN / 32;  // 16-byte loads per thread per k-tile
   constexpr int CROW = TN + 8;               // epilogue LDS row (bf16 elements)
+  constexpr bool kGated = ACT == kActSwiglu;
+  constexpr int OTN = kGated ? TN / 2 : TN;  // output columns per tile
   static_assert(TM * CROW <= 2 * TM * kLdsRow, "epilogue tile must fit in As");
   __shared__ __attribute__((aligned(16))) uint16_t As[2 * TM * kLdsRow];
   __shared__ __attribute__((aligned(16))) uint16_t Bs[2 * TN * kLdsRow];
@@ -170,13 +233,14 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(
   const int lane = tid & 63;
   const int wv = tid >> 6;
   const int wm = wv >> 1, wn = wv & 1;
-  const int NT = Nout / TN;
-  const int total = tile_off[E];
+  const int total = tile_off[G];
   const int per = (total + kXcds - 1) / kXcds;
   const int lo = (blockIdx.x % kXcds) * per;
   const int hi = min(total, lo + per);
   const int stride = gridDim.x / kXcds;
-  const int my_toff = lane < E ? tile_off[lane] : 0x7fffffff;
+  const int toff0 = lane < G ? tile_off[lane] : 0x7fffffff;
+  const int toff1 = lane + 64 < G ? tile_off[lane + 64] : 0x7fffffff;
+  const int Nw = kGated ? Nout / 2 : Nout;  // output row width
 
   const int lrow = tid >> 3;       // 0..31
   const int lcol = (tid & 7) * 8;  // element offset of this thread's 16 bytes
@@ -185,8 +249,8 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(
   const int KT = K / kTK;
 
   for (int L = lo + static_cast<int>(blockIdx.x) / kXcds; L < hi; L += stride) {
-    const int e = __popcll(__ballot(my_toff <= L)) - 1;
-    const int e_base = __shfl(my_toff, e, 64);
+    int e_base;
+    const int e = tile_group(L, toff0, toff1, e_base);
     const int o0 = off[e];
     const int cnt = off[e + 1] - o0;
     const int mt = (cnt + TM - 1) / TM;
@@ -195,19 +259,11 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(
     const int r0 = o0 + m * TM;
     const int rows = min(TM, cnt - m * TM);
     const int n0 = (local / mt) * TN;
-    (void)NT;
+    const uint16_t* Wg = e < E ? W + int64_t(e) * Nout * K : Wsh + int64_t(e - E) * Nout * K;
+    uint16_t* const og = e < E ? dst : dst_sh;
 
-    for (int r = tid; r < TM; r += kGemmThreads) {
-      const int rr = r < rows ? r : 0;  // padding rows re-read row 0, never stored
-      const int f = list[r0 + rr];
-      if (KIND == kUp) {
-        s_src[r] = f / k;
-        s_dst[r] = r < rows ? r0 + r : -1;
-      } else {
-        s_src[r] = r0 + rr;
-        s_dst[r] = r < rows ? (f / k) * k + sigma[f] : -1;
-      }
-    }
+    for (int r = tid; r < TM; r += kGemmThreads)
+      group_row<KIND>(e, E, r0, rows, r, k, off, list, row_dst, s_src[r], s_dst[r]);
     __syncthreads();
 
     const uint16_t* a_ptr[LA];
@@ -215,8 +271,7 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(
 #pragma unroll
     for (int i = 0; i < LA; ++i) a_ptr[i] = A + int64_t(s_src[lrow + 32 * i]) * K + lcol;
 #pragma unroll
-    for (int i = 0; i < LB; ++i)
-      b_ptr[i] = W + (int64_t(e) * Nout + n0 + lrow + 32 * i) * K + lcol;
+    for (int i = 0; i < LB; ++i) b_ptr[i] = Wg + int64_t(n0 + lrow + 32 * i) * K + lcol;
 
     f32x16_t acc[FM][FN];
 #pragma unroll
@@ -258,7 +313,8 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(
 
     // epilogue: activation, bf16, through LDS (reusing As), 16-byte stores.
     // D layout of a 32x32 MFMA tile: lane holds column (lane & 31) and rows
-    // 8*(r/4) + 4*(lane/32) + (r%4) for r = 0..15.
+    // 8*(r/4) + 4*(lane/32) + (r%4) for r = 0..15.  Gated: the (gate, up)
+    // pair of an output column sits in lanes 2c and 2c+1.
     uint16_t* cs = As;
 #pragma unroll
     for (int i = 0; i < FM; ++i)
@@ -268,18 +324,23 @@ __global__ __launch_bounds__(kGemmThreads, 2) void gemm_bf16_kernel(
         for (int r = 0; r < 16; ++r) {
           const int mr = wm * WM + i * 32 + 8 * (r >> 2) + 4 * (lane >> 5) + (r & 3);
           const int nc = wn * WN + j * 32 + (lane & 31);
-          float v = acc[i][j][r];
-          v = act_fn<ACT>(v);
-          cs[mr * CROW + nc] = f32_to_bf16(v);
+          const float v = acc[i][j][r];
+          if constexpr (kGated) {
+            const float up = __shfl_xor(v, 1, kWave);
+            if ((lane & 1) == 0) cs[mr * CROW + (nc >> 1)] = f32_to_bf16(silu_f(v) * up);
+          } else {
+            cs[mr * CROW + nc] = f32_to_bf16(act_fn<ACT>(v));
+          }
         }
     __syncthreads();
-    constexpr int CPR = TN / 8;  // 16-byte chunks per row
+    constexpr int CPR = OTN / 8;  // 16-byte chunks per row
+    const int on0 = kGated ? n0 / 2 : n0;
     for (int c = tid; c < TM * CPR; c += kGemmThreads) {
       const int mr = c / CPR;
       const int cc = (c % CPR) * 8;
       const int drow = s_dst[mr];
       if (drow >= 0)
-        *reinterpret_cast<u32x4_t*>(dst + int64_t(drow) * Nout + n0 + cc) =
+        *reinterpret_cast<u32x4_t*>(og + int64_t(drow) * Nw + on0 + cc) =
             *reinterpret_cast<const u32x4_t*>(&cs[mr * CROW + cc]);
     }
     __syncthreads();
@@ -416,16 +477,17 @@ __device__ __forceinline__ u32x2_t pack4_bf16(float a, float b, float c, float d
   return u32x2_t{__builtin_bit_cast(uint32_t, lo), __builtin_bit_cast(uint32_t, hi)};
 }
 
-// One tile of the persistent walk: expert, first list row, rows, first
+// One tile of the persistent walk: group, first list row, rows, first
 // output column.
 struct BigTile {
   int e, r0, rows, n0;
 };
 
-__device__ __forceinline__ BigTile big_tile(int L, int my_toff, const int32_t* __restrict__ off) {
+__device__ __forceinline__ BigTile big_tile(int L, int toff0, int toff1,
+                                            const int32_t* __restrict__ off) {
   BigTile t;
-  t.e = __popcll(__ballot(my_toff <= L)) - 1;
-  const int e_base = __shfl(my_toff, t.e, 64);
+  int e_base;
+  t.e = tile_group(L, toff0, toff1, e_base);
   const int o0 = off[t.e];
   const int cnt = off[t.e + 1] - o0;
   const int mt = (cnt + kBigTM - 1) / kBigTM;
@@ -437,30 +499,20 @@ __device__ __forceinline__ BigTile big_tile(int L, int my_toff, const int32_t* _
   return t;
 }
 
-// Row table entry r of a tile: the source row of the A operand and the
-// destination row of the output (-1: padding, never stored).
-template <int KIND>
-__device__ __forceinline__ void big_rows(const BigTile& t, int r, int k,
-                                         const int32_t* __restrict__ list,
-                                         const int32_t* __restrict__ row_dst, int& src,
-                                         int& dst) {
-  const int rr = r < t.rows ? r : 0;  // padding rows re-read row 0
-  if (KIND == kUp) {
-    src = list[t.r0 + rr] / k;
-    dst = r < t.rows ? t.r0 + r : -1;
-  } else {
-    src = t.r0 + rr;
-    dst = r < t.rows ? row_dst[t.r0 + r] : -1;
-  }
+// Two fp32 -> two bf16 (hardware round to nearest even), packed in 4 bytes.
+__device__ __forceinline__ uint32_t pack2_bf16(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
 }
 
 template <int KIND, int ACT>
 __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
     const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
-    const int32_t* __restrict__ off, const int32_t* __restrict__ tile_off,
-    const int32_t* __restrict__ list, const int32_t* __restrict__ row_dst, int E, int k, int K,
-    int Nout, uint16_t* __restrict__ dst) {
+    const uint16_t* __restrict__ Wsh, const int32_t* __restrict__ off,
+    const int32_t* __restrict__ tile_off, const int32_t* __restrict__ list,
+    const int32_t* __restrict__ row_dst, int E, int G, int k, int K, int Nout,
+    uint16_t* __restrict__ dst, uint16_t* __restrict__ dst_sh) {
   constexpr int TM = kBigTM, TN = kBigTN;
+  constexpr bool kGated = ACT == kActSwiglu;
   constexpr int FM = 2, FN = 2;  // wave tile: 64 rows x 64 columns
   constexpr int WN = TN / (FN * 32);  // waves along N
   static_assert(kBigWaves == (TM / (FM * 32)) * WN, "wave grid must cover the tile");
@@ -472,13 +524,15 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
   const int lane = tid & 63;
   const int wv = tid >> 6;
   const int wm = wv / WN, wn = wv % WN;
-  const int total = tile_off[E];
+  const int total = tile_off[G];
   const int per = (total + kXcds - 1) / kXcds;
   const int lo = (blockIdx.x % kXcds) * per;
   const int hi = min(total, lo + per);
   const int stride = gridDim.x / kXcds;
-  const int my_toff = lane < E ? tile_off[lane] : 0x7fffffff;
+  const int toff0 = lane < G ? tile_off[lane] : 0x7fffffff;
+  const int toff1 = lane + 64 < G ? tile_off[lane + 64] : 0x7fffffff;
   const int KT = K / kTK;
+  const int Nw = kGated ? Nout / 2 : Nout;  // output row width
   // Logical chunk this lane fetches.  DMA instruction i covers rows 8i..8i+7
   // (lane l: row 8i + l/8, stored position l & 7); the stored position is
   // chunk ^ ((row >> 1) & 7) = chunk ^ (4 (i & 1) + l / 16), and
@@ -500,11 +554,12 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
       const int r = 8 * (wv + kBigWaves * u) + (lane >> 3);
       ga[u] = A + int64_t(s_src[r]) * K + chunk * 8;
     }
+    const uint16_t* Wg = t.e < E ? W + int64_t(t.e) * Nout * K : Wsh + int64_t(t.e - E) * Nout * K;
 #pragma unroll
     for (int u = 0; u < kLoadsB; ++u) {
       const int r = 8 * (wv + kBigWaves * u) + (lane >> 3);
       const int n = min(t.n0 + r, Nout - 1);
-      gb[u] = W + (int64_t(t.e) * Nout + n) * K + chunk * 8;
+      gb[u] = Wg + int64_t(n) * K + chunk * 8;
     }
   };
   auto issue = [&](int kt, int st) __attribute__((always_inline)) {
@@ -518,10 +573,10 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
 
   int L = lo + static_cast<int>(blockIdx.x) / kXcds;
   if (L >= hi) return;
-  BigTile cur = big_tile(L, my_toff, off);
+  BigTile cur = big_tile(L, toff0, toff1, off);
   {
     int src = 0, dstr = -1;
-    if (tid < TM) big_rows<KIND>(cur, tid, k, list, row_dst, src, dstr);
+    if (tid < TM) group_row<KIND>(cur.e, E, cur.r0, cur.rows, tid, k, off, list, row_dst, src, dstr);
     start_tile(cur, src, dstr);
   }
   issue(0, 0);
@@ -535,8 +590,9 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
     BigTile nxt = cur;
     int nsrc = 0, ndst = -1;
     if (has_next) {
-      nxt = big_tile(Ln, my_toff, off);
-      if (tid < TM) big_rows<KIND>(nxt, tid, k, list, row_dst, nsrc, ndst);
+      nxt = big_tile(Ln, toff0, toff1, off);
+      if (tid < TM)
+        group_row<KIND>(nxt.e, E, nxt.r0, nxt.rows, tid, k, off, list, row_dst, nsrc, ndst);
     }
 
     f32x16_t acc[FN][FM];
@@ -579,20 +635,27 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
 
     // epilogue: lane holds columns 8*(r/4) + 4*(lane/32) + (r%4) of row
     // (lane & 31) in each 32 x 32 tile; activation, bf16, 8-byte stores
+    // (gated: two (gate, up) pairs -> two outputs, 4-byte stores)
     const int c0 = cur.n0 + wn * FN * 32 + 4 * (lane >> 5);
+    uint16_t* const og = cur.e < E ? dst : dst_sh;
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
       if (drow[j] < 0) continue;
-      uint16_t* orow = dst + int64_t(drow[j]) * Nout + c0;
 #pragma unroll
       for (int i = 0; i < FN; ++i)
 #pragma unroll
         for (int g = 0; g < 4; ++g) {
-          if (c0 + i * 32 + 8 * g >= Nout) continue;
+          const int c = c0 + i * 32 + 8 * g;
+          if (c >= Nout) continue;
           const f32x16_t& a = acc[i][j];
-          *reinterpret_cast<u32x2_t*>(orow + i * 32 + 8 * g) =
-              pack4_bf16(act_fn<ACT>(a[4 * g]), act_fn<ACT>(a[4 * g + 1]),
-                         act_fn<ACT>(a[4 * g + 2]), act_fn<ACT>(a[4 * g + 3]));
+          if constexpr (kGated) {
+            *reinterpret_cast<uint32_t*>(og + int64_t(drow[j]) * Nw + (c >> 1)) =
+                pack2_bf16(silu_f(a[4 * g]) * a[4 * g + 1], silu_f(a[4 * g + 2]) * a[4 * g + 3]);
+          } else {
+            *reinterpret_cast<u32x2_t*>(og + int64_t(drow[j]) * Nw + c) =
+                pack4_bf16(act_fn<ACT>(a[4 * g]), act_fn<ACT>(a[4 * g + 1]),
+                           act_fn<ACT>(a[4 * g + 2]), act_fn<ACT>(a[4 * g + 3]));
+          }
         }
     }
     if (!has_next) break;
@@ -609,9 +672,11 @@ constexpr int kF32K = 16;
 
 template <int KIND, int ACT>
 __global__ __launch_bounds__(256) void gemm_f32_kernel(
-    const float* __restrict__ A, const float* __restrict__ W, const int32_t* __restrict__ off,
-    const int32_t* __restrict__ list, const int32_t* __restrict__ sigma, int E, int k, int K,
-    int Nout, float* __restrict__ dst) {
+    const float* __restrict__ A, const float* __restrict__ W, const float* __restrict__ Wsh,
+    const int32_t* __restrict__ off, const int32_t* __restrict__ list,
+    const int32_t* __restrict__ row_dst, int E, int G, int k, int K, int Nout,
+    float* __restrict__ dst, float* __restrict__ dst_sh) {
+  constexpr bool kGated = ACT == kActSwiglu;
   __shared__ float As[kF32K][kF32T + 4];
   __shared__ float Bs[kF32K][kF32T + 4];
   __shared__ int s_src[kF32T];
@@ -619,7 +684,7 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(
   __shared__ int s_tile[4];
   const int tid = threadIdx.x;
   if (tid == 0) {
-    const Tile t = decode_tile<kF32T>(off, E, Nout / kF32T);
+    const Tile t = decode_tile<kF32T>(off, G, Nout / kF32T);
     s_tile[0] = t.e;
     s_tile[1] = t.r0;
     s_tile[2] = t.rows;
@@ -629,22 +694,13 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(
   const int e = s_tile[0];
   if (e < 0) return;
   const int r0 = s_tile[1], rows = s_tile[2], n0 = s_tile[3];
-  if (tid < kF32T) {
-    const int r = tid;
-    const int rr = r < rows ? r : 0;
-    const int f = list[r0 + rr];
-    if (KIND == kUp) {
-      s_src[r] = f / k;
-      s_dst[r] = r < rows ? r0 + r : -1;
-    } else {
-      s_src[r] = r0 + rr;
-      s_dst[r] = r < rows ? (f / k) * k + sigma[f] : -1;
-    }
-  }
+  if (tid < kF32T) group_row<KIND>(e, E, r0, rows, tid, k, off, list, row_dst, s_src[tid], s_dst[tid]);
   __syncthreads();
   const int lr = tid >> 2, lk = (tid & 3) * 4;
+  const float* Wg = e < E ? W + int64_t(e) * Nout * K : Wsh + int64_t(e - E) * Nout * K;
+  float* const og = e < E ? dst : dst_sh;
   const float* ap = A + int64_t(s_src[lr]) * K + lk;
-  const float* bp = W + (int64_t(e) * Nout + n0 + lr) * K + lk;
+  const float* bp = Wg + int64_t(n0 + lr) * K + lk;
   const int tx = tid & 15, ty = tid >> 4;
   float acc[4][4] = {};
   for (int k0 = 0; k0 < K; k0 += kF32K) {
@@ -677,58 +733,72 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(
   for (int i = 0; i < 4; ++i) {
     const int drow = s_dst[ty * 4 + i];
     if (drow < 0) continue;
-    float* out = dst + int64_t(drow) * Nout + n0 + tx * 4;
+    if constexpr (kGated) {  // columns (gate, up, gate, up) -> two outputs
+      float* out = og + int64_t(drow) * (Nout / 2) + (n0 + tx * 4) / 2;
+      out[0] = silu_f(acc[i][0]) * acc[i][1];
+      out[1] = silu_f(acc[i][2]) * acc[i][3];
+    } else {
+      float* out = og + int64_t(drow) * Nout + n0 + tx * 4;
 #pragma unroll
-    for (int j = 0; j < 4; ++j) out[j] = act_fn<ACT>(acc[i][j]);
+      for (int j = 0; j < 4; ++j) out[j] = act_fn<ACT>(acc[i][j]);
+    }
   }
 }
 
 int max_tiles(const Shape& s, int TM, int NT) {
-  const int64_t mt = (s.branches() + TM - 1) / TM + s.E;
+  const int64_t mt = (s.mid_rows() + TM - 1) / TM + s.groups();
   const int64_t g = mt * NT;
   return static_cast<int>((g + kXcds - 1) / kXcds * kXcds);
 }
 
 constexpr int kBlocksPerCu = 2;
 
+// Grouped GEMM over the E routed groups (weights W, outputs dst) and the S
+// shared groups (weights Wsh, outputs dst_sh) with Nout weight rows and K
+// inputs per group.
 template <int KIND, int ACT>
-hipError_t launch_gemm(const Shape& s, const void* A, const void* W, int K, int Nout,
-                       const Buffers& b, void* dst, hipStream_t st) {
+hipError_t launch_gemm(const Shape& s, const void* A, const void* W, const void* Wsh, int K,
+                       int Nout, const Buffers& b, void* dst, void* dst_sh, hipStream_t st) {
+  const int G = s.groups();
   if (s.bf16) {
     const FfnPlan plan = ffn_plan(s);
     const int tn = KIND == kUp ? plan.tn_up : plan.tn_down;
-    const int32_t* toff = b.tiles + (KIND == kUp ? 0 : s.E + 1);
+    const int32_t* toff = b.tiles + (KIND == kUp ? 0 : G + 1);
     const int grid = device_cus() * kBlocksPerCu;  // multiple of 8
     const auto* a = static_cast<const uint16_t*>(A);
     const auto* w = static_cast<const uint16_t*>(W);
+    const auto* wsh = static_cast<const uint16_t*>(Wsh);
     auto* o = static_cast<uint16_t*>(dst);
+    auto* osh = static_cast<uint16_t*>(dst_sh);
     if (tn == kBigTN) {
       launch_kernel(&gemm_bf16_big_kernel<KIND, ACT>, dim3(device_cus()), dim3(kBigThreads), 0, st,
-          a, w, b.off, toff, b.list, b.row_dst, s.E, s.k, K, Nout, o);
+          a, w, wsh, b.off, toff, b.list, b.row_dst, s.E, G, s.k, K, Nout, o, osh);
     } else if (tn == 128) {
       launch_kernel(&gemm_bf16_kernel<128, 128, KIND, ACT>, dim3(grid), dim3(kGemmThreads), 0, st,
-          a, w, b.off, toff, b.list, b.sigma, s.E, s.k, K, Nout, o);
+          a, w, wsh, b.off, toff, b.list, b.row_dst, s.E, G, s.k, K, Nout, o, osh);
     } else {
       launch_kernel(&gemm_bf16_kernel<128, 64, KIND, ACT>, dim3(grid), dim3(kGemmThreads), 0, st,
-          a, w, b.off, toff, b.list, b.sigma, s.E, s.k, K, Nout, o);
+          a, w, wsh, b.off, toff, b.list, b.row_dst, s.E, G, s.k, K, Nout, o, osh);
     }
   } else {
     launch_kernel(&gemm_f32_kernel<KIND, ACT>, dim3(max_tiles(s, kF32T, Nout / kF32T)), dim3(256),
-        0, st, static_cast<const float*>(A), static_cast<const float*>(W), b.off, b.list, b.sigma, s.E,
-        s.k, K, Nout, static_cast<float*>(dst));
+        0, st, static_cast<const float*>(A), static_cast<const float*>(W),
+        static_cast<const float*>(Wsh), b.off, b.list, b.row_dst, s.E, G, s.k, K, Nout,
+        static_cast<float*>(dst), static_cast<float*>(dst_sh));
   }
   return hipGetLastError();
 }
 
 }  // namespace
 
-// Output widths of at least 512 take the large 128 x 256 tile (a partial
-// last N tile is masked); smaller ones the 128 x 128 / 128 x 64 tiles.
+// Weight-row counts of at least 512 take the large 128 x 256 tile (a
+// partial last N tile is masked); smaller ones the 128 x 128 / 128 x 64
+// tiles.
 FfnPlan ffn_plan(const Shape& s) {
   auto tn = [](int n) { return n >= 512 ? kBigTN : (n % 128 == 0 ? 128 : 64); };
   FfnPlan p;
   p.tm = 128;
-  p.tn_up = tn(s.d_ff);
+  p.tn_up = tn(s.up_rows());
   p.tn_down = tn(s.d);
   return p;
 }
@@ -747,16 +817,20 @@ int device_cus() {
   return cus;
 }
 
-hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, int act,
-                         const Buffers& b, hipStream_t st) {
-  if (act == kActGeluErf)
-    return launch_gemm<kUp, kActGeluErf>(s, x, W_up, s.d, s.d_ff, b, b.mid, st);
-  return launch_gemm<kUp, kActGeluTanh>(s, x, W_up, s.d, s.d_ff, b, b.mid, st);
+hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, const void* W_up_sh,
+                         int act, const Buffers& b, hipStream_t st) {
+  const int n = s.up_rows();
+  if (act == MOECA_ACT_SWIGLU)
+    return launch_gemm<kUp, kActSwiglu>(s, x, W_up, W_up_sh, s.d, n, b, b.mid, b.mid, st);
+  if (act == MOECA_ACT_GELU_ERF)
+    return launch_gemm<kUp, kActGeluErf>(s, x, W_up, W_up_sh, s.d, n, b, b.mid, b.mid, st);
+  return launch_gemm<kUp, kActGeluTanh>(s, x, W_up, W_up_sh, s.d, n, b, b.mid, b.mid, st);
 }
 
-hipError_t launch_ffn_down(const Shape& s, const void* W_down, const Buffers& b,
-                           hipStream_t st) {
-  return launch_gemm<kDown, kActNone>(s, b.mid, W_down, s.d_ff, s.d, b, b.h_c, st);
+hipError_t launch_ffn_down(const Shape& s, const void* W_down, const void* W_down_sh,
+                           const Buffers& b, hipStream_t st) {
+  return launch_gemm<kDown, kActNone>(s, b.mid, W_down, W_down_sh, s.d_ff, s.d, b, b.h_c, b.h_sh,
+                                      st);
 }
 
 }  // namespace moeca

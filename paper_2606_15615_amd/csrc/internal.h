@@ -34,9 +34,14 @@ inline void launch_kernel(void (*kernel)(P...), dim3 grid, dim3 block, uint32_t 
 struct Shape {
   int d, E, k, d_ff, B, N;
   bool bf16;
+  int S = 0;            // shared experts
+  bool swiglu = false;  // gated experts: 2 d_ff up-projection rows
   int64_t tokens() const { return int64_t(B) * N; }
   int64_t branches() const { return int64_t(B) * N * k; }
   size_t act_bytes() const { return bf16 ? 2 : 4; }
+  int groups() const { return E + S; }                // grouped-GEMM groups
+  int up_rows() const { return swiglu ? 2 * d_ff : d_ff; }
+  int64_t mid_rows() const { return branches() + int64_t(S) * tokens(); }
 };
 
 // Device views of the workspace regions (see moeca_debug_buffer for the
@@ -57,15 +62,17 @@ struct Buffers {
   uint8_t* mask;
   int32_t* sigma;
   uint8_t* sync;    // [B*N]
-  int32_t* off;     // [E+1]
+  int32_t* off;     // [E+S+1] group row offsets: routed experts into `list`,
+                    // then the shared experts (T rows each) after them
   int32_t* list;
   int32_t* pos;
   int32_t* cnt_bs;  // [B][E] recomputed branches per sample and expert
   int32_t* stats_bs;// [B][4] recompute, unmatched, matched, sync per sample
   int32_t* rflags;  // router: one non-finite flag per block
-  int32_t* tiles;   // [2][E+1] grouped-GEMM tile prefix per expert (up, down)
+  int32_t* tiles;   // [2][E+S+1] grouped-GEMM tile prefix per group (up, down)
   int32_t* row_dst; // [B*N*k] cache row of each listed branch: (f/k)*k + sigma(f)
-  void* mid;        // [B*N*k][d_ff] FFN activation of listed rows
+  void* mid;        // [B*N*k + S*T][d_ff] FFN activation of listed and shared rows
+  void* h_sh;       // [S][T][d] shared experts' outputs
 };
 
 // Tiling of the grouped expert FFN: M tile (rows of one expert) and N tile
@@ -91,10 +98,11 @@ hipError_t launch_entropy(const Shape& s, float tau0, float alpha, const Buffers
 hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1, float lambda2,
                          const Buffers& b, hipStream_t st);
 hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st);
-hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, int act,
-                         const Buffers& b, hipStream_t st);
-hipError_t launch_ffn_down(const Shape& s, const void* W_down, const Buffers& b,
-                           hipStream_t st);
+// act: MOECA_ACT_* of the policy.  W_*_sh: the shared experts (S > 0).
+hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, const void* W_up_sh,
+                         int act, const Buffers& b, hipStream_t st);
+hipError_t launch_ffn_down(const Shape& s, const void* W_down, const void* W_down_sh,
+                           const Buffers& b, hipStream_t st);
 hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void* attn_in,
                           void* attn_cache, const Buffers& b, hipStream_t st);
 hipError_t launch_reset(const Shape& s, const Buffers& b, hipStream_t st);

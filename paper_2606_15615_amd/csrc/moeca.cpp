@@ -47,7 +47,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 enum Region {
   R_E_C, R_W_C, R_N_C, R_H_C, R_STAT, R_LOGITS, R_E_T, R_W_T, R_HBAR, R_TAU, R_MARGIN, R_Q,
   R_MASK, R_SIGMA, R_SYNC, R_OFF, R_LIST, R_POS,
-  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_MID, R_COUNT
+  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_MID, R_H_SH, R_COUNT
 };
 
 struct Layout {
@@ -76,15 +76,16 @@ Layout make_layout(const Shape& s) {
   b[R_MASK] = nbr;
   b[R_SIGMA] = nbr * 4;
   b[R_SYNC] = ntok;
-  b[R_OFF] = size_t(s.E + 1) * 4;
+  b[R_OFF] = size_t(s.groups() + 1) * 4;
   b[R_LIST] = nbr * 4;
   b[R_POS] = nbr * 4;
   b[R_CNT_BS] = size_t(s.B) * s.E * 4;
   b[R_STATS_BS] = size_t(s.B) * 4 * 4;
   b[R_RFLAGS] = size_t(moeca::router_blocks(s)) * 4;
-  b[R_TILES] = size_t(2) * (s.E + 1) * 4;
+  b[R_TILES] = size_t(2) * (s.groups() + 1) * 4;
   b[R_ROW_DST] = nbr * 4;
-  b[R_MID] = nbr * s.d_ff * act;
+  b[R_MID] = size_t(s.mid_rows()) * s.d_ff * act;
+  b[R_H_SH] = size_t(s.S) * ntok * s.d * act;
   Layout L;
   size_t cur = 0;
   for (int i = 0; i < R_COUNT; ++i) {
@@ -93,6 +94,8 @@ Layout make_layout(const Shape& s) {
     cur = align_up(cur + b[i]);
   }
   L.total = cur;
+  // the public view of the offsets covers the routed experts only
+  L.bytes[R_OFF] = size_t(s.E + 1) * 4;
   return L;
 }
 
@@ -106,6 +109,8 @@ struct moeca_layer {
   const float* b_r = nullptr;
   const void* W_up = nullptr;
   const void* W_down = nullptr;
+  const void* W_up_sh = nullptr;
+  const void* W_down_sh = nullptr;
   char* ws = nullptr;
   Buffers buf{};
   const void* attn_in = nullptr;
@@ -135,6 +140,7 @@ void moeca_policy_default(moeca_policy* p) {
   p->dtype = MOECA_DTYPE_BF16;
   p->batch = 1;
   p->tokens = 1;
+  p->n_shared = 0;
 }
 
 const char* moeca_last_error(void) { return g_error.c_str(); }
@@ -147,13 +153,17 @@ moeca_layer* moeca_layer_create(int d, int E, int k, int d_ff, const moeca_polic
   };
   if (p == nullptr) return bad("policy is NULL");
   if (d <= 0 || d % 64 != 0 || d > 16384) return bad("d must be a positive multiple of 64, <= 16384");
-  if (d_ff <= 0 || d_ff % 64 != 0 || d_ff > 65536)
-    return bad("d_ff must be a positive multiple of 64, <= 65536");
+  if (p->act != MOECA_ACT_GELU_TANH && p->act != MOECA_ACT_GELU_ERF &&
+      p->act != MOECA_ACT_SWIGLU)
+    return bad("unknown act");
+  const int max_ff = p->act == MOECA_ACT_SWIGLU ? 32768 : 65536;
+  if (d_ff <= 0 || d_ff % 64 != 0 || d_ff > max_ff)
+    return bad("d_ff must be a positive multiple of 64, <= " + std::to_string(max_ff));
   if (E < 1 || E > 64) return bad("E must be in [1, 64]");
   if (k < 1 || k > 8 || k > E) return bad("k must be in [1, min(E, 8)]");
+  if (p->n_shared < 0 || p->n_shared > 8) return bad("n_shared must be in [0, 8]");
   if (p->mode < MOECA_MODE_FULL || p->mode > MOECA_MODE_RATIO) return bad("unknown mode");
   if (p->dtype != MOECA_DTYPE_BF16 && p->dtype != MOECA_DTYPE_FP32) return bad("unknown dtype");
-  if (p->act != MOECA_ACT_GELU_TANH && p->act != MOECA_ACT_GELU_ERF) return bad("unknown act");
   if (!(p->ratio >= 0.0f && p->ratio <= 1.0f)) return bad("ratio must be in [0, 1]");
   if (!(p->tau0 > 0.0f) || !std::isfinite(p->tau0)) return bad("tau0 must be finite and > 0");
   if (!(p->alpha >= 0.0f && p->alpha < 1.0f)) return bad("alpha must be in [0, 1)");
@@ -164,13 +174,15 @@ moeca_layer* moeca_layer_create(int d, int E, int k, int d_ff, const moeca_polic
   if (p->refresh_cycle < 0) return bad("refresh_cycle must be >= 0");
   if (p->norm_topk != 0 && p->norm_topk != 1) return bad("norm_topk must be 0 or 1");
   if (p->batch < 1 || p->tokens < 1) return bad("batch and tokens must be >= 1");
-  const int64_t nbr = int64_t(p->batch) * p->tokens * k;
-  if (nbr >= (int64_t(1) << 31) - 1024) return bad("batch * tokens * k too large");
+  const int64_t nbr = int64_t(p->batch) * p->tokens * (k + p->n_shared);
+  if (nbr >= (int64_t(1) << 31) - 1024) return bad("batch * tokens * (k + n_shared) too large");
   if (int64_t(p->batch) * p->tokens * d >= (int64_t(1) << 40)) return bad("batch too large");
 
   auto* L = new (std::nothrow) moeca_layer();
   if (L == nullptr) return bad("out of host memory");
   L->shape = Shape{d, E, k, d_ff, p->batch, p->tokens, p->dtype == MOECA_DTYPE_BF16};
+  L->shape.S = p->n_shared;
+  L->shape.swiglu = p->act == MOECA_ACT_SWIGLU;
   L->pol = *p;
   L->layout = make_layout(L->shape);
   return L;
@@ -194,6 +206,18 @@ int moeca_layer_set_weights(moeca_layer* L, const void* W_r, const float* b_r, c
   L->b_r = b_r;
   L->W_up = W_up;
   L->W_down = W_down;
+  return MOECA_OK;
+}
+
+int moeca_layer_set_shared(moeca_layer* L, const void* W_up_s, const void* W_down_s) {
+  if (L == nullptr) return fail(MOECA_E_INVAL, "layer is NULL");
+  if (L->shape.S == 0) return fail(MOECA_E_INVAL, "the layer has no shared experts");
+  if (W_up_s == nullptr || W_down_s == nullptr)
+    return fail(MOECA_E_INVAL, "W_up_s and W_down_s are required");
+  if (!aligned16(W_up_s) || !aligned16(W_down_s))
+    return fail(MOECA_E_INVAL, "shared weights must be 16-byte aligned");
+  L->W_up_sh = W_up_s;
+  L->W_down_sh = W_down_s;
   return MOECA_OK;
 }
 
@@ -234,6 +258,7 @@ int moeca_bind_workspace(moeca_layer* L, void* dev, size_t bytes) {
   b.tiles = reinterpret_cast<int32_t*>(w + o[R_TILES]);
   b.row_dst = reinterpret_cast<int32_t*>(w + o[R_ROW_DST]);
   b.mid = w + o[R_MID];
+  b.h_sh = w + o[R_H_SH];
   L->ws = w;
   L->valid = false;
   return MOECA_OK;
@@ -258,6 +283,8 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
     return fail(MOECA_E_INVAL, "x_t and out must be 16-byte aligned");
   if (L->W_r == nullptr) return fail(MOECA_E_STATE, "weights are not bound");
   if (L->ws == nullptr) return fail(MOECA_E_STATE, "workspace is not bound");
+  if (L->shape.S > 0 && L->W_up_sh == nullptr)
+    return fail(MOECA_E_STATE, "shared expert weights are not bound");
   const Shape& s = L->shape;
   const moeca_policy& p = L->pol;
   hipStream_t st = static_cast<hipStream_t>(stream);
@@ -314,9 +341,11 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
   arm();
   if (!check(moeca::launch_lists(s, moeca::ffn_plan(s), b, st), "lists")) return MOECA_E_HIP;
   arm();
-  if (!check(moeca::launch_ffn_up(s, x_t, L->W_up, p.act, b, st), "ffn up")) return MOECA_E_HIP;
+  if (!check(moeca::launch_ffn_up(s, x_t, L->W_up, L->W_up_sh, p.act, b, st), "ffn up"))
+    return MOECA_E_HIP;
   arm();
-  if (!check(moeca::launch_ffn_down(s, L->W_down, b, st), "ffn down")) return MOECA_E_HIP;
+  if (!check(moeca::launch_ffn_down(s, L->W_down, L->W_down_sh, b, st), "ffn down"))
+    return MOECA_E_HIP;
   arm();
   if (!check(moeca::launch_combine(s, uncached ? 0 : 1, out, L->attn_in, L->attn_cache, b, st),
              "combine"))

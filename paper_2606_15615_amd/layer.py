@@ -39,16 +39,18 @@ class MoecaLayer:
     def __init__(self, d, E, k, d_ff, *, batch, tokens, mode=_lib.MOECA_MODE_THRESHOLD,
                  ratio=0.3, tau0=0.80, alpha=0.6, beta=0.65, lambda1=1.0, lambda2=1.0,
                  refresh_cycle=4, norm_topk=True, act="gelu_tanh", dtype="bf16",
-                 device="cuda:0"):
+                 n_shared=0, device="cuda:0"):
         torch = _torch()
         p = _lib.moeca_policy_default()
         p.mode, p.ratio, p.tau0, p.alpha, p.beta = mode, ratio, tau0, alpha, beta
         p.lambda1, p.lambda2, p.refresh_cycle = lambda1, lambda2, refresh_cycle
         p.norm_topk = 1 if norm_topk else 0
-        p.act = {"gelu_tanh": _lib.MOECA_ACT_GELU_TANH, "gelu_erf": _lib.MOECA_ACT_GELU_ERF}[act]
+        p.act = {"gelu_tanh": _lib.MOECA_ACT_GELU_TANH, "gelu_erf": _lib.MOECA_ACT_GELU_ERF,
+                 "swiglu": _lib.MOECA_ACT_SWIGLU}[act]
         p.dtype = {"bf16": _lib.MOECA_DTYPE_BF16, "fp32": _lib.MOECA_DTYPE_FP32}[dtype]
-        p.batch, p.tokens = batch, tokens
+        p.batch, p.tokens, p.n_shared = batch, tokens, n_shared
         self.d, self.E, self.k, self.d_ff, self.B, self.N = d, E, k, d_ff, batch, tokens
+        self.n_shared = n_shared
         self.dtype = dtype
         self.act_np = np.uint16 if dtype == "bf16" else np.float32
         self.device = torch.device(device)
@@ -67,6 +69,10 @@ class MoecaLayer:
         _lib.moeca_layer_set_weights(self.h, W_r.data_ptr(),
                                      None if b_r is None else b_r.data_ptr(),
                                      W_up.data_ptr(), W_down.data_ptr())
+
+    def set_shared(self, W_up_s, W_down_s):
+        self._keep_shared = [W_up_s, W_down_s]
+        _lib.moeca_layer_set_shared(self.h, W_up_s.data_ptr(), W_down_s.data_ptr())
 
     def bind_attention(self, attn_in, attn_cache):
         self._attn = (attn_in, attn_cache)

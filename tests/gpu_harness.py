@@ -35,8 +35,12 @@ class Setup:
         self.shape = shape
         self.sy = Synth(shape, seed)
         W = self.sy.weights(bias)
-        self.dims = O.Dims(shape.d, shape.E, shape.k, shape.d_ff, shape.B, shape.N, shape.dtype)
-        self.W = O.Weights(self.dims, *W)
+        self.dims = O.Dims(shape.d, shape.E, shape.k, shape.d_ff, shape.B, shape.N, shape.dtype,
+                           shape.n_shared)
+        Wsh = self.sy.shared_weights()
+        self.W = O.Weights(self.dims, *W, *(Wsh or (None, None)))
+        if shape.ffn == "swiglu":
+            pol.setdefault("act", "swiglu")
         self.xs = list(self.sy.trajectory(T, drift)) if T else []
         self.attn = list(self.sy.attention_trajectory(T)) if (T and attention) else None
         self.pol = O.Policy(mode=OMODE[mode], **pol)
@@ -46,12 +50,16 @@ class Setup:
                                 alpha=self.pol.alpha, beta=self.pol.beta,
                                 lambda1=self.pol.lambda1, lambda2=self.pol.lambda2,
                                 refresh_cycle=self.pol.refresh_cycle,
-                                norm_topk=self.pol.norm_topk, act=self.pol.act)
+                                norm_topk=self.pol.norm_topk, act=self.pol.act,
+                                n_shared=shape.n_shared)
         dev = self.layer.device
         self.dW = [np_to_device(W[0], dev),
                    None if W[1] is None else np_to_device(W[1], dev),
                    np_to_device(W[2], dev), np_to_device(W[3], dev)]
         self.layer.set_weights(*self.dW)
+        if Wsh is not None:
+            self.dWsh = [np_to_device(w, dev) for w in Wsh]
+            self.layer.set_shared(*self.dWsh)
         self.act_np = np.uint16 if shape.dtype == "bf16" else np.float32
         tdt = torch.int16 if shape.dtype == "bf16" else torch.float32
         self.attn_in = torch.zeros((shape.B, shape.N, shape.d), dtype=tdt, device=dev)

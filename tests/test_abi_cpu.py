@@ -76,7 +76,8 @@ BAD_POLICY = [
     dict(ratio=math.nan), dict(alpha=1.0), dict(alpha=-0.2), dict(beta=1.0), dict(beta=-0.1),
     dict(tau0=0.0), dict(tau0=math.inf), dict(lambda1=-1.0), dict(lambda2=math.nan),
     dict(refresh_cycle=-1), dict(norm_topk=2), dict(batch=0), dict(tokens=0),
-    dict(batch=1 << 20, tokens=1 << 12),
+    dict(batch=1 << 20, tokens=1 << 12), dict(n_shared=-1), dict(n_shared=9),
+    dict(batch=1 << 14, tokens=1 << 14, n_shared=6),
 ]
 
 
@@ -146,3 +147,39 @@ def test_workspace_grows_with_the_layer(L):
     finally:
         for h in (a, b, c):
             L.moeca_layer_destroy(h)
+
+
+def test_shared_experts_and_gated_ffn_host_paths(L):
+    """Shared experts (Sec. 2.3, shared-expert MoE eq.) and the gated FFN:
+    argument checks and workspace size, host only."""
+    lib = L.load()
+    fake = 1 << 40  # never dereferenced
+    # the gated form doubles the up-projection rows: d_ff up to 32768
+    assert not lib.moeca_layer_create(64, 8, 2, 32768 + 64,
+                                      ctypes.byref(_pol(L, act=L.MOECA_ACT_SWIGLU)))
+    h0 = L.moeca_layer_create(64, 8, 2, 32768 + 64, _pol(L))
+    L.moeca_layer_destroy(h0)
+    plain = L.moeca_layer_create(128, 8, 2, 192, _pol(L, batch=2, tokens=40))
+    h = L.moeca_layer_create(128, 8, 2, 192, _pol(L, batch=2, tokens=40, n_shared=3,
+                                                  act=L.MOECA_ACT_SWIGLU))
+    try:
+        # a layer without shared experts rejects shared weights
+        assert lib.moeca_layer_set_shared(plain, fake, fake) == L.MOECA_E_INVAL
+        assert "no shared experts" in L.moeca_last_error()
+        # shared outputs [S][T][d] and S*T more intermediate rows [d_ff]
+        extra = L.moeca_workspace_bytes(h) - L.moeca_workspace_bytes(plain)
+        T = 2 * 40
+        assert extra >= 3 * T * (128 + 192) * 2
+        nbytes = L.moeca_workspace_bytes(h)
+        assert L.moeca_layer_set_weights(h, fake, None, fake, fake) == L.MOECA_OK
+        assert L.moeca_bind_workspace(h, fake, nbytes) == L.MOECA_OK
+        assert lib.moeca_step(h, fake, 0, fake, None) == L.MOECA_E_STATE
+        assert "shared" in L.moeca_last_error()
+        assert lib.moeca_layer_set_shared(h, None, fake) == L.MOECA_E_INVAL
+        assert lib.moeca_layer_set_shared(h, fake, fake + 8) == L.MOECA_E_INVAL
+        assert L.moeca_layer_set_shared(h, fake, fake) == L.MOECA_OK
+        # the public offsets view stays [E+1]
+        assert L.moeca_debug_buffer(h, L.BUF["off"])[1] == (8 + 1) * 4
+    finally:
+        L.moeca_layer_destroy(h)
+        L.moeca_layer_destroy(plain)

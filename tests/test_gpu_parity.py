@@ -215,3 +215,80 @@ def test_free_running_agreement():
             assert rel_err(out_g, out_o, "bf16") <= 2e-2
     say(f"  free-running mask agreement per step: {agree}")
     assert min(agree) >= 0.99
+
+
+# ---------------------------------------------------------------------------
+# Fine-grained layer with shared experts (Sec. 2.3, shared-expert MoE eq.):
+# gated (SwiGLU) experts, top-k over many small experts, always-on shared
+# experts that are never cached, unnormalised gates.  The shapes cover the
+# large-tile GEMM (>= 512 weight rows), the 128- and 64-wide tiles, the
+# fp32 kernels, more than 64 GEMM groups, a GELU layer with a shared expert
+# and the uncached comparator.
+# ---------------------------------------------------------------------------
+FINE_SHAPES = [
+    LayerShape(d=512, E=16, k=4, d_ff=320, B=2, N=256, dtype="bf16", ffn="swiglu", n_shared=2),
+    LayerShape(d=256, E=8, k=2, d_ff=128, B=2, N=77, dtype="bf16", ffn="swiglu", n_shared=1),
+    LayerShape(d=192, E=6, k=3, d_ff=64, B=3, N=41, dtype="bf16", ffn="swiglu", n_shared=3),
+    LayerShape(d=128, E=8, k=4, d_ff=64, B=2, N=50, dtype="fp32", ffn="swiglu", n_shared=2),
+    LayerShape(d=256, E=64, k=8, d_ff=256, B=1, N=96, dtype="bf16", ffn="swiglu", n_shared=2),
+    LayerShape(d=128, E=64, k=8, d_ff=64, B=1, N=60, dtype="fp32", ffn="swiglu", n_shared=8),
+    LayerShape(d=256, E=6, k=2, d_ff=320, B=2, N=77, dtype="bf16", n_shared=1),
+]
+
+
+@pytest.mark.parametrize("shape", FINE_SHAPES)
+def test_fine_shared_trajectory(shape):
+    S = Setup(shape, mode="ratio", seed=16, T=5, ratio=0.25, refresh_cycle=3, norm_topk=False)
+    infos = run_forced(S, 5, label=f"fine {shape}")
+    say(f"  fine {shape}: {infos}")
+
+
+def test_fine_shared_threshold_and_uncached():
+    shape = FINE_SHAPES[0]
+    S = Setup(shape, mode="threshold", seed=17, T=4, refresh_cycle=0, norm_topk=False)
+    run_forced(S, 4, label="fine threshold")
+    U = Setup(shape, mode="full", seed=18, T=2, norm_topk=False)
+    run_forced(U, 2, label="fine uncached")
+
+
+def test_fine_nothing_recomputed_still_runs_shared_experts():
+    """Ratio 0 on a new input: every matched branch is reused, yet the
+    output carries the shared experts of the new input."""
+    shape = FINE_SHAPES[1]
+    S = Setup(shape, mode="ratio", seed=19, T=2, ratio=0.0, refresh_cycle=0, norm_topk=False)
+    st0 = O.State(S.dims, attention=True)
+    _, st1, _ = O.step(S.dims, S.pol, S.W, st0, S.xs[0], 0, attn_in=S.attn[0])
+    S.import_state(st1)
+    out_g = S.gpu_step(S.xs[1], 1, S.attn[1])
+    out_o, st2, rec = O.step(S.dims, S.pol, S.W, st1, S.xs[1], 1, attn_in=S.attn[1])
+    assert rec["mask"].sum() == (~rec["matched"]).sum()
+    info = check_step(S, 1, rec, out_o, st1, st2, out_g, label="fine reuse")
+    say(f"  fine reuse: {info}")
+
+
+@pytest.mark.timeout(600)
+def test_fine_sampled():
+    """The benchmarked fine-grained layer (d=2048, 64 experts, top-8, 1408
+    hidden SwiGLU, 2 shared experts, 4096 tokens x 4, 25 % refresh):
+    decisions over the whole batch, outputs and rows on sampled tokens."""
+    shape = WORKLOADS["fine"]
+    S = Setup(shape, mode="ratio", seed=20, T=3, ratio=0.25, refresh_cycle=0, norm_topk=False)
+    dims = S.dims
+    rng = np.random.default_rng(21)
+    sample = np.sort(rng.choice(shape.tokens, size=24, replace=False))
+    ev = np.zeros(shape.tokens, bool)
+    ev[sample] = True
+    ev = ev.reshape(shape.B, shape.N)
+    st = O.State(dims, attention=True)
+    for t in range(2):
+        _, st, _ = O.step(dims, S.pol, S.W, st, S.xs[t], t, attn_in=S.attn[t], tokens=sample)
+        fill = ~ev
+        rows = S.sy.rows((int(fill.sum()), shape.k, shape.d), scale=0.05)
+        st.h_c[fill] = rows
+        st.n_c[fill] = O.row_norms(rows, shape.dtype)
+    S.import_state(st)
+    out_g = S.gpu_step(S.xs[2], 2, S.attn[2])
+    out_o, st_new, rec = O.step(dims, S.pol, S.W, st, S.xs[2], 2, attn_in=S.attn[2],
+                                tokens=sample)
+    info = check_step(S, 2, rec, out_o, st, st_new, out_g, evaluated=ev, label="fine sampled")
+    say(f"  fine sampled: {info}")
