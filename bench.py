@@ -47,7 +47,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=20)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default="xl1024")
-    ap.add_argument("--ratio", type=float, default=0.3)
+    ap.add_argument("--ratio", type=float, default=None,
+                    help="refresh ratio (default 0.3; 0.25 for the fine-grained layer)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--no-cpu", action="store_true", help="skip the oracle CPU baseline")
     ap.add_argument("--phase", choices=("both", "cached", "full"), default="both",
@@ -63,27 +64,29 @@ def parse():
     return ap.parse_args()
 
 
-def cpu_baseline(shape, ratio, seed):
+def cpu_baseline(shape, ratio, seed, norm_topk, act, reps):
     """The oracle, as it stands, on one sample of the batch: a refresh step
-    and then a timed cache step (median of 3), scaled to the whole batch."""
+    and then timed cache steps (median of ``reps``), scaled to the whole
+    batch."""
+    import dataclasses
     from oracle import moeca_oracle as O
-    from paper_2606_15615_amd.synth import LayerShape, Synth
+    from paper_2606_15615_amd.synth import Synth
     try:
         from threadpoolctl import threadpool_info
         cores = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
         cores = 1
-    one = LayerShape(shape.d, shape.E, shape.k, shape.d_ff, 1, shape.N, shape.dtype)
+    one = dataclasses.replace(shape, B=1)
     sy = Synth(one, seed)
     W = sy.weights()
-    dims = O.Dims(one.d, one.E, one.k, one.d_ff, 1, one.N, one.dtype)
-    Wo = O.Weights(dims, *W)
-    xs = list(sy.trajectory(5))
-    pol = O.Policy(mode=O.MODE_RATIO, ratio=ratio, refresh_cycle=0)
+    dims = O.Dims(one.d, one.E, one.k, one.d_ff, 1, one.N, one.dtype, one.n_shared)
+    Wo = O.Weights(dims, *W, *(sy.shared_weights() or (None, None)))
+    xs = list(sy.trajectory(reps + 1))
+    pol = O.Policy(mode=O.MODE_RATIO, ratio=ratio, refresh_cycle=0, norm_topk=norm_topk, act=act)
     st = O.State(dims)
     _, st, _ = O.step(dims, pol, Wo, st, xs[0], 0)
     times = []
-    for t in range(1, 4):
+    for t in range(1, reps + 1):
         t0 = time.perf_counter()
         _, st2, _ = O.step(dims, pol, Wo, st, xs[t], t)
         times.append(time.perf_counter() - t0)
@@ -91,7 +94,7 @@ def cpu_baseline(shape, ratio, seed):
     ms = float(np.median(times)) * 1e3 * shape.B
     return {"value": round(ms, 3), "unit": "ms/step", "cores": int(cores), "kind": "oracle",
             "sample": f"1 of {shape.B} samples ({shape.N} tokens), cache step at ratio {ratio}, "
-                      f"median of 3, scaled x{shape.B}"}
+                      f"median of {reps}, scaled x{shape.B}"}
 
 
 def kernel_traffic(kernel_src: str, summary: str):
@@ -120,7 +123,7 @@ def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
-              "this build has no multi-GPU path", file=sys.stderr)
+              "the library has no multi-GPU path", file=sys.stderr)
         sys.exit(2)
     import torch
     from paper_2606_15615_amd import _lib
@@ -129,6 +132,11 @@ def main():
 
     _lib.load()  # fails loudly when the library is not built
     shape = WORKLOADS[args.workload]
+    fine = shape.n_shared > 0 or shape.ffn == "swiglu"
+    if args.ratio is None:
+        args.ratio = 0.25 if fine else 0.3
+    act = "swiglu" if shape.ffn == "swiglu" else "gelu_tanh"
+    norm_topk = not fine  # the fine-grained layer keeps the softmax gate values
     dev = torch.device("cuda:0")
     K, Wm = args.steps, args.warmup
     T = Wm + K
@@ -142,6 +150,9 @@ def main():
     dW = [np_to_device(W[0], dev), None if W[1] is None else np_to_device(W[1], dev),
           np_to_device(W[2], dev), np_to_device(W[3], dev)]
     del W
+    Wsh = sy.shared_weights()
+    dWsh = None if Wsh is None else [np_to_device(w, dev) for w in Wsh]
+    del Wsh
     xs = [np_to_device(x, dev) for x in sy.trajectory(T, drift)]
     attn = np_to_device(next(sy.attention_trajectory(1, drift)), dev)
     attn_cache = torch.zeros_like(attn)
@@ -150,8 +161,11 @@ def main():
 
     def make(mode, ratio=args.ratio):
         L = MoecaLayer(shape.d, shape.E, shape.k, shape.d_ff, batch=shape.B, tokens=shape.N,
-                       mode=mode, ratio=ratio, refresh_cycle=0, dtype=shape.dtype)
+                       mode=mode, ratio=ratio, refresh_cycle=0, dtype=shape.dtype, act=act,
+                       norm_topk=norm_topk, n_shared=shape.n_shared)
         L.set_weights(*dW)
+        if dWsh is not None:
+            L.set_shared(*dWsh)
         L.bind_attention(attn, attn_cache)
         L.reset()
         return L
@@ -258,11 +272,18 @@ def main():
         torch.cuda.synchronize()
 
     branches = shape.B * shape.N * shape.k
-    up_flop = 2.0 * shape.d * shape.d_ff       # per recomputed branch, each projection
+    # flop per row of the up and the down projection (routed branch or
+    # shared-expert token row); the shared experts add S * T rows per step
+    up_flop = 2.0 * shape.d * shape.up_rows
+    down_flop = 2.0 * shape.d * shape.d_ff
+    shared_rows = shape.n_shared * shape.tokens
     peak = PEAK_BF16_TFLOPS if shape.dtype == "bf16" else PEAK_FP32_TFLOPS
-    act = 2 if shape.dtype == "bf16" else 4
+    abytes = 2 if shape.dtype == "bf16" else 4
     wl = (f"{args.workload}: MoE layer d={shape.d}, E={shape.E}, top-{shape.k}, "
-          f"d_ff={shape.d_ff} GELU, {shape.N} tokens x batch {shape.B}, ratio mode rho={args.ratio}"
+          f"d_ff={shape.d_ff} {'SwiGLU' if act == 'swiglu' else 'GELU'}"
+          + (f", {shape.n_shared} shared experts" if shape.n_shared else "")
+          + (", unnormalised top-k gates" if not norm_topk else "")
+          + f", {shape.N} tokens x batch {shape.B}, ratio mode rho={args.ratio}"
           + (", Zipf(1.2) router prior, bimodal drift" if bias else ""))
     res = {"metric": METRIC, "unit": "ms/step", "n_gpus": 1, "steps": K, "warmup": Wm,
            "higher_is_better": False, "scaling": "weak", "vs_baseline": None,
@@ -273,17 +294,22 @@ def main():
         mean_rec = float(np.mean(rec))
         up_ms = stage["ffn_up"]
         ffn_ms = stage["ffn_up"] + stage["ffn_down"]
-        up_tf = mean_rec * up_flop / (up_ms * 1e-3) / 1e12
-        ffn_tf = mean_rec * 2 * up_flop / (ffn_ms * 1e-3) / 1e12
-        # algorithmic HBM bytes of a cache step: expert weights, inputs,
-        # reused cached rows, recomputed rows written, outputs (the
-        # attention refresh excluded)
-        wbytes = shape.E * 2 * shape.d * shape.d_ff * act
-        step_bytes = wbytes + shape.tokens * shape.d * act * 2 + branches * shape.d * act
+        rows = mean_rec + shared_rows
+        up_tf = rows * up_flop / (up_ms * 1e-3) / 1e12
+        ffn_tf = rows * (up_flop + down_flop) / (ffn_ms * 1e-3) / 1e12
+        # algorithmic HBM bytes of a cache step: expert weights (routed and
+        # shared), inputs, cached rows, recomputed rows written, shared
+        # outputs written and read, outputs (the attention refresh excluded)
+        wbytes = (shape.E + shape.n_shared) * (shape.up_rows + shape.d_ff) * shape.d * abytes
+        step_bytes = (wbytes + shape.tokens * shape.d * abytes * 2 + branches * shape.d * abytes
+                      + 2 * shared_rows * shape.d * abytes)
         traffic = kernel_traffic(os.path.join(ROOT, "paper_2606_15615_amd", "csrc", "ffn.hip"),
                                  os.path.join(ROOT, "profiles", "xl1024_cached_counters.txt"))
         if args.workload != "xl1024":
             traffic = None
+        up_kernel = ("gemm_bf16_big_kernel<0,3> (expert FFN up-projection + SwiGLU)"
+                     if act == "swiglu" else
+                     "gemm_bf16_big_kernel<0,0> (expert FFN up-projection + GELU)")
         res.update({
             "value": round(ms_graph, 4),
             "ms_per_step": round(ms_graph, 4),
@@ -293,19 +319,20 @@ def main():
             "tflops_recomputed": round(ffn_tf, 2),
             "refresh_ratio_actual": round(mean_rec / branches, 4),
             "recomputed_branches": round(mean_rec, 1),
+            "shared_expert_rows": shared_rows,
             "synchronized_tokens": round(float(np.mean(syn)), 1),
             "stage_ms": {k: round(v, 4) for k, v in stage.items()},
             "step_hbm_frac": round(step_bytes / (ms_graph * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             "roofline": {
                 "bound": "mfma",
-                "kernel": "gemm_bf16_big_kernel<0,0> (expert FFN up-projection + GELU)",
+                "kernel": up_kernel,
                 "achieved": round(up_tf, 2),
                 "peak": peak,
                 "unit": "TFLOP/s",
                 "frac": round(up_tf / peak, 4),
                 "traffic": None if traffic is None else int(traffic),
                 "launch_ms": round(up_ms, 4),
-                "flop_per_launch": mean_rec * up_flop,
+                "flop_per_launch": rows * up_flop,
             },
         })
     if res_f is not None:
@@ -323,7 +350,8 @@ def main():
         res["ratio_sweep"] = sweep
     if not args.no_cpu and res_c is not None:
         log("[bench] cpu baseline (oracle)")
-        res["cpu_baseline"] = cpu_baseline(shape, args.ratio, args.seed)
+        res["cpu_baseline"] = cpu_baseline(shape, args.ratio, args.seed, norm_topk, act,
+                                           reps=1 if fine else 3)
     print(json.dumps(res), flush=True)
 
 
