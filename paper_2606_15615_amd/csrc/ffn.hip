@@ -633,30 +633,48 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
       if (KT > 1) issue(1, 1);
     }
 
-    // epilogue: lane holds columns 8*(r/4) + 4*(lane/32) + (r%4) of row
-    // (lane & 31) in each 32 x 32 tile; activation, bf16, 8-byte stores
-    // (gated: two (gate, up) pairs -> two outputs, 4-byte stores)
-    const int c0 = cur.n0 + wn * FN * 32 + 4 * (lane >> 5);
+    // epilogue: per 32 x 32 tile the lane holds row (lane & 31) and columns
+    // 8q + 4h + s (q, s = 0..3, h = lane >> 5).  Activation and bf16 rounding, then
+    // the lane pair (l, l ^ 32) exchanges runs so that lane h holds columns
+    // 16p + 8h .. +7 (p = 0, 1) and each store writes 16 bytes (a 32-byte row
+    // segment per lane pair).  Gated: two (gate, up) pairs -> two outputs.
+    const int h = lane >> 5;
+    const int c0 = cur.n0 + wn * FN * 32;
     uint16_t* const og = cur.e < E ? dst : dst_sh;
 #pragma unroll
     for (int j = 0; j < FM; ++j) {
-      if (drow[j] < 0) continue;
 #pragma unroll
-      for (int i = 0; i < FN; ++i)
+      for (int i = 0; i < FN; ++i) {
+        const f32x16_t& a = acc[i][j];
+        if constexpr (kGated) {
 #pragma unroll
-        for (int g = 0; g < 4; ++g) {
-          const int c = c0 + i * 32 + 8 * g;
-          if (c >= Nout) continue;
-          const f32x16_t& a = acc[i][j];
-          if constexpr (kGated) {
-            *reinterpret_cast<uint32_t*>(og + int64_t(drow[j]) * Nw + (c >> 1)) =
-                pack2_bf16(silu_f(a[4 * g]) * a[4 * g + 1], silu_f(a[4 * g + 2]) * a[4 * g + 3]);
-          } else {
-            *reinterpret_cast<u32x2_t*>(og + int64_t(drow[j]) * Nw + c) =
-                pack4_bf16(act_fn<ACT>(a[4 * g]), act_fn<ACT>(a[4 * g + 1]),
-                           act_fn<ACT>(a[4 * g + 2]), act_fn<ACT>(a[4 * g + 3]));
+          for (int q = 0; q < 4; ++q) {
+            const int c = c0 + i * 32 + 8 * q + 4 * h;
+            if (drow[j] >= 0 && c < Nout)
+              *reinterpret_cast<uint32_t*>(og + int64_t(drow[j]) * Nw + (c >> 1)) =
+                  pack2_bf16(silu_f(a[4 * q]) * a[4 * q + 1], silu_f(a[4 * q + 2]) * a[4 * q + 3]);
+          }
+        } else {
+          uint32_t pk[4][2];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) {
+            pk[q][0] = pack2_bf16(act_fn<ACT>(a[4 * q]), act_fn<ACT>(a[4 * q + 1]));
+            pk[q][1] = pack2_bf16(act_fn<ACT>(a[4 * q + 2]), act_fn<ACT>(a[4 * q + 3]));
+          }
+#pragma unroll
+          for (int p = 0; p < 2; ++p) {
+            // h = 0 keeps run 2p and sends run 2p + 1; h = 1 keeps 2p + 1 and sends 2p
+            const uint32_t r0 = __shfl_xor(h ? pk[2 * p][0] : pk[2 * p + 1][0], 32, kWave);
+            const uint32_t r1 = __shfl_xor(h ? pk[2 * p][1] : pk[2 * p + 1][1], 32, kWave);
+            const uint32_t k0 = h ? pk[2 * p + 1][0] : pk[2 * p][0];
+            const uint32_t k1 = h ? pk[2 * p + 1][1] : pk[2 * p][1];
+            const int c = c0 + i * 32 + 16 * p + 8 * h;
+            if (drow[j] >= 0 && c < Nout)
+              *reinterpret_cast<u32x4_t*>(og + int64_t(drow[j]) * Nw + c) =
+                  h ? u32x4_t{r0, r1, k0, k1} : u32x4_t{k0, k1, r0, r1};
           }
         }
+      }
     }
     if (!has_next) break;
     L = Ln;

@@ -9,15 +9,20 @@
 // waves split d into four ranges.  Lane l feeds token l % 16 (A operand) and
 // expert l % 16 (B operand) at MFMA k-row l / 16; the k-rows interleave in
 // runs of one load vector, so a row's four lanes read a contiguous segment
-// of both the token row and the expert row with each load.  Two accumulator
-// chains alternate to hide the MFMA latency; the chains and then the four
+// of both the token row and the expert row with each load.  Four accumulator
+// chains rotate to hide the MFMA latency; the chains and then the four
 // waves' partial sums are added in a fixed order (deterministic).
+//
+// Loads are software-pipelined: a wave's share of d is walked in chunks,
+// the next chunk's loads issued before the current chunk's MFMAs.
 //
 // Epilogue.  Wave w takes the four tokens 4w + g (g = l / 16), one per
 // 16-lane group, lane l % 16 holding experts l % 16 + 16 q.  Top-k: k rounds
 // of a group argmax (ties to the lower expert id, NaN never wins); gate: a
 // softmax in fp64 over the top-k (renormalised) or over all experts, rounded
-// once to fp32.  The statistic C[b][e][i] of the token's experts is read at
+// once to fp32, written by the lane that holds the selected expert.  The
+// 16-lane reductions use DPP row permutations (quad swaps, half-row and row
+// mirrors), so every lane of the group ends with the same value.  The statistic C[b][e][i] of the token's experts is read at
 // kernel start and updated here: C <- f32(f32(beta C) + f32(1 - beta) [e in B_i]).
 #include "common.h"
 #include "internal.h"
@@ -72,14 +77,54 @@ template <> struct Vec<float, 4> {
   }
 };
 
-// Group (16-lane) argmax step: keep the larger value, ties to the lower id.
-__device__ __forceinline__ void argmax_step(float& v, int& i, int o) {
-  const float ov = __shfl_xor(v, o, kWave);
-  const int oi = __shfl_xor(i, o, kWave);
+// 16-lane row permutations (DPP): xor 1, xor 2, half-row mirror, row mirror.
+// Applied in this order, a commutative reduction leaves every lane of the
+// row with the same result.
+constexpr int kDppRow[4] = {0xB1, 0x4E, 0x141, 0x140};
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(dpp_i32<CTRL>(__float_as_int(v)));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const int lo = dpp_i32<CTRL>(static_cast<int>(u & 0xffffffffu));
+  const int hi = dpp_i32<CTRL>(static_cast<int>(u >> 32));
+  return __builtin_bit_cast(double, (uint64_t(uint32_t(hi)) << 32) | uint32_t(lo));
+}
+
+// Row max, row sum (fp64) and row argmax (ties to the lower id).
+__device__ __forceinline__ float row_max(float v) {
+  v = fmaxf(v, dpp_f32<kDppRow[0]>(v));
+  v = fmaxf(v, dpp_f32<kDppRow[1]>(v));
+  v = fmaxf(v, dpp_f32<kDppRow[2]>(v));
+  return fmaxf(v, dpp_f32<kDppRow[3]>(v));
+}
+__device__ __forceinline__ double row_sum(double v) {
+  v += dpp_f64<kDppRow[0]>(v);
+  v += dpp_f64<kDppRow[1]>(v);
+  v += dpp_f64<kDppRow[2]>(v);
+  return v + dpp_f64<kDppRow[3]>(v);
+}
+template <int CTRL>
+__device__ __forceinline__ void argmax_dpp(float& v, int& i) {
+  const float ov = dpp_f32<CTRL>(v);
+  const int oi = dpp_i32<CTRL>(i);
   if (ov > v || (ov == v && oi < i)) {
     v = ov;
     i = oi;
   }
+}
+__device__ __forceinline__ void row_argmax(float& v, int& i) {
+  argmax_dpp<kDppRow[0]>(v, i);
+  argmax_dpp<kDppRow[1]>(v, i);
+  argmax_dpp<kDppRow[2]>(v, i);
+  argmax_dpp<kDppRow[3]>(v, i);
 }
 
 template <typename T, int VW, int NG>
@@ -118,16 +163,18 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
 #pragma unroll
   for (int q = 0; q < NG; ++q) wp[q] = Wg + int64_t(min(16 * q + n, E - 1)) * d + kbase;
 
-  f64x4_t acc[2][NG];
+  constexpr int NCH = 4;  // independent accumulator chains per expert group
+  f64x4_t acc[NCH][NG];
 #pragma unroll
-  for (int c = 0; c < 2; ++c)
+  for (int c = 0; c < NCH; ++c)
 #pragma unroll
     for (int q = 0; q < NG; ++q) acc[c][q] = f64x4_t{0.0, 0.0, 0.0, 0.0};
-  // chunks of CH vectors: every load of a chunk is issued before its MFMAs
-  constexpr int CH = NG == 1 ? 12 : (NG == 2 ? 8 : 4);
-  for (int c0 = 0; c0 < nv; c0 += CH) {
-    typename Vec<T, VW>::raw xr[CH];
-    typename Vec<T, VW>::raw wr[CH][NG];
+  // chunks of CH vectors, double-buffered: the next chunk's loads are issued
+  // before the current chunk's MFMAs
+  constexpr int CH = NG == 1 ? 3 : (NG == 2 ? 2 : 1);
+  typedef typename Vec<T, VW>::raw Raw;
+  Raw xa[CH], wa[CH][NG], xb[CH], wb[CH][NG];
+  auto load = [&](Raw (&xr)[CH], Raw (&wr)[CH][NG], int c0) __attribute__((always_inline)) {
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
       if (c0 + c < nv) {
@@ -137,9 +184,11 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
         for (int q = 0; q < NG; ++q) wr[c][q] = Vec<T, VW>::load(wp[q] + o);
       }
     }
+  };
+  auto compute = [&](const Raw (&xr)[CH], const Raw (&wr)[CH][NG], int c0) __attribute__((always_inline)) {
 #pragma unroll
     for (int c = 0; c < CH; ++c) {
-      if (c0 + c >= nv) continue;  // (not break: a break keeps xr / wr out of registers)
+      if (c0 + c >= nv) continue;
       double xv[VW];
       Vec<T, VW>::widen(xr[c], xv);
 #pragma unroll
@@ -148,16 +197,24 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
         Vec<T, VW>::widen(wr[c][q], wv2);
 #pragma unroll
         for (int u = 0; u < VW; ++u)
-          acc[u & 1][q] =
-              __builtin_amdgcn_mfma_f64_16x16x4f64(xv[u], wv2[u], acc[u & 1][q], 0, 0, 0);
+          acc[u % NCH][q] =
+              __builtin_amdgcn_mfma_f64_16x16x4f64(xv[u], wv2[u], acc[u % NCH][q], 0, 0, 0);
       }
     }
+  };
+  load(xa, wa, 0);
+  for (int c0 = 0; c0 < nv; c0 += 2 * CH) {
+    if (c0 + CH < nv) load(xb, wb, c0 + CH);
+    compute(xa, wa, c0);
+    if (c0 + 2 * CH < nv) load(xa, wa, c0 + 2 * CH);
+    if (c0 + CH < nv) compute(xb, wb, c0 + CH);
   }
   // lane l, register r of a 16 x 16 result: token 4 r + l / 16, expert l % 16
 #pragma unroll
   for (int q = 0; q < NG; ++q)
 #pragma unroll
-    for (int r = 0; r < 4; ++r) s_part[wv][q][r][lane] = acc[0][q][r] + acc[1][q][r];
+    for (int r = 0; r < 4; ++r)
+      s_part[wv][q][r][lane] = (acc[0][q][r] + acc[1][q][r]) + (acc[2][q][r] + acc[3][q][r]);
   __syncthreads();
 
   // ---- epilogue: tokens 4 wv + g, register r = wv of every wave's partial --
@@ -183,8 +240,7 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
   float mx = lv[0];
 #pragma unroll
   for (int q = 1; q < NG; ++q) mx = fmaxf(mx, lv[q]);
-#pragma unroll
-  for (int o = 8; o > 0; o >>= 1) mx = fmaxf(mx, __shfl_xor(mx, o, kWave));
+  mx = row_max(mx);
 
   // top-k: k rounds of a group argmax over the untaken experts
   uint64_t taken = 0;
@@ -200,14 +256,14 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
         ci = e;
       }
     }
-#pragma unroll
-    for (int o = 8; o > 0; o >>= 1) argmax_step(cv, ci, o);
+    row_argmax(cv, ci);
     if (ci >= E) ci = __builtin_ctzll(~taken);  // defensive: cannot happen for k <= E
     sel[p] = ci;
     taken |= 1ull << ci;
   }
 
-  // gate: softmax in fp64 over the top-k (renormalised) or all experts
+  // gate: softmax in fp64 over the top-k (renormalised) or all experts; the
+  // lane holding a selected expert writes its id and weight
   double z[NG];
   double part = 0.0;
 #pragma unroll
@@ -217,19 +273,16 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
     z[q] = in_den ? exp(static_cast<double>(lv[q]) - static_cast<double>(mx)) : 0.0;
     part += z[q];
   }
+  part = row_sum(part);
+  if (live) {
+    for (int p = 0; p < k; ++p) {
 #pragma unroll
-  for (int o = 8; o > 0; o >>= 1) part += __shfl_xor(part, o, kWave);
-  for (int p = 0; p < k; ++p) {
-    const int src = (lane & 48) | (sel[p] & 15);
-    double zs = 0.0;
-#pragma unroll
-    for (int q = 0; q < NG; ++q) {
-      const double v = __shfl(z[q], src, kWave);
-      if ((sel[p] >> 4) == q) zs = v;
-    }
-    if (n == p && live) {
-      e_out[te * k + p] = sel[p];
-      w_out[te * k + p] = static_cast<float>(zs / part);
+      for (int q = 0; q < NG; ++q) {
+        if (sel[p] == 16 * q + n) {
+          e_out[te * k + p] = sel[p];
+          w_out[te * k + p] = static_cast<float>(z[q] / part);
+        }
+      }
     }
   }
 
