@@ -223,7 +223,10 @@ int moeca_debug_set_valid(moeca_layer* layer, int valid);
 /* ---- per-stage timing --------------------------------------------------- */
 enum {
   MOECA_STAGE_ROUTER = 0,  /* router logits, top-k, gate; EMA statistic update */
-  MOECA_STAGE_STAT = 1,    /* entropy of the statistic, thresholds            */
+  MOECA_STAGE_STAT = 1,    /* reserved: the entropy of the statistic and the
+                              thresholds are computed at the start of the
+                              SELECT stage's kernel; this stage launches
+                              nothing and reads as 0                          */
   MOECA_STAGE_SELECT = 2,  /* matching, branch scores, recomputation set,
                               slots, sync mask                                */
   MOECA_STAGE_LISTS = 3,   /* per-expert compaction                            */

@@ -17,55 +17,16 @@ namespace moeca {
 namespace {
 
 // ---------------------------------------------------------------------------
-// Normalised entropy and per-expert threshold, one block per (sample,
-// expert).  The statistic C was advanced by the router in this step.
-//   P(i) = C_i / sum C,  H = -sum P log P,  Hbar = clamp(H / log N, 0, 1)
-//   tau_e = tau0 * (1 + alpha * (2*Hbar - 1))                 (Sec. 4.3)
-// ---------------------------------------------------------------------------
-constexpr int kStatThreads = 256;
-
-__global__ __launch_bounds__(kStatThreads) void entropy_kernel(
-    const float* __restrict__ C, int N, int E, float tau0, float alpha,
-    float* __restrict__ hbar, float* __restrict__ tau) {
-  __shared__ double s_red[kStatThreads / kWave];
-  const int b = blockIdx.x / E;
-  const int e = blockIdx.x % E;
-  const float* Cr = C + (int64_t(b) * E + e) * N;
-
-  double part = 0.0;
-  for (int i = threadIdx.x; i < N; i += kStatThreads) part += static_cast<double>(Cr[i]);
-  const double S = block_sum_f64<kStatThreads / kWave>(part, s_red);
-
-  double hpart = 0.0;
-  if (S > 0.0) {
-    for (int i = threadIdx.x; i < N; i += kStatThreads) {
-      const float c = Cr[i];
-      if (c > 0.0f) {
-        const double P = static_cast<double>(c) / S;
-        hpart -= P * log(P);
-      }
-    }
-  }
-  const double H = block_sum_f64<kStatThreads / kWave>(hpart, s_red);
-
-  if (threadIdx.x == 0) {
-    float hb = 0.0f;
-    if (N > 1 && S > 0.0) {
-      double v = H / log(static_cast<double>(N));
-      v = v < 0.0 ? 0.0 : (v > 1.0 ? 1.0 : v);
-      hb = static_cast<float>(v);
-    }
-    const float centred = __fsub_rn(__fmul_rn(2.0f, hb), 1.0f);
-    const float scaled = __fmul_rn(alpha, centred);
-    hbar[b * E + e] = hb;
-    tau[b * E + e] = __fmul_rn(tau0, __fadd_rn(1.0f, scaled));
-  }
-}
-
-// ---------------------------------------------------------------------------
-// Matching, branch scores, recomputation set, slots, sync mask and
-// per-expert counts; one block per sample, each thread holding up to R of
-// the sample's branches (j = tid + 1024 r) in registers.
+// Thresholds, matching, branch scores, recomputation set, slots, sync mask
+// and per-expert counts; one block per sample, each thread holding up to R
+// of the sample's branches (j = tid + 1024 r) in registers.
+//   entropy (when the router advanced the statistic C in this step; one
+//   wave per expert, fixed-order fp64 sums, Sec. 4.3):
+//     S = sum_i C_i,  H = -sum_{C_i > 0} (C_i / S) (log C_i - log S),
+//     Hbar = clamp(H / log N, 0, 1),  tau_e = tau0 * (1 + alpha * (2*Hbar - 1))
+//   with log C_i stored by the router; log(C_i / S) is formed as the
+//   difference of the two logarithms, so one occupied position gives H = 0
+//   exactly.
 //   q(p): cached slot with the same expert, or -1           (Sec. 4.2)
 //   Delta = |w_p - w_c[q]|,  o = n_c[q] / f32(sum_j n_c[j]),
 //   s = (w_p + lambda1*Delta) + lambda2*o,  m = s - tau_{b,e_p}
@@ -85,8 +46,10 @@ template <int R>
 __global__ __launch_bounds__(kSelThreads) void decide_kernel(
     const int32_t* __restrict__ e_t, const float* __restrict__ w_t,
     const int32_t* __restrict__ e_c, const float* __restrict__ w_c,
-    const float* __restrict__ n_c, const float* __restrict__ tau, int N, int E, int k, int mode,
-    int budget, float lambda1, float lambda2, int32_t* __restrict__ q_out,
+    const float* __restrict__ n_c, const float* __restrict__ C, const double* __restrict__ logc,
+    int with_stat, float tau0, float alpha, float* __restrict__ hbar, float* __restrict__ tau,
+    int N, int E, int k, int mode, int budget, float lambda1, float lambda2,
+    int32_t* __restrict__ q_out,
     float* __restrict__ margin, uint8_t* __restrict__ mask, int32_t* __restrict__ sigma,
     uint8_t* __restrict__ sync, int32_t* __restrict__ cnt_bs, int32_t* __restrict__ stats_bs) {
   extern __shared__ __attribute__((aligned(16))) unsigned char s_dyn[];
@@ -109,7 +72,58 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
 
   if (tid < 64) {
     s_cnt[tid] = 0;
-    if (tid < E) s_tau[tid] = tau[b * E + tid];
+    if (tid < E && !with_stat) s_tau[tid] = tau[b * E + tid];
+  }
+  if (with_stat) {
+    // 0. entropy of the statistic and the threshold, one wave per expert
+    for (int e = wv; e < E; e += kSelWaves) {
+      const float* Cr = C + (int64_t(b) * E + e) * N;
+      const double* Lr = logc + (int64_t(b) * E + e) * N;
+      // positions lane + 64 v of each 1024-position chunk, all loads of a
+      // chunk (C and log C) issued together; four partial sums per lane
+      constexpr int PER = 16;
+      double s4[4] = {0.0, 0.0, 0.0, 0.0};
+      double h4[4] = {0.0, 0.0, 0.0, 0.0};
+      float c[PER];
+      double lc[PER];
+      auto load_chunk = [&](int i0) __attribute__((always_inline)) {
+#pragma unroll
+        for (int v = 0; v < PER; ++v) {
+          const int i = i0 + lane + v * kWave;
+          c[v] = i < N ? Cr[i] : 0.0f;
+          lc[v] = i < N ? Lr[i] : 0.0;
+        }
+      };
+      for (int i0 = 0; i0 < N; i0 += PER * kWave) {
+        load_chunk(i0);
+#pragma unroll
+        for (int v = 0; v < PER; ++v) s4[v & 3] += static_cast<double>(c[v]);
+      }
+      const double S = wave_sum_f64((s4[0] + s4[1]) + (s4[2] + s4[3]));
+      if (S > 0.0) {
+        const double logS = log(S);
+        for (int i0 = 0; i0 < N; i0 += PER * kWave) {
+          if (N > PER * kWave) load_chunk(i0);  // a single chunk is still in registers
+#pragma unroll
+          for (int v = 0; v < PER; ++v)
+            if (c[v] > 0.0f) h4[v & 3] -= (static_cast<double>(c[v]) / S) * (lc[v] - logS);
+        }
+      }
+      const double Hs = wave_sum_f64((h4[0] + h4[1]) + (h4[2] + h4[3]));
+      if (lane == 0) {
+        float hb = 0.0f;
+        if (N > 1 && S > 0.0) {
+          double v = Hs / log(static_cast<double>(N));
+          v = v < 0.0 ? 0.0 : (v > 1.0 ? 1.0 : v);
+          hb = static_cast<float>(v);
+        }
+        const float centred = __fsub_rn(__fmul_rn(2.0f, hb), 1.0f);
+        const float th = __fmul_rn(tau0, __fadd_rn(1.0f, __fmul_rn(alpha, centred)));
+        hbar[b * E + e] = hb;
+        tau[b * E + e] = th;
+        s_tau[e] = th;
+      }
+    }
   }
   if (tid < 256) s_hist[0][tid] = 0;
   if (tid == 0) {
@@ -593,22 +607,17 @@ __global__ void reset_kernel(int32_t* __restrict__ e_c, float* __restrict__ w_c,
 
 }  // namespace
 
-hipError_t launch_entropy(const Shape& s, float tau0, float alpha, const Buffers& b,
-                          hipStream_t st) {
-  launch_kernel(&entropy_kernel, dim3(s.B * s.E), dim3(kStatThreads), 0, st, b.stat, s.N, s.E,
-                tau0, alpha, b.hbar, b.tau);
-  return hipGetLastError();
-}
-
 hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1, float lambda2,
-                         const Buffers& b, hipStream_t st) {
+                         bool with_stat, float tau0, float alpha, const Buffers& b,
+                         hipStream_t st) {
   const int nb = s.N * s.k;
   const size_t lds = size_t(2) * nb;
   if (lds > 64 * 1024) return hipErrorInvalidValue;
 #define MOECA_DECIDE(RR)                                                                      \
   launch_kernel(&decide_kernel<RR>, dim3(s.B), dim3(kSelThreads), uint32_t(lds), st, b.e_t,   \
-                b.w_t, b.e_c, b.w_c, b.n_c, b.tau, s.N, s.E, s.k, sel_mode, budget, lambda1,  \
-                lambda2, b.q, b.margin, b.mask, b.sigma, b.sync, b.cnt_bs, b.stats_bs)
+                b.w_t, b.e_c, b.w_c, b.n_c, b.stat, b.logc, with_stat ? 1 : 0, tau0, alpha,   \
+                b.hbar, b.tau, s.N, s.E, s.k, sel_mode, budget, lambda1, lambda2, b.q,        \
+                b.margin, b.mask, b.sigma, b.sync, b.cnt_bs, b.stats_bs)
   if (nb <= 2 * kSelThreads) {
     MOECA_DECIDE(2);
   } else if (nb <= 8 * kSelThreads) {

@@ -52,6 +52,7 @@ struct Buffers {
   float* n_c;
   void* h_c;
   float* stat;      // [B][E][N]
+  double* logc;     // [B][E][N] log of the statistic (0 where it is 0)
   float* logits;    // [B*N][E]
   int32_t* e_t;
   float* w_t;
@@ -93,10 +94,11 @@ int router_blocks(const Shape& s);
 hipError_t launch_router(const Shape& s, const void* x, const void* W_r, const float* b_r,
                          int norm_topk, float beta, bool update_stat, const Buffers& b,
                          hipStream_t st);
-hipError_t launch_entropy(const Shape& s, float tau0, float alpha, const Buffers& b,
-                          hipStream_t st);
+// with_stat: the router advanced the statistic in this step; the decide
+// kernel then derives the entropy and thresholds first (hbar, tau).
 hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1, float lambda2,
-                         const Buffers& b, hipStream_t st);
+                         bool with_stat, float tau0, float alpha, const Buffers& b,
+                         hipStream_t st);
 hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st);
 // act: MOECA_ACT_* of the policy.  W_*_sh: the shared experts (S > 0).
 hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, const void* W_up_sh,

@@ -47,7 +47,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 enum Region {
   R_E_C, R_W_C, R_N_C, R_H_C, R_STAT, R_LOGITS, R_E_T, R_W_T, R_HBAR, R_TAU, R_MARGIN, R_Q,
   R_MASK, R_SIGMA, R_SYNC, R_OFF, R_LIST, R_POS,
-  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_MID, R_H_SH, R_COUNT
+  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_LOGC, R_MID, R_H_SH, R_COUNT
 };
 
 struct Layout {
@@ -84,6 +84,7 @@ Layout make_layout(const Shape& s) {
   b[R_RFLAGS] = size_t(moeca::router_blocks(s)) * 4;
   b[R_TILES] = size_t(2) * (s.groups() + 1) * 4;
   b[R_ROW_DST] = nbr * 4;
+  b[R_LOGC] = size_t(s.B) * s.E * s.N * 8;
   b[R_MID] = size_t(s.mid_rows()) * s.d_ff * act;
   b[R_H_SH] = size_t(s.S) * ntok * s.d * act;
   Layout L;
@@ -239,6 +240,7 @@ int moeca_bind_workspace(moeca_layer* L, void* dev, size_t bytes) {
   b.n_c = reinterpret_cast<float*>(w + o[R_N_C]);
   b.h_c = w + o[R_H_C];
   b.stat = reinterpret_cast<float*>(w + o[R_STAT]);
+  b.logc = reinterpret_cast<double*>(w + o[R_LOGC]);
   b.logits = reinterpret_cast<float*>(w + o[R_LOGITS]);
   b.e_t = reinterpret_cast<int32_t*>(w + o[R_E_T]);
   b.w_t = reinterpret_cast<float*>(w + o[R_W_T]);
@@ -325,10 +327,10 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
   if (!check(moeca::launch_router(s, x_t, L->W_r, L->b_r, p.norm_topk, p.beta, !uncached, b, st),
              "router"))
     return MOECA_E_HIP;
+  // the entropy and thresholds are derived inside the decide kernel; the
+  // statistic stage launches nothing of its own
   arm();
-  if (!check(uncached ? hipSuccess : moeca::launch_entropy(s, p.tau0, p.alpha, b, st),
-             "entropy"))
-    return MOECA_E_HIP;
+  if (!check(hipSuccess, "entropy")) return MOECA_E_HIP;
   int sel = moeca::kSelFull;
   int budget = 0;
   if (!full) {
@@ -336,7 +338,9 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
     budget = static_cast<int>(std::floor(static_cast<double>(p.ratio) * s.N * s.k + 0.5));
   }
   arm();
-  if (!check(moeca::launch_decide(s, sel, budget, p.lambda1, p.lambda2, b, st), "decide"))
+  if (!check(moeca::launch_decide(s, sel, budget, p.lambda1, p.lambda2, !uncached, p.tau0,
+                                  p.alpha, b, st),
+             "decide"))
     return MOECA_E_HIP;
   arm();
   if (!check(moeca::launch_lists(s, moeca::ffn_plan(s), b, st), "lists")) return MOECA_E_HIP;

@@ -22,8 +22,11 @@
 // softmax in fp64 over the top-k (renormalised) or over all experts, rounded
 // once to fp32, written by the lane that holds the selected expert.  The
 // 16-lane reductions use DPP row permutations (quad swaps, half-row and row
-// mirrors), so every lane of the group ends with the same value.  The statistic C[b][e][i] of the token's experts is read at
-// kernel start and updated here: C <- f32(f32(beta C) + f32(1 - beta) [e in B_i]).
+// mirrors), so every lane of the group ends with the same value.  The
+// statistic C[b][e][i] of the token's experts is read at kernel start and
+// updated here: C <- f32(f32(beta C) + f32(1 - beta) [e in B_i]); with it the
+// kernel stores log C in fp64 (0 where C is 0), the per-position logarithm
+// the entropy of the statistic needs.
 #include "common.h"
 #include "internal.h"
 
@@ -132,7 +135,7 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
     const T* __restrict__ x, const T* __restrict__ Wg, const float* __restrict__ bias,
     int64_t T_tokens, int d, int E, int k, int norm_topk, float* __restrict__ logits,
     int32_t* __restrict__ e_out, float* __restrict__ w_out, int32_t* __restrict__ rflags,
-    float* __restrict__ C, int N, float beta) {
+    float* __restrict__ C, double* __restrict__ logc, int N, float beta) {
   __shared__ double s_part[kRouterWaves][NG][4][kWave];
   __shared__ int s_bad;
   const int lane = threadIdx.x & (kWave - 1);
@@ -295,6 +298,9 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
       float c = __fmul_rn(beta, c_old[q]);
       if ((taken >> e) & 1ull) c = __fadd_rn(c, __fsub_rn(1.0f, beta));
       C[(sb * E + e) * N + si] = c;
+      // log of the new value for the entropy of the statistic (Sec. 4.3),
+      // which the decision kernel sums per (sample, expert)
+      logc[(sb * E + e) * N + si] = c > 0.0f ? log(static_cast<double>(c)) : 0.0;
     }
   }
   if (bad && live) s_bad = 1;
@@ -304,13 +310,14 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
 
 template <typename T, int VW>
 hipError_t launch_vw(const Shape& s, const void* x, const void* W_r, const float* b_r,
-                     int norm_topk, float beta, float* C, const Buffers& b, hipStream_t st) {
+                     int norm_topk, float beta, float* C, double* logc, const Buffers& b,
+                     hipStream_t st) {
   const dim3 grid(router_blocks(s)), block(kRouterWaves * kWave);
   const int ng = (s.E + 15) / 16;
 #define MOECA_ROUTER(NGV)                                                                 \
   launch_kernel(&router_kernel<T, VW, NGV>, grid, block, 0, st, static_cast<const T*>(x), \
                 static_cast<const T*>(W_r), b_r, s.tokens(), s.d, s.E, s.k, norm_topk,    \
-                b.logits, b.e_t, b.w_t, b.rflags, C, s.N, beta)
+                b.logits, b.e_t, b.w_t, b.rflags, C, logc, s.N, beta)
   switch (ng) {
     case 1: MOECA_ROUTER(1); break;
     case 2: MOECA_ROUTER(2); break;
@@ -336,12 +343,13 @@ hipError_t launch_router(const Shape& s, const void* x, const void* W_r, const f
                          hipStream_t st) {
   if (s.d % 64 != 0 || s.E > 64 || s.k > 8 || s.k > s.E) return hipErrorInvalidValue;
   float* C = update_stat ? b.stat : nullptr;
+  double* logc = update_stat ? b.logc : nullptr;
   if (s.bf16) {
     if ((s.d / 16) % 8 == 0)
-      return launch_vw<uint16_t, 8>(s, x, W_r, b_r, norm_topk, beta, C, b, st);
-    return launch_vw<uint16_t, 4>(s, x, W_r, b_r, norm_topk, beta, C, b, st);
+      return launch_vw<uint16_t, 8>(s, x, W_r, b_r, norm_topk, beta, C, logc, b, st);
+    return launch_vw<uint16_t, 4>(s, x, W_r, b_r, norm_topk, beta, C, logc, b, st);
   }
-  return launch_vw<float, 4>(s, x, W_r, b_r, norm_topk, beta, C, b, st);
+  return launch_vw<float, 4>(s, x, W_r, b_r, norm_topk, beta, C, logc, b, st);
 }
 
 }  // namespace moeca
