@@ -51,12 +51,14 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
     int N, int E, int k, int mode, int budget, float lambda1, float lambda2,
     int32_t* __restrict__ q_out,
     float* __restrict__ margin, uint8_t* __restrict__ mask, int32_t* __restrict__ sigma,
-    uint8_t* __restrict__ sync, int32_t* __restrict__ cnt_bs, int32_t* __restrict__ stats_bs) {
+    uint8_t* __restrict__ sync, int32_t* __restrict__ cnt_bs, int32_t* __restrict__ stats_bs,
+    int32_t* __restrict__ cnt_ch) {
   extern __shared__ __attribute__((aligned(16))) unsigned char s_dyn[];
   int8_t* s_q = reinterpret_cast<int8_t*>(s_dyn);            // [N*k] matched slot or -1
   uint8_t* s_mask = reinterpret_cast<uint8_t*>(s_dyn) + N * k; // [N*k]
   __shared__ int s_hist[2][256];
   __shared__ int s_cnt[64];
+  __shared__ int s_cntr[R][64];  // per 1024-branch chunk of the sample
   __shared__ float s_tau[64];
   __shared__ int s_tcnt[R][kSelWaves];
   __shared__ int s_unmatched, s_recompute, s_sync;
@@ -70,6 +72,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   const int lane = tid & (kWave - 1);
   const int wv = tid / kWave;
 
+  for (int i = tid; i < R * 64; i += kSelThreads) (&s_cntr[0][0])[i] = 0;
   if (tid < 64) {
     s_cnt[tid] = 0;
     if (tid < E && !with_stat) s_tau[tid] = tau[b * E + tid];
@@ -135,20 +138,22 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
 
   // 1. matching and scores (cache steps); every operand of a branch is
   // loaded before any is used
-  int qv[R];
+  // per branch: margin and the packed (matched slot + 1) | expert << 4
+  // (few registers per branch: a thread may hold 32 branches)
   float mv[R];
-  int ev[R];
+  int qe[R];
+  auto q_of = [&](int r) __attribute__((always_inline)) { return (qe[r] & 15) - 1; };
+  auto e_of = [&](int r) __attribute__((always_inline)) { return qe[r] >> 4; };
   int unmatched = 0;
 #pragma unroll
   for (int r = 0; r < R; ++r) {
     const int j = tid + kSelThreads * r;
-    qv[r] = -1;
     mv[r] = __int_as_float(0x7f800000);  // +inf: unmatched, always recomputed
-    ev[r] = 0;
+    qe[r] = 0;                            // slot -1, expert 0
     if (j < nb) {
       const int64_t f = base + j;
       const int e = e_t[f];
-      ev[r] = e;
+      qe[r] = e << 4;
       if (mode != kSelFull) {
         const int64_t c0 = base + (j / k) * k;  // the token's first slot
         const float w = w_t[f];
@@ -186,11 +191,14 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
         } else {
           ++unmatched;
         }
-        qv[r] = q;
+        qe[r] = (e << 4) | (q + 1);
         q_out[f] = q;
         margin[f] = mv[r];
       }
     }
+    // keep the scheduler from hoisting the loads of every branch at once
+    // (a thread holds up to 32 branches): four branches per group
+    if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
   }
   if (mode != kSelFull) {
     unmatched = wave_sum_i32(unmatched);
@@ -208,17 +216,12 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   bool take_all_matched = false;
   uint32_t thr = 0;
   int tie_rem = 0;
-  bool tie_take[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) tie_take[r] = false;
+  uint32_t tie_bits = 0;  // bit r: branch r is one of the taken ties
   if (mode == kSelRatio) {
     need = budget - n_unmatched;
     if (need < 0) need = 0;
     if (need >= n_matched) take_all_matched = true;
     if (need > 0 && !take_all_matched) {
-      uint32_t mk[R];
-#pragma unroll
-      for (int r = 0; r < R; ++r) mk[r] = f32_order_key(mv[r]);
       uint32_t prefix = 0;
       int rem = need;
 #pragma unroll
@@ -231,8 +234,9 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
         // once by one lane, the remaining lanes add their own
 #pragma unroll
         for (int r = 0; r < R; ++r) {
-          bool part = qv[r] >= 0 && ((mk[r] ^ prefix) & hi_mask) == 0u;
-          const int bin = static_cast<int>((mk[r] >> shift) & 255u);
+          const uint32_t mk = f32_order_key(mv[r]);
+          bool part = q_of(r) >= 0 && ((mk ^ prefix) & hi_mask) == 0u;
+          const int bin = static_cast<int>((mk >> shift) & 255u);
 #pragma unroll
           for (int it = 0; it < 2; ++it) {
             const uint64_t todo = __ballot(part);
@@ -279,11 +283,10 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
       tie_rem = rem;
       // keys equal to T: take the tie_rem lowest flat ids (j = tid + 1024 r,
       // so the order is r-major, then wave, then lane)
-      uint64_t tb[R];
 #pragma unroll
       for (int r = 0; r < R; ++r) {
-        tb[r] = __ballot(qv[r] >= 0 && mk[r] == thr);
-        if (lane == 0) s_tcnt[r][wv] = __popcll(tb[r]);
+        const uint64_t tb = __ballot(q_of(r) >= 0 && f32_order_key(mv[r]) == thr);
+        if (lane == 0) s_tcnt[r][wv] = __popcll(tb);
       }
       __syncthreads();
       int before = 0;
@@ -295,8 +298,9 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
           in_r += c;
           if (w2 < wv) below += c;
         }
-        const bool flag = ((tb[r] >> lane) & 1ull) != 0;
-        tie_take[r] = flag && before + below + lane_rank(tb[r]) < tie_rem;
+        const uint64_t tb = __ballot(q_of(r) >= 0 && f32_order_key(mv[r]) == thr);
+        const bool flag = ((tb >> lane) & 1ull) != 0;
+        if (flag && before + below + lane_rank(tb) < tie_rem) tie_bits |= 1u << r;
         before += in_r;
       }
     }
@@ -308,7 +312,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
     const int j = tid + kSelThreads * r;
     bool rc = false;
     if (j < nb) {
-      if (mode == kSelFull || qv[r] < 0) {
+      if (mode == kSelFull || q_of(r) < 0) {
         rc = true;
       } else if (mode == kSelThreshold) {
         rc = mv[r] > 0.0f;
@@ -318,12 +322,15 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
         rc = false;
       } else {
         const uint32_t mk = f32_order_key(mv[r]);
-        rc = mk > thr || tie_take[r];
+        rc = mk > thr || ((tie_bits >> r) & 1u) != 0;
       }
       mask[base + j] = rc ? 1 : 0;
       s_mask[j] = rc ? 1 : 0;
-      s_q[j] = static_cast<int8_t>(qv[r]);
-      if (rc) atomicAdd(&s_cnt[ev[r]], 1);
+      s_q[j] = static_cast<int8_t>(q_of(r));
+      if (rc) {
+        atomicAdd(&s_cnt[e_of(r)], 1);
+        atomicAdd(&s_cntr[r][e_of(r)], 1);
+      }
     }
   }
   __syncthreads();
@@ -369,6 +376,10 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   }
   __syncthreads();
   if (tid < E) cnt_bs[b * E + tid] = s_cnt[tid];
+  // per-chunk counts [B][RC][E] for the lists kernel (RC chunks of 1024 branches)
+  const int rc_n = (nb + kSelThreads - 1) / kSelThreads;
+  for (int i = tid; i < rc_n * E; i += kSelThreads)
+    cnt_ch[(int64_t(b) * rc_n + i / E) * E + i % E] = s_cntr[i / E][i % E];
   if (tid == 0) {
     stats_bs[b * 4 + 0] = s_recompute;
     stats_bs[b * 4 + 1] = mode == kSelFull ? 0 : n_unmatched;
@@ -377,16 +388,6 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   }
 }
 
-// ---------------------------------------------------------------------------
-// Per-expert lists of recomputed branches, ascending flat id within each
-// expert; one block per sample, each thread holding up to R of the sample's
-// branches (j = tid + 1024 r).  All inputs are loaded first.  Wave 0 turns the
-// [B][E] count table into this sample's write base per expert (and, in block
-// 0, the expert offsets and the GEMM tile tables); each wave counts and ranks
-// its selected branches per expert with ballots; after one barrier every
-// branch knows its place: branches of earlier r, then of earlier waves, then
-// of lower lanes come first (stable, no atomics).
-// ---------------------------------------------------------------------------
 // Group table entries E..E+S: the shared experts (Sec. 2.3, shared-expert
 // MoE eq.) follow the routed ones in the FFN's grouped GEMM, T rows each (every
 // token, in token order), so their offsets and tile prefixes continue the
@@ -404,48 +405,69 @@ __device__ __forceinline__ void write_shared_groups(int32_t* __restrict__ off,
   }
 }
 
-template <int R>
+// ---------------------------------------------------------------------------
+// Per-expert lists of recomputed branches, ascending flat id within each
+// expert; one 1024-thread block per chunk of 1024 consecutive branches of a
+// sample (chunk c of sample b covers flat ids b N k + 1024 c ..).  Every
+// block reads the [B][RC][E] chunk count table written by the decide kernel
+// and derives, per expert, the total (-> expert offsets, block 0 also writes
+// them and the GEMM tile tables) and the count in the chunks before its own
+// in flat order (-> its write base).  Within the chunk each wave ranks its
+// selected branches per expert with ballots; branches of earlier waves, then
+// of lower lanes come first (stable, no atomics).
+// ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kSelThreads) void lists_kernel(
     const uint8_t* __restrict__ mask, const int32_t* __restrict__ e_t,
-    const int32_t* __restrict__ cnt_bs, int B, int N, int E, int S, int k, int tm, int nt_up,
+    const int32_t* __restrict__ cnt_ch, int B, int N, int E, int S, int k, int tm, int nt_up,
     int nt_down, const int32_t* __restrict__ sigma, int32_t* __restrict__ off,
     int32_t* __restrict__ tiles, int32_t* __restrict__ list, int32_t* __restrict__ pos,
     int32_t* __restrict__ row_dst) {
+  __shared__ int s_part_tot[kSelThreads];
+  __shared__ int s_part_bef[kSelThreads];
   __shared__ int s_base[64];
-  __shared__ int s_wcnt[R][kSelWaves][64];
-  const int b = blockIdx.x;
+  __shared__ int s_wcnt[kSelWaves][64];
   const int nb = N * k;
-  const int64_t base = int64_t(b) * nb;
+  const int rc_n = (nb + kSelThreads - 1) / kSelThreads;
+  const int b = blockIdx.x / rc_n;
+  const int c = blockIdx.x % rc_n;
+  const int my = blockIdx.x;  // flat chunk index (b rc_n + c)
+  const int nchunks = B * rc_n;
   const int tid = threadIdx.x;
   const int lane = tid & (kWave - 1);
   const int wv = tid / kWave;
 
-  int ev[R], sg[R];
-  bool sel[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int j = tid + kSelThreads * r;
-    sel[r] = false;
-    ev[r] = -1;
-    sg[r] = 0;
-    if (j < nb) {
-      sel[r] = mask[base + j] != 0;
-      ev[r] = e_t[base + j];
-      sg[r] = sigma[base + j];
+  // this block's branch, loaded first
+  const int j = c * kSelThreads + tid;
+  const int64_t f = int64_t(b) * nb + j;
+  const bool in = j < nb;
+  const bool sel = in && mask[f] != 0;
+  const int ev = sel ? e_t[f] : -1;
+  const int sg = sel ? sigma[f] : 0;
+
+  // per expert: total over all chunks and count in the chunks before this one
+  const int parts = kSelThreads / E;  // thread (e0, part) for part < parts; E <= 64
+  const int e0 = tid % E, part = tid / E;
+  int tot = 0, bef = 0;
+  if (part < parts) {
+    for (int ch = part; ch < nchunks; ch += parts) {
+      const int v = cnt_ch[int64_t(ch) * E + e0];
+      tot += v;
+      if (ch < my) bef += v;
     }
   }
+  s_part_tot[tid] = tot;
+  s_part_bef[tid] = bef;
+  __syncthreads();
   if (wv == 0) {
-    // lane e: expert e's total over all samples and over the samples before b
-    int tot = 0, below = 0;
+    int t = 0, bf = 0;
     if (lane < E) {
-      for (int b2 = 0; b2 < B; ++b2) {
-        const int c = cnt_bs[b2 * E + lane];
-        tot += c;
-        if (b2 < b) below += c;
+      for (int pp = 0; pp < parts; ++pp) {
+        t += s_part_tot[pp * E + lane];
+        bf += s_part_bef[pp * E + lane];
       }
     }
-    const int mt = (tot + tm - 1) / tm;
-    int o = tot, tu = mt * nt_up, td = mt * nt_down;  // inclusive scans over experts
+    const int mt = (t + tm - 1) / tm;
+    int o = t, tu = mt * nt_up, td = mt * nt_down;  // inclusive scans over experts
 #pragma unroll
     for (int dd = 1; dd < kWave; dd <<= 1) {
       const int vo = __shfl_up(o, dd, kWave);
@@ -457,136 +479,35 @@ __global__ __launch_bounds__(kSelThreads) void lists_kernel(
         td += vd;
       }
     }
-    if (lane < E) s_base[lane] = o - tot + below;
-    if (b == 0 && lane < E) {
+    if (lane < E) s_base[lane] = o - t + bf;
+    if (my == 0 && lane < E) {
       // exclusive prefixes per expert; the last expert also writes the
       // prefixes of the shared experts and the totals
-      off[lane] = o - tot;
+      off[lane] = o - t;
       tiles[lane] = tu - mt * nt_up;
       tiles[E + S + 1 + lane] = td - mt * nt_down;
       if (lane == E - 1) write_shared_groups(off, tiles, E, S, B * N, tm, nt_up, nt_down, o, tu, td);
     }
   }
-  int rk[R];
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    rk[r] = 0;
-    for (int ee = 0; ee < E; ++ee) {
-      const bool mine = sel[r] && ev[r] == ee;
-      const uint64_t bal = __ballot(mine);
-      if (lane == ee) s_wcnt[r][wv][ee] = __popcll(bal);
-      if (mine) rk[r] = lane_rank(bal);
-    }
+  int rk = 0;
+  for (int ee = 0; ee < E; ++ee) {
+    const bool mine = ev == ee;
+    const uint64_t bal = __ballot(mine);
+    if (lane == ee) s_wcnt[wv][ee] = __popcll(bal);
+    if (mine) rk = lane_rank(bal);
   }
   __syncthreads();
-
-#pragma unroll
-  for (int r = 0; r < R; ++r) {
-    const int j = tid + kSelThreads * r;
-    if (j >= nb) continue;
-    const int64_t f = base + j;
-    if (!sel[r]) {
-      pos[f] = -1;
-      continue;
-    }
-    const int e = ev[r];
-    int before = 0;
-    for (int r2 = 0; r2 < r; ++r2)
-      for (int w2 = 0; w2 < kSelWaves; ++w2) before += s_wcnt[r2][w2][e];
-    for (int w2 = 0; w2 < wv; ++w2) before += s_wcnt[r][w2][e];
-    const int idx = s_base[e] + before + rk[r];
-    list[idx] = static_cast<int32_t>(f);
-    pos[f] = idx;
-    row_dst[idx] = static_cast<int32_t>((f / k) * k + sg[r]);
+  if (!in) return;
+  if (!sel) {
+    pos[f] = -1;
+    return;
   }
-}
-
-// ---------------------------------------------------------------------------
-// Per-expert lists for samples of more than 8192 branches (the register
-// version below would not fit its count table in LDS): ascending flat id
-// within each expert; one block per sample.  Each block derives its write base per
-// expert from the [B][E] count table, then walks its branches in flat order
-// in chunks of 1024 and ranks them with wave ballots (stable, no atomics).
-// ---------------------------------------------------------------------------
-__global__ __launch_bounds__(kSelThreads) void lists_chunked_kernel(
-    const uint8_t* __restrict__ mask, const int32_t* __restrict__ e_t,
-    const int32_t* __restrict__ cnt_bs, int B, int N, int E, int S, int k, int tm, int nt_up,
-    int nt_down, const int32_t* __restrict__ sigma, int32_t* __restrict__ off,
-    int32_t* __restrict__ tiles, int32_t* __restrict__ list, int32_t* __restrict__ pos,
-    int32_t* __restrict__ row_dst) {
-  __shared__ int s_base[64];
-  __shared__ int s_run[64];
-  __shared__ int s_wcnt[kSelWaves][64];
-  const int b = blockIdx.x;
-  const int nb = N * k;
-  const int64_t base = int64_t(b) * nb;
-  const int tid = threadIdx.x;
-  const int lane = tid & (kWave - 1);
-  const int wv = tid / kWave;
-
-  // per expert: total count and count in samples before this one
-  if (tid < E) {
-    int tot = 0, below = 0;
-    for (int b2 = 0; b2 < B; ++b2) {
-      const int c = cnt_bs[b2 * E + tid];
-      tot += c;
-      if (b2 < b) below += c;
-    }
-    s_base[tid] = below;
-    s_run[tid] = tot;
-  }
-  __syncthreads();
-  if (tid == 0) {
-    int acc = 0, tu = 0, td = 0;
-    for (int e = 0; e < E; ++e) {
-      const int tot = s_run[e];
-      if (b == 0) {
-        off[e] = acc;
-        tiles[e] = tu;
-        tiles[E + S + 1 + e] = td;
-      }
-      s_base[e] += acc;
-      s_run[e] = 0;
-      acc += tot;
-      const int mt = (tot + tm - 1) / tm;
-      tu += mt * nt_up;
-      td += mt * nt_down;
-    }
-    if (b == 0) write_shared_groups(off, tiles, E, S, B * N, tm, nt_up, nt_down, acc, tu, td);
-  }
-  __syncthreads();
-
-  for (int c0 = 0; c0 < nb; c0 += kSelThreads) {
-    const int j = c0 + tid;
-    const bool in = j < nb;
-    const bool sel = in && mask[base + j] != 0;
-    const int e = sel ? e_t[base + j] : -1;
-    int rank = 0;
-    for (int ee = 0; ee < E; ++ee) {
-      const uint64_t bal = __ballot(e == ee);
-      if (lane == 0) s_wcnt[wv][ee] = __popcll(bal);
-      if (e == ee) rank = lane_rank(bal);
-    }
-    __syncthreads();
-    if (sel) {
-      int before = 0;
-      for (int w2 = 0; w2 < wv; ++w2) before += s_wcnt[w2][e];
-      const int idx = s_base[e] + s_run[e] + before + rank;
-      const int64_t f = base + j;
-      list[idx] = static_cast<int32_t>(f);
-      pos[f] = idx;
-      row_dst[idx] = static_cast<int32_t>((f / k) * k + sigma[f]);
-    } else if (in) {
-      pos[base + j] = -1;
-    }
-    __syncthreads();
-    if (tid < E) {
-      int tot = 0;
-      for (int w2 = 0; w2 < kSelWaves; ++w2) tot += s_wcnt[w2][tid];
-      s_run[tid] += tot;
-    }
-    __syncthreads();
-  }
+  int before = 0;
+  for (int w2 = 0; w2 < wv; ++w2) before += s_wcnt[w2][ev];
+  const int idx = s_base[ev] + before + rk;
+  list[idx] = static_cast<int32_t>(f);
+  pos[f] = idx;
+  row_dst[idx] = static_cast<int32_t>((f / k) * k + sg);
 }
 
 // ---------------------------------------------------------------------------
@@ -617,7 +538,7 @@ hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1
   launch_kernel(&decide_kernel<RR>, dim3(s.B), dim3(kSelThreads), uint32_t(lds), st, b.e_t,   \
                 b.w_t, b.e_c, b.w_c, b.n_c, b.stat, b.logc, with_stat ? 1 : 0, tau0, alpha,   \
                 b.hbar, b.tau, s.N, s.E, s.k, sel_mode, budget, lambda1, lambda2, b.q,        \
-                b.margin, b.mask, b.sigma, b.sync, b.cnt_bs, b.stats_bs)
+                b.margin, b.mask, b.sigma, b.sync, b.cnt_bs, b.stats_bs, b.cnt_ch)
   if (nb <= 2 * kSelThreads) {
     MOECA_DECIDE(2);
   } else if (nb <= 8 * kSelThreads) {
@@ -635,18 +556,11 @@ hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, h
   const int nb = s.N * s.k;
   const int nt_up = (s.up_rows() + plan.tn_up - 1) / plan.tn_up;
   const int nt_down = (s.d + plan.tn_down - 1) / plan.tn_down;
-#define MOECA_LISTS(KER)                                                                       \
-  launch_kernel(&KER, dim3(s.B), dim3(kSelThreads), 0, st, b.mask, b.e_t, b.cnt_bs, s.B, s.N, \
-                s.E, s.S, s.k, plan.tm, nt_up, nt_down, b.sigma, b.off, b.tiles, b.list,      \
-                b.pos, b.row_dst)
-  if (nb <= 2 * kSelThreads) {
-    MOECA_LISTS(lists_kernel<2>);
-  } else if (nb <= 8 * kSelThreads) {
-    MOECA_LISTS(lists_kernel<8>);
-  } else {
-    MOECA_LISTS(lists_chunked_kernel);
-  }
-#undef MOECA_LISTS
+  const int rc_n = (nb + kSelThreads - 1) / kSelThreads;
+  if (s.E > 64) return hipErrorInvalidValue;
+  launch_kernel(&lists_kernel, dim3(s.B * rc_n), dim3(kSelThreads), 0, st, b.mask, b.e_t,
+                b.cnt_ch, s.B, s.N, s.E, s.S, s.k, plan.tm, nt_up, nt_down, b.sigma, b.off,
+                b.tiles, b.list, b.pos, b.row_dst);
   return hipGetLastError();
 }
 

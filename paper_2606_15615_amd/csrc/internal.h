@@ -68,6 +68,7 @@ struct Buffers {
   int32_t* list;
   int32_t* pos;
   int32_t* cnt_bs;  // [B][E] recomputed branches per sample and expert
+  int32_t* cnt_ch;  // [B][RC][E] the same per chunk of 1024 branches (RC = ceil(N k / 1024))
   int32_t* stats_bs;// [B][4] recompute, unmatched, matched, sync per sample
   int32_t* rflags;  // router: one non-finite flag per block
   int32_t* tiles;   // [2][E+S+1] grouped-GEMM tile prefix per group (up, down)

@@ -47,7 +47,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 enum Region {
   R_E_C, R_W_C, R_N_C, R_H_C, R_STAT, R_LOGITS, R_E_T, R_W_T, R_HBAR, R_TAU, R_MARGIN, R_Q,
   R_MASK, R_SIGMA, R_SYNC, R_OFF, R_LIST, R_POS,
-  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_LOGC, R_MID, R_H_SH, R_COUNT
+  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_LOGC, R_CNT_CH, R_MID, R_H_SH, R_COUNT
 };
 
 struct Layout {
@@ -85,6 +85,7 @@ Layout make_layout(const Shape& s) {
   b[R_TILES] = size_t(2) * (s.groups() + 1) * 4;
   b[R_ROW_DST] = nbr * 4;
   b[R_LOGC] = size_t(s.B) * s.E * s.N * 8;
+  b[R_CNT_CH] = size_t(s.B) * ((size_t(s.N) * s.k + 1023) / 1024) * s.E * 4;
   b[R_MID] = size_t(s.mid_rows()) * s.d_ff * act;
   b[R_H_SH] = size_t(s.S) * ntok * s.d * act;
   Layout L;
@@ -255,6 +256,7 @@ int moeca_bind_workspace(moeca_layer* L, void* dev, size_t bytes) {
   b.list = reinterpret_cast<int32_t*>(w + o[R_LIST]);
   b.pos = reinterpret_cast<int32_t*>(w + o[R_POS]);
   b.cnt_bs = reinterpret_cast<int32_t*>(w + o[R_CNT_BS]);
+  b.cnt_ch = reinterpret_cast<int32_t*>(w + o[R_CNT_CH]);
   b.stats_bs = reinterpret_cast<int32_t*>(w + o[R_STATS_BS]);
   b.rflags = reinterpret_cast<int32_t*>(w + o[R_RFLAGS]);
   b.tiles = reinterpret_cast<int32_t*>(w + o[R_TILES]);
