@@ -232,11 +232,17 @@ def main():
         torch.cuda.synchronize()
         return e0.elapsed_time(e1) / (t1 - t0)
 
-    def graph_timed(L):
-        """Capture the K steps in one HIP graph, replay it once, time it."""
+    def graph_timed(L, warm):
+        """Capture the K steps in one HIP graph; replay it once untimed (the
+        first replay also uploads the graph), rewind the layer to the same
+        state (reset + the warm-up steps, eager), then time one replay."""
         g = torch.cuda.CUDAGraph()
         with torch.cuda.graph(g):
             run(L, Wm, T)
+        g.replay()
+        torch.cuda.synchronize()
+        L.reset()
+        run(L, 0, warm)
         torch.cuda.synchronize()
         e0.record(stream)
         g.replay()
@@ -262,7 +268,7 @@ def main():
             try:
                 L.reset()
                 run(L, 0, warm)
-                ms_graph = graph_timed(L)
+                ms_graph = graph_timed(L, warm)
                 graphed = True
             except Exception as exc:  # capture unsupported: report the eager numbers
                 log(f"[bench] graph capture failed ({exc}); reporting eager timings")

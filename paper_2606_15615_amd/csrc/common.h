@@ -30,17 +30,76 @@ template <> struct Act<float> {
   static __device__ __forceinline__ float from_f32(float v) { return v; }
 };
 
-// ---- wave reductions (xor butterfly: every lane ends with the same sum) ---
+// ---- lane exchange within 16-lane rows (DPP) -------------------------------
+// Row permutations: xor 1, xor 2, half-row mirror, row mirror.  Applied in
+// this order, a commutative reduction leaves every lane of the row with the
+// same result (each step combines two lanes that already agree).
+constexpr int kDppRow[4] = {0xB1, 0x4E, 0x141, 0x140};
+
+template <int CTRL>
+__device__ __forceinline__ int dpp_i32(int v) {
+  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
+}
+template <int CTRL>
+__device__ __forceinline__ float dpp_f32(float v) {
+  return __int_as_float(dpp_i32<CTRL>(__float_as_int(v)));
+}
+template <int CTRL>
+__device__ __forceinline__ double dpp_f64(double v) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const int lo = dpp_i32<CTRL>(static_cast<int>(u & 0xffffffffu));
+  const int hi = dpp_i32<CTRL>(static_cast<int>(u >> 32));
+  return __builtin_bit_cast(double, (uint64_t(uint32_t(hi)) << 32) | uint32_t(lo));
+}
+
+__device__ __forceinline__ double row_sum_f64(double v) {
+  v += dpp_f64<kDppRow[0]>(v);
+  v += dpp_f64<kDppRow[1]>(v);
+  v += dpp_f64<kDppRow[2]>(v);
+  return v + dpp_f64<kDppRow[3]>(v);
+}
+__device__ __forceinline__ int row_sum_i32(int v) {
+  v += dpp_i32<kDppRow[0]>(v);
+  v += dpp_i32<kDppRow[1]>(v);
+  v += dpp_i32<kDppRow[2]>(v);
+  return v + dpp_i32<kDppRow[3]>(v);
+}
+
+// ---- wave reductions: every lane ends with the same value -----------------
+// Row sums (DPP), then the four row results in a fixed order,
+// (row0 + row1) + (row2 + row3).
 __device__ __forceinline__ double wave_sum_f64(double v) {
+  v = row_sum_f64(v);
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  double r[4];
 #pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  for (int q = 0; q < 4; ++q) {
+    const uint32_t lo = __builtin_amdgcn_readlane(static_cast<int>(u & 0xffffffffu), 16 * q);
+    const uint32_t hi = __builtin_amdgcn_readlane(static_cast<int>(u >> 32), 16 * q);
+    r[q] = __builtin_bit_cast(double, (uint64_t(hi) << 32) | lo);
+  }
+  return (r[0] + r[1]) + (r[2] + r[3]);
 }
 
 __device__ __forceinline__ int wave_sum_i32(int v) {
-#pragma unroll
-  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, kWave);
-  return v;
+  v = row_sum_i32(v);
+  return (__builtin_amdgcn_readlane(v, 0) + __builtin_amdgcn_readlane(v, 16)) +
+         (__builtin_amdgcn_readlane(v, 32) + __builtin_amdgcn_readlane(v, 48));
+}
+
+// Inclusive prefix sum over the wave's lanes (integers): a Hillis-Steele
+// scan inside each 16-lane row (row shifts by 1, 2, 4, 8; lanes shifted in
+// from outside the row read 0), then the totals of the rows before.
+__device__ __forceinline__ int wave_incl_scan_i32(int v) {
+  v += __builtin_amdgcn_update_dpp(0, v, 0x111, 0xF, 0xF, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x112, 0xF, 0xF, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x114, 0xF, 0xF, true);
+  v += __builtin_amdgcn_update_dpp(0, v, 0x118, 0xF, 0xF, true);
+  const int row = (threadIdx.x & (kWave - 1)) >> 4;
+  const int t0 = __builtin_amdgcn_readlane(v, 15);
+  const int t1 = __builtin_amdgcn_readlane(v, 31);
+  const int t2 = __builtin_amdgcn_readlane(v, 47);
+  return v + (row > 0 ? t0 : 0) + (row > 1 ? t1 : 0) + (row > 2 ? t2 : 0);
 }
 
 // Block-wide fp64 sum for blocks of NW waves; every thread gets the result.

@@ -8,6 +8,8 @@
 // in the order the method states them (this file is built without FMA
 // contraction), and reductions are fp64 sums of exact values rounded once.
 // No atomic operation decides an order: counts use integer atomics only.
+#include <cmath>
+
 #include "common.h"
 #include "internal.h"
 
@@ -22,11 +24,11 @@ namespace {
 // of the sample's branches (j = tid + 1024 r) in registers.
 //   entropy (when the router advanced the statistic C in this step; one
 //   wave per expert, fixed-order fp64 sums, Sec. 4.3):
-//     S = sum_i C_i,  H = -sum_{C_i > 0} (C_i / S) (log C_i - log S),
+//     S = sum_i C_i,  H = -(1/S) sum_{C_i > 0} C_i (log C_i - log S),
 //     Hbar = clamp(H / log N, 0, 1),  tau_e = tau0 * (1 + alpha * (2*Hbar - 1))
-//   with log C_i stored by the router; log(C_i / S) is formed as the
-//   difference of the two logarithms, so one occupied position gives H = 0
-//   exactly.
+//   with log C_i stored by the router and log N from the host's libm;
+//   log(C_i / S) is formed as the difference of the two logarithms, so one
+//   occupied position gives H = 0 exactly.
 //   q(p): cached slot with the same expert, or -1           (Sec. 4.2)
 //   Delta = |w_p - w_c[q]|,  o = n_c[q] / f32(sum_j n_c[j]),
 //   s = (w_p + lambda1*Delta) + lambda2*o,  m = s - tau_{b,e_p}
@@ -47,7 +49,8 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
     const int32_t* __restrict__ e_t, const float* __restrict__ w_t,
     const int32_t* __restrict__ e_c, const float* __restrict__ w_c,
     const float* __restrict__ n_c, const float* __restrict__ C, const double* __restrict__ logc,
-    int with_stat, float tau0, float alpha, float* __restrict__ hbar, float* __restrict__ tau,
+    int with_stat, double log_n, float tau0, float alpha, float* __restrict__ hbar,
+    float* __restrict__ tau,
     int N, int E, int k, int mode, int budget, float lambda1, float lambda2,
     int32_t* __restrict__ q_out,
     float* __restrict__ margin, uint8_t* __restrict__ mask, int32_t* __restrict__ sigma,
@@ -56,14 +59,12 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   extern __shared__ __attribute__((aligned(16))) unsigned char s_dyn[];
   int8_t* s_q = reinterpret_cast<int8_t*>(s_dyn);            // [N*k] matched slot or -1
   uint8_t* s_mask = reinterpret_cast<uint8_t*>(s_dyn) + N * k; // [N*k]
-  __shared__ int s_hist[2][256];
+  __shared__ int s_hist[3][256];
   __shared__ int s_cnt[64];
   __shared__ int s_cntr[R][64];  // per 1024-branch chunk of the sample
   __shared__ float s_tau[64];
   __shared__ int s_tcnt[R][kSelWaves];
   __shared__ int s_unmatched, s_recompute, s_sync;
-  __shared__ unsigned s_bin;
-  __shared__ int s_remaining;
 
   const int b = blockIdx.x;
   const int nb = N * k;
@@ -87,36 +88,36 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
       constexpr int PER = 16;
       double s4[4] = {0.0, 0.0, 0.0, 0.0};
       double h4[4] = {0.0, 0.0, 0.0, 0.0};
-      float c[PER];
-      double lc[PER];
+      double c[PER], lc[PER];  // C and log C; both 0 where C = 0 or past N
       auto load_chunk = [&](int i0) __attribute__((always_inline)) {
 #pragma unroll
         for (int v = 0; v < PER; ++v) {
           const int i = i0 + lane + v * kWave;
-          c[v] = i < N ? Cr[i] : 0.0f;
+          c[v] = i < N ? static_cast<double>(Cr[i]) : 0.0;
           lc[v] = i < N ? Lr[i] : 0.0;
         }
       };
       for (int i0 = 0; i0 < N; i0 += PER * kWave) {
         load_chunk(i0);
 #pragma unroll
-        for (int v = 0; v < PER; ++v) s4[v & 3] += static_cast<double>(c[v]);
+        for (int v = 0; v < PER; ++v) s4[v & 3] += c[v];
       }
       const double S = wave_sum_f64((s4[0] + s4[1]) + (s4[2] + s4[3]));
+      double Hs = 0.0;
       if (S > 0.0) {
         const double logS = log(S);
         for (int i0 = 0; i0 < N; i0 += PER * kWave) {
           if (N > PER * kWave) load_chunk(i0);  // a single chunk is still in registers
+          // a position with C = 0 adds an exact zero (0 * finite)
 #pragma unroll
-          for (int v = 0; v < PER; ++v)
-            if (c[v] > 0.0f) h4[v & 3] -= (static_cast<double>(c[v]) / S) * (lc[v] - logS);
+          for (int v = 0; v < PER; ++v) h4[v & 3] += c[v] * (lc[v] - logS);
         }
+        Hs = -wave_sum_f64((h4[0] + h4[1]) + (h4[2] + h4[3])) / S;
       }
-      const double Hs = wave_sum_f64((h4[0] + h4[1]) + (h4[2] + h4[3]));
       if (lane == 0) {
         float hb = 0.0f;
         if (N > 1 && S > 0.0) {
-          double v = Hs / log(static_cast<double>(N));
+          double v = Hs / log_n;
           v = v < 0.0 ? 0.0 : (v > 1.0 ? 1.0 : v);
           hb = static_cast<float>(v);
         }
@@ -128,7 +129,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
       }
     }
   }
-  if (tid < 256) s_hist[0][tid] = 0;
+  if (tid < 512) (&s_hist[0][0])[tid] = 0;
   if (tid == 0) {
     s_unmatched = 0;
     s_recompute = 0;
@@ -138,22 +139,47 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
 
   // 1. matching and scores (cache steps); every operand of a branch is
   // loaded before any is used
-  // per branch: margin and the packed (matched slot + 1) | expert << 4
-  // (few registers per branch: a thread may hold 32 branches)
-  float mv[R];
-  int qe[R];
-  auto q_of = [&](int r) __attribute__((always_inline)) { return (qe[r] & 15) - 1; };
-  auto e_of = [&](int r) __attribute__((always_inline)) { return qe[r] >> 4; };
+  // per branch: margin and the packed (matched slot + 1) | expert << 4,
+  // kept in registers while a thread holds at most 8 branches.  With more
+  // (up to 32) nothing per branch stays in registers and the per-branch
+  // loops are not unrolled: the later passes read the margin back from the
+  // margin buffer this thread wrote (the values stay in L2), the slot from
+  // its LDS copy s_q and the expert from e_t.
+  constexpr bool kMvRegs = R <= 8;
+  constexpr int kU = kMvRegs ? R : 1;  // unroll factor of the per-branch loops
+  float mv[kMvRegs ? R : 1];
+  int qe[kMvRegs ? R : 1];
+  // outside the sample (j >= nb) a branch reads as unmatched with margin +inf
+  auto mval = [&](int r) __attribute__((always_inline)) -> float {
+    if constexpr (kMvRegs) {
+      return mv[r];
+    } else {
+      const int j = tid + kSelThreads * r;
+      return j < nb ? margin[base + j] : __int_as_float(0x7f800000);
+    }
+  };
+  auto q_of = [&](int r) __attribute__((always_inline)) -> int {
+    if constexpr (kMvRegs) {
+      return (qe[r] & 15) - 1;
+    } else {
+      const int j = tid + kSelThreads * r;
+      return j < nb ? static_cast<int>(s_q[j]) : -1;
+    }
+  };
+  auto e_of = [&](int r) __attribute__((always_inline)) -> int {
+    if constexpr (kMvRegs) return qe[r] >> 4;
+    else return e_t[base + tid + kSelThreads * r];
+  };
   int unmatched = 0;
-#pragma unroll
+#pragma unroll kU
   for (int r = 0; r < R; ++r) {
     const int j = tid + kSelThreads * r;
-    mv[r] = __int_as_float(0x7f800000);  // +inf: unmatched, always recomputed
-    qe[r] = 0;                            // slot -1, expert 0
+    float m = __int_as_float(0x7f800000);  // +inf: unmatched, always recomputed
+    int qv = 0;                           // packed: slot -1, expert 0
     if (j < nb) {
       const int64_t f = base + j;
       const int e = e_t[f];
-      qe[r] = e << 4;
+      qv = e << 4;
       if (mode != kSelFull) {
         const int64_t c0 = base + (j / k) * k;  // the token's first slot
         const float w = w_t[f];
@@ -187,18 +213,25 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
           const float o = denf > 0.0f ? __fdiv_rn(ncq, denf) : 0.0f;
           float sc = __fadd_rn(w, __fmul_rn(lambda1, delta));
           sc = __fadd_rn(sc, __fmul_rn(lambda2, o));
-          mv[r] = __fsub_rn(sc, s_tau[e]);
+          m = __fsub_rn(sc, s_tau[e]);
         } else {
           ++unmatched;
         }
-        qe[r] = (e << 4) | (q + 1);
+        qv = (e << 4) | (q + 1);
         q_out[f] = q;
-        margin[f] = mv[r];
+        margin[f] = m;
       }
     }
+    if constexpr (kMvRegs) {
+      mv[r] = m;
+      qe[r] = qv;
+    } else if (j < nb) {
+      s_q[j] = static_cast<int8_t>((qv & 15) - 1);
+    }
     // keep the scheduler from hoisting the loads of every branch at once
-    // (a thread holds up to 32 branches): four branches per group
-    if ((r & 3) == 3) __builtin_amdgcn_sched_barrier(0);
+    // (a thread holds up to 32 branches, each with up to 3 k slot loads):
+    // groups of four branches, single branches when a thread holds many
+    if (kMvRegs ? (r & 3) == 3 : true) __builtin_amdgcn_sched_barrier(0);
   }
   if (mode != kSelFull) {
     unmatched = wave_sum_i32(unmatched);
@@ -227,14 +260,14 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
 #pragma unroll
       for (int pass = 0; pass < 4; ++pass) {
         const int shift = 24 - 8 * pass;
-        int* hist = s_hist[pass & 1];
+        int* hist = s_hist[pass % 3];
         const uint32_t hi_mask = pass == 0 ? 0u : (~0u << (shift + 8));
         // histogram of this digit over the matched keys that share the
         // prefix: the (at most two) most frequent bins of a wave are added
         // once by one lane, the remaining lanes add their own
-#pragma unroll
+#pragma unroll kU
         for (int r = 0; r < R; ++r) {
-          const uint32_t mk = f32_order_key(mv[r]);
+          const uint32_t mk = f32_order_key(mval(r));
           bool part = q_of(r) >= 0 && ((mk ^ prefix) & hi_mask) == 0u;
           const int bin = static_cast<int>((mk >> shift) & 255u);
 #pragma unroll
@@ -249,48 +282,50 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
           }
           if (part) atomicAdd(&hist[bin], 1);
         }
+        // one barrier per pass: every wave scans the histogram itself; the
+        // last wave clears the buffer of pass + 2 (three buffers in turn:
+        // that one was last read by the scans of pass - 1, which every wave
+        // finished before this barrier, and is next written after the
+        // barrier of pass + 1)
         __syncthreads();
-        if (wv == 0) {
-          // lane l holds bins 255 - 4l .. 252 - 4l (descending)
-          int c[4];
+        if (wv == kSelWaves - 1 && pass + 2 < 4) {
 #pragma unroll
-          for (int u = 0; u < 4; ++u) c[u] = hist[255 - 4 * lane - u];
-          const int tot = c[0] + c[1] + c[2] + c[3];
-          int incl = tot;
-#pragma unroll
-          for (int o = 1; o < kWave; o <<= 1) {
-            const int v = __shfl_up(incl, o, kWave);
-            if (lane >= o) incl += v;
-          }
-          int run = incl - tot;
-#pragma unroll
-          for (int u = 0; u < 4; ++u) {
-            if (c[u] > 0 && run < rem && rem <= run + c[u]) {
-              s_bin = static_cast<unsigned>(255 - 4 * lane - u);
-              s_remaining = rem - run;
-            }
-            run += c[u];
-          }
-        } else if (wv == 1) {
-#pragma unroll
-          for (int u = 0; u < 4; ++u) s_hist[(pass + 1) & 1][4 * lane + u] = 0;
+          for (int u = 0; u < 4; ++u) s_hist[(pass + 2) % 3][4 * lane + u] = 0;
         }
-        __syncthreads();
-        prefix |= static_cast<uint32_t>(s_bin) << shift;
-        rem = s_remaining;
+        // lane l holds bins 255 - 4l .. 252 - 4l (descending); the lane whose
+        // run of bins reaches rem names the digit and what remains of rem
+        int c[4];
+#pragma unroll
+        for (int u = 0; u < 4; ++u) c[u] = hist[255 - 4 * lane - u];
+        const int tot = c[0] + c[1] + c[2] + c[3];
+        int run = wave_incl_scan_i32(tot) - tot;
+        int fbin = 0, frem = 0;
+        bool found = false;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) {
+          if (c[u] > 0 && run < rem && rem <= run + c[u]) {
+            found = true;
+            fbin = 255 - 4 * lane - u;
+            frem = rem - run;
+          }
+          run += c[u];
+        }
+        const int leader = __builtin_ctzll(__ballot(found));
+        prefix |= static_cast<uint32_t>(__builtin_amdgcn_readlane(fbin, leader)) << shift;
+        rem = __builtin_amdgcn_readlane(frem, leader);
       }
       thr = prefix;
       tie_rem = rem;
       // keys equal to T: take the tie_rem lowest flat ids (j = tid + 1024 r,
       // so the order is r-major, then wave, then lane)
-#pragma unroll
+#pragma unroll kU
       for (int r = 0; r < R; ++r) {
-        const uint64_t tb = __ballot(q_of(r) >= 0 && f32_order_key(mv[r]) == thr);
+        const uint64_t tb = __ballot(q_of(r) >= 0 && f32_order_key(mval(r)) == thr);
         if (lane == 0) s_tcnt[r][wv] = __popcll(tb);
       }
       __syncthreads();
       int before = 0;
-#pragma unroll
+#pragma unroll kU
       for (int r = 0; r < R; ++r) {
         int in_r = 0, below = 0;
         for (int w2 = 0; w2 < kSelWaves; ++w2) {
@@ -298,7 +333,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
           in_r += c;
           if (w2 < wv) below += c;
         }
-        const uint64_t tb = __ballot(q_of(r) >= 0 && f32_order_key(mv[r]) == thr);
+        const uint64_t tb = __ballot(q_of(r) >= 0 && f32_order_key(mval(r)) == thr);
         const bool flag = ((tb >> lane) & 1ull) != 0;
         if (flag && before + below + lane_rank(tb) < tie_rem) tie_bits |= 1u << r;
         before += in_r;
@@ -307,7 +342,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   }
 
   // 3. mask and per-expert counts
-#pragma unroll
+#pragma unroll kU
   for (int r = 0; r < R; ++r) {
     const int j = tid + kSelThreads * r;
     bool rc = false;
@@ -315,18 +350,18 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
       if (mode == kSelFull || q_of(r) < 0) {
         rc = true;
       } else if (mode == kSelThreshold) {
-        rc = mv[r] > 0.0f;
+        rc = mval(r) > 0.0f;
       } else if (take_all_matched) {
         rc = true;
       } else if (need == 0) {
         rc = false;
       } else {
-        const uint32_t mk = f32_order_key(mv[r]);
+        const uint32_t mk = f32_order_key(mval(r));
         rc = mk > thr || ((tie_bits >> r) & 1u) != 0;
       }
       mask[base + j] = rc ? 1 : 0;
       s_mask[j] = rc ? 1 : 0;
-      s_q[j] = static_cast<int8_t>(q_of(r));
+      if constexpr (kMvRegs) s_q[j] = static_cast<int8_t>(q_of(r));
       if (rc) {
         atomicAdd(&s_cnt[e_of(r)], 1);
         atomicAdd(&s_cntr[r][e_of(r)], 1);
@@ -534,9 +569,11 @@ hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1
   const int nb = s.N * s.k;
   const size_t lds = size_t(2) * nb;
   if (lds > 64 * 1024) return hipErrorInvalidValue;
+  const double log_n = std::log(static_cast<double>(s.N));  // the entropy's normaliser
 #define MOECA_DECIDE(RR)                                                                      \
   launch_kernel(&decide_kernel<RR>, dim3(s.B), dim3(kSelThreads), uint32_t(lds), st, b.e_t,   \
-                b.w_t, b.e_c, b.w_c, b.n_c, b.stat, b.logc, with_stat ? 1 : 0, tau0, alpha,   \
+                b.w_t, b.e_c, b.w_c, b.n_c, b.stat, b.logc, with_stat ? 1 : 0, log_n, tau0,   \
+                alpha,                                                                        \
                 b.hbar, b.tau, s.N, s.E, s.k, sel_mode, budget, lambda1, lambda2, b.q,        \
                 b.margin, b.mask, b.sigma, b.sync, b.cnt_bs, b.stats_bs, b.cnt_ch)
   if (nb <= 2 * kSelThreads) {

@@ -516,6 +516,7 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
   constexpr int FM = 2, FN = 2;  // wave tile: 64 rows x 64 columns
   constexpr int WN = TN / (FN * 32);  // waves along N
   static_assert(kBigWaves == (TM / (FM * 32)) * WN, "wave grid must cover the tile");
+  static_assert(WN == 4 && kBigWaves == 8, "the wave rotation below assumes 2 x 4 waves");
   __shared__ __attribute__((aligned(16))) uint16_t lds[kStages * kStageElems];
   __shared__ int s_src[TM];
   __shared__ int s_dst[TM];
@@ -523,7 +524,11 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
   const int tid = threadIdx.x;
   const int lane = tid & 63;
   const int wv = tid >> 6;
-  const int wm = wv / WN, wn = wv % WN;
+  // waves w and w + 4 share a SIMD; the second row of waves is rotated by
+  // two columns so that each SIMD holds one wave of either row half and one
+  // of either column half: a tile with only its first 64 rows, or only its
+  // first 128 columns, still keeps every SIMD busy with one wave
+  const int wm = wv / WN, wn = (wv + 2 * wm) % WN;
   const int total = tile_off[G];
   const int per = (total + kXcds - 1) / kXcds;
   const int lo = (blockIdx.x % kXcds) * per;

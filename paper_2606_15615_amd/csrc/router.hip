@@ -80,39 +80,12 @@ template <> struct Vec<float, 4> {
   }
 };
 
-// 16-lane row permutations (DPP): xor 1, xor 2, half-row mirror, row mirror.
-// Applied in this order, a commutative reduction leaves every lane of the
-// row with the same result.
-constexpr int kDppRow[4] = {0xB1, 0x4E, 0x141, 0x140};
-
-template <int CTRL>
-__device__ __forceinline__ int dpp_i32(int v) {
-  return __builtin_amdgcn_update_dpp(0, v, CTRL, 0xF, 0xF, false);
-}
-template <int CTRL>
-__device__ __forceinline__ float dpp_f32(float v) {
-  return __int_as_float(dpp_i32<CTRL>(__float_as_int(v)));
-}
-template <int CTRL>
-__device__ __forceinline__ double dpp_f64(double v) {
-  const uint64_t u = __builtin_bit_cast(uint64_t, v);
-  const int lo = dpp_i32<CTRL>(static_cast<int>(u & 0xffffffffu));
-  const int hi = dpp_i32<CTRL>(static_cast<int>(u >> 32));
-  return __builtin_bit_cast(double, (uint64_t(uint32_t(hi)) << 32) | uint32_t(lo));
-}
-
-// Row max, row sum (fp64) and row argmax (ties to the lower id).
+// Row max and row argmax (ties to the lower id).
 __device__ __forceinline__ float row_max(float v) {
   v = fmaxf(v, dpp_f32<kDppRow[0]>(v));
   v = fmaxf(v, dpp_f32<kDppRow[1]>(v));
   v = fmaxf(v, dpp_f32<kDppRow[2]>(v));
   return fmaxf(v, dpp_f32<kDppRow[3]>(v));
-}
-__device__ __forceinline__ double row_sum(double v) {
-  v += dpp_f64<kDppRow[0]>(v);
-  v += dpp_f64<kDppRow[1]>(v);
-  v += dpp_f64<kDppRow[2]>(v);
-  return v + dpp_f64<kDppRow[3]>(v);
 }
 template <int CTRL>
 __device__ __forceinline__ void argmax_dpp(float& v, int& i) {
@@ -276,7 +249,7 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
     z[q] = in_den ? exp(static_cast<double>(lv[q]) - static_cast<double>(mx)) : 0.0;
     part += z[q];
   }
-  part = row_sum(part);
+  part = row_sum_f64(part);
   if (live) {
     for (int p = 0; p < k; ++p) {
 #pragma unroll
