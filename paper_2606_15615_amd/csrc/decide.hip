@@ -24,11 +24,12 @@ namespace {
 // of the sample's branches (j = tid + 1024 r) in registers.
 //   entropy (when the router advanced the statistic C in this step; one
 //   wave per expert, fixed-order fp64 sums, Sec. 4.3):
-//     S = sum_i C_i,  H = -(1/S) sum_{C_i > 0} C_i (log C_i - log S),
+//     S = sum_i C_i,  A = sum_i C_i log C_i  (the router's sums per chunk of
+//     16 positions, then over the chunks),
+//     H = -(1/S) sum_{C_i > 0} C_i (log C_i - log S) = (S log S - A) / S,
 //     Hbar = clamp(H / log N, 0, 1),  tau_e = tau0 * (1 + alpha * (2*Hbar - 1))
-//   with log C_i stored by the router and log N from the host's libm;
-//   log(C_i / S) is formed as the difference of the two logarithms, so one
-//   occupied position gives H = 0 exactly.
+//   with log N from the host's libm.  One occupied position gives H = 0
+//   exactly: S log S and A are then the same rounded product.
 //   q(p): cached slot with the same expert, or -1           (Sec. 4.2)
 //   Delta = |w_p - w_c[q]|,  o = n_c[q] / f32(sum_j n_c[j]),
 //   s = (w_p + lambda1*Delta) + lambda2*o,  m = s - tau_{b,e_p}
@@ -48,7 +49,7 @@ template <int R>
 __global__ __launch_bounds__(kSelThreads) void decide_kernel(
     const int32_t* __restrict__ e_t, const float* __restrict__ w_t,
     const int32_t* __restrict__ e_c, const float* __restrict__ w_c,
-    const float* __restrict__ n_c, const float* __restrict__ C, const double* __restrict__ logc,
+    const float* __restrict__ n_c, const double* __restrict__ ent,
     int with_stat, double log_n, float tau0, float alpha, float* __restrict__ hbar,
     float* __restrict__ tau,
     int N, int E, int k, int mode, int budget, float lambda1, float lambda2,
@@ -79,44 +80,24 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
     if (tid < E && !with_stat) s_tau[tid] = tau[b * E + tid];
   }
   if (with_stat) {
-    // 0. entropy of the statistic and the threshold, one wave per expert
+    // 0. entropy of the statistic and the threshold, one wave per expert:
+    // the router's per-chunk sums, lane-strided then across the wave
+    const int nch = (N + 15) / 16;
     for (int e = wv; e < E; e += kSelWaves) {
-      const float* Cr = C + (int64_t(b) * E + e) * N;
-      const double* Lr = logc + (int64_t(b) * E + e) * N;
-      // positions lane + 64 v of each 1024-position chunk, all loads of a
-      // chunk (C and log C) issued together; four partial sums per lane
-      constexpr int PER = 16;
-      double s4[4] = {0.0, 0.0, 0.0, 0.0};
-      double h4[4] = {0.0, 0.0, 0.0, 0.0};
-      double c[PER], lc[PER];  // C and log C; both 0 where C = 0 or past N
-      auto load_chunk = [&](int i0) __attribute__((always_inline)) {
-#pragma unroll
-        for (int v = 0; v < PER; ++v) {
-          const int i = i0 + lane + v * kWave;
-          c[v] = i < N ? static_cast<double>(Cr[i]) : 0.0;
-          lc[v] = i < N ? Lr[i] : 0.0;
-        }
-      };
-      for (int i0 = 0; i0 < N; i0 += PER * kWave) {
-        load_chunk(i0);
-#pragma unroll
-        for (int v = 0; v < PER; ++v) s4[v & 3] += c[v];
+      const double* P = ent + (int64_t(b) * E + e) * nch * 2;
+      double sp = 0.0, ap = 0.0;
+      for (int c = lane; c < nch; c += kWave) {
+        sp += P[2 * c];
+        ap += P[2 * c + 1];
       }
-      const double S = wave_sum_f64((s4[0] + s4[1]) + (s4[2] + s4[3]));
-      double Hs = 0.0;
-      if (S > 0.0) {
-        const double logS = log(S);
-        for (int i0 = 0; i0 < N; i0 += PER * kWave) {
-          if (N > PER * kWave) load_chunk(i0);  // a single chunk is still in registers
-          // a position with C = 0 adds an exact zero (0 * finite)
-#pragma unroll
-          for (int v = 0; v < PER; ++v) h4[v & 3] += c[v] * (lc[v] - logS);
-        }
-        Hs = -wave_sum_f64((h4[0] + h4[1]) + (h4[2] + h4[3])) / S;
-      }
+      const double S = wave_sum_f64(sp);
+      const double A = wave_sum_f64(ap);
       if (lane == 0) {
         float hb = 0.0f;
         if (N > 1 && S > 0.0) {
+          // H = -(1/S) sum_i C_i (log C_i - log S) = (S log S - A) / S; with
+          // one occupied position S log S and A are the same product
+          const double Hs = (S * log(S) - A) / S;
           double v = Hs / log_n;
           v = v < 0.0 ? 0.0 : (v > 1.0 ? 1.0 : v);
           hb = static_cast<float>(v);
@@ -142,11 +123,13 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   // per branch: margin and the packed (matched slot + 1) | expert << 4,
   // kept in registers while a thread holds at most 8 branches.  With more
   // (up to 32) nothing per branch stays in registers and the per-branch
-  // loops are not unrolled: the later passes read the margin back from the
+  // loops are runtime loops: the later passes read the margin back from the
   // margin buffer this thread wrote (the values stay in L2), the slot from
   // its LDS copy s_q and the expert from e_t.
   constexpr bool kMvRegs = R <= 8;
-  constexpr int kU = kMvRegs ? R : 1;  // unroll factor of the per-branch loops
+  // unroll factor of the per-branch loops (by four when they are runtime
+  // loops, so that a few branches' loads are in flight together)
+  constexpr int kU = kMvRegs ? R : 4;
   float mv[kMvRegs ? R : 1];
   int qe[kMvRegs ? R : 1];
   // outside the sample (j >= nb) a branch reads as unmatched with margin +inf
@@ -230,8 +213,8 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
     }
     // keep the scheduler from hoisting the loads of every branch at once
     // (a thread holds up to 32 branches, each with up to 3 k slot loads):
-    // groups of four branches, single branches when a thread holds many
-    if (kMvRegs ? (r & 3) == 3 : true) __builtin_amdgcn_sched_barrier(0);
+    // groups of four branches, pairs when a thread holds many
+    if (kMvRegs ? (r & 3) == 3 : (r & 1) == 1) __builtin_amdgcn_sched_barrier(0);
   }
   if (mode != kSelFull) {
     unmatched = wave_sum_i32(unmatched);
@@ -572,7 +555,7 @@ hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1
   const double log_n = std::log(static_cast<double>(s.N));  // the entropy's normaliser
 #define MOECA_DECIDE(RR)                                                                      \
   launch_kernel(&decide_kernel<RR>, dim3(s.B), dim3(kSelThreads), uint32_t(lds), st, b.e_t,   \
-                b.w_t, b.e_c, b.w_c, b.n_c, b.stat, b.logc, with_stat ? 1 : 0, log_n, tau0,   \
+                b.w_t, b.e_c, b.w_c, b.n_c, b.ent, with_stat ? 1 : 0, log_n, tau0,            \
                 alpha,                                                                        \
                 b.hbar, b.tau, s.N, s.E, s.k, sel_mode, budget, lambda1, lambda2, b.q,        \
                 b.margin, b.mask, b.sigma, b.sync, b.cnt_bs, b.stats_bs, b.cnt_ch)

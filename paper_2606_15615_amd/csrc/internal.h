@@ -52,7 +52,8 @@ struct Buffers {
   float* n_c;
   void* h_c;
   float* stat;      // [B][E][N]
-  double* logc;     // [B][E][N] log of the statistic (0 where it is 0)
+  double* ent;      // [B][E][ceil(N/16)][2] per 16 positions of the statistic:
+                    // sum C and sum C log C (the router writes them)
   float* logits;    // [B*N][E]
   int32_t* e_t;
   float* w_t;

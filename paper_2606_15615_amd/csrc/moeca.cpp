@@ -47,7 +47,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 enum Region {
   R_E_C, R_W_C, R_N_C, R_H_C, R_STAT, R_LOGITS, R_E_T, R_W_T, R_HBAR, R_TAU, R_MARGIN, R_Q,
   R_MASK, R_SIGMA, R_SYNC, R_OFF, R_LIST, R_POS,
-  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_LOGC, R_CNT_CH, R_MID, R_H_SH, R_COUNT
+  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_ENT, R_CNT_CH, R_MID, R_H_SH, R_COUNT
 };
 
 struct Layout {
@@ -84,7 +84,7 @@ Layout make_layout(const Shape& s) {
   b[R_RFLAGS] = size_t(moeca::router_blocks(s)) * 4;
   b[R_TILES] = size_t(2) * (s.groups() + 1) * 4;
   b[R_ROW_DST] = nbr * 4;
-  b[R_LOGC] = size_t(s.B) * s.E * s.N * 8;
+  b[R_ENT] = size_t(s.B) * s.E * ((size_t(s.N) + 15) / 16) * 2 * 8;
   b[R_CNT_CH] = size_t(s.B) * ((size_t(s.N) * s.k + 1023) / 1024) * s.E * 4;
   b[R_MID] = size_t(s.mid_rows()) * s.d_ff * act;
   b[R_H_SH] = size_t(s.S) * ntok * s.d * act;
@@ -241,7 +241,7 @@ int moeca_bind_workspace(moeca_layer* L, void* dev, size_t bytes) {
   b.n_c = reinterpret_cast<float*>(w + o[R_N_C]);
   b.h_c = w + o[R_H_C];
   b.stat = reinterpret_cast<float*>(w + o[R_STAT]);
-  b.logc = reinterpret_cast<double*>(w + o[R_LOGC]);
+  b.ent = reinterpret_cast<double*>(w + o[R_ENT]);
   b.logits = reinterpret_cast<float*>(w + o[R_LOGITS]);
   b.e_t = reinterpret_cast<int32_t*>(w + o[R_E_T]);
   b.w_t = reinterpret_cast<float*>(w + o[R_W_T]);

@@ -1,7 +1,8 @@
 // Router: logits, top-k experts and gate weights (Sec. 4.1, B_i^t), and the
 // EMA of the expert statistic (Sec. 4.3, EMA eq.).
 //
-// Logits.  A block takes 16 tokens.  The dot products x_i . W_r[e] run on
+// Logits.  A block takes 16 consecutive positions of one sample (the last
+// chunk of a sample may hold fewer).  The dot products x_i . W_r[e] run on
 // the fp64 matrix cores (v_mfma_f64_16x16x4f64: 16 tokens x 16 experts x 4
 // k per instruction).  Every product of two bf16 (or two fp32) values is
 // exact in fp64, so this is the exact-product, fp64-accumulated sum the
@@ -24,9 +25,11 @@
 // 16-lane reductions use DPP row permutations (quad swaps, half-row and row
 // mirrors), so every lane of the group ends with the same value.  The
 // statistic C[b][e][i] of the token's experts is read at kernel start and
-// updated here: C <- f32(f32(beta C) + f32(1 - beta) [e in B_i]); with it the
-// kernel stores log C in fp64 (0 where C is 0), the per-position logarithm
-// the entropy of the statistic needs.
+// updated here: C <- f32(f32(beta C) + f32(1 - beta) [e in B_i]).  For the
+// entropy of the statistic the block also writes, per expert, the fp64 sums
+// over its positions of C and of C log C (log in fp64 of the stored value,
+// the product rounded once; positions with C = 0 add nothing), in a fixed
+// order: token pairs within a wave by lane exchange, then the four waves.
 #include "common.h"
 #include "internal.h"
 
@@ -106,22 +109,28 @@ __device__ __forceinline__ void row_argmax(float& v, int& i) {
 template <typename T, int VW, int NG>
 __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
     const T* __restrict__ x, const T* __restrict__ Wg, const float* __restrict__ bias,
-    int64_t T_tokens, int d, int E, int k, int norm_topk, float* __restrict__ logits,
+    int d, int E, int k, int norm_topk, float* __restrict__ logits,
     int32_t* __restrict__ e_out, float* __restrict__ w_out, int32_t* __restrict__ rflags,
-    float* __restrict__ C, double* __restrict__ logc, int N, float beta) {
+    float* __restrict__ C, double* __restrict__ ent, int N, float beta) {
   __shared__ double s_part[kRouterWaves][NG][4][kWave];
+  __shared__ double s_ent[kRouterWaves][NG][2][16];
   __shared__ int s_bad;
   const int lane = threadIdx.x & (kWave - 1);
   const int wv = threadIdx.x / kWave;
   const int n = lane & 15, g = lane >> 4;
-  const int64_t t0 = int64_t(blockIdx.x) * kTokensPerBlock;
+  // block = (sample, chunk of 16 positions): it never spans two samples
+  const int nch = (N + kTokensPerBlock - 1) / kTokensPerBlock;
+  const int64_t sb = blockIdx.x / nch;
+  const int chunk = blockIdx.x % nch;
+  const int64_t t0 = sb * N + int64_t(chunk) * kTokensPerBlock;
+  const int nlive = min(kTokensPerBlock, N - chunk * kTokensPerBlock);
   if (threadIdx.x == 0) s_bad = 0;
 
   // the epilogue token of this lane, and its statistic values (read early)
-  const int64_t te = t0 + g + 4 * wv;
-  const bool live = te < T_tokens;
+  const bool live = g + 4 * wv < nlive;
+  const int64_t si = live ? int64_t(chunk) * kTokensPerBlock + g + 4 * wv : 0;
+  const int64_t te = sb * N + si;
   float c_old[NG];
-  const int64_t sb = live ? te / N : 0, si = live ? te % N : 0;
 #pragma unroll
   for (int q = 0; q < NG; ++q) {
     const int e = 16 * q + n;
@@ -134,7 +143,7 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
   // lanes of a row read one contiguous 4 VW-element segment per load.
   const int nv = d / (16 * VW);  // vectors per lane
   const int64_t kbase = int64_t(wv) * (d >> 2) + int64_t(g) * VW;
-  const T* xp = x + min(t0 + n, T_tokens - 1) * d + kbase;  // A: token row n
+  const T* xp = x + (t0 + min(n, nlive - 1)) * d + kbase;  // A: token row n
   const T* wp[NG];
 #pragma unroll
   for (int q = 0; q < NG; ++q) wp[q] = Wg + int64_t(min(16 * q + n, E - 1)) * d + kbase;
@@ -262,35 +271,63 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
     }
   }
 
-  // expert statistic C_{e,i} <- f32(f32(beta*C) + f32(1-beta)*[e in B_i])
-  if (C != nullptr && live) {
+  // expert statistic C_{e,i} <- f32(f32(beta*C) + f32(1-beta)*[e in B_i]),
+  // and for the entropy of the statistic (Sec. 4.3) this chunk's sums
+  // sum_i C_i and sum_i C_i log C_i per expert (fp64, exact products of
+  // the stored fp32 value and its fp64 logarithm; C_i = 0 adds 0): the
+  // token pairs (g, g ^ 1), then (g, g ^ 2), then the four waves in order
+  if (C != nullptr) {
+    double sv[NG], av[NG];
 #pragma unroll
     for (int q = 0; q < NG; ++q) {
       const int e = 16 * q + n;
-      if (e >= E) continue;
-      float c = __fmul_rn(beta, c_old[q]);
-      if ((taken >> e) & 1ull) c = __fadd_rn(c, __fsub_rn(1.0f, beta));
-      C[(sb * E + e) * N + si] = c;
-      // log of the new value for the entropy of the statistic (Sec. 4.3),
-      // which the decision kernel sums per (sample, expert)
-      logc[(sb * E + e) * N + si] = c > 0.0f ? log(static_cast<double>(c)) : 0.0;
+      sv[q] = 0.0;
+      av[q] = 0.0;
+      if (e < E && live) {
+        float c = __fmul_rn(beta, c_old[q]);
+        if ((taken >> e) & 1ull) c = __fadd_rn(c, __fsub_rn(1.0f, beta));
+        C[(sb * E + e) * N + si] = c;
+        if (c > 0.0f) {
+          const double cd = static_cast<double>(c);
+          sv[q] = cd;
+          av[q] = __dmul_rn(cd, log(cd));
+        }
+      }
+      sv[q] += __shfl_xor(sv[q], 16, kWave);
+      av[q] += __shfl_xor(av[q], 16, kWave);
+      sv[q] += __shfl_xor(sv[q], 32, kWave);
+      av[q] += __shfl_xor(av[q], 32, kWave);
+      if (g == 0) {
+        s_ent[wv][q][0][n] = sv[q];
+        s_ent[wv][q][1][n] = av[q];
+      }
     }
   }
   if (bad && live) s_bad = 1;
   __syncthreads();
   if (threadIdx.x == 0) rflags[blockIdx.x] = s_bad;
+  if (C != nullptr && wv == 0 && g < 2) {
+    // lane (g, n): sum (g = 0) or sum of C log C (g = 1) of experts 16 q + n
+#pragma unroll
+    for (int q = 0; q < NG; ++q) {
+      const int e = 16 * q + n;
+      if (e < E)
+        ent[((sb * E + e) * nch + chunk) * 2 + g] =
+            (s_ent[0][q][g][n] + s_ent[1][q][g][n]) + (s_ent[2][q][g][n] + s_ent[3][q][g][n]);
+    }
+  }
 }
 
 template <typename T, int VW>
 hipError_t launch_vw(const Shape& s, const void* x, const void* W_r, const float* b_r,
-                     int norm_topk, float beta, float* C, double* logc, const Buffers& b,
+                     int norm_topk, float beta, float* C, double* ent, const Buffers& b,
                      hipStream_t st) {
   const dim3 grid(router_blocks(s)), block(kRouterWaves * kWave);
   const int ng = (s.E + 15) / 16;
 #define MOECA_ROUTER(NGV)                                                                 \
   launch_kernel(&router_kernel<T, VW, NGV>, grid, block, 0, st, static_cast<const T*>(x), \
-                static_cast<const T*>(W_r), b_r, s.tokens(), s.d, s.E, s.k, norm_topk,    \
-                b.logits, b.e_t, b.w_t, b.rflags, C, logc, s.N, beta)
+                static_cast<const T*>(W_r), b_r, s.d, s.E, s.k, norm_topk,                \
+                b.logits, b.e_t, b.w_t, b.rflags, C, ent, s.N, beta)
   switch (ng) {
     case 1: MOECA_ROUTER(1); break;
     case 2: MOECA_ROUTER(2); break;
@@ -305,7 +342,7 @@ hipError_t launch_vw(const Shape& s, const void* x, const void* W_r, const float
 }  // namespace
 
 int router_blocks(const Shape& s) {
-  return static_cast<int>((s.tokens() + kTokensPerBlock - 1) / kTokensPerBlock);
+  return s.B * ((s.N + kTokensPerBlock - 1) / kTokensPerBlock);
 }
 
 // d is a multiple of 64 (checked at layer creation), so each lane's quarter
@@ -316,13 +353,13 @@ hipError_t launch_router(const Shape& s, const void* x, const void* W_r, const f
                          hipStream_t st) {
   if (s.d % 64 != 0 || s.E > 64 || s.k > 8 || s.k > s.E) return hipErrorInvalidValue;
   float* C = update_stat ? b.stat : nullptr;
-  double* logc = update_stat ? b.logc : nullptr;
+  double* ent = update_stat ? b.ent : nullptr;
   if (s.bf16) {
     if ((s.d / 16) % 8 == 0)
-      return launch_vw<uint16_t, 8>(s, x, W_r, b_r, norm_topk, beta, C, logc, b, st);
-    return launch_vw<uint16_t, 4>(s, x, W_r, b_r, norm_topk, beta, C, logc, b, st);
+      return launch_vw<uint16_t, 8>(s, x, W_r, b_r, norm_topk, beta, C, ent, b, st);
+    return launch_vw<uint16_t, 4>(s, x, W_r, b_r, norm_topk, beta, C, ent, b, st);
   }
-  return launch_vw<float, 4>(s, x, W_r, b_r, norm_topk, beta, C, logc, b, st);
+  return launch_vw<float, 4>(s, x, W_r, b_r, norm_topk, beta, C, ent, b, st);
 }
 
 }  // namespace moeca
