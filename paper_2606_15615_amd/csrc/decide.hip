@@ -44,6 +44,9 @@ namespace {
 // ---------------------------------------------------------------------------
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
+// Ratio mode: once a digit leaves at most this many keys sharing the
+// threshold's prefix, one wave ranks them directly.
+constexpr int kDirect = 64;
 
 template <int R>
 __global__ __launch_bounds__(kSelThreads) void decide_kernel(
@@ -66,6 +69,10 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   __shared__ float s_tau[64];
   __shared__ int s_tcnt[R][kSelWaves];
   __shared__ int s_unmatched, s_recompute, s_sync;
+  __shared__ uint32_t s_ckey[kDirect];  // ratio mode: the candidates of the last digit
+  __shared__ int s_cj[kDirect];
+  __shared__ int s_csel[kDirect];
+  __shared__ int s_ncand;
 
   const int b = blockIdx.x;
   const int nb = N * k;
@@ -115,6 +122,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
     s_unmatched = 0;
     s_recompute = 0;
     s_sync = 0;
+    s_ncand = 0;
   }
   __syncthreads();
 
@@ -224,13 +232,18 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   const int n_unmatched = s_unmatched;
   const int n_matched = mode == kSelFull ? 0 : nb - n_unmatched;
 
-  // 2. ratio mode: the need-th best matched branch.  Four 8-bit radix
-  // passes (most significant first) find the margin key T with fewer than
-  // `need` matched keys above it and at least `need` at or above it; of the
-  // keys equal to T the lowest flat ids are taken (rank by ballots).
+  // 2. ratio mode: the need-th best matched branch.  8-bit radix passes
+  // (most significant first) narrow the margin key T down: after a pass the
+  // prefix P of T is known, with fewer than `need` matched keys above it and
+  // rem of the keys sharing it still to take.  When at most kDirect keys
+  // share P, one wave ranks them by (key desc, flat id asc) and takes the
+  // first rem (direct); otherwise, after the fourth pass, the keys equal to
+  // T are ties and the lowest flat ids among them are taken (ballots).
   int need = 0;
   bool take_all_matched = false;
+  bool direct = false;
   uint32_t thr = 0;
+  uint32_t dmask = ~0u;   // key bits compared with thr
   int tie_rem = 0;
   uint32_t tie_bits = 0;  // bit r: branch r is one of the taken ties
   if (mode == kSelRatio) {
@@ -282,7 +295,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
         for (int u = 0; u < 4; ++u) c[u] = hist[255 - 4 * lane - u];
         const int tot = c[0] + c[1] + c[2] + c[3];
         int run = wave_incl_scan_i32(tot) - tot;
-        int fbin = 0, frem = 0;
+        int fbin = 0, frem = 0, fcnt = 0;
         bool found = false;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
@@ -290,15 +303,52 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
             found = true;
             fbin = 255 - 4 * lane - u;
             frem = rem - run;
+            fcnt = c[u];
           }
           run += c[u];
         }
         const int leader = __builtin_ctzll(__ballot(found));
         prefix |= static_cast<uint32_t>(__builtin_amdgcn_readlane(fbin, leader)) << shift;
         rem = __builtin_amdgcn_readlane(frem, leader);
+        if (__builtin_amdgcn_readlane(fcnt, leader) <= kDirect) {
+          direct = true;  // the same decision in every wave
+          dmask = ~0u << shift;
+          break;
+        }
       }
       thr = prefix;
       tie_rem = rem;
+    }
+    if (direct) {
+      // the keys sharing the prefix (candidate index kept in s_mask[j],
+      // free until step 3), ranked by wave 0; the order of the appends does
+      // not matter
+#pragma unroll kU
+      for (int r = 0; r < R; ++r) {
+        const int j = tid + kSelThreads * r;
+        const uint32_t mk = f32_order_key(mval(r));
+        if (q_of(r) >= 0 && (mk & dmask) == thr) {
+          const int ci = atomicAdd(&s_ncand, 1);
+          s_ckey[ci] = mk;
+          s_cj[ci] = j;
+          s_mask[j] = static_cast<uint8_t>(ci);
+        }
+      }
+      __syncthreads();
+      if (wv == 0) {
+        const int nc = s_ncand;
+        const uint32_t ki = lane < nc ? s_ckey[lane] : 0u;
+        const int ji = lane < nc ? s_cj[lane] : 0;
+        int rank = 0;
+        for (int t = 0; t < nc; ++t) {
+          const uint32_t kt = __builtin_amdgcn_readlane(ki, t);
+          const int jt = __builtin_amdgcn_readlane(ji, t);
+          rank += (kt > ki || (kt == ki && jt < ji)) ? 1 : 0;
+        }
+        if (lane < nc) s_csel[lane] = rank < tie_rem ? 1 : 0;
+      }
+      __syncthreads();
+    } else if (need > 0 && !take_all_matched) {
       // keys equal to T: take the tie_rem lowest flat ids (j = tid + 1024 r,
       // so the order is r-major, then wave, then lane)
 #pragma unroll kU
@@ -338,6 +388,9 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
         rc = true;
       } else if (need == 0) {
         rc = false;
+      } else if (direct) {
+        const uint32_t mk = f32_order_key(mval(r)) & dmask;
+        rc = mk > thr || (mk == thr && s_csel[s_mask[j]] != 0);
       } else {
         const uint32_t mk = f32_order_key(mval(r));
         rc = mk > thr || ((tie_bits >> r) & 1u) != 0;
