@@ -95,6 +95,28 @@ def test_nothing_recomputed_is_bit_exact(mode):
     assert np.array_equal(out_o, out0)
 
 
+@pytest.mark.parametrize("N,E,k", [(40, 8, 2), (300, 8, 2), (2000, 8, 2), (2100, 16, 8)])
+def test_all_branches_tied(N, E, k):
+    """Every token carries the same input as at the refresh step, so every
+    branch is matched and all branches of one slot tie on the margin.  The
+    ratio selection must then take the lowest flat ids among the tied keys:
+    ranked directly when at most 64 keys share the threshold's prefix (N=40),
+    by the tie ballots after the fourth digit otherwise; one, eight and
+    thirty-two branches per thread."""
+    shape = LayerShape(d=128, E=E, k=k, d_ff=128, B=2, N=N, dtype="bf16")
+    S = Setup(shape, mode="ratio", seed=11, T=1, ratio=0.3, refresh_cycle=0)
+    x = np.repeat(S.xs[0][:, :1, :], N, axis=1)
+    st0 = O.State(S.dims, attention=True)
+    _, st1, _ = O.step(S.dims, S.pol, S.W, st0, x, 0, attn_in=S.attn[0])
+    S.import_state(st1)
+    out_g = S.gpu_step(x, 1, S.attn[0])
+    out_o, st2, rec = O.step(S.dims, S.pol, S.W, st1, x, 1, attn_in=S.attn[0])
+    assert rec["matched"].all()
+    assert all(len(np.unique(rec["m"][b])) <= k for b in range(2))  # one margin per slot
+    assert 0 < rec["mask"].sum() < rec["mask"].size
+    check_step(S, 1, rec, out_o, st1, st2, out_g, label=f"ties N={N} k={k}")
+
+
 def test_reset_mid_trajectory():
     S = Setup(RAGGED, mode="ratio", seed=7, T=4, ratio=0.3, refresh_cycle=0)
     for t in range(3):
