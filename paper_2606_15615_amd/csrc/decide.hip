@@ -81,6 +81,40 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   const int lane = tid & (kWave - 1);
   const int wv = tid / kWave;
 
+  // operands of branch j = tid + 1024 r: its expert and gate weight, and the
+  // k cached slots of its token (expert, norm, gate weight)
+  struct BranchIn {
+    int e;
+    float w;
+    int ej[8];
+    float nc[8], wc[8];
+  };
+  auto load_branch = [&](int r, BranchIn& in) __attribute__((always_inline)) {
+    const int j = tid + kSelThreads * r;
+    if (j >= nb) return;
+    const int64_t f = base + j;
+    in.e = e_t[f];
+    if (mode == kSelFull) return;
+    in.w = w_t[f];
+    const int64_t c0 = base + (j / k) * k;  // the token's first slot
+#pragma unroll
+    for (int jj = 0; jj < 8; ++jj) {
+      if (jj < k) {
+        in.ej[jj] = e_c[c0 + jj];
+        in.nc[jj] = n_c[c0 + jj];
+        in.wc[jj] = w_c[c0 + jj];
+      }
+    }
+  };
+  // with two branches per thread their loads are issued before the entropy
+  // phase, whose own round trip then covers theirs
+  constexpr bool kPre = R <= 2;
+  BranchIn pre[kPre ? R : 1];
+  if constexpr (kPre) {
+#pragma unroll
+    for (int r = 0; r < R; ++r) load_branch(r, pre[r]);
+  }
+
   for (int i = tid; i < R * 64; i += kSelThreads) (&s_cntr[0][0])[i] = 0;
   if (tid < 64) {
     s_cnt[tid] = 0;
@@ -169,21 +203,16 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
     int qv = 0;                           // packed: slot -1, expert 0
     if (j < nb) {
       const int64_t f = base + j;
-      const int e = e_t[f];
+      BranchIn in;
+      if constexpr (kPre) in = pre[r];
+      else load_branch(r, in);
+      const int e = in.e;
       qv = e << 4;
       if (mode != kSelFull) {
-        const int64_t c0 = base + (j / k) * k;  // the token's first slot
-        const float w = w_t[f];
-        int ejs[8];
-        float ncs[8], wcs[8];
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) {
-          if (jj < k) {
-            ejs[jj] = e_c[c0 + jj];
-            ncs[jj] = n_c[c0 + jj];
-            wcs[jj] = w_c[c0 + jj];
-          }
-        }
+        const float w = in.w;
+        const int* ejs = in.ej;
+        const float* ncs = in.nc;
+        const float* wcs = in.wc;
         int q = -1;
         double den = 0.0;
         float ncq = 0.0f, wcq = 0.0f;
