@@ -145,6 +145,7 @@ class Policy:
     beta: float = 0.65
     lambda1: float = 1.0
     lambda2: float = 1.0
+    lambda0: float = 1.0
     refresh_cycle: int = 4
     norm_topk: bool = True
     act: str = "gelu_tanh"
@@ -328,9 +329,12 @@ def match(e_t: np.ndarray, e_c: np.ndarray):
     return q >= 0, q
 
 
-def score(w_t, w_c, n_c, e_c, q, matched, lambda1: float, lambda2: float):
+def score(w_t, w_c, n_c, e_c, q, matched, lambda1: float, lambda2: float,
+          lambda0: float = 1.0):
     """Delta = |w_p - w_c[q]|,  o = n_c[q] / sum_{valid j} n_c[j],
-    s = w_p + lambda1*Delta + lambda2*o  (evaluated left to right in fp32).
+    s = lambda0*w_p + lambda1*Delta + lambda2*o  (evaluated left to right in
+    fp32; the score eq. of Sec. 4.2 has lambda0 = 1, and 0 drops the routing
+    weight as in the score-signal ablation table of Sec. 5).
 
     The denominator is summed in fp64 and rounded once.  Unmatched branches
     get Delta = o = s = 0 (they are never scored).  Returns (Delta, o, s)."""
@@ -342,7 +346,7 @@ def score(w_t, w_c, n_c, e_c, q, matched, lambda1: float, lambda2: float):
     den_b = np.broadcast_to(den[..., None], w_t.shape)
     safe = np.where(den_b > 0, den_b, F32(1.0))
     o = np.where(den_b > 0, (nc_q / safe).astype(F32), F32(0.0)).astype(F32)
-    s = (w_t + (F32(lambda1) * delta).astype(F32)).astype(F32)
+    s = ((F32(lambda0) * w_t).astype(F32) + (F32(lambda1) * delta).astype(F32)).astype(F32)
     s = (s + (F32(lambda2) * o).astype(F32)).astype(F32)
     zero = F32(0.0)
     return (np.where(matched, delta, zero), np.where(matched, o, zero),
@@ -547,7 +551,7 @@ def step(dims: Dims, policy: Policy, W: Weights, state: State, x_t: np.ndarray,
     else:
         matched, q = match(e_t, state.e_c)
         _, _, s = score(w_t, state.w_c, state.n_c, state.e_c, q, matched,
-                        policy.lambda1, policy.lambda2)
+                        policy.lambda1, policy.lambda2, policy.lambda0)
         m = margins(s, tau, e_t, matched)
         rec["s"] = s
         if policy.mode == MODE_THRESHOLD:

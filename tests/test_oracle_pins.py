@@ -356,7 +356,8 @@ def test_score_worked_example():
         e_c = np.array([case["e_c"]], np.int32)
         matched, q = O.match(e_t, e_c)
         assert list(q[0]) == case["q"]
-        delta, o, s = O.score(w, w_c, n_c, e_c, q, matched, case["lambda1"], case["lambda2"])
+        delta, o, s = O.score(w, w_c, n_c, e_c, q, matched, case["lambda1"], case["lambda2"],
+                              case.get("lambda0", 1.0))
         np.testing.assert_allclose(delta[0], case["delta"], atol=1e-6)
         np.testing.assert_allclose(o[0], case["o"], atol=1e-6)
         np.testing.assert_allclose(s[0], case["s"], atol=1e-6)
@@ -365,6 +366,25 @@ def test_score_worked_example():
         m = O.margins(s[None], tau, e_t[None], matched[None])
         mask = O.select_threshold(matched[None], m)
         assert [bool(v) for v in mask[0, 0]] == case["recompute"]
+
+
+def test_score_signal_ablations_are_exact():
+    """lambda0 = 1 is the score eq. of Sec. 4.2 bit for bit; a single
+    remaining signal is that signal exactly (the other terms add +0)."""
+    rng = np.random.default_rng(12)
+    T, k = 300, 4
+    w = rng.random((T, k)).astype(F32)
+    w_c = rng.random((T, k)).astype(F32)
+    n_c = rng.random((T, k)).astype(F32) + F32(0.1)
+    e = np.tile(np.arange(k, dtype=np.int32), (T, 1))
+    e_c = e[:, ::-1].copy()
+    matched, q = O.match(e, e_c)
+    delta, o, s_all = O.score(w, w_c, n_c, e_c, q, matched, 1.0, 1.0)
+    _, _, s_one = O.score(w, w_c, n_c, e_c, q, matched, 1.0, 1.0, 1.0)
+    assert np.array_equal(s_all, s_one)
+    assert np.array_equal(O.score(w, w_c, n_c, e_c, q, matched, 1.0, 0.0, 0.0)[2], delta)
+    assert np.array_equal(O.score(w, w_c, n_c, e_c, q, matched, 0.0, 1.0, 0.0)[2], o)
+    assert np.array_equal(O.score(w, w_c, n_c, e_c, q, matched, 0.0, 0.0, 1.0)[2], w)
 
 
 def test_score_reduces_to_weight_threshold_without_lambdas():
