@@ -15,6 +15,7 @@ source no longer matches the one the counters were taken on.
     python bench.py [--steps K] [--warmup W] [--workload xl1024]
                     [--phase both|cached|full] [--no-cpu] [--no-graph]
                     [--sweep 0,0.1,...]   (extra cache-step timings per refresh ratio)
+                    [--policy-study]      (threshold-mode controller study instead)
 
 Prints one JSON line.
 """
@@ -61,6 +62,10 @@ def parse():
                     help="MALL-flushed timing: write this many MiB between single timed steps (0: off)")
     ap.add_argument("--copy-mib", type=int, default=0,
                     help="also run a plain device copy of this many MiB (counter calibration)")
+    ap.add_argument("--policy-study", action="store_true",
+                    help="instead of the headline line: threshold-mode controller study (alpha, "
+                         "tau0, beta sweeps and score-signal ablations) over --steps steps of the "
+                         "synthetic trajectory, against the uncached layer; one JSON line")
     ap.add_argument("--blas-reference", action="store_true",
                     help="instead of the layer: time the vendor bf16 batched GEMM (torch.bmm) on "
                          "the per-expert shapes of the workload's two projections, as a reference "
@@ -161,6 +166,91 @@ def kernel_traffic(kernel_src: str, summary: str):
         return None
 
 
+def bf16_bits_to_f32(t):
+    """bf16 bit patterns held in an int16 tensor -> float32 values."""
+    import torch
+    return ((t.to(torch.int32) & 0xFFFF) << 16).view(torch.float32)
+
+
+def policy_study(args, shape, make_layer, xs, out, _lib):
+    """Threshold-mode controller study on the synthetic trajectory: the
+    mechanisms behind the ablations of Sec. 5 (adaptive vs fixed threshold,
+    tau0 and beta sweeps, score-signal ablation) and the reuse-over-match
+    ratio of Fig. 8, measured as recompute share, reuse over match, time per
+    step and output deviation from the uncached layer (the same kernels in
+    MOECA_MODE_FULL) on the same inputs.  The paper's image-quality metrics
+    need its trained models and datasets and are not reproduced; the output
+    deviation is this study's stand-in.  Forced full steps every 4 steps
+    (Sec. 5.1), tau0 0.8, alpha 0.6, beta 0.65, lambda 1 unless varied."""
+    import torch
+    T = len(xs)
+    f32 = bf16_bits_to_f32 if shape.dtype == "bf16" else (lambda t: t.float())
+    ref = []
+    Lf = make_layer(_lib.MOECA_MODE_FULL, {})
+    for t in range(T):
+        Lf.step(xs[t], t, out)
+        ref.append(f32(out).clone())
+    Lf.close()
+    base = dict(tau0=0.80, alpha=0.6, beta=0.65, lambda0=1.0, lambda1=1.0, lambda2=1.0)
+    THR, RAT = _lib.MOECA_MODE_THRESHOLD, _lib.MOECA_MODE_RATIO
+    configs = [("paper (adaptive, alpha 0.6)", {})]
+    configs += [(f"fixed threshold (alpha 0)", dict(alpha=0.0))]
+    configs += [(f"alpha {a}", dict(alpha=a)) for a in (0.4, 0.8)]
+    configs += [(f"tau0 {v:.2f}", dict(tau0=v)) for v in (0.65, 0.70, 0.75, 0.85, 0.90, 0.95, 1.00)]
+    configs += [(f"beta {v:.2f}", dict(beta=v)) for v in (0.45, 0.55, 0.75, 0.85)]
+    signals = (("w only", (1, 0, 0)), ("Delta only", (0, 1, 0)), ("o only", (0, 0, 1)),
+               ("w + Delta", (1, 1, 0)), ("w + o", (1, 0, 1)), ("Delta + o", (0, 1, 1)))
+    for name, lam in signals:
+        configs.append((f"score: {name}", dict(lambda0=float(lam[0]), lambda1=float(lam[1]),
+                                               lambda2=float(lam[2]))))
+    # the same ablation at an equal budget (ratio mode, 30 % of the branches
+    # per sample): the output deviation then compares how well each score
+    # ranks branches, at the same compute
+    configs.append(("ratio 0.3, score: all", dict(mode=RAT, ratio=0.3)))
+    for name, lam in signals:
+        configs.append((f"ratio 0.3, score: {name}",
+                        dict(mode=RAT, ratio=0.3, lambda0=float(lam[0]),
+                             lambda1=float(lam[1]), lambda2=float(lam[2]))))
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    rows = []
+    for name, kw in configs:
+        pol = dict(base, **kw)
+        mode = pol.pop("mode", THR)
+        L = make_layer(mode, pol)
+        L.reset()
+        rec, rom, err_l2, err_max = [], [], [], []
+        for t in range(T):
+            L.step(xs[t], t, out)
+            st = L.stats()  # synchronises
+            y = f32(out)
+            r = ref[t]
+            err_l2.append(float(torch.linalg.vector_norm(y - r) / torch.linalg.vector_norm(r)))
+            err_max.append(float((y - r).abs().max() / r.abs().max()))
+            if not st.full_step:
+                rec.append(st.n_recompute / st.n_branches)
+                rom.append(st.reuse_over_match)
+        L.reset()
+        torch.cuda.synchronize()
+        e0.record()
+        for t in range(T):
+            L.step(xs[t], t, out)
+        e1.record()
+        torch.cuda.synchronize()
+        L.close()
+        rows.append({"config": name, "mode": "ratio" if mode == RAT else "threshold",
+                     "ratio": pol.get("ratio"), **{k: pol[k] for k in base},
+                     "recompute_share": round(float(np.mean(rec)), 4),
+                     "reuse_over_match": round(float(np.mean(rom)), 4),
+                     "reuse_over_match_per_step": [round(v, 4) for v in rom],
+                     "rel_l2_err": round(float(np.mean(err_l2)), 5),
+                     "max_rel_err": round(float(np.mean(err_max)), 5),
+                     "ms_per_step": round(e0.elapsed_time(e1) / T, 4)})
+        log(f"[policy] {name}: recompute {rows[-1]['recompute_share']:.3f} "
+            f"reuse/match {rows[-1]['reuse_over_match']:.3f} l2 {rows[-1]['rel_l2_err']:.4f} "
+            f"{rows[-1]['ms_per_step']:.3f} ms")
+    return rows
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -217,6 +307,20 @@ def main():
         return L
 
     stream = torch.cuda.current_stream()
+    if args.policy_study:
+        def make_policy_layer(mode, pol):
+            L = MoecaLayer(shape.d, shape.E, shape.k, shape.d_ff, batch=shape.B,
+                           tokens=shape.N, mode=mode, refresh_cycle=4, dtype=shape.dtype,
+                           act=act, norm_topk=norm_topk, n_shared=shape.n_shared, **pol)
+            L.set_weights(*dW)
+            if dWsh is not None:
+                L.set_shared(*dWsh)
+            L.reset()
+            return L
+        rows = policy_study(args, shape, make_policy_layer, xs, out, _lib)
+        print(json.dumps({"policy_study": rows, "workload": args.workload, "steps": T,
+                          "data": "synthetic", "drift": drift}), flush=True)
+        return
 
     def run(L, t0, t1):
         for t in range(t0, t1):

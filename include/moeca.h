@@ -79,11 +79,15 @@ typedef struct moeca_policy {
                             MoE eq.), 0..8; they have the routed experts' shape
                             and activation, no gate, run on every token at
                             every step and are never cached                   */
+  float lambda0;         /* weight of the routing weight w in the score
+                            s = lambda0 w + lambda1 Delta + lambda2 o; 1.0 is
+                            the score eq. of Sec. 4.2, 0 drops w (the
+                            score-signal ablation of Sec. 5)                   */
 } moeca_policy;
 
 /* Fill *p with the paper's settings: THRESHOLD mode, tau0 0.80, alpha 0.6,
- * beta 0.65 (Sec. 5.4, Tab. 4), refresh cycle 4 (Sec. 5.1), lambda1 =
- * lambda2 = 1 (not reported by the paper), ratio 0.3, bf16, tanh GELU,
+ * beta 0.65 (Sec. 5.4, Tab. 4), refresh cycle 4 (Sec. 5.1), lambda0 = 1,
+ * lambda1 = lambda2 = 1 (not reported by the paper), ratio 0.3, bf16, tanh GELU,
  * renormalised top-k, batch 1, tokens 1, no shared experts.  NULL is
  * ignored. */
 void moeca_policy_default(moeca_policy* p);

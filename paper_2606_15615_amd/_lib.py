@@ -34,6 +34,7 @@ class moeca_policy(ctypes.Structure):
         ("lambda2", ctypes.c_float), ("refresh_cycle", ctypes.c_int32),
         ("norm_topk", ctypes.c_int32), ("act", ctypes.c_int32), ("dtype", ctypes.c_int32),
         ("batch", ctypes.c_int32), ("tokens", ctypes.c_int32), ("n_shared", ctypes.c_int32),
+        ("lambda0", ctypes.c_float),
     ]
 
 

@@ -32,7 +32,9 @@ namespace {
 //   exactly: S log S and A are then the same rounded product.
 //   q(p): cached slot with the same expert, or -1           (Sec. 4.2)
 //   Delta = |w_p - w_c[q]|,  o = n_c[q] / f32(sum_j n_c[j]),
-//   s = (w_p + lambda1*Delta) + lambda2*o,  m = s - tau_{b,e_p}
+//   s = (lambda0*w_p + lambda1*Delta) + lambda2*o,  m = s - tau_{b,e_p}
+//   (lambda0 = 1 is the score eq.; other values serve the score-signal
+//   ablation of Sec. 5)
 //   full step : R = all, sigma(p) = p
 //   threshold : R = unmatched U {m > 0}                    (Sec. 4.2)
 //   ratio     : R = unmatched U the first max(0, K_b - |U|) matched branches
@@ -55,7 +57,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
     const float* __restrict__ n_c, const double* __restrict__ ent,
     int with_stat, double log_n, float tau0, float alpha, float* __restrict__ hbar,
     float* __restrict__ tau,
-    int N, int E, int k, int mode, int budget, float lambda1, float lambda2,
+    int N, int E, int k, int mode, int budget, float lambda0, float lambda1, float lambda2,
     int32_t* __restrict__ q_out,
     float* __restrict__ margin, uint8_t* __restrict__ mask, int32_t* __restrict__ sigma,
     uint8_t* __restrict__ sync, int32_t* __restrict__ cnt_bs, int32_t* __restrict__ stats_bs,
@@ -231,7 +233,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
           const float denf = static_cast<float>(den);
           const float delta = fabsf(__fsub_rn(w, wcq));
           const float o = denf > 0.0f ? __fdiv_rn(ncq, denf) : 0.0f;
-          float sc = __fadd_rn(w, __fmul_rn(lambda1, delta));
+          float sc = __fadd_rn(__fmul_rn(lambda0, w), __fmul_rn(lambda1, delta));
           sc = __fadd_rn(sc, __fmul_rn(lambda2, o));
           m = __fsub_rn(sc, s_tau[e]);
         } else {
@@ -628,9 +630,9 @@ __global__ void reset_kernel(int32_t* __restrict__ e_c, float* __restrict__ w_c,
 
 }  // namespace
 
-hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1, float lambda2,
-                         bool with_stat, float tau0, float alpha, const Buffers& b,
-                         hipStream_t st) {
+hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda0, float lambda1,
+                         float lambda2, bool with_stat, float tau0, float alpha,
+                         const Buffers& b, hipStream_t st) {
   const int nb = s.N * s.k;
   const size_t lds = size_t(2) * nb;
   if (lds > 64 * 1024) return hipErrorInvalidValue;
@@ -639,7 +641,8 @@ hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1
   launch_kernel(&decide_kernel<RR>, dim3(s.B), dim3(kSelThreads), uint32_t(lds), st, b.e_t,   \
                 b.w_t, b.e_c, b.w_c, b.n_c, b.ent, with_stat ? 1 : 0, log_n, tau0,            \
                 alpha,                                                                        \
-                b.hbar, b.tau, s.N, s.E, s.k, sel_mode, budget, lambda1, lambda2, b.q,        \
+                b.hbar, b.tau, s.N, s.E, s.k, sel_mode, budget, lambda0, lambda1, lambda2,    \
+                b.q,                                                                          \
                 b.margin, b.mask, b.sigma, b.sync, b.cnt_bs, b.stats_bs, b.cnt_ch)
   if (nb <= 2 * kSelThreads) {
     MOECA_DECIDE(2);

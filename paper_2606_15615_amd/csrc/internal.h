@@ -98,9 +98,9 @@ hipError_t launch_router(const Shape& s, const void* x, const void* W_r, const f
                          hipStream_t st);
 // with_stat: the router advanced the statistic in this step; the decide
 // kernel then derives the entropy and thresholds first (hbar, tau).
-hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda1, float lambda2,
-                         bool with_stat, float tau0, float alpha, const Buffers& b,
-                         hipStream_t st);
+hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda0, float lambda1,
+                         float lambda2, bool with_stat, float tau0, float alpha,
+                         const Buffers& b, hipStream_t st);
 hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st);
 // act: MOECA_ACT_* of the policy.  W_*_sh: the shared experts (S > 0).
 hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, const void* W_up_sh,

@@ -134,6 +134,7 @@ void moeca_policy_default(moeca_policy* p) {
   p->tau0 = 0.80f;
   p->alpha = 0.6f;
   p->beta = 0.65f;
+  p->lambda0 = 1.0f;
   p->lambda1 = 1.0f;
   p->lambda2 = 1.0f;
   p->refresh_cycle = 4;
@@ -171,8 +172,8 @@ moeca_layer* moeca_layer_create(int d, int E, int k, int d_ff, const moeca_polic
   if (!(p->alpha >= 0.0f && p->alpha < 1.0f)) return bad("alpha must be in [0, 1)");
   if (!(p->beta >= 0.0f && p->beta < 1.0f)) return bad("beta must be in [0, 1)");
   if (!(p->lambda1 >= 0.0f) || !std::isfinite(p->lambda1) || !(p->lambda2 >= 0.0f) ||
-      !std::isfinite(p->lambda2))
-    return bad("lambda1, lambda2 must be finite and >= 0");
+      !std::isfinite(p->lambda2) || !(p->lambda0 >= 0.0f) || !std::isfinite(p->lambda0))
+    return bad("lambda0, lambda1, lambda2 must be finite and >= 0");
   if (p->refresh_cycle < 0) return bad("refresh_cycle must be >= 0");
   if (p->norm_topk != 0 && p->norm_topk != 1) return bad("norm_topk must be 0 or 1");
   if (p->batch < 1 || p->tokens < 1) return bad("batch and tokens must be >= 1");
@@ -340,7 +341,7 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
     budget = static_cast<int>(std::floor(static_cast<double>(p.ratio) * s.N * s.k + 0.5));
   }
   arm();
-  if (!check(moeca::launch_decide(s, sel, budget, p.lambda1, p.lambda2, !uncached, p.tau0,
+  if (!check(moeca::launch_decide(s, sel, budget, p.lambda0, p.lambda1, p.lambda2, !uncached, p.tau0,
                                   p.alpha, b, st),
              "decide"))
     return MOECA_E_HIP;

@@ -38,12 +38,13 @@ class MoecaLayer:
 
     def __init__(self, d, E, k, d_ff, *, batch, tokens, mode=_lib.MOECA_MODE_THRESHOLD,
                  ratio=0.3, tau0=0.80, alpha=0.6, beta=0.65, lambda1=1.0, lambda2=1.0,
-                 refresh_cycle=4, norm_topk=True, act="gelu_tanh", dtype="bf16",
+                 lambda0=1.0, refresh_cycle=4, norm_topk=True, act="gelu_tanh", dtype="bf16",
                  n_shared=0, device="cuda:0"):
         torch = _torch()
         p = _lib.moeca_policy_default()
         p.mode, p.ratio, p.tau0, p.alpha, p.beta = mode, ratio, tau0, alpha, beta
-        p.lambda1, p.lambda2, p.refresh_cycle = lambda1, lambda2, refresh_cycle
+        p.lambda0, p.lambda1, p.lambda2 = lambda0, lambda1, lambda2
+        p.refresh_cycle = refresh_cycle
         p.norm_topk = 1 if norm_topk else 0
         p.act = {"gelu_tanh": _lib.MOECA_ACT_GELU_TANH, "gelu_erf": _lib.MOECA_ACT_GELU_ERF,
                  "swiglu": _lib.MOECA_ACT_SWIGLU}[act]

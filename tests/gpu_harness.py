@@ -49,6 +49,7 @@ class Setup:
                                 ratio=self.pol.ratio, tau0=self.pol.tau0,
                                 alpha=self.pol.alpha, beta=self.pol.beta,
                                 lambda1=self.pol.lambda1, lambda2=self.pol.lambda2,
+                                lambda0=self.pol.lambda0,
                                 refresh_cycle=self.pol.refresh_cycle,
                                 norm_topk=self.pol.norm_topk, act=self.pol.act,
                                 n_shared=shape.n_shared)

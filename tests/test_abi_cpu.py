@@ -47,6 +47,7 @@ def test_policy_default_is_the_papers(L):
     assert p.beta == pytest.approx(hp["beta"]["value"])
     assert p.refresh_cycle == hp["refresh_cycle"]["value"]
     assert p.norm_topk == 1 and p.dtype == L.MOECA_DTYPE_BF16
+    assert p.lambda0 == 1.0 and p.lambda1 == 1.0 and p.lambda2 == 1.0
 
 
 def _pol(L, **kw):
@@ -75,6 +76,7 @@ BAD_POLICY = [
     dict(mode=7), dict(dtype=3), dict(act=9), dict(ratio=-0.1), dict(ratio=1.5),
     dict(ratio=math.nan), dict(alpha=1.0), dict(alpha=-0.2), dict(beta=1.0), dict(beta=-0.1),
     dict(tau0=0.0), dict(tau0=math.inf), dict(lambda1=-1.0), dict(lambda2=math.nan),
+    dict(lambda0=-0.5), dict(lambda0=math.inf),
     dict(refresh_cycle=-1), dict(norm_topk=2), dict(batch=0), dict(tokens=0),
     dict(batch=1 << 20, tokens=1 << 12), dict(n_shared=-1), dict(n_shared=9),
     dict(batch=1 << 14, tokens=1 << 14, n_shared=6),

@@ -68,6 +68,19 @@ def test_unnormalised_gate_erf_gelu_and_bias():
     run_forced(S, 4, label="variants")
 
 
+@pytest.mark.parametrize("lams", [(1.0, 0.0, 0.0), (0.0, 1.0, 0.0), (0.0, 0.0, 1.0),
+                                  (0.0, 1.0, 1.0), (0.5, 2.0, 0.25)])
+def test_score_signal_ablations(lams):
+    """Score-signal ablation (Sec. 5): s = lambda0 w + lambda1 Delta +
+    lambda2 o with single signals, a pair and unequal weights, threshold
+    mode (thresholds scaled so each variant recomputes a share)."""
+    l0, l1, l2 = lams
+    shape = LayerShape(d=128, E=8, k=2, d_ff=192, B=2, N=64, dtype="bf16")
+    S = Setup(shape, mode="threshold", seed=17, T=4, lambda0=l0, lambda1=l1, lambda2=l2,
+              tau0=0.3, alpha=0.6, refresh_cycle=0)
+    run_forced(S, 4, label=f"score {lams}")
+
+
 # ---------------------------------------------------------------------------
 # uncached comparator, empty recomputation set, ratio 0 bit-exact combine
 # ---------------------------------------------------------------------------
