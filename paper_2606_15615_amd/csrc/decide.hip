@@ -547,7 +547,8 @@ __global__ __launch_bounds__(kSelThreads) void lists_kernel(
   const int sg = sel ? sigma[f] : 0;
 
   // per expert: total over all chunks and count in the chunks before this one
-  const int parts = kSelThreads / E;  // thread (e0, part) for part < parts; E <= 64
+  // thread (e0, part) for part < parts; E <= 64
+  const int parts = min(kSelThreads / E, nchunks);
   const int e0 = tid % E, part = tid / E;
   int tot = 0, bef = 0;
   if (part < parts) {
@@ -563,24 +564,17 @@ __global__ __launch_bounds__(kSelThreads) void lists_kernel(
   if (wv == 0) {
     int t = 0, bf = 0;
     if (lane < E) {
+#pragma unroll 4
       for (int pp = 0; pp < parts; ++pp) {
         t += s_part_tot[pp * E + lane];
         bf += s_part_bef[pp * E + lane];
       }
     }
     const int mt = (t + tm - 1) / tm;
-    int o = t, tu = mt * nt_up, td = mt * nt_down;  // inclusive scans over experts
-#pragma unroll
-    for (int dd = 1; dd < kWave; dd <<= 1) {
-      const int vo = __shfl_up(o, dd, kWave);
-      const int vu = __shfl_up(tu, dd, kWave);
-      const int vd = __shfl_up(td, dd, kWave);
-      if (lane >= dd) {
-        o += vo;
-        tu += vu;
-        td += vd;
-      }
-    }
+    // inclusive scans over experts
+    const int o = wave_incl_scan_i32(t);
+    const int tu = wave_incl_scan_i32(mt * nt_up);
+    const int td = wave_incl_scan_i32(mt * nt_down);
     if (lane < E) s_base[lane] = o - t + bf;
     if (my == 0 && lane < E) {
       // exclusive prefixes per expert; the last expert also writes the
