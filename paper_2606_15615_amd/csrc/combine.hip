@@ -261,6 +261,99 @@ __global__ __launch_bounds__(kCombWaves * kWave) void combine_fast_kernel(
   }
 }
 
+// bf16 layers outside the fast path (k up to 8, shared experts): one wave
+// per token as in combine_kernel, but for each 16-byte group every row load
+// (the S shared rows, the k cache rows and, when synchronised, the attention
+// row) is issued before any is used.  Same arithmetic and order.
+template <int KMAX, int SMAX>
+__global__ __launch_bounds__(kCombWaves * kWave) void combine_wide_kernel(
+    const float* __restrict__ w_t, const int32_t* __restrict__ e_t,
+    const int32_t* __restrict__ sigma, const uint8_t* __restrict__ mask,
+    const uint8_t* __restrict__ sync, uint16_t* __restrict__ h_c, int32_t* __restrict__ e_c,
+    float* __restrict__ w_c, float* __restrict__ n_c, uint16_t* __restrict__ out,
+    const uint16_t* __restrict__ attn_in, uint16_t* __restrict__ attn_cache,
+    const uint16_t* __restrict__ h_sh, int S, int64_t T_tokens, int d, int k,
+    int write_cache) {
+  typedef Raw8<uint16_t>::v raw;
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t t = __builtin_amdgcn_readfirstlane(
+      static_cast<int>(blockIdx.x) * kCombWaves + static_cast<int>(threadIdx.x) / kWave);
+  if (t >= T_tokens) return;
+  const int groups = d / 8;
+
+  float wp[KMAX];
+  int slot[KMAX];
+  bool rec[KMAX];
+#pragma unroll
+  for (int p = 0; p < KMAX; ++p) {
+    wp[p] = 0.0f;
+    slot[p] = 0;
+    rec[p] = false;
+    if (p < k) {
+      const int64_t f = t * k + p;
+      wp[p] = w_t[f];
+      slot[p] = sigma[f];
+      rec[p] = mask[f] != 0;
+    }
+  }
+  const bool syn = write_cache && attn_in != nullptr && sync[t] != 0;
+  double ss[KMAX];
+#pragma unroll
+  for (int p = 0; p < KMAX; ++p) ss[p] = 0.0;
+
+  for (int g = lane; g < groups; g += kWave) {
+    raw hs[SMAX], hk[KMAX], av;
+#pragma unroll
+    for (int sh = 0; sh < SMAX; ++sh)
+      if (sh < S) hs[sh] = Raw8<uint16_t>::load(h_sh + (sh * T_tokens + t) * d + g * 8);
+#pragma unroll
+    for (int p = 0; p < KMAX; ++p)
+      if (p < k) hk[p] = Raw8<uint16_t>::load(h_c + (t * k + slot[p]) * d + g * 8);
+    if (syn) av = Raw8<uint16_t>::load(attn_in + t * d + g * 8);
+    float acc[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc[u] = 0.0f;
+#pragma unroll
+    for (int sh = 0; sh < SMAX; ++sh) {
+      if (sh < S) {
+        float h[8];
+        Raw8<uint16_t>::widen(hs[sh], h);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc[u] = __fadd_rn(acc[u], h[u]);
+      }
+    }
+#pragma unroll
+    for (int p = 0; p < KMAX; ++p) {
+      if (p < k) {
+        float h[8];
+        Raw8<uint16_t>::widen(hk[p], h);
+#pragma unroll
+        for (int u = 0; u < 8; ++u) acc[u] = __fadd_rn(acc[u], __fmul_rn(wp[p], h[u]));
+        if (rec[p]) {
+#pragma unroll
+          for (int u = 0; u < 8; ++u)
+            ss[p] += static_cast<double>(h[u]) * static_cast<double>(h[u]);
+        }
+      }
+    }
+    Raw8<uint16_t>::store(out + t * d + g * 8, Raw8<uint16_t>::narrow(acc));
+    if (syn) Raw8<uint16_t>::store(attn_cache + t * d + g * 8, av);
+  }
+
+  if (!write_cache) return;
+#pragma unroll
+  for (int p = 0; p < KMAX; ++p) {
+    if (p >= k || !rec[p]) continue;  // uniform across the wave (one token per wave)
+    const double sq = wave_sum_f64(ss[p]);
+    if (lane == 0) {
+      const int64_t c = t * k + slot[p];
+      n_c[c] = static_cast<float>(sqrt(sq));
+      e_c[c] = e_t[t * k + p];
+      w_c[c] = wp[p];
+    }
+  }
+}
+
 }  // namespace
 
 hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void* attn_in,
@@ -285,6 +378,8 @@ hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void
     if (s.k == 1) { MOECA_FAST(uint16_t, 1) } else { MOECA_FAST(uint16_t, 2) }
   } else if (fast) {
     if (s.k == 1) { MOECA_FAST(float, 1) } else { MOECA_FAST(float, 2) }
+  } else if (s.bf16 && s.tokens() < (int64_t(1) << 31)) {
+    MOECA_COMBINE((combine_wide_kernel<8, 8>), uint16_t);
   } else if (s.bf16) {
     MOECA_COMBINE(combine_kernel<uint16_t>, uint16_t);
   } else {
