@@ -11,8 +11,9 @@
 // expert l % 16 (B operand) at MFMA k-row l / 16; the k-rows interleave in
 // runs of one load vector, so a row's four lanes read a contiguous segment
 // of both the token row and the expert row with each load.  Four accumulator
-// chains rotate to hide the MFMA latency; the chains and then the four
-// waves' partial sums are added in a fixed order (deterministic).
+// chains (two with more than 32 experts) rotate to hide the MFMA latency;
+// the chains and then the four waves' partial sums are added in a fixed
+// order (deterministic).
 //
 // Loads are software-pipelined: a wave's share of d is walked in chunks,
 // the next chunk's loads issued before the current chunk's MFMAs.
@@ -148,7 +149,10 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
 #pragma unroll
   for (int q = 0; q < NG; ++q) wp[q] = Wg + int64_t(min(16 * q + n, E - 1)) * d + kbase;
 
-  constexpr int NCH = 4;  // independent accumulator chains per expert group
+  // independent accumulator chains per expert group: four, or two when the
+  // expert groups alone give enough independent MFMAs (and registers for
+  // two waves per SIMD are wanted)
+  constexpr int NCH = NG >= 3 ? 2 : 4;
   f64x4_t acc[NCH][NG];
 #pragma unroll
   for (int c = 0; c < NCH; ++c)
@@ -156,7 +160,7 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
     for (int q = 0; q < NG; ++q) acc[c][q] = f64x4_t{0.0, 0.0, 0.0, 0.0};
   // chunks of CH vectors, double-buffered: the next chunk's loads are issued
   // before the current chunk's MFMAs
-  constexpr int CH = NG == 1 ? 3 : (NG == 2 ? 2 : 1);
+  constexpr int CH = NG == 1 ? 3 : 2;
   typedef typename Vec<T, VW>::raw Raw;
   Raw xa[CH], wa[CH][NG], xb[CH], wb[CH][NG];
   auto load = [&](Raw (&xr)[CH], Raw (&wr)[CH][NG], int c0) __attribute__((always_inline)) {
@@ -199,7 +203,9 @@ __global__ __launch_bounds__(kRouterWaves * kWave) void router_kernel(
   for (int q = 0; q < NG; ++q)
 #pragma unroll
     for (int r = 0; r < 4; ++r)
-      s_part[wv][q][r][lane] = (acc[0][q][r] + acc[1][q][r]) + (acc[2][q][r] + acc[3][q][r]);
+      s_part[wv][q][r][lane] = NCH == 4
+                                   ? (acc[0][q][r] + acc[1][q][r]) + (acc[2 % NCH][q][r] + acc[3 % NCH][q][r])
+                                   : acc[0][q][r] + acc[1][q][r];
   __syncthreads();
 
   // ---- epilogue: tokens 4 wv + g, register r = wv of every wave's partial --
