@@ -8,6 +8,7 @@
 // in the order the method states them (this file is built without FMA
 // contraction), and reductions are fp64 sums of exact values rounded once.
 // No atomic operation decides an order: counts use integer atomics only.
+#include <algorithm>
 #include <cmath>
 
 #include "common.h"
@@ -70,6 +71,9 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   __shared__ int s_cntr[R][64];  // per 1024-branch chunk of the sample
   __shared__ float s_tau[64];
   __shared__ int s_tcnt[R][kSelWaves];
+  // with more than 8 branches per thread: the high 16 bits of each branch's
+  // margin key, so that most key decisions need no global read
+  __shared__ uint16_t s_k16[R <= 8 ? 1 : R * kSelThreads];
   __shared__ int s_unmatched, s_recompute, s_sync;
   __shared__ uint32_t s_ckey[kDirect];  // ratio mode: the candidates of the last digit
   __shared__ int s_cj[kDirect];
@@ -99,12 +103,27 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
     if (mode == kSelFull) return;
     in.w = w_t[f];
     const int64_t c0 = base + (j / k) * k;  // the token's first slot
+    if (k == 8 || k == 4) {
+      // 16-byte vectors: the token's slots start at a multiple of k entries
 #pragma unroll
-    for (int jj = 0; jj < 8; ++jj) {
-      if (jj < k) {
-        in.ej[jj] = e_c[c0 + jj];
-        in.nc[jj] = n_c[c0 + jj];
-        in.wc[jj] = w_c[c0 + jj];
+      for (int h = 0; h < 2; ++h) {
+        if (h * 4 < k) {
+          const int4 ev = *reinterpret_cast<const int4*>(e_c + c0 + 4 * h);
+          const float4 nv = *reinterpret_cast<const float4*>(n_c + c0 + 4 * h);
+          const float4 wv4 = *reinterpret_cast<const float4*>(w_c + c0 + 4 * h);
+          in.ej[4 * h] = ev.x; in.ej[4 * h + 1] = ev.y; in.ej[4 * h + 2] = ev.z; in.ej[4 * h + 3] = ev.w;
+          in.nc[4 * h] = nv.x; in.nc[4 * h + 1] = nv.y; in.nc[4 * h + 2] = nv.z; in.nc[4 * h + 3] = nv.w;
+          in.wc[4 * h] = wv4.x; in.wc[4 * h + 1] = wv4.y; in.wc[4 * h + 2] = wv4.z; in.wc[4 * h + 3] = wv4.w;
+        }
+      }
+    } else {
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        if (jj < k) {
+          in.ej[jj] = e_c[c0 + jj];
+          in.nc[jj] = n_c[c0 + jj];
+          in.wc[jj] = w_c[c0 + jj];
+        }
       }
     }
   };
@@ -185,6 +204,26 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
       return j < nb ? margin[base + j] : __int_as_float(0x7f800000);
     }
   };
+  auto key_full = [&](int r) __attribute__((always_inline)) -> uint32_t {
+    return f32_order_key(mval(r));
+  };
+  // (key & msk) compared with t (t has no bits outside msk; msk keeps the
+  // high bits): -1, 0 or 1.  With the key halves in LDS the low half is
+  // read only when the high halves are equal.
+  auto cmp_masked = [&](int r, uint32_t msk, uint32_t t) __attribute__((always_inline)) -> int {
+    if constexpr (kMvRegs) {
+      const uint32_t mk = key_full(r) & msk;
+      return mk > t ? 1 : (mk < t ? -1 : 0);
+    } else {
+      const int j = tid + kSelThreads * r;
+      const uint32_t hm = msk & 0xFFFF0000u;
+      const uint32_t h = (j < nb ? static_cast<uint32_t>(s_k16[j]) << 16 : 0xFF800000u) & hm;
+      if (h != (t & hm)) return h > (t & hm) ? 1 : -1;
+      if ((msk & 0xFFFFu) == 0u) return 0;
+      const uint32_t mk = key_full(r) & msk;
+      return mk > t ? 1 : (mk < t ? -1 : 0);
+    }
+  };
   auto q_of = [&](int r) __attribute__((always_inline)) -> int {
     if constexpr (kMvRegs) {
       return (qe[r] & 15) - 1;
@@ -249,6 +288,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
       qe[r] = qv;
     } else if (j < nb) {
       s_q[j] = static_cast<int8_t>((qv & 15) - 1);
+      s_k16[j] = static_cast<uint16_t>(f32_order_key(m) >> 16);
     }
     // keep the scheduler from hoisting the loads of every branch at once
     // (a thread holds up to 32 branches, each with up to 3 k slot loads):
@@ -294,9 +334,20 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
         // once by one lane, the remaining lanes add their own
 #pragma unroll kU
         for (int r = 0; r < R; ++r) {
-          const uint32_t mk = f32_order_key(mval(r));
-          bool part = q_of(r) >= 0 && ((mk ^ prefix) & hi_mask) == 0u;
-          const int bin = static_cast<int>((mk >> shift) & 255u);
+          bool part = q_of(r) >= 0 && cmp_masked(r, hi_mask, prefix) == 0;
+          int bin = 0;
+          if (part) {
+            if constexpr (!kMvRegs) {
+              if (shift >= 16) {
+                const int j = tid + kSelThreads * r;
+                bin = static_cast<int>((static_cast<uint32_t>(s_k16[j]) >> (shift - 16)) & 255u);
+              } else {
+                bin = static_cast<int>((key_full(r) >> shift) & 255u);
+              }
+            } else {
+              bin = static_cast<int>((key_full(r) >> shift) & 255u);
+            }
+          }
 #pragma unroll
           for (int it = 0; it < 2; ++it) {
             const uint64_t todo = __ballot(part);
@@ -357,10 +408,9 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
 #pragma unroll kU
       for (int r = 0; r < R; ++r) {
         const int j = tid + kSelThreads * r;
-        const uint32_t mk = f32_order_key(mval(r));
-        if (q_of(r) >= 0 && (mk & dmask) == thr) {
+        if (q_of(r) >= 0 && cmp_masked(r, dmask, thr) == 0) {
           const int ci = atomicAdd(&s_ncand, 1);
-          s_ckey[ci] = mk;
+          s_ckey[ci] = key_full(r);
           s_cj[ci] = j;
           s_mask[j] = static_cast<uint8_t>(ci);
         }
@@ -384,7 +434,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
       // so the order is r-major, then wave, then lane)
 #pragma unroll kU
       for (int r = 0; r < R; ++r) {
-        const uint64_t tb = __ballot(q_of(r) >= 0 && f32_order_key(mval(r)) == thr);
+        const uint64_t tb = __ballot(q_of(r) >= 0 && cmp_masked(r, ~0u, thr) == 0);
         if (lane == 0) s_tcnt[r][wv] = __popcll(tb);
       }
       __syncthreads();
@@ -397,7 +447,7 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
           in_r += c;
           if (w2 < wv) below += c;
         }
-        const uint64_t tb = __ballot(q_of(r) >= 0 && f32_order_key(mval(r)) == thr);
+        const uint64_t tb = __ballot(q_of(r) >= 0 && cmp_masked(r, ~0u, thr) == 0);
         const bool flag = ((tb >> lane) & 1ull) != 0;
         if (flag && before + below + lane_rank(tb) < tie_rem) tie_bits |= 1u << r;
         before += in_r;
@@ -414,17 +464,16 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
       if (mode == kSelFull || q_of(r) < 0) {
         rc = true;
       } else if (mode == kSelThreshold) {
-        rc = mval(r) > 0.0f;
+        rc = cmp_masked(r, ~0u, 0x80000000u) > 0;  // m > 0 (+0 and -0 have this key)
       } else if (take_all_matched) {
         rc = true;
       } else if (need == 0) {
         rc = false;
       } else if (direct) {
-        const uint32_t mk = f32_order_key(mval(r)) & dmask;
-        rc = mk > thr || (mk == thr && s_csel[s_mask[j]] != 0);
+        const int c = cmp_masked(r, dmask, thr);
+        rc = c > 0 || (c == 0 && s_csel[s_mask[j]] != 0);
       } else {
-        const uint32_t mk = f32_order_key(mval(r));
-        rc = mk > thr || ((tie_bits >> r) & 1u) != 0;
+        rc = cmp_masked(r, ~0u, thr) > 0 || ((tie_bits >> r) & 1u) != 0;
       }
       mask[base + j] = rc ? 1 : 0;
       s_mask[j] = rc ? 1 : 0;
@@ -607,6 +656,434 @@ __global__ __launch_bounds__(kSelThreads) void lists_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// Multi-block decision path for samples of more than 8192 branches (k a
+// divisor of 1024): the decisions of decide_kernel with a sample spread over
+// ceil(N k / 1024) blocks of one branch per thread; block (b, c) takes the
+// flat ids c 1024 + tid of sample b, whole tokens.  The steps that need the
+// whole sample meet at kernel boundaries:
+//   wide_prep   entropy and thresholds, one wave per (sample, expert); clears
+//               the per-sample scratch, the expert counts and the statistics
+//   wide_score  matching, scores and margins; unmatched counts; in ratio
+//               steps the histogram of the first radix digit, in threshold
+//               and full steps the whole decision
+//   wide_pass p (ratio steps, p = 1, 2, 3) every block derives the digits so
+//               far from the histograms, then adds its keys to the histogram
+//               of digit p, or, right after the digit that left at most
+//               kDirect keys sharing the prefix, appends those keys and their
+//               flat ids to the sample's candidate list
+//   wide_final  the ratio decision: the candidates ranked by (key desc, flat
+//               id asc), or, with more equal keys than kDirect after the
+//               fourth digit, the keys equal to the threshold ranked by flat
+//               id; then mask, counts, slots and sync
+// Scratch per sample (kWideWords ints): four 256-bin histograms, counters
+// (0: unmatched, 3: candidates), candidate keys and flat ids.
+// ---------------------------------------------------------------------------
+constexpr int kWsCtr = 1024, kWsCKey = 1032, kWsCJ = 1096;
+
+// The digit of a radix pass from its 256-bin histogram h (keys descending
+// from bin 255): the bin holding the rem-th key, what remains of rem inside
+// it, and the bin's count.  Wave-wide; every lane gets the same values.
+__device__ __forceinline__ void digit_select(const int* h, int rem, int& bin, int& nrem,
+                                             int& cnt) {
+  const int lane = threadIdx.x & (kWave - 1);
+  int c[4];
+#pragma unroll
+  for (int u = 0; u < 4; ++u) c[u] = h[255 - 4 * lane - u];
+  const int tot = c[0] + c[1] + c[2] + c[3];
+  int run = wave_incl_scan_i32(tot) - tot;
+  int fbin = 0, frem = 0, fcnt = 0;
+  bool found = false;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    if (c[u] > 0 && run < rem && rem <= run + c[u]) {
+      found = true;
+      fbin = 255 - 4 * lane - u;
+      frem = rem - run;
+      fcnt = c[u];
+    }
+    run += c[u];
+  }
+  const int leader = __builtin_ctzll(__ballot(found));
+  bin = __builtin_amdgcn_readlane(fbin, leader);
+  nrem = __builtin_amdgcn_readlane(frem, leader);
+  cnt = __builtin_amdgcn_readlane(fcnt, leader);
+}
+
+// The ratio selection of a sample as far as the first `upto` digit
+// histograms take it.
+struct WideChain {
+  int need = 0;
+  bool take_all = false;
+  bool active = false;     // a threshold key has to be found
+  uint32_t prefix = 0;     // digits found so far
+  uint32_t dmask = 0;      // their bits
+  int rem = 0;             // keys still to take among those sharing prefix
+  int digits = 0;
+  int direct_at = -1;      // digit after which at most kDirect keys remain
+};
+
+__device__ __forceinline__ WideChain wide_chain(const int32_t* ws, int budget, int nb, int upto) {
+  WideChain ch;
+  const int n_unmatched = ws[kWsCtr + 0];
+  const int n_matched = nb - n_unmatched;
+  ch.need = budget - n_unmatched;
+  if (ch.need < 0) ch.need = 0;
+  ch.take_all = ch.need >= n_matched;
+  ch.active = ch.need > 0 && !ch.take_all;
+  ch.rem = ch.need;
+  if (!ch.active) return ch;
+  for (int p = 0; p < upto; ++p) {
+    int bin, nrem, cnt;
+    digit_select(ws + 256 * p, ch.rem, bin, nrem, cnt);
+    const int shift = 24 - 8 * p;
+    ch.prefix |= static_cast<uint32_t>(bin) << shift;
+    ch.dmask = ~0u << shift;
+    ch.rem = nrem;
+    ch.digits = p + 1;
+    if (cnt <= kDirect && p < 3) {
+      ch.direct_at = p;
+      break;
+    }
+  }
+  return ch;
+}
+
+// Adds the block's keys to a 256-bin histogram in LDS (the at most two most
+// frequent bins of a wave by one lane each), then to the global one.
+__device__ __forceinline__ void wide_hist(int* s_h, bool part, int bin, int32_t* gh) {
+  const int lane = threadIdx.x & (kWave - 1);
+#pragma unroll
+  for (int it = 0; it < 2; ++it) {
+    const uint64_t todo = __ballot(part);
+    if (todo == 0ull) break;
+    const int leader = __builtin_ctzll(todo);
+    const int lb = __builtin_amdgcn_readlane(bin, leader);
+    const uint64_t same = __ballot(part && bin == lb);
+    if (lane == leader) atomicAdd(&s_h[lb], __popcll(same));
+    if (bin == lb) part = false;
+  }
+  if (part) atomicAdd(&s_h[bin], 1);
+  __syncthreads();
+  if (threadIdx.x < 256 && s_h[threadIdx.x] != 0) atomicAdd(&gh[threadIdx.x], s_h[threadIdx.x]);
+}
+
+__global__ __launch_bounds__(kSelThreads) void wide_prep_kernel(
+    const double* __restrict__ ent, int with_stat, double log_n, float tau0, float alpha,
+    float* __restrict__ hbar, float* __restrict__ tau, int B, int N, int E,
+    int32_t* __restrict__ ws, int32_t* __restrict__ cnt_bs, int32_t* __restrict__ stats_bs) {
+  const int64_t gt = int64_t(blockIdx.x) * kSelThreads + threadIdx.x;
+  const int64_t gs = int64_t(gridDim.x) * kSelThreads;
+  for (int64_t i = gt; i < int64_t(B) * kWideWords; i += gs) ws[i] = 0;
+  for (int64_t i = gt; i < int64_t(B) * E; i += gs) cnt_bs[i] = 0;
+  for (int64_t i = gt; i < int64_t(B) * 4; i += gs) stats_bs[i] = 0;
+  if (!with_stat) return;
+  // entropy of the statistic and tau (Sec. 4.3), as in decide_kernel
+  const int lane = threadIdx.x & (kWave - 1);
+  const int row = blockIdx.x * kSelWaves + threadIdx.x / kWave;  // b E + e
+  if (row >= B * E) return;
+  const int nch = (N + 15) / 16;
+  const double* P = ent + int64_t(row) * nch * 2;
+  double sp = 0.0, ap = 0.0;
+  for (int c = lane; c < nch; c += kWave) {
+    sp += P[2 * c];
+    ap += P[2 * c + 1];
+  }
+  const double S = wave_sum_f64(sp);
+  const double A = wave_sum_f64(ap);
+  if (lane == 0) {
+    float hb = 0.0f;
+    if (N > 1 && S > 0.0) {
+      const double Hs = (S * log(S) - A) / S;
+      double v = Hs / log_n;
+      v = v < 0.0 ? 0.0 : (v > 1.0 ? 1.0 : v);
+      hb = static_cast<float>(v);
+    }
+    const float centred = __fsub_rn(__fmul_rn(2.0f, hb), 1.0f);
+    hbar[row] = hb;
+    tau[row] = __fmul_rn(tau0, __fadd_rn(1.0f, __fmul_rn(alpha, centred)));
+  }
+}
+
+// Mask, counts, slots and sync of one block (one branch per thread, whole
+// tokens), as steps 3 and 4 of decide_kernel.
+__device__ __forceinline__ void wide_finish(int b, int c, int j, bool in, bool rc, int q, int e,
+                                            int mode, int N, int E, int k, int nb,
+                                            uint8_t* __restrict__ mask,
+                                            int32_t* __restrict__ sigma,
+                                            uint8_t* __restrict__ sync,
+                                            int32_t* __restrict__ cnt_bs,
+                                            int32_t* __restrict__ cnt_ch,
+                                            int32_t* __restrict__ stats_bs) {
+  __shared__ int8_t s_q[kSelThreads];
+  __shared__ uint8_t s_m[kSelThreads];
+  __shared__ int s_cnt[64];
+  __shared__ int s_rs[2];
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int64_t base = int64_t(b) * nb;
+  if (tid < 64) s_cnt[tid] = 0;
+  if (tid < 2) s_rs[tid] = 0;
+  __syncthreads();
+  if (in) {
+    mask[base + j] = rc ? 1 : 0;
+    if (rc) atomicAdd(&s_cnt[e], 1);
+  }
+  s_m[tid] = in && rc ? 1 : 0;
+  s_q[tid] = static_cast<int8_t>(in ? q : -1);
+  __syncthreads();
+  // tokens of the block: t_local = tid < 1024 / k, token c (1024 / k) + t_local
+  const int tpb = kSelThreads / k;
+  const int i = c * tpb + tid;
+  int rec = 0, syn = 0;
+  if (tid < tpb && i < N) {
+    bool any = false;
+    uint32_t taken = 0;
+    if (mode != kSelFull) {
+      for (int p = 0; p < k; ++p) {
+        const int qp = s_q[tid * k + p];
+        if (qp >= 0) taken |= 1u << qp;
+      }
+    }
+    for (int p = 0; p < k; ++p) {
+      const bool r = s_m[tid * k + p] != 0;
+      any |= r;
+      rec += r ? 1 : 0;
+      int sg;
+      if (mode == kSelFull) {
+        sg = p;
+      } else {
+        const int qp = s_q[tid * k + p];
+        if (qp >= 0) {
+          sg = qp;
+        } else {
+          sg = 0;
+          while ((taken >> sg) & 1u) ++sg;
+          taken |= 1u << sg;
+        }
+      }
+      sigma[base + int64_t(tid) * k + int64_t(c) * kSelThreads + p] = sg;
+    }
+    sync[int64_t(b) * N + i] = any ? 1 : 0;
+    syn = any ? 1 : 0;
+  }
+  rec = wave_sum_i32(rec);
+  syn = wave_sum_i32(syn);
+  if (lane == 0 && (rec | syn) != 0) {
+    atomicAdd(&s_rs[0], rec);
+    atomicAdd(&s_rs[1], syn);
+  }
+  __syncthreads();
+  const int rc_n = (nb + kSelThreads - 1) / kSelThreads;
+  if (tid < E) {
+    cnt_ch[(int64_t(b) * rc_n + c) * E + tid] = s_cnt[tid];
+    if (s_cnt[tid] != 0) atomicAdd(&cnt_bs[b * E + tid], s_cnt[tid]);
+  }
+  if (tid == 0) {
+    atomicAdd(&stats_bs[b * 4 + 0], s_rs[0]);
+    atomicAdd(&stats_bs[b * 4 + 3], s_rs[1]);
+  }
+}
+
+__global__ __launch_bounds__(kSelThreads) void wide_score_kernel(
+    const int32_t* __restrict__ e_t, const float* __restrict__ w_t,
+    const int32_t* __restrict__ e_c, const float* __restrict__ w_c,
+    const float* __restrict__ n_c, const float* __restrict__ tau, int N, int E, int k,
+    int mode, float lambda0, float lambda1, float lambda2, int32_t* __restrict__ q_out,
+    float* __restrict__ margin, int32_t* __restrict__ ws, uint8_t* __restrict__ mask,
+    int32_t* __restrict__ sigma, uint8_t* __restrict__ sync, int32_t* __restrict__ cnt_bs,
+    int32_t* __restrict__ cnt_ch, int32_t* __restrict__ stats_bs) {
+  __shared__ float s_tau[64];
+  __shared__ int s_h[256];
+  __shared__ int s_un;
+  const int nb = N * k;
+  const int rc_n = (nb + kSelThreads - 1) / kSelThreads;
+  const int b = blockIdx.x / rc_n, c = blockIdx.x % rc_n;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int j = c * kSelThreads + tid;
+  const bool in = j < nb;
+  const int64_t f = int64_t(b) * nb + j;
+  if (tid < 256) s_h[tid] = 0;
+  if (tid < E) s_tau[tid] = tau[b * E + tid];
+  if (tid == 0) s_un = 0;
+  __syncthreads();
+  int e = 0, q = -1;
+  float m = __int_as_float(0x7f800000);  // +inf: unmatched
+  if (in) {
+    e = e_t[f];
+    if (mode != kSelFull) {
+      const float w = w_t[f];
+      const int64_t c0 = int64_t(b) * nb + (j / k) * k;
+      int ejs[8];
+      float ncs[8], wcs[8];
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        if (jj < k) {
+          ejs[jj] = e_c[c0 + jj];
+          ncs[jj] = n_c[c0 + jj];
+          wcs[jj] = w_c[c0 + jj];
+        }
+      }
+      double den = 0.0;
+      float ncq = 0.0f, wcq = 0.0f;
+#pragma unroll
+      for (int jj = 0; jj < 8; ++jj) {
+        if (jj < k) {
+          if (ejs[jj] >= 0) den += static_cast<double>(ncs[jj]);
+          if (q < 0 && ejs[jj] >= 0 && ejs[jj] == e) {
+            q = jj;
+            ncq = ncs[jj];
+            wcq = wcs[jj];
+          }
+        }
+      }
+      if (q >= 0) {
+        const float denf = static_cast<float>(den);
+        const float delta = fabsf(__fsub_rn(w, wcq));
+        const float o = denf > 0.0f ? __fdiv_rn(ncq, denf) : 0.0f;
+        float sc = __fadd_rn(__fmul_rn(lambda0, w), __fmul_rn(lambda1, delta));
+        sc = __fadd_rn(sc, __fmul_rn(lambda2, o));
+        m = __fsub_rn(sc, s_tau[e]);
+      }
+      q_out[f] = q;
+      margin[f] = m;
+    }
+  }
+  if (mode != kSelFull) {
+    const int un = wave_sum_i32(in && q < 0 ? 1 : 0);
+    const int nin = wave_sum_i32(in ? 1 : 0);
+    if (lane == 0 && un != 0) atomicAdd(&s_un, un);
+    if (lane == 0 && nin != 0) {
+      // matched count: nin - un of this wave
+      atomicAdd(&stats_bs[b * 4 + 2], nin - un);
+    }
+  }
+  __syncthreads();
+  if (mode != kSelFull && tid == 0 && s_un != 0) {
+    atomicAdd(&ws[int64_t(b) * kWideWords + kWsCtr + 0], s_un);
+    atomicAdd(&stats_bs[b * 4 + 1], s_un);
+  }
+  if (mode == kSelRatio) {
+    const uint32_t mk = f32_order_key(m);
+    wide_hist(s_h, in && q >= 0, static_cast<int>(mk >> 24), ws + int64_t(b) * kWideWords);
+    return;
+  }
+  const bool rc = mode == kSelFull || q < 0 || m > 0.0f;
+  wide_finish(b, c, j, in, rc, q, e, mode, N, E, k, nb, mask, sigma, sync, cnt_bs, cnt_ch,
+              stats_bs);
+}
+
+__global__ __launch_bounds__(kSelThreads) void wide_pass_kernel(
+    int pass, const int32_t* __restrict__ q_out, const float* __restrict__ margin, int N,
+    int k, int budget, int32_t* __restrict__ ws) {
+  __shared__ int s_h[256];
+  const int nb = N * k;
+  const int rc_n = (nb + kSelThreads - 1) / kSelThreads;
+  const int b = blockIdx.x / rc_n, c = blockIdx.x % rc_n;
+  const int tid = threadIdx.x;
+  int32_t* w = ws + int64_t(b) * kWideWords;
+  const WideChain ch = wide_chain(w, budget, nb, pass);
+  if (!ch.active || (ch.direct_at >= 0 && ch.direct_at < pass - 1)) return;  // block-uniform
+  const int j = c * kSelThreads + tid;
+  const int64_t f = int64_t(b) * nb + j;
+  const bool matched = j < nb && q_out[f] >= 0;
+  const uint32_t mk = matched ? f32_order_key(margin[f]) : 0u;
+  const bool share = matched && (mk & ch.dmask) == ch.prefix;
+  if (ch.direct_at == pass - 1) {
+    // at most kDirect keys share the prefix: append them
+    if (share) {
+      const int ci = atomicAdd(&w[kWsCtr + 3], 1);  // below kDirect by the count above
+      if (ci < kDirect) {
+        w[kWsCKey + ci] = static_cast<int32_t>(mk);
+        w[kWsCJ + ci] = j;
+      }
+    }
+    return;
+  }
+  if (tid < 256) s_h[tid] = 0;
+  __syncthreads();
+  const int shift = 24 - 8 * pass;
+  wide_hist(s_h, share, static_cast<int>((mk >> shift) & 255u), w + 256 * pass);
+}
+
+__global__ __launch_bounds__(kSelThreads) void wide_final_kernel(
+    const int32_t* __restrict__ e_t, const int32_t* __restrict__ q_out,
+    const float* __restrict__ margin, int N, int E, int k, int budget,
+    int32_t* __restrict__ ws, uint8_t* __restrict__ mask, int32_t* __restrict__ sigma,
+    uint8_t* __restrict__ sync, int32_t* __restrict__ cnt_bs, int32_t* __restrict__ cnt_ch,
+    int32_t* __restrict__ stats_bs) {
+  __shared__ int s_csel[kDirect];
+  __shared__ int s_cjl[kDirect];
+  __shared__ int s_wt[kSelWaves];
+  __shared__ int s_before;
+  const int nb = N * k;
+  const int rc_n = (nb + kSelThreads - 1) / kSelThreads;
+  const int b = blockIdx.x / rc_n, c = blockIdx.x % rc_n;
+  const int tid = threadIdx.x;
+  const int lane = tid & (kWave - 1);
+  const int wv = tid / kWave;
+  const int32_t* w = ws + int64_t(b) * kWideWords;
+  const WideChain ch = wide_chain(w, budget, nb, 4);
+  const int j = c * kSelThreads + tid;
+  const bool in = j < nb;
+  const int64_t base = int64_t(b) * nb;
+  const int64_t f = base + j;
+  const int q = in ? q_out[f] : -1;
+  const int e = in ? e_t[f] : 0;
+  const uint32_t mk = in && q >= 0 ? f32_order_key(margin[f]) : 0u;
+  bool rc = in && (q < 0 || ch.take_all);
+  if (ch.active && ch.direct_at >= 0) {
+    if (wv == 0) {
+      // rank the candidates by (key desc, flat id asc)
+      const int nc = min(w[kWsCtr + 3], kDirect);
+      const uint32_t ki = lane < nc ? static_cast<uint32_t>(w[kWsCKey + lane]) : 0u;
+      const int ji = lane < nc ? w[kWsCJ + lane] : -1;
+      int rank = 0;
+      for (int t = 0; t < nc; ++t) {
+        const uint32_t kt = __builtin_amdgcn_readlane(ki, t);
+        const int jt = __builtin_amdgcn_readlane(ji, t);
+        rank += (kt > ki || (kt == ki && jt < ji)) ? 1 : 0;
+      }
+      if (lane < kDirect) {
+        s_csel[lane] = lane < nc && rank < ch.rem ? 1 : 0;
+        s_cjl[lane] = ji;
+      }
+    }
+    __syncthreads();
+    if (in && q >= 0) {
+      const uint32_t hm = mk & ch.dmask;
+      if (hm > ch.prefix) {
+        rc = true;
+      } else if (hm == ch.prefix) {
+        for (int t = 0; t < kDirect; ++t)
+          if (s_cjl[t] == j) rc = s_csel[t] != 0;
+      }
+    }
+  } else if (ch.active) {
+    // threshold key T = prefix (all four digits); the keys equal to T rank by
+    // flat id: those in the sample's earlier blocks, then within the block
+    if (tid == 0) s_before = 0;
+    __syncthreads();
+    int cnt = 0;
+    for (int jj = tid; jj < c * kSelThreads; jj += kSelThreads) {
+      const int64_t ff = base + jj;
+      if (q_out[ff] >= 0 && f32_order_key(margin[ff]) == ch.prefix) ++cnt;
+    }
+    cnt = wave_sum_i32(cnt);
+    if (lane == 0 && cnt != 0) atomicAdd(&s_before, cnt);
+    const bool tie = in && q >= 0 && mk == ch.prefix;
+    const uint64_t tb = __ballot(tie);
+    if (lane == 0) s_wt[wv] = __popcll(tb);
+    __syncthreads();
+    int below = s_before;
+    for (int w2 = 0; w2 < wv; ++w2) below += s_wt[w2];
+    if (in && q >= 0) rc = mk > ch.prefix || (tie && below + lane_rank(tb) < ch.rem);
+  }
+  wide_finish(b, c, j, in, rc, q, e, kSelRatio, N, E, k, nb, mask, sigma, sync, cnt_bs, cnt_ch,
+              stats_bs);
+}
+
+// ---------------------------------------------------------------------------
 // Cache reset: empty slots, zero statistic.
 // ---------------------------------------------------------------------------
 __global__ void reset_kernel(int32_t* __restrict__ e_c, float* __restrict__ w_c,
@@ -628,9 +1105,36 @@ hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda0
                          float lambda2, bool with_stat, float tau0, float alpha,
                          const Buffers& b, hipStream_t st) {
   const int nb = s.N * s.k;
+  const double log_n = std::log(static_cast<double>(s.N));  // the entropy's normaliser
+  if (nb > 8 * kSelThreads && kSelThreads % s.k == 0 && s.E <= 64) {
+    // multi-block path: the stage's start event goes with the first launch,
+    // its stop event with the last
+    const LaunchEvents ev = launch_events();
+    launch_events() = LaunchEvents{};
+    const int rc_n = (nb + kSelThreads - 1) / kSelThreads;
+    const int grid = s.B * rc_n;
+    const int prep = std::max((s.B * s.E + kSelWaves - 1) / kSelWaves,
+                              (s.B * kWideWords + kSelThreads - 1) / kSelThreads);
+    const bool ratio = sel_mode == kSelRatio;
+    launch_kernel_ev(&wide_prep_kernel, dim3(prep), dim3(kSelThreads), 0, st, ev.start, nullptr,
+                     b.ent, with_stat ? 1 : 0, log_n, tau0, alpha, b.hbar, b.tau, s.B, s.N, s.E,
+                     b.wide, b.cnt_bs, b.stats_bs);
+    launch_kernel_ev(&wide_score_kernel, dim3(grid), dim3(kSelThreads), 0, st, nullptr,
+                     ratio ? nullptr : ev.stop, b.e_t, b.w_t, b.e_c, b.w_c, b.n_c, b.tau, s.N,
+                     s.E, s.k, sel_mode, lambda0, lambda1, lambda2, b.q, b.margin, b.wide,
+                     b.mask, b.sigma, b.sync, b.cnt_bs, b.cnt_ch, b.stats_bs);
+    if (ratio) {
+      for (int pass = 1; pass < 4; ++pass)
+        launch_kernel_ev(&wide_pass_kernel, dim3(grid), dim3(kSelThreads), 0, st, nullptr,
+                         nullptr, pass, b.q, b.margin, s.N, s.k, budget, b.wide);
+      launch_kernel_ev(&wide_final_kernel, dim3(grid), dim3(kSelThreads), 0, st, nullptr,
+                       ev.stop, b.e_t, b.q, b.margin, s.N, s.E, s.k, budget, b.wide, b.mask,
+                       b.sigma, b.sync, b.cnt_bs, b.cnt_ch, b.stats_bs);
+    }
+    return hipGetLastError();
+  }
   const size_t lds = size_t(2) * nb;
   if (lds > 64 * 1024) return hipErrorInvalidValue;
-  const double log_n = std::log(static_cast<double>(s.N));  // the entropy's normaliser
 #define MOECA_DECIDE(RR)                                                                      \
   launch_kernel(&decide_kernel<RR>, dim3(s.B), dim3(kSelThreads), uint32_t(lds), st, b.e_t,   \
                 b.w_t, b.e_c, b.w_c, b.n_c, b.ent, with_stat ? 1 : 0, log_n, tau0,            \

@@ -31,6 +31,23 @@ inline void launch_kernel(void (*kernel)(P...), dim3 grid, dim3 block, uint32_t 
   }
 }
 
+// A launch that records `start` before and/or `stop` after its dispatch
+// (either may be null): the first and last kernels of a stage that launches
+// several.
+template <typename... P, typename... A>
+inline void launch_kernel_ev(void (*kernel)(P...), dim3 grid, dim3 block, uint32_t shmem,
+                             hipStream_t st, hipEvent_t start, hipEvent_t stop, A... args) {
+  if (start != nullptr || stop != nullptr)
+    hipExtLaunchKernelGGL(kernel, grid, block, shmem, st, start, stop, 0u,
+                          static_cast<P>(args)...);
+  else
+    kernel<<<grid, block, shmem, st>>>(static_cast<P>(args)...);
+}
+
+// Per-sample scratch words of the multi-block decision path: four 256-bin
+// digit histograms, counters, and up to 64 ranked candidates.
+constexpr int kWideWords = 1280;
+
 struct Shape {
   int d, E, k, d_ff, B, N;
   bool bf16;
@@ -74,6 +91,7 @@ struct Buffers {
   int32_t* rflags;  // router: one non-finite flag per block
   int32_t* tiles;   // [2][E+S+1] grouped-GEMM tile prefix per group (up, down)
   int32_t* row_dst; // [B*N*k] cache row of each listed branch: (f/k)*k + sigma(f)
+  int32_t* wide;    // [B][kWideWords] per-sample scratch of the multi-block decision path
   void* mid;        // [B*N*k + S*T][d_ff] FFN activation of listed and shared rows
   void* h_sh;       // [S][T][d] shared experts' outputs
 };

@@ -47,7 +47,7 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 enum Region {
   R_E_C, R_W_C, R_N_C, R_H_C, R_STAT, R_LOGITS, R_E_T, R_W_T, R_HBAR, R_TAU, R_MARGIN, R_Q,
   R_MASK, R_SIGMA, R_SYNC, R_OFF, R_LIST, R_POS,
-  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_ENT, R_CNT_CH, R_MID, R_H_SH, R_COUNT
+  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_ENT, R_CNT_CH, R_WIDE, R_MID, R_H_SH, R_COUNT
 };
 
 struct Layout {
@@ -86,6 +86,7 @@ Layout make_layout(const Shape& s) {
   b[R_ROW_DST] = nbr * 4;
   b[R_ENT] = size_t(s.B) * s.E * ((size_t(s.N) + 15) / 16) * 2 * 8;
   b[R_CNT_CH] = size_t(s.B) * ((size_t(s.N) * s.k + 1023) / 1024) * s.E * 4;
+  b[R_WIDE] = size_t(s.B) * moeca::kWideWords * 4;
   b[R_MID] = size_t(s.mid_rows()) * s.d_ff * act;
   b[R_H_SH] = size_t(s.S) * ntok * s.d * act;
   Layout L;
@@ -179,6 +180,8 @@ moeca_layer* moeca_layer_create(int d, int E, int k, int d_ff, const moeca_polic
   if (p->batch < 1 || p->tokens < 1) return bad("batch and tokens must be >= 1");
   const int64_t nbr = int64_t(p->batch) * p->tokens * (k + p->n_shared);
   if (nbr >= (int64_t(1) << 31) - 1024) return bad("batch * tokens * (k + n_shared) too large");
+  if (int64_t(p->tokens) * k > 32768 && 1024 % k != 0)
+    return bad("tokens * k above 32768 needs k in {1, 2, 4, 8}");
   if (int64_t(p->batch) * p->tokens * d >= (int64_t(1) << 40)) return bad("batch too large");
 
   auto* L = new (std::nothrow) moeca_layer();
@@ -258,6 +261,7 @@ int moeca_bind_workspace(moeca_layer* L, void* dev, size_t bytes) {
   b.pos = reinterpret_cast<int32_t*>(w + o[R_POS]);
   b.cnt_bs = reinterpret_cast<int32_t*>(w + o[R_CNT_BS]);
   b.cnt_ch = reinterpret_cast<int32_t*>(w + o[R_CNT_CH]);
+  b.wide = reinterpret_cast<int32_t*>(w + o[R_WIDE]);
   b.stats_bs = reinterpret_cast<int32_t*>(w + o[R_STATS_BS]);
   b.rflags = reinterpret_cast<int32_t*>(w + o[R_RFLAGS]);
   b.tiles = reinterpret_cast<int32_t*>(w + o[R_TILES]);

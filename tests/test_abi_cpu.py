@@ -83,6 +83,16 @@ BAD_POLICY = [
 ]
 
 
+def test_create_limits_tokens_times_k(L):
+    """Above 32768 branches per sample the decision path needs k | 1024."""
+    lib = L.load()
+    assert not lib.moeca_layer_create(64, 8, 3, 128, ctypes.byref(_pol(L, tokens=11000)))
+    assert "k in" in lib.moeca_last_error().decode()
+    h = lib.moeca_layer_create(64, 8, 4, 128, ctypes.byref(_pol(L, tokens=11000)))
+    assert h
+    lib.moeca_layer_destroy(h)
+
+
 @pytest.mark.parametrize("kw", BAD_POLICY)
 def test_create_rejects_bad_policy(L, kw):
     lib = L.load()

@@ -68,6 +68,19 @@ def test_unnormalised_gate_erf_gelu_and_bias():
     run_forced(S, 4, label="variants")
 
 
+WIDE = LayerShape(d=128, E=16, k=8, d_ff=128, B=2, N=1100, dtype="bf16")
+
+
+@pytest.mark.parametrize("mode,ratio", [("ratio", 0.25), ("ratio", 0.02), ("threshold", 0.3),
+                                        ("full", 0.3)])
+def test_wide_decision_path(mode, ratio):
+    """Samples of more than 8192 branches take the multi-block decision path
+    (8800 branches here: eight full blocks and a partial one, 128 tokens per
+    block): every decision bit for bit, refresh and cache steps."""
+    S = Setup(WIDE, mode=mode, seed=18, T=4, ratio=ratio, refresh_cycle=3)
+    run_forced(S, 4, label=f"wide {mode} {ratio}")
+
+
 @pytest.mark.parametrize("lams", [(1.0, 0.0, 0.0), (0.0, 1.0, 0.0), (0.0, 0.0, 1.0),
                                   (0.0, 1.0, 1.0), (0.5, 2.0, 0.25)])
 def test_score_signal_ablations(lams):
