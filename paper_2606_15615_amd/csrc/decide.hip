@@ -894,7 +894,7 @@ __global__ __launch_bounds__(kSelThreads) void wide_score_kernel(
     int32_t* __restrict__ cnt_ch, int32_t* __restrict__ stats_bs) {
   __shared__ float s_tau[64];
   __shared__ int s_h[256];
-  __shared__ int s_un;
+  __shared__ int s_un, s_mt;
   const int nb = N * k;
   const int rc_n = (nb + kSelThreads - 1) / kSelThreads;
   const int b = blockIdx.x / rc_n, c = blockIdx.x % rc_n;
@@ -905,7 +905,10 @@ __global__ __launch_bounds__(kSelThreads) void wide_score_kernel(
   const int64_t f = int64_t(b) * nb + j;
   if (tid < 256) s_h[tid] = 0;
   if (tid < E) s_tau[tid] = tau[b * E + tid];
-  if (tid == 0) s_un = 0;
+  if (tid == 0) {
+    s_un = 0;
+    s_mt = 0;
+  }
   __syncthreads();
   int e = 0, q = -1;
   float m = __int_as_float(0x7f800000);  // +inf: unmatched
@@ -951,17 +954,19 @@ __global__ __launch_bounds__(kSelThreads) void wide_score_kernel(
   }
   if (mode != kSelFull) {
     const int un = wave_sum_i32(in && q < 0 ? 1 : 0);
-    const int nin = wave_sum_i32(in ? 1 : 0);
+    const int mt = wave_sum_i32(in && q >= 0 ? 1 : 0);
     if (lane == 0 && un != 0) atomicAdd(&s_un, un);
-    if (lane == 0 && nin != 0) {
-      // matched count: nin - un of this wave
-      atomicAdd(&stats_bs[b * 4 + 2], nin - un);
-    }
+    if (lane == 0 && mt != 0) atomicAdd(&s_mt, mt);
   }
   __syncthreads();
-  if (mode != kSelFull && tid == 0 && s_un != 0) {
-    atomicAdd(&ws[int64_t(b) * kWideWords + kWsCtr + 0], s_un);
-    atomicAdd(&stats_bs[b * 4 + 1], s_un);
+  // one device atomic per block and counter (the blocks of a sample share
+  // its counters)
+  if (mode != kSelFull && tid == 0) {
+    if (s_un != 0) {
+      atomicAdd(&ws[int64_t(b) * kWideWords + kWsCtr + 0], s_un);
+      atomicAdd(&stats_bs[b * 4 + 1], s_un);
+    }
+    if (s_mt != 0) atomicAdd(&stats_bs[b * 4 + 2], s_mt);
   }
   if (mode == kSelRatio) {
     const uint32_t mk = f32_order_key(m);
