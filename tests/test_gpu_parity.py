@@ -81,6 +81,16 @@ def test_wide_decision_path(mode, ratio):
     run_forced(S, 4, label=f"wide {mode} {ratio}")
 
 
+@pytest.mark.parametrize("mode,ratio", [("ratio", 0.3), ("threshold", 0.3)])
+def test_one_block_many_branches_per_thread(mode, ratio):
+    """k = 3 does not divide 1024, so 9000 branches per sample stay in one
+    block per sample: nine branches per thread, the runtime-loop variant
+    with the key halves in LDS."""
+    shape = LayerShape(d=128, E=16, k=3, d_ff=128, B=1, N=3000, dtype="bf16")
+    S = Setup(shape, mode=mode, seed=19, T=3, ratio=ratio, refresh_cycle=0)
+    run_forced(S, 3, label=f"one-block {mode}")
+
+
 @pytest.mark.parametrize("lams", [(1.0, 0.0, 0.0), (0.0, 1.0, 0.0), (0.0, 0.0, 1.0),
                                   (0.0, 1.0, 1.0), (0.5, 2.0, 0.25)])
 def test_score_signal_ablations(lams):
