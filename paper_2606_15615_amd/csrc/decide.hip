@@ -47,6 +47,77 @@ namespace {
 // ---------------------------------------------------------------------------
 constexpr int kSelThreads = 1024;
 constexpr int kSelWaves = kSelThreads / kWave;
+
+// Matching and score of one branch (Sec. 4.2): q(p) = the first of the
+// token's k cached slots (expert ej, norm nc, gate weight wc) that holds the
+// branch's expert e, or -1; for a matched branch the margin
+// m = ((lambda0 w + lambda1 Delta) + lambda2 o) - tau_e, with the norm sum of
+// o accumulated in fp64 and rounded once.  m is left alone when unmatched.
+__device__ __forceinline__ int match_score(int e, float w, const int* ej, const float* nc,
+                                           const float* wc, int k, float tau_e, float lambda0,
+                                           float lambda1, float lambda2, float& m) {
+  int q = -1;
+  double den = 0.0;
+  float ncq = 0.0f, wcq = 0.0f;
+#pragma unroll
+  for (int jj = 0; jj < 8; ++jj) {
+    if (jj < k) {
+      if (ej[jj] >= 0) den += static_cast<double>(nc[jj]);
+      if (q < 0 && ej[jj] >= 0 && ej[jj] == e) {
+        q = jj;
+        ncq = nc[jj];
+        wcq = wc[jj];
+      }
+    }
+  }
+  if (q >= 0) {
+    const float denf = static_cast<float>(den);
+    const float delta = fabsf(__fsub_rn(w, wcq));
+    const float o = denf > 0.0f ? __fdiv_rn(ncq, denf) : 0.0f;
+    float sc = __fadd_rn(__fmul_rn(lambda0, w), __fmul_rn(lambda1, delta));
+    sc = __fadd_rn(sc, __fmul_rn(lambda2, o));
+    m = __fsub_rn(sc, tau_e);
+  }
+  return q;
+}
+
+// Slots of one token's k branches (Sec. 4.1): a matched branch keeps its
+// slot q(p), unmatched ones (ascending p) take the free slots in ascending
+// order; on full steps branch p takes slot p.  sq / sm: the token's matched
+// slots and recompute flags; writes the k slots to sg and returns whether
+// any branch of the token is recomputed (its sync flag), adding the
+// recomputed count to rec.
+__device__ __forceinline__ bool token_slots(const int8_t* sq, const uint8_t* sm, int k, bool full,
+                                            int32_t* __restrict__ sg, int& rec) {
+  bool any = false;
+  uint32_t taken = 0;
+  if (!full) {
+    for (int p = 0; p < k; ++p) {
+      const int qp = sq[p];
+      if (qp >= 0) taken |= 1u << qp;
+    }
+  }
+  for (int p = 0; p < k; ++p) {
+    const bool rc = sm[p] != 0;
+    any |= rc;
+    rec += rc ? 1 : 0;
+    int slot;
+    if (full) {
+      slot = p;
+    } else {
+      const int qp = sq[p];
+      if (qp >= 0) {
+        slot = qp;
+      } else {
+        slot = 0;
+        while ((taken >> slot) & 1u) ++slot;
+        taken |= 1u << slot;
+      }
+    }
+    sg[p] = slot;
+  }
+  return any;
+}
 // Ratio mode: once a digit leaves at most this many keys sharing the
 // threshold's prefix, one wave ranks them directly.
 constexpr int kDirect = 64;
@@ -250,34 +321,9 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
       const int e = in.e;
       qv = e << 4;
       if (mode != kSelFull) {
-        const float w = in.w;
-        const int* ejs = in.ej;
-        const float* ncs = in.nc;
-        const float* wcs = in.wc;
-        int q = -1;
-        double den = 0.0;
-        float ncq = 0.0f, wcq = 0.0f;
-#pragma unroll
-        for (int jj = 0; jj < 8; ++jj) {
-          if (jj < k) {
-            if (ejs[jj] >= 0) den += static_cast<double>(ncs[jj]);
-            if (q < 0 && ejs[jj] >= 0 && ejs[jj] == e) {
-              q = jj;
-              ncq = ncs[jj];
-              wcq = wcs[jj];
-            }
-          }
-        }
-        if (q >= 0) {
-          const float denf = static_cast<float>(den);
-          const float delta = fabsf(__fsub_rn(w, wcq));
-          const float o = denf > 0.0f ? __fdiv_rn(ncq, denf) : 0.0f;
-          float sc = __fadd_rn(__fmul_rn(lambda0, w), __fmul_rn(lambda1, delta));
-          sc = __fadd_rn(sc, __fmul_rn(lambda2, o));
-          m = __fsub_rn(sc, s_tau[e]);
-        } else {
-          ++unmatched;
-        }
+        const int q = match_score(e, in.w, in.ej, in.nc, in.wc, k, s_tau[e], lambda0, lambda1,
+                                  lambda2, m);
+        if (q < 0) ++unmatched;
         qv = (e << 4) | (q + 1);
         q_out[f] = q;
         margin[f] = m;
@@ -489,33 +535,8 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
   // 4. per token: sync flag and slots
   int rec = 0, syn = 0;
   for (int i = tid; i < N; i += kSelThreads) {
-    bool any = false;
-    uint32_t taken = 0;
-    if (mode != kSelFull) {
-      for (int p = 0; p < k; ++p) {
-        const int qp = s_q[i * k + p];
-        if (qp >= 0) taken |= 1u << qp;
-      }
-    }
-    for (int p = 0; p < k; ++p) {
-      const bool rc = s_mask[i * k + p] != 0;
-      any |= rc;
-      rec += rc ? 1 : 0;
-      int sg;
-      if (mode == kSelFull) {
-        sg = p;
-      } else {
-        const int qp = s_q[i * k + p];
-        if (qp >= 0) {
-          sg = qp;
-        } else {
-          sg = 0;
-          while ((taken >> sg) & 1u) ++sg;
-          taken |= 1u << sg;
-        }
-      }
-      sigma[base + int64_t(i) * k + p] = sg;
-    }
+    const bool any = token_slots(s_q + i * k, s_mask + i * k, k, mode == kSelFull,
+                                 sigma + base + int64_t(i) * k, rec);
     sync[int64_t(b) * N + i] = any ? 1 : 0;
     syn += any ? 1 : 0;
   }
@@ -836,33 +857,8 @@ __device__ __forceinline__ void wide_finish(int b, int c, int j, bool in, bool r
   const int i = c * tpb + tid;
   int rec = 0, syn = 0;
   if (tid < tpb && i < N) {
-    bool any = false;
-    uint32_t taken = 0;
-    if (mode != kSelFull) {
-      for (int p = 0; p < k; ++p) {
-        const int qp = s_q[tid * k + p];
-        if (qp >= 0) taken |= 1u << qp;
-      }
-    }
-    for (int p = 0; p < k; ++p) {
-      const bool r = s_m[tid * k + p] != 0;
-      any |= r;
-      rec += r ? 1 : 0;
-      int sg;
-      if (mode == kSelFull) {
-        sg = p;
-      } else {
-        const int qp = s_q[tid * k + p];
-        if (qp >= 0) {
-          sg = qp;
-        } else {
-          sg = 0;
-          while ((taken >> sg) & 1u) ++sg;
-          taken |= 1u << sg;
-        }
-      }
-      sigma[base + int64_t(tid) * k + int64_t(c) * kSelThreads + p] = sg;
-    }
+    const bool any = token_slots(s_q + tid * k, s_m + tid * k, k, mode == kSelFull,
+                                 sigma + base + int64_t(c) * kSelThreads + int64_t(tid) * k, rec);
     sync[int64_t(b) * N + i] = any ? 1 : 0;
     syn = any ? 1 : 0;
   }
@@ -927,27 +923,7 @@ __global__ __launch_bounds__(kSelThreads) void wide_score_kernel(
           wcs[jj] = w_c[c0 + jj];
         }
       }
-      double den = 0.0;
-      float ncq = 0.0f, wcq = 0.0f;
-#pragma unroll
-      for (int jj = 0; jj < 8; ++jj) {
-        if (jj < k) {
-          if (ejs[jj] >= 0) den += static_cast<double>(ncs[jj]);
-          if (q < 0 && ejs[jj] >= 0 && ejs[jj] == e) {
-            q = jj;
-            ncq = ncs[jj];
-            wcq = wcs[jj];
-          }
-        }
-      }
-      if (q >= 0) {
-        const float denf = static_cast<float>(den);
-        const float delta = fabsf(__fsub_rn(w, wcq));
-        const float o = denf > 0.0f ? __fdiv_rn(ncq, denf) : 0.0f;
-        float sc = __fadd_rn(__fmul_rn(lambda0, w), __fmul_rn(lambda1, delta));
-        sc = __fadd_rn(sc, __fmul_rn(lambda2, o));
-        m = __fsub_rn(sc, s_tau[e]);
-      }
+      q = match_score(e, w, ejs, ncs, wcs, k, s_tau[e], lambda0, lambda1, lambda2, m);
       q_out[f] = q;
       margin[f] = m;
     }
