@@ -508,8 +508,14 @@ def combine(w_t: np.ndarray, hhat: np.ndarray, dtype: str, shared=()) -> np.ndar
 # the whole step
 # ---------------------------------------------------------------------------
 def step(dims: Dims, policy: Policy, W: Weights, state: State, x_t: np.ndarray,
-         t: int, attn_in: np.ndarray | None = None, tokens=None):
+         t: int, attn_in: np.ndarray | None = None, tokens=None,
+         x_ffn: np.ndarray | None = None):
     """One layer step at sampling step ``t``.
+
+    ``x_ffn`` (same shape and dtype as ``x_t``), when given, is the input of
+    the expert FFNs while the router still reads ``x_t``: inside a block the
+    routing input of a cache step is built from the cached attention feature
+    and the recomputed branches read the refreshed one.
 
     ``state`` is not modified; the new state is returned.  ``tokens`` (flat
     token indices) limits the expert FFN, combine and row writes to those
@@ -573,6 +579,7 @@ def step(dims: Dims, policy: Policy, W: Weights, state: State, x_t: np.ndarray,
     rec["evaluated"] = evaluated.reshape(B, N)
 
     # 9. expert FFN on the recomputed branches of evaluated tokens
+    xf64 = x64 if x_ffn is None else to_f64(x_ffn, dt).reshape(T, d)
     act_t = np.uint16 if dt == BF16 else F32
     h_new = np.zeros((B * N * k, d), dtype=act_t)
     for e in range(E):
@@ -580,13 +587,13 @@ def step(dims: Dims, policy: Policy, W: Weights, state: State, x_t: np.ndarray,
         f = f[evaluated[f // k]]
         if f.size == 0:
             continue
-        h_new[f] = expert_ffn(x64[f // k], W.up64(e), W.down64(e), policy.act, dt)
+        h_new[f] = expert_ffn(xf64[f // k], W.up64(e), W.down64(e), policy.act, dt)
     h_new = h_new.reshape(B, N, k, d)
     rec["h_new"] = h_new
 
     # shared experts (Sec. 2.3 shared-expert eq.): every evaluated token
     ev = evaluated
-    shared = [expert_ffn(x64[ev], W.shared_up64(s_), W.shared_down64(s_), policy.act, dt)
+    shared = [expert_ffn(xf64[ev], W.shared_up64(s_), W.shared_down64(s_), policy.act, dt)
               for s_ in range(dims.n_shared)]
     rec["h_shared"] = shared
 

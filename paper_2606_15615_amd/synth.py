@@ -207,3 +207,115 @@ class Synth:
 
     def uniform(self, low, high, size) -> np.ndarray:
         return self._rng_misc.uniform(low, high, size=size)
+
+
+# ---------------------------------------------------------------------------
+# a stack of DiT-MoE blocks (attention + AdaLN + the MoE layer per block)
+# ---------------------------------------------------------------------------
+@dataclasses.dataclass(frozen=True)
+class StackShape:
+    """Shape of a stack of DiT-MoE blocks (bf16 weights and activations)."""
+    L: int          # blocks
+    d: int          # model width
+    heads: int      # attention heads (head width d / heads)
+    E: int
+    k: int
+    d_ff: int
+    B: int
+    N: int
+    n_classes: int = 1000
+    freq_dim: int = 256
+
+    def layer(self) -> LayerShape:
+        return LayerShape(d=self.d, E=self.E, k=self.k, d_ff=self.d_ff, B=self.B, N=self.N,
+                          dtype=BF16)
+
+
+# "dit28": 28 DiT-MoE-XL-like blocks at a 64x64 latent (1024 tokens, batch 8;
+# 16 heads of 72); "stack_tiny": the two-block parity stack (ragged 80 tokens).
+STACKS = {
+    "dit28": StackShape(L=28, d=1152, heads=16, E=16, k=2, d_ff=4608, B=8, N=1024),
+    "stack_tiny": StackShape(L=2, d=576, heads=8, E=4, k=2, d_ff=256, B=2, N=80),
+}
+
+
+class StackSynth:
+    """Seeded weights and inputs of a block stack.
+
+    Matrices ~N(0, 1/fan_in), biases ~N(0, 0.02^2) (fp32), the class table
+    ~N(0, 1); every block draws from its own stream, so a block's weights do
+    not depend on L.  Inputs: x_0 ~ N(0, 1) and the per-token drift model of
+    the layer workloads (``Synth``), the diffusion timestep value decreasing
+    over the steps, one class label per sample.
+    """
+
+    def __init__(self, shape: StackShape, seed: int = 0):
+        self.shape = shape
+        self.seed = seed
+        self._layer = Synth(shape.layer(), seed)
+
+    def _rng(self, *key) -> np.random.Generator:
+        return np.random.Generator(np.random.PCG64(np.random.SeedSequence([self.seed, *key])))
+
+    @staticmethod
+    def _mat(g, rows, cols) -> np.ndarray:
+        return fp32_to_bf16_bits(g.standard_normal((rows, cols), dtype=np.float32)
+                                 * np.float32(1.0 / math.sqrt(cols)))
+
+    @staticmethod
+    def _bias(g, n) -> np.ndarray:
+        return (g.standard_normal(n, dtype=np.float32) * np.float32(0.02)).astype(np.float32)
+
+    def block(self, l: int) -> dict:
+        """Weights of block l: W_ada (6d, d), b_ada, W_qkv (3d, d), b_qkv,
+        W_o (d, d), b_o, W_r (E, d), W_up (E, d_ff, d), W_down (E, d, d_ff)."""
+        s = self.shape
+        g = self._rng(1000 + l)
+        d = s.d
+        out = {
+            "W_ada": self._mat(g, 6 * d, d), "b_ada": self._bias(g, 6 * d),
+            "W_qkv": self._mat(g, 3 * d, d), "b_qkv": self._bias(g, 3 * d),
+            "W_o": self._mat(g, d, d), "b_o": self._bias(g, d),
+            "W_r": self._mat(g, s.E, d),
+        }
+        up = g.standard_normal((s.E, s.d_ff, d), dtype=np.float32) * np.float32(1 / math.sqrt(d))
+        out["W_up"] = fp32_to_bf16_bits(up)
+        del up
+        down = (g.standard_normal((s.E, d, s.d_ff), dtype=np.float32)
+                * np.float32(1 / math.sqrt(s.d_ff)))
+        out["W_down"] = fp32_to_bf16_bits(down)
+        return out
+
+    def embedder(self) -> dict:
+        """Timestep/class embedder: W1 (d, freq_dim), b1, W2 (d, d), b2 and
+        the class table (n_classes, d), bf16 matrices and fp32 biases."""
+        s = self.shape
+        g = self._rng(7)
+        return {
+            "W1": self._mat(g, s.d, s.freq_dim), "b1": self._bias(g, s.d),
+            "W2": self._mat(g, s.d, s.d), "b2": self._bias(g, s.d),
+            "table": fp32_to_bf16_bits(g.standard_normal((s.n_classes, s.d), dtype=np.float32)),
+        }
+
+    def labels(self) -> np.ndarray:
+        return self._rng(8).integers(0, self.shape.n_classes, size=self.shape.B)
+
+    @staticmethod
+    def timestep_values(T: int, t_max: float = 999.0) -> np.ndarray:
+        """Diffusion timestep value of sampling step 0..T-1 (evenly spaced,
+        decreasing from t_max), float32."""
+        return (t_max * (1.0 - np.arange(T, dtype=np.float64) / T)).astype(np.float32)
+
+    def trajectory(self, T: int, drift: str = "loguniform"):
+        """Yield ``T`` stack inputs x_t, shape (B, N, d), fp32."""
+        s = self.shape
+        lay = self._layer
+        a = lay.drift_rates(drift)[..., None].astype(np.float32)
+        keep = np.sqrt(1.0 - a).astype(np.float32)
+        mix = np.sqrt(a).astype(np.float32)
+        g = self._rng(9)
+        x = g.standard_normal((s.B, s.N, s.d), dtype=np.float32)
+        for t in range(T):
+            if t > 0:
+                x = keep * x + mix * g.standard_normal((s.B, s.N, s.d), dtype=np.float32)
+            yield x.copy()
