@@ -253,6 +253,138 @@ int moeca_set_timing(moeca_layer* layer, int enable);
  * steps.  Synchronises the recorded events and clears the record. */
 int moeca_get_timing(moeca_layer* layer, double* ms, int n, int* steps);
 
+/* ---- DiT-MoE block stack ----------------------------------------------
+ * L DiT-MoE blocks (Sec. 2.1, composition eq. and residual form; the MoE FFN
+ * of Sec. 2.3) under MoECa (Sec. 4.1).  Block l computes, per token,
+ *   x1 = x  + g_a * a,  a = W_o Attn(h) + b_o,  h = LN(x)  * (1 + sc_a) + sh_a
+ *   x' = x1 + g_m * y,  y = MoE(u),             u = LN(x1) * (1 + sc_m) + sh_m
+ * where (sh_a, sc_a, g_a, sh_m, sc_m, g_m) are the six d-vectors of
+ * W_ada SiLU(c) + b_ada (AdaLN conditioned on c, one c per sample), LN has
+ * no affine parameters (eps 1e-6), and Attn is multi-head self-attention
+ * over the tokens of a sample: [q k v] = W_qkv h + b_qkv, head j on columns
+ * j d_h .. (j+1) d_h - 1, softmax(q k^T / sqrt(d_h)) v per head.
+ *
+ * Every block keeps the attention feature a_i of each token (Sec. 4.1) and
+ * a MoE layer with its branch cache.  A full step runs the block as written
+ * and refills both.  A cache step routes on u built from the cached a_i,
+ * decides R_i and S_i = [R_i non-empty] (Sec. 4.2-4.3), recomputes the
+ * attention feature of the tokens in S only (their queries against the keys
+ * and values of every token of the sample at this step), rebuilds their x1
+ * and u, and recomputes the branches in R_i on the rebuilt u (Sec. 4.1,
+ * synchronised update); other tokens reuse a_i and their branches.  Full vs
+ * cache step follows the policy as for moeca_step.
+ *
+ * Precision: x, x1, x' and the AdaLN vectors fp32; h, q, k, v, the
+ * attention output, a, u and y bf16, rounded where produced; fp32
+ * accumulation.  Limits: bf16 policy, n_shared = 0, d a multiple of 64 and
+ * at most 2048, d_h = d / heads a multiple of 8 and at most 96, and the MoE
+ * layer's limits. */
+typedef struct moeca_stack moeca_stack;
+
+/* Weights of one block: device, bf16 matrices (row-major, out x in) and
+ * fp32 biases, not copied; matrices 16-byte aligned, biases 4-byte. */
+typedef struct moeca_block_weights {
+  const void* W_ada;  /* [6d][d] AdaLN rows: sh_a, sc_a, g_a, sh_m, sc_m, g_m */
+  const float* b_ada; /* [6d]                                                  */
+  const void* W_qkv;  /* [3d][d] rows q, then k, then v                         */
+  const float* b_qkv; /* [3d]                                                  */
+  const void* W_o;    /* [d][d] output projection                               */
+  const float* b_o;   /* [d]                                                   */
+  const void* W_r;    /* [E][d] router                                          */
+  const float* b_r;   /* [E] router bias, or NULL                               */
+  const void* W_up;   /* [E][U][d] as in moeca_layer_set_weights               */
+  const void* W_down; /* [E][d][d_ff]                                          */
+} moeca_block_weights;
+
+/* Create a stack of n_blocks (>= 1) blocks of width d with `heads`
+ * attention heads and the MoE layer (E, k, d_ff, policy) of
+ * moeca_layer_create in each.  Host only; NULL on a bad argument. */
+moeca_stack* moeca_stack_create(int n_blocks, int d, int heads, int E, int k, int d_ff,
+                                const moeca_policy* policy);
+
+/* Release the stack and its layers.  Never frees caller memory. */
+void moeca_stack_destroy(moeca_stack* stack);
+
+/* Bind block l's weights (0 <= l < n_blocks).  MOECA_E_INVAL on a NULL
+ * required pointer (all but b_r) or misalignment. */
+int moeca_stack_set_block(moeca_stack* stack, int l, const moeca_block_weights* w);
+
+/* Device workspace: per block the cached attention features [B*N][d] and
+ * the MoE layer's workspace; shared per-step activations (x1, h, u, the
+ * rebuilt u, q, k/v, attention output, y), the AdaLN vectors of every block
+ * and the token lists.  0 if stack is NULL. */
+size_t moeca_stack_workspace_bytes(const moeca_stack* stack);
+
+/* Bind caller-owned device memory (256-byte aligned, at least
+ * moeca_stack_workspace_bytes()).  Invalidates every cache; clear them with
+ * moeca_stack_cache_reset() before the first step. */
+int moeca_stack_bind_workspace(moeca_stack* stack, void* dev, size_t bytes);
+
+/* One step of blocks first .. first + count - 1 at sampling step t.
+ *   x [B][N][d] fp32, device, in/out: the input of block `first`; on return
+ *     the output of the last block run.  The stack also uses it for the
+ *     residual stream between blocks.
+ *   c [B][d] fp32, device: the conditioning vector of each sample.
+ * Running all blocks is one model evaluation; a range lets a caller run
+ * the stack in parts.  The step kind (full or cache) is decided per block
+ * as in moeca_step.  Asynchronous on the stream; no allocation.
+ * MOECA_E_INVAL on a bad range, NULL or misaligned pointers; MOECA_E_STATE
+ * if a block's weights or the workspace are unbound. */
+int moeca_stack_step_blocks(moeca_stack* stack, float* x, const float* c, int t, int first,
+                            int count, void* stream);
+
+/* moeca_stack_step_blocks over every block. */
+int moeca_stack_step(moeca_stack* stack, float* x, const float* c, int t, void* stream);
+
+/* Enqueue a reset of every block's caches; the next step is a full step. */
+int moeca_stack_cache_reset(moeca_stack* stack, void* stream);
+
+/* The MoE layer of block l (statistics, timing, inspection), owned by the
+ * stack; NULL on a bad index. */
+moeca_layer* moeca_stack_layer(moeca_stack* stack, int l);
+
+/* Timestep and class conditioning (the DiT embedder): per sample
+ *   c = W2 SiLU(W1 e(t) + b1) + b2 + table[label],
+ * e(t) = [cos(t f_j), sin(t f_j)], f_j = 10^(-4 j / 128), j = 0..127.
+ *   t_values [B] fp32 and labels [B] int32 (NULL: no class row) device;
+ *   W1 [d][256], W2 [d][d], table [n_classes][d] bf16; b1, b2 [d] fp32;
+ *   c [B][d] fp32 out.
+ * A label outside [0, n_classes) adds no class row.  Uses the stack's
+ * workspace for its intermediate; asynchronous. */
+int moeca_stack_embed(moeca_stack* stack, const float* t_values, const int32_t* labels,
+                      const void* W1, const float* b1, const void* W2, const float* b2,
+                      const void* table, int n_classes, float* c, void* stream);
+
+/* Shared activation buffers of the stack (values of the last block run). */
+enum {
+  MOECA_SBUF_MOD = 0,   /* fp32  [L][B][6][d] AdaLN vectors of every block     */
+  MOECA_SBUF_H = 1,     /* bf16  [B*N][d]  attention input h                   */
+  MOECA_SBUF_U = 2,     /* bf16  [B*N][d]  MoE routing input u                 */
+  MOECA_SBUF_U2 = 3,    /* bf16  [B*N][d]  rebuilt u of the synchronised tokens
+                           (the FFN input of a cache step; the same buffer as
+                           U on a full step)                                  */
+  MOECA_SBUF_Q = 4,     /* bf16  [B*N][d]  queries (rows of synchronised tokens) */
+  MOECA_SBUF_KV = 5,    /* bf16  [B*N][2d] keys, then values                   */
+  MOECA_SBUF_O = 6,     /* bf16  [B*N][d]  attention output before W_o (rows of
+                           synchronised tokens)                               */
+  MOECA_SBUF_X1 = 7,    /* fp32  [B*N][d]  x1                                  */
+  MOECA_SBUF_Y = 8,     /* bf16  [B*N][d]  MoE output y                        */
+  MOECA_SBUF_SLIST = 9, /* int32 [B*N]     synchronised tokens (flat ids
+                           b*N + i), by sample, ascending                     */
+  MOECA_SBUF_SOFF = 10, /* int32 [B+1]     start of each sample in SLIST       */
+  MOECA_SBUF_A = 11,    /* bf16  [B*N][d]  cached attention feature a of block l */
+  MOECA_SBUF_LAYER = 12,/* the MoE layer workspace of block l: the offsets of
+                           moeca_debug_buffer on moeca_stack_layer(l) are
+                           relative to its start                              */
+  MOECA_SBUF_COUNT = 13
+};
+
+/* Byte offset and size of a stack buffer inside the bound workspace (l is
+ * used by the per-block ids A and LAYER only).  MOECA_E_INVAL for an unknown
+ * id or block. */
+int moeca_stack_debug_buffer(const moeca_stack* stack, int which, int l, size_t* offset,
+                             size_t* bytes);
+
 #ifdef __cplusplus
 }
 #endif

@@ -25,6 +25,10 @@ BUF = {
     "off": 15, "list": 16, "pos": 17,
 }
 STAGES = ["router", "stat", "select", "lists", "ffn_up", "ffn_down", "combine"]
+SBUF = {
+    "mod": 0, "h": 1, "u": 2, "u2": 3, "q": 4, "kv": 5, "o": 6, "x1": 7, "y": 8, "slist": 9,
+    "soff": 10, "a": 11, "layer": 12,
+}
 
 
 class moeca_policy(ctypes.Structure):
@@ -48,6 +52,12 @@ class moeca_stats(ctypes.Structure):
     ]
 
 
+class moeca_block_weights(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_void_p) for n in (
+        "W_ada", "b_ada", "W_qkv", "b_qkv", "W_o", "b_o", "W_r", "b_r", "W_up", "W_down")]
+
+
+_vp = ctypes.c_void_p
 _SIGS = {
     "moeca_policy_default": (None, [ctypes.POINTER(moeca_policy)]),
     "moeca_layer_create": (ctypes.c_void_p, [ctypes.c_int, ctypes.c_int, ctypes.c_int,
@@ -73,6 +83,21 @@ _SIGS = {
     "moeca_set_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_int]),
     "moeca_get_timing": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(ctypes.c_double),
                                         ctypes.c_int, ctypes.POINTER(ctypes.c_int)]),
+    "moeca_stack_create": (_vp, [ctypes.c_int] * 6 + [ctypes.POINTER(moeca_policy)]),
+    "moeca_stack_destroy": (None, [_vp]),
+    "moeca_stack_set_block": (ctypes.c_int, [_vp, ctypes.c_int,
+                                             ctypes.POINTER(moeca_block_weights)]),
+    "moeca_stack_workspace_bytes": (ctypes.c_size_t, [_vp]),
+    "moeca_stack_bind_workspace": (ctypes.c_int, [_vp, _vp, ctypes.c_size_t]),
+    "moeca_stack_step_blocks": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_int, ctypes.c_int,
+                                               ctypes.c_int, _vp]),
+    "moeca_stack_step": (ctypes.c_int, [_vp, _vp, _vp, ctypes.c_int, _vp]),
+    "moeca_stack_cache_reset": (ctypes.c_int, [_vp, _vp]),
+    "moeca_stack_layer": (_vp, [_vp, ctypes.c_int]),
+    "moeca_stack_embed": (ctypes.c_int, [_vp] * 8 + [ctypes.c_int, _vp, _vp]),
+    "moeca_stack_debug_buffer": (ctypes.c_int, [_vp, ctypes.c_int, ctypes.c_int,
+                                                ctypes.POINTER(ctypes.c_size_t),
+                                                ctypes.POINTER(ctypes.c_size_t)]),
 }
 EXPORTED = tuple(_SIGS)
 
@@ -180,3 +205,58 @@ def moeca_get_timing(h, n: int = 7) -> tuple[list[float], int]:
     steps = ctypes.c_int()
     _check(load().moeca_get_timing(h, arr, n, ctypes.byref(steps)))
     return list(arr), steps.value
+
+
+# ---- block stack -----------------------------------------------------------
+def moeca_stack_create(n_blocks: int, d: int, heads: int, E: int, k: int, d_ff: int,
+                       policy: moeca_policy) -> int:
+    h = load().moeca_stack_create(n_blocks, d, heads, E, k, d_ff, ctypes.byref(policy))
+    if not h:
+        raise MoecaError(MOECA_E_INVAL, load().moeca_last_error().decode())
+    return h
+
+
+def moeca_stack_destroy(h) -> None:
+    load().moeca_stack_destroy(h)
+
+
+def moeca_stack_set_block(h, l: int, w: moeca_block_weights) -> int:
+    return _check(load().moeca_stack_set_block(h, l, ctypes.byref(w)))
+
+
+def moeca_stack_workspace_bytes(h) -> int:
+    return load().moeca_stack_workspace_bytes(h)
+
+
+def moeca_stack_bind_workspace(h, dev, nbytes) -> int:
+    return _check(load().moeca_stack_bind_workspace(h, dev, nbytes))
+
+
+def moeca_stack_step_blocks(h, x, c, t, first, count, stream) -> int:
+    return _check(load().moeca_stack_step_blocks(h, x, c, t, first, count, stream))
+
+
+def moeca_stack_step(h, x, c, t, stream) -> int:
+    return _check(load().moeca_stack_step(h, x, c, t, stream))
+
+
+def moeca_stack_cache_reset(h, stream) -> int:
+    return _check(load().moeca_stack_cache_reset(h, stream))
+
+
+def moeca_stack_layer(h, l: int) -> int:
+    p = load().moeca_stack_layer(h, l)
+    if not p:
+        raise MoecaError(MOECA_E_INVAL, load().moeca_last_error().decode())
+    return p
+
+
+def moeca_stack_embed(h, t_values, labels, W1, b1, W2, b2, table, n_classes, c, stream) -> int:
+    return _check(load().moeca_stack_embed(h, t_values, labels, W1, b1, W2, b2, table,
+                                           n_classes, c, stream))
+
+
+def moeca_stack_debug_buffer(h, which: int, l: int = 0) -> tuple[int, int]:
+    off, nb = ctypes.c_size_t(), ctypes.c_size_t()
+    _check(load().moeca_stack_debug_buffer(h, which, l, ctypes.byref(off), ctypes.byref(nb)))
+    return off.value, nb.value

@@ -33,7 +33,9 @@ SOURCES = {
     "decide.hip": ["-ffp-contract=off"],
     "combine.hip": ["-ffp-contract=off"],
     "ffn.hip": [],
+    "block.hip": ["-ffp-contract=off"],
     "moeca.cpp": ["-ffp-contract=off"],
+    "stack.cpp": [],
 }
 
 

@@ -1,0 +1,632 @@
+// Kernels of the DiT-MoE block around the MoE layer (Sec. 2.1 block form):
+// conditioning (timestep embedding, AdaLN vectors), LayerNorm with AdaLN
+// modulation and the gated residuals, the list of synchronised tokens
+// (Sec. 4.1, synchronised update) and multi-head self-attention of those
+// tokens' queries over every token of the sample.  The q/k/v and output
+// projections are the grouped GEMM's projection instantiation (ffn.hip).
+#include <cmath>
+
+#include "common.h"
+#include "internal.h"
+
+namespace moeca {
+namespace {
+
+typedef __attribute__((ext_vector_type(8))) __bf16 bf16x8_t;
+typedef __attribute__((ext_vector_type(16))) float f32x16_t;
+typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;
+typedef __attribute__((ext_vector_type(2))) unsigned int u32x2_t;
+typedef __attribute__((ext_vector_type(2))) float f32x2_t;
+typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+
+__device__ __forceinline__ uint32_t pack2(float a, float b) {
+  return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
+}
+
+__device__ __forceinline__ double silu64(double z) { return z / (1.0 + exp(-z)); }
+
+// One correct rounding of an fp64 value to bf16 (nearest, ties to even):
+// rounding to odd into fp32 first (truncate, then set the last bit if
+// anything was dropped) keeps the second rounding from landing on a false
+// tie.
+__device__ __forceinline__ uint32_t f64_to_bf16(double v) {
+  uint32_t u = __float_as_uint(__double2float_rz(v));
+  if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
+  if (static_cast<double>(__uint_as_float(u)) != v && (u & 0x7fffffffu) < 0x7f800000u) u |= 1u;
+  u += 0x7fffu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// fp32(x + g f), the product exact in fp64, one rounding of the fp64 sum
+__device__ __forceinline__ float gated_add(float x, float g, float f) {
+  return static_cast<float>(static_cast<double>(x) +
+                            static_cast<double>(g) * static_cast<double>(f));
+}
+
+// ---------------------------------------------------------------------------
+// conditioning
+// ---------------------------------------------------------------------------
+// e[b][j] = cos(t_b f_j) for j < 128, sin(t_b f_{j-128}) after, f_j =
+// 10^(-4 j / 128); fp64 throughout.
+__global__ void sinusoid_kernel(const float* __restrict__ t_values, int B,
+                                double* __restrict__ e) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= B * kFreqDim) return;
+  const int b = i / kFreqDim, j = i % kFreqDim, half = kFreqDim / 2;
+  const int jj = j < half ? j : j - half;
+  const double f = exp(-log(10000.0) * jj / half);
+  const double arg = static_cast<double>(t_values[b]) * f;
+  e[i] = j < half ? cos(arg) : sin(arg);
+}
+
+__global__ void silu_kernel(const float* __restrict__ in, int n, double* __restrict__ out) {
+  const int i = blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < n) out[i] = silu64(static_cast<double>(in[i]));
+}
+
+// v[b][r] = (sum_k W[r][k] in[b][k] + bias[r]) (+ table[labels[b]][r]) in
+// fp64 (products and sums), then out = fp32(v), or out64 = silu(v) when
+// out64 is set; one wave per weight row r, every sample.  W rows are bf16
+// [Nout][K] (K a multiple of 8), in fp64 [B][K].  The AdaLN vectors feed the
+// routing input, so they take the decision path's arithmetic: one rounding.
+constexpr int kGemvWaves = 4;
+
+__global__ __launch_bounds__(kGemvWaves * kWave) void gemv_kernel(
+    const double* __restrict__ in, int B, int K, const uint16_t* __restrict__ W,
+    const float* __restrict__ bias, int Nout, const uint16_t* __restrict__ table,
+    const int32_t* __restrict__ labels, int n_classes, float* __restrict__ out,
+    double* __restrict__ out64) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * kGemvWaves + (threadIdx.x >> 6);
+  if (r >= Nout) return;
+  const uint16_t* wr = W + int64_t(r) * K;
+  const int nc = K / 8;
+  for (int b0 = 0; b0 < B; b0 += 8) {
+    const int nb = min(8, B - b0);
+    double acc[8];
+#pragma unroll
+    for (int u = 0; u < 8; ++u) acc[u] = 0.0;
+    for (int c = lane; c < nc; c += kWave) {
+      const u32x4_t wv = *reinterpret_cast<const u32x4_t*>(wr + 8 * c);
+      double w[8];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        w[2 * e] = __uint_as_float(wv[e] << 16);
+        w[2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
+      }
+#pragma unroll
+      for (int u = 0; u < 8; ++u) {
+        if (u < nb) {
+          const double* ip = in + int64_t(b0 + u) * K + 8 * c;
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc[u] += w[e] * ip[e];
+        }
+      }
+    }
+#pragma unroll
+    for (int u = 0; u < 8; ++u) {
+      if (u < nb) {
+        const double s = wave_sum_f64(acc[u]);
+        if (lane == 0) {
+          const int b = b0 + u;
+          double v = s + static_cast<double>(bias[r]);
+          if (table != nullptr) {
+            const int lab = labels[b];
+            if (lab >= 0 && lab < n_classes) v += bf16_to_f32(table[int64_t(lab) * Nout + r]);
+          }
+          if (out64 != nullptr) out64[int64_t(b) * Nout + r] = silu64(v);
+          else out[int64_t(b) * Nout + r] = static_cast<float>(v);
+        }
+      }
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// LayerNorm + AdaLN modulation and the gated residuals, one wave per row
+// ---------------------------------------------------------------------------
+// d <= kMaxWidth: a lane holds float4 chunks lane + 64 j of the row.
+constexpr int kLnWaves = 4;
+constexpr int kLnChunks = kMaxWidth / 4 / kWave;  // 8
+
+enum { kLnAttn = 0, kLnMlp = 1, kLnFinal = 2 };
+
+struct LnArgs {
+  float* x;                 // [T][d] residual stream (block input)
+  float* x1;                // [T][d]
+  const uint16_t* y;        // [T][d] MoE output of the previous block
+  const uint16_t* a;        // [T][d] attention feature of this block
+  uint16_t* h;              // [T][d] attention input
+  uint16_t* u;              // [T][d] MoE input
+  const float* mod;         // [B][6][d] this block's AdaLN vectors
+  const float* mod_prev;    // [B][6][d] the previous block's (pending residual)
+  const int32_t* rows;      // kLnMlp: the rows to process
+  const int32_t* count;     // kLnMlp: device row count
+  int T, N, d;
+  int pending;              // x = x1 + g_m(prev) * y first (kLnAttn)
+  int cached;               // kLnAttn on a cache step: also x1 and u from a
+};
+
+__device__ __forceinline__ void ln_stats(const float (&v)[kLnChunks][4], int n4, int lane,
+                                         int d, double& mean, double& rstd) {
+  double s = 0.0;
+#pragma unroll
+  for (int j = 0; j < kLnChunks; ++j)
+    if (lane + kWave * j < n4)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) s += v[j][e];
+  const double mu = wave_sum_f64(s) / d;
+  double q = 0.0;
+#pragma unroll
+  for (int j = 0; j < kLnChunks; ++j)
+    if (lane + kWave * j < n4)
+#pragma unroll
+      for (int e = 0; e < 4; ++e) {
+        const double t = v[j][e] - mu;
+        q += t * t;
+      }
+  const double var = wave_sum_f64(q) / d;
+  mean = mu;
+  rstd = 1.0 / sqrt(var + 1e-6);
+}
+
+// bf16(LN(v) * (1 + scale) + shift) into row `dst`, in fp64 and rounded
+// once: this is the MoE routing input (decision-path arithmetic)
+__device__ __forceinline__ void ln_store(const float (&v)[kLnChunks][4], int n4, int lane,
+                                         double mean, double rstd, const float* shift,
+                                         const float* scale, uint16_t* dst) {
+#pragma unroll
+  for (int j = 0; j < kLnChunks; ++j) {
+    const int c = lane + kWave * j;
+    if (c < n4) {
+      const float4 sh = reinterpret_cast<const float4*>(shift)[c];
+      const float4 sc = reinterpret_cast<const float4*>(scale)[c];
+      const float s4[4] = {sc.x, sc.y, sc.z, sc.w};
+      const float h4[4] = {sh.x, sh.y, sh.z, sh.w};
+      uint32_t z[4];
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        z[e] = f64_to_bf16((static_cast<double>(v[j][e]) - mean) * rstd *
+                               (1.0 + static_cast<double>(s4[e])) +
+                           static_cast<double>(h4[e]));
+      reinterpret_cast<u32x2_t*>(dst)[c] = u32x2_t{z[0] | (z[1] << 16), z[2] | (z[3] << 16)};
+    }
+  }
+}
+
+template <int MODE>
+__global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
+  const int lane = threadIdx.x & 63;
+  const int r = blockIdx.x * kLnWaves + (threadIdx.x >> 6);
+  int row;
+  if constexpr (MODE == kLnMlp) {
+    if (r >= *p.count) return;
+    row = p.rows[r];
+  } else {
+    if (r >= p.T) return;
+    row = r;
+  }
+  const int d = p.d, n4 = d / 4;
+  const int b = row / p.N;
+  const int64_t o = int64_t(row) * d;
+  const float* m = p.mod + int64_t(b) * 6 * d;  // sh_a, sc_a, g_a, sh_m, sc_m, g_m
+  float v[kLnChunks][4];
+
+  if constexpr (MODE == kLnFinal) {
+    const float* g = m + 5 * d;
+#pragma unroll
+    for (int j = 0; j < kLnChunks; ++j) {
+      const int c = lane + kWave * j;
+      if (c < n4) {
+        const float4 x1 = reinterpret_cast<const float4*>(p.x1 + o)[c];
+        const u32x2_t yy = reinterpret_cast<const u32x2_t*>(p.y + o)[c];
+        const float4 gg = reinterpret_cast<const float4*>(g)[c];
+        float4 r4;
+        r4.x = gated_add(x1.x, gg.x, __uint_as_float(yy[0] << 16));
+        r4.y = gated_add(x1.y, gg.y, __uint_as_float(yy[0] & 0xffff0000u));
+        r4.z = gated_add(x1.z, gg.z, __uint_as_float(yy[1] << 16));
+        r4.w = gated_add(x1.w, gg.w, __uint_as_float(yy[1] & 0xffff0000u));
+        reinterpret_cast<float4*>(p.x + o)[c] = r4;
+      }
+    }
+    return;
+  }
+
+  // the row's x: the block input, or the previous block's x1 + g_m y
+  if (MODE == kLnAttn && p.pending) {
+    const float* gp = p.mod_prev + int64_t(b) * 6 * d + 5 * d;
+#pragma unroll
+    for (int j = 0; j < kLnChunks; ++j) {
+      const int c = lane + kWave * j;
+      if (c < n4) {
+        const float4 x1 = reinterpret_cast<const float4*>(p.x1 + o)[c];
+        const u32x2_t yy = reinterpret_cast<const u32x2_t*>(p.y + o)[c];
+        const float4 gg = reinterpret_cast<const float4*>(gp)[c];
+        v[j][0] = gated_add(x1.x, gg.x, __uint_as_float(yy[0] << 16));
+        v[j][1] = gated_add(x1.y, gg.y, __uint_as_float(yy[0] & 0xffff0000u));
+        v[j][2] = gated_add(x1.z, gg.z, __uint_as_float(yy[1] << 16));
+        v[j][3] = gated_add(x1.w, gg.w, __uint_as_float(yy[1] & 0xffff0000u));
+        reinterpret_cast<float4*>(p.x + o)[c] = float4{v[j][0], v[j][1], v[j][2], v[j][3]};
+      }
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < kLnChunks; ++j) {
+      const int c = lane + kWave * j;
+      if (c < n4) {
+        const float4 xx = reinterpret_cast<const float4*>(p.x + o)[c];
+        v[j][0] = xx.x;
+        v[j][1] = xx.y;
+        v[j][2] = xx.z;
+        v[j][3] = xx.w;
+      }
+    }
+  }
+  double mean, rstd;
+  if (MODE == kLnAttn) {
+    ln_stats(v, n4, lane, d, mean, rstd);
+    ln_store(v, n4, lane, mean, rstd, m, m + d, p.h + o);
+    if (!p.cached) return;
+  }
+  // x1 = x + g_a * a, then the MoE input from LN(x1)
+  const float* ga = m + 2 * d;
+#pragma unroll
+  for (int j = 0; j < kLnChunks; ++j) {
+    const int c = lane + kWave * j;
+    if (c < n4) {
+      const u32x2_t aa = reinterpret_cast<const u32x2_t*>(p.a + o)[c];
+      const float4 gg = reinterpret_cast<const float4*>(ga)[c];
+      v[j][0] = gated_add(v[j][0], gg.x, __uint_as_float(aa[0] << 16));
+      v[j][1] = gated_add(v[j][1], gg.y, __uint_as_float(aa[0] & 0xffff0000u));
+      v[j][2] = gated_add(v[j][2], gg.z, __uint_as_float(aa[1] << 16));
+      v[j][3] = gated_add(v[j][3], gg.w, __uint_as_float(aa[1] & 0xffff0000u));
+      reinterpret_cast<float4*>(p.x1 + o)[c] = float4{v[j][0], v[j][1], v[j][2], v[j][3]};
+    }
+  }
+  ln_stats(v, n4, lane, d, mean, rstd);
+  ln_store(v, n4, lane, mean, rstd, m + 3 * d, m + 4 * d, p.u + o);
+}
+
+// ---------------------------------------------------------------------------
+// synchronised tokens: per-sample ascending lists and the projection tables
+// ---------------------------------------------------------------------------
+// One 1024-thread block.  all: every token (full steps); else sync[t] != 0.
+// Writes slist (flat token ids, by sample), soff[B + 1], ident[t] = t and
+// tab = {0, nS, 0, tiles of nS rows x ntn_q, 0, T, 0, tiles of T rows x ntn_kv}
+// for the projections (128-row tiles).
+constexpr int kListThreads = 1024;
+
+__global__ __launch_bounds__(kListThreads) void slist_kernel(
+    const uint8_t* __restrict__ sync, int all, int B, int N, int ntn_q, int ntn_kv,
+    int32_t* __restrict__ slist, int32_t* __restrict__ soff, int32_t* __restrict__ ident,
+    int32_t* __restrict__ tab) {
+  __shared__ int s_wave[kListThreads / kWave];
+  __shared__ int s_base;
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int T = B * N;
+  for (int i = tid; i < T; i += kListThreads) ident[i] = i;
+  if (tid == 0) s_base = 0;
+  __syncthreads();
+  for (int b = 0; b < B; ++b) {
+    if (tid == 0) soff[b] = s_base;
+    for (int i0 = 0; i0 < N; i0 += kListThreads) {
+      const int i = i0 + tid;
+      const bool f = i < N && (all || sync[int64_t(b) * N + i] != 0);
+      const uint64_t bal = __ballot(f);
+      if (lane == 0) s_wave[wv] = __popcll(bal);
+      __syncthreads();
+      int before = s_base;
+      for (int w = 0; w < wv; ++w) before += s_wave[w];
+      if (f) slist[before + __popcll(bal & ((1ull << lane) - 1ull))] = b * N + i;
+      __syncthreads();
+      if (tid == 0) {
+        int tot = 0;
+        for (int w = 0; w < kListThreads / kWave; ++w) tot += s_wave[w];
+        s_base += tot;
+      }
+      __syncthreads();
+    }
+  }
+  if (tid == 0) {
+    const int ns = s_base;
+    soff[B] = ns;
+    tab[0] = 0;
+    tab[1] = ns;
+    tab[2] = 0;
+    tab[3] = (ns + kProjTM - 1) / kProjTM * ntn_q;
+    tab[4] = 0;
+    tab[5] = T;
+    tab[6] = 0;
+    tab[7] = (T + kProjTM - 1) / kProjTM * ntn_kv;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// multi-head attention of the listed queries (bf16 MFMA, fp32 softmax)
+// ---------------------------------------------------------------------------
+// Block: 4 waves, 128 listed queries of one (sample, head); wave w takes 32.
+// Per tile of 64 keys the wave forms S^T = K Q^T with
+// v_mfma_f32_32x32x16_bf16 (keys as rows, queries as columns), so a lane
+// owns one query (column lane & 31) and 16 of the 32 keys of each half
+// tile: the online softmax (running max and sum per query) needs one lane
+// exchange (l, l ^ 32) per tile.  The probabilities, rounded to bf16, are
+// the B operand of O^T += V^T P^T, whose k order (keys) follows the S^T
+// accumulator layout, so P never leaves registers; V^T sits in LDS.  K and
+// V tiles are double-buffered: the next tile's global loads are in flight
+// during the current tile's MFMAs.  KS = ceil(d_h / 16) k-steps for q.k,
+// OT = ceil(d_h / 32) output tiles of O^T; columns and rows past d_h are zero.
+constexpr int kAttnQ = 128;
+constexpr int kAttnKeys = 64;
+constexpr int kAttnThreads = 256;
+
+template <int KS, int OT>
+__global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kv,
+    const int32_t* __restrict__ slist, const int32_t* __restrict__ soff, int B, int N, int H,
+    int dh, float scale_log2, uint16_t* __restrict__ o) {
+  constexpr int KP = 16 * KS + 8;     // K row in LDS (bf16), padded
+  constexpr int VR = 32 * OT;         // V^T rows (head dims)
+  constexpr int VP = kAttnKeys + 8;   // V^T row (keys), padded
+  constexpr int KE = kAttnKeys * KP;  // elements of one K stage
+  constexpr int VE = VR * VP;
+  constexpr int kMaxLd = (2 * kAttnKeys * (VR / 8) + kAttnThreads - 1) / kAttnThreads;
+  __shared__ __attribute__((aligned(16))) uint16_t sk[2 * KE];
+  __shared__ __attribute__((aligned(16))) uint16_t sv[2 * VE];
+
+  // (sample, head, query tile); the query tiles of one (sample, head) are
+  // consecutive logical blocks on one XCD, so they share its L2 copy of K, V
+  const int QT = (N + kAttnQ - 1) / kAttnQ;
+  const int nblk = gridDim.x;
+  const int L = nblk % 8 == 0 ? (blockIdx.x % 8) * (nblk / 8) + blockIdx.x / 8 : blockIdx.x;
+  const int qt = L % QT;
+  const int hh = (L / QT) % H;
+  const int b = L / (QT * H);
+  const int q0 = soff[b];
+  const int nq = soff[b + 1] - q0;
+  if (qt * kAttnQ >= nq) return;
+
+  const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int n = lane & 31, hf = lane >> 5;
+  const int d = H * dh;
+  const int cpr = dh / 8;  // 16-byte chunks per head row
+
+  // zero both stages once: K columns and V^T rows past d_h stay zero
+  for (int i = tid; i < (2 * KE) / 8; i += kAttnThreads)
+    reinterpret_cast<u32x4_t*>(sk)[i] = u32x4_t{0, 0, 0, 0};
+  for (int i = tid; i < (2 * VE) / 8; i += kAttnThreads)
+    reinterpret_cast<u32x4_t*>(sv)[i] = u32x4_t{0, 0, 0, 0};
+
+  // this lane's query and its fragments (B operand of S^T)
+  const int qi = qt * kAttnQ + wv * 32 + n;
+  const int tok = slist[q0 + min(qi, nq - 1)];
+  const uint16_t* qrow = q + int64_t(tok) * d + hh * dh;
+  bf16x8_t qf[KS];
+#pragma unroll
+  for (int s = 0; s < KS; ++s) {
+    const int c = 16 * s + 8 * hf;
+    const u32x4_t w = c < dh ? *reinterpret_cast<const u32x4_t*>(qrow + c) : u32x4_t{0, 0, 0, 0};
+    qf[s] = __builtin_bit_cast(bf16x8_t, w);
+  }
+
+  const int64_t row0 = int64_t(b) * N;
+  const int nld = 2 * kAttnKeys * cpr;  // chunks of one K + V tile
+  u32x4_t ld[kMaxLd];
+  auto load_tile = [&](int kt) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < kMaxLd; ++u) {
+      const int c = tid + kAttnThreads * u;
+      if (c < nld) {
+        const int which = c / (kAttnKeys * cpr);
+        const int r = c % (kAttnKeys * cpr);
+        const int key = min(kt * kAttnKeys + r / cpr, N - 1);
+        const int ch = r % cpr;
+        ld[u] = *reinterpret_cast<const u32x4_t*>(kv + (row0 + key) * (2 * d) + which * d +
+                                                   hh * dh + ch * 8);
+      }
+    }
+  };
+  auto store_tile = [&](int st) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < kMaxLd; ++u) {
+      const int c = tid + kAttnThreads * u;
+      if (c < nld) {
+        const int which = c / (kAttnKeys * cpr);
+        const int r = c % (kAttnKeys * cpr);
+        const int key = r / cpr;
+        const int ch = r % cpr;
+        if (which == 0) {
+          *reinterpret_cast<u32x4_t*>(sk + st * KE + key * KP + ch * 8) = ld[u];
+        } else {
+          uint16_t* vt = sv + st * VE + (ch * 8) * VP + key;
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            vt[(2 * e) * VP] = static_cast<uint16_t>(ld[u][e] & 0xffffu);
+            vt[(2 * e + 1) * VP] = static_cast<uint16_t>(ld[u][e] >> 16);
+          }
+        }
+      }
+    }
+  };
+
+  const int nkt = (N + kAttnKeys - 1) / kAttnKeys;
+  load_tile(0);
+  __syncthreads();  // zeroing done before the first tile lands
+  store_tile(0);
+  __syncthreads();
+
+  float m_run = -INFINITY, l_run = 0.0f;
+  f32x16_t acc[OT];
+#pragma unroll
+  for (int t = 0; t < OT; ++t)
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[t][v] = 0.0f;
+
+  for (int kt = 0; kt < nkt; ++kt) {
+    const int st = kt & 1;
+    if (kt + 1 < nkt) load_tile(kt + 1);
+    const uint16_t* ks = sk + st * KE;
+    const uint16_t* vs = sv + st * VE;
+    // S^T for keys 32 t' + (0..31) of the tile
+    f32x16_t sacc[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+#pragma unroll
+      for (int v = 0; v < 16; ++v) sacc[t][v] = 0.0f;
+#pragma unroll
+      for (int s = 0; s < KS; ++s) {
+        const bf16x8_t kf =
+            *reinterpret_cast<const bf16x8_t*>(ks + (32 * t + n) * KP + 16 * s + 8 * hf);
+        sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[t], 0, 0, 0);
+      }
+    }
+    // online softmax in log2 units; lane keys: 32 t + 8 (v / 4) + 4 hf + v % 4
+    float mx = -INFINITY;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int key = kt * kAttnKeys + 32 * t + 8 * (v >> 2) + 4 * hf + (v & 3);
+        const float sv2 = key < N ? sacc[t][v] * scale_log2 : -INFINITY;
+        sacc[t][v] = sv2;
+        mx = fmaxf(mx, sv2);
+      }
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+    const float m_new = fmaxf(m_run, mx);
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    float ps = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float pv = __builtin_amdgcn_exp2f(sacc[t][v] - m_new);
+        sacc[t][v] = pv;
+        ps += pv;
+      }
+    l_run = l_run * alpha + ps;
+    m_run = m_new;
+#pragma unroll
+    for (int t = 0; t < OT; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[t][v] *= alpha;
+    // O^T += V^T P^T, k-steps of 16 keys: registers v = 8 j .. 8 j + 7 of
+    // half tile t are keys 32 t + 16 j + 4 hf + {0..3, 8..11}
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const u32x4_t pw{pack2(sacc[t][8 * j], sacc[t][8 * j + 1]),
+                         pack2(sacc[t][8 * j + 2], sacc[t][8 * j + 3]),
+                         pack2(sacc[t][8 * j + 4], sacc[t][8 * j + 5]),
+                         pack2(sacc[t][8 * j + 6], sacc[t][8 * j + 7])};
+        const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
+#pragma unroll
+        for (int ot = 0; ot < OT; ++ot) {
+          const uint16_t* vp = vs + (32 * ot + n) * VP + 32 * t + 16 * j + 4 * hf;
+          const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vp);
+          const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vp + 8);
+          const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], hi[0], hi[1]});
+          acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[ot], 0, 0, 0);
+        }
+      }
+    // the other stage was last read before the previous barrier
+    if (kt + 1 < nkt) store_tile(st ^ 1);
+    __syncthreads();
+  }
+
+  // normalise and store: lane holds head dims 32 ot + 8 g + 4 hf + (0..3)
+  const float l_tot = l_run + __shfl_xor(l_run, 32, kWave);
+  const float inv = 1.0f / l_tot;
+  if (qi < nq) {
+    uint16_t* orow = o + int64_t(tok) * d + hh * dh;
+#pragma unroll
+    for (int ot = 0; ot < OT; ++ot)
+#pragma unroll
+      for (int g = 0; g < 4; ++g) {
+        const int m0 = 32 * ot + 8 * g + 4 * hf;
+        if (m0 < dh)
+          *reinterpret_cast<u32x2_t*>(orow + m0) =
+              u32x2_t{pack2(acc[ot][4 * g] * inv, acc[ot][4 * g + 1] * inv),
+                      pack2(acc[ot][4 * g + 2] * inv, acc[ot][4 * g + 3] * inv)};
+      }
+  }
+}
+
+}  // namespace
+
+// ---------------------------------------------------------------------------
+// launchers
+// ---------------------------------------------------------------------------
+hipError_t launch_sinusoid(const float* t_values, int B, double* e, hipStream_t st) {
+  const int n = B * kFreqDim;
+  launch_kernel(&sinusoid_kernel, dim3((n + 255) / 256), dim3(256), 0, st, t_values, B, e);
+  return hipGetLastError();
+}
+
+hipError_t launch_silu(const float* in, int n, double* out, hipStream_t st) {
+  launch_kernel(&silu_kernel, dim3((n + 255) / 256), dim3(256), 0, st, in, n, out);
+  return hipGetLastError();
+}
+
+hipError_t launch_gemv(const double* in, int B, int K, const void* W, const float* bias, int Nout,
+                       const void* table, const int32_t* labels, int n_classes, float* out,
+                       double* out64, hipStream_t st) {
+  if (K % 8 != 0) return hipErrorInvalidValue;
+  launch_kernel(&gemv_kernel, dim3((Nout + kGemvWaves - 1) / kGemvWaves), dim3(kGemvWaves * kWave),
+                0, st, in, B, K, static_cast<const uint16_t*>(W), bias, Nout,
+                static_cast<const uint16_t*>(table), labels, n_classes, out, out64);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_attn(const BlockBufs& k, int T, int N, int d, const float* mod,
+                          const float* mod_prev, const uint16_t* a, bool cached,
+                          hipStream_t st) {
+  LnArgs p{k.x, k.x1, k.y, a, k.h, k.u, mod, mod_prev, nullptr, nullptr, T, N, d,
+           mod_prev != nullptr ? 1 : 0, cached ? 1 : 0};
+  launch_kernel(&ln_kernel<kLnAttn>, dim3((T + kLnWaves - 1) / kLnWaves), dim3(kLnWaves * kWave),
+                0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_mlp(const BlockBufs& k, int T, int N, int d, const float* mod,
+                         const uint16_t* a, uint16_t* u_out, hipStream_t st) {
+  LnArgs p{k.x, k.x1, k.y, a, k.h, u_out, mod, nullptr, k.slist, k.soff + k.B, T, N, d, 0, 1};
+  launch_kernel(&ln_kernel<kLnMlp>, dim3((T + kLnWaves - 1) / kLnWaves), dim3(kLnWaves * kWave),
+                0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_ln_final(const BlockBufs& k, int T, int N, int d, const float* mod,
+                           hipStream_t st) {
+  LnArgs p{k.x, k.x1, k.y, nullptr, nullptr, nullptr, mod, nullptr, nullptr, nullptr, T, N, d,
+           0, 0};
+  launch_kernel(&ln_kernel<kLnFinal>, dim3((T + kLnWaves - 1) / kLnWaves),
+                dim3(kLnWaves * kWave), 0, st, p);
+  return hipGetLastError();
+}
+
+hipError_t launch_slist(const BlockBufs& k, const uint8_t* sync, int N, int d, hipStream_t st) {
+  const int ntn_q = (d + kProjTN - 1) / kProjTN;
+  const int ntn_kv = (2 * d + kProjTN - 1) / kProjTN;
+  launch_kernel(&slist_kernel, dim3(1), dim3(kListThreads), 0, st, sync, sync == nullptr ? 1 : 0,
+                k.B, N, ntn_q, ntn_kv, k.slist, k.soff, k.ident, k.tab);
+  return hipGetLastError();
+}
+
+hipError_t launch_attention(const BlockBufs& k, int N, int H, int dh, hipStream_t st) {
+  const int QT = (N + kAttnQ - 1) / kAttnQ;
+  const dim3 grid(k.B * H * QT);
+  const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(double(dh)));
+  if (dh % 8 != 0 || dh > 96) return hipErrorInvalidValue;
+  if (dh <= 64)
+    launch_kernel(&attention_kernel<4, 2>, grid, dim3(kAttnThreads), 0, st, k.q, k.kv, k.slist,
+                  k.soff, k.B, N, H, dh, scale_log2, k.o);
+  else if (dh <= 80)
+    launch_kernel(&attention_kernel<5, 3>, grid, dim3(kAttnThreads), 0, st, k.q, k.kv, k.slist,
+                  k.soff, k.B, N, H, dh, scale_log2, k.o);
+  else
+    launch_kernel(&attention_kernel<6, 3>, grid, dim3(kAttnThreads), 0, st, k.q, k.kv, k.slist,
+                  k.soff, k.B, N, H, dh, scale_log2, k.o);
+  return hipGetLastError();
+}
+
+}  // namespace moeca

@@ -40,7 +40,9 @@ typedef __attribute__((ext_vector_type(16))) float f32x16_t;
 typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;  // 16 bytes, a native vector
 typedef __attribute__((ext_vector_type(2))) unsigned int u32x2_t;
 
-enum { kUp = 0, kDown = 1 };
+// kProj: a dense projection of listed token rows (the attention path of a
+// block): row r reads token list[r] and writes row list[r] of the output.
+enum { kUp = 0, kDown = 1, kProj = 2 };
 constexpr int kXcds = 8;
 
 // Activation of the up projection.  tanh GELU:
@@ -48,7 +50,7 @@ constexpr int kXcds = 8;
 // with exp(-2u) = 2^(-2u log2 e) from the hardware exp2 (about 1 ulp) and a
 // hardware reciprocal; the erf form uses erff.  kActSwiglu marks the gated
 // epilogue (silu below), which pairs columns instead of mapping each one.
-enum { kActGeluTanh = 0, kActGeluErf = 1, kActNone = 2, kActSwiglu = 3 };
+enum { kActGeluTanh = 0, kActGeluErf = 1, kActNone = 2, kActSwiglu = 3, kActBias = 4 };
 
 // silu(z) = z / (1 + exp(-z)), exp(-z) = 2^(-z log2 e) by the hardware exp2.
 __device__ __forceinline__ float silu_f(float z) {
@@ -128,7 +130,10 @@ __device__ __forceinline__ void group_row(int e, int E, int r0, int rows, int r,
                                           const int32_t* __restrict__ row_dst, int& src,
                                           int& dst) {
   const int rr = r < rows ? r : 0;
-  if (e < E) {
+  if (KIND == kProj) {
+    src = list[r0 + rr];
+    dst = r < rows ? list[r0 + r] : -1;
+  } else if (e < E) {
     if (KIND == kUp) {
       src = list[r0 + rr] / k;
       dst = r < rows ? r0 + r : -1;
@@ -373,6 +378,7 @@ constexpr int kStageElems = kTileA + kTileB;  // 48 KB
 constexpr int kLoadsA = kBigTM / 8 / kBigWaves;  // DMA instructions per wave per stage (A)
 constexpr int kLoadsB = kBigTN / 8 / kBigWaves;  // (B)
 constexpr int kLoadsPerStage = kLoadsA + kLoadsB;
+static_assert(kProjTM == kBigTM && kProjTN == kBigTN, "projection tables use the big tile");
 
 __device__ __forceinline__ void s_waitcnt_vm(int n) {
   // gfx9 encoding: vmcnt[3:0] | expcnt[6:4] | lgkmcnt[11:8] | vmcnt[5:4] << 14
@@ -510,7 +516,7 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
     const uint16_t* __restrict__ Wsh, const int32_t* __restrict__ off,
     const int32_t* __restrict__ tile_off, const int32_t* __restrict__ list,
     const int32_t* __restrict__ row_dst, int E, int G, int k, int K, int Nout,
-    uint16_t* __restrict__ dst, uint16_t* __restrict__ dst_sh) {
+    const float* __restrict__ bias, uint16_t* __restrict__ dst, uint16_t* __restrict__ dst_sh) {
   constexpr int TM = kBigTM, TN = kBigTN;
   constexpr bool kGated = ACT == kActSwiglu;
   constexpr int FM = 2, FN = 2;  // wave tile: 64 rows x 64 columns
@@ -663,8 +669,18 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
           uint32_t pk[4][2];
 #pragma unroll
           for (int q = 0; q < 4; ++q) {
-            pk[q][0] = pack2_bf16(act_fn<ACT>(a[4 * q]), act_fn<ACT>(a[4 * q + 1]));
-            pk[q][1] = pack2_bf16(act_fn<ACT>(a[4 * q + 2]), act_fn<ACT>(a[4 * q + 3]));
+            if constexpr (ACT == kActBias) {
+              // columns c .. c + 3 of the bias (clamped: masked columns are not stored)
+              const int c = c0 + i * 32 + 8 * q + 4 * h;
+              float bv[4];
+#pragma unroll
+              for (int s2 = 0; s2 < 4; ++s2) bv[s2] = bias[min(c + s2, Nout - 1)];
+              pk[q][0] = pack2_bf16(a[4 * q] + bv[0], a[4 * q + 1] + bv[1]);
+              pk[q][1] = pack2_bf16(a[4 * q + 2] + bv[2], a[4 * q + 3] + bv[3]);
+            } else {
+              pk[q][0] = pack2_bf16(act_fn<ACT>(a[4 * q]), act_fn<ACT>(a[4 * q + 1]));
+              pk[q][1] = pack2_bf16(act_fn<ACT>(a[4 * q + 2]), act_fn<ACT>(a[4 * q + 3]));
+            }
           }
 #pragma unroll
           for (int p = 0; p < 2; ++p) {
@@ -795,7 +811,8 @@ hipError_t launch_gemm(const Shape& s, const void* A, const void* W, const void*
     auto* osh = static_cast<uint16_t*>(dst_sh);
     if (tn == kBigTN) {
       launch_kernel(&gemm_bf16_big_kernel<KIND, ACT>, dim3(device_cus()), dim3(kBigThreads), 0, st,
-          a, w, wsh, b.off, toff, b.list, b.row_dst, s.E, G, s.k, K, Nout, o, osh);
+          a, w, wsh, b.off, toff, b.list, b.row_dst, s.E, G, s.k, K, Nout,
+          static_cast<const float*>(nullptr), o, osh);
     } else if (tn == 128) {
       launch_kernel(&gemm_bf16_kernel<128, 128, KIND, ACT>, dim3(grid), dim3(kGemmThreads), 0, st,
           a, w, wsh, b.off, toff, b.list, b.row_dst, s.E, G, s.k, K, Nout, o, osh);
@@ -854,6 +871,18 @@ hipError_t launch_ffn_down(const Shape& s, const void* W_down, const void* W_dow
                            const Buffers& b, hipStream_t st) {
   return launch_gemm<kDown, kActNone>(s, b.mid, W_down, W_down_sh, s.d_ff, s.d, b, b.h_c, b.h_sh,
                                       st);
+}
+
+hipError_t launch_proj(const void* A, const void* W, const float* bias, const int32_t* off,
+                       const int32_t* tiles, const int32_t* list, int K, int Nout, void* dst,
+                       hipStream_t st) {
+  if (K % kTK != 0 || Nout < 1) return hipErrorInvalidValue;
+  const auto* w = static_cast<const uint16_t*>(W);
+  launch_kernel(&gemm_bf16_big_kernel<kProj, kActBias>, dim3(device_cus()), dim3(kBigThreads), 0,
+                st, static_cast<const uint16_t*>(A), w, w, off, tiles, list,
+                static_cast<const int32_t*>(nullptr), 1, 1, 1, K, Nout, bias,
+                static_cast<uint16_t*>(dst), static_cast<uint16_t*>(dst));
+  return hipGetLastError();
 }
 
 }  // namespace moeca

@@ -5,6 +5,10 @@
 #include <hip/hip_ext.h>
 #include <cstddef>
 #include <cstdint>
+#include <functional>
+#include <string>
+
+#include "moeca.h"
 
 namespace moeca {
 
@@ -128,5 +132,67 @@ hipError_t launch_ffn_down(const Shape& s, const void* W_down, const void* W_dow
 hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void* attn_in,
                           void* attn_cache, const Buffers& b, hipStream_t st);
 hipError_t launch_reset(const Shape& s, const Buffers& b, hipStream_t st);
+
+// ---- the MoE layer step, as used by a block (moeca.cpp) ----------------
+// The step of moeca_step with the router reading x_route and the expert FFN
+// reading x_ffn; `between`, when set, is called after the decision and the
+// expert lists are enqueued and before the FFN (a nonzero return aborts the
+// step with that code).
+// Set this thread's moeca_last_error() text; returns code.
+int set_error(int code, const std::string& msg);
+
+int layer_step(moeca_layer* L, const void* x_route, const void* x_ffn, int t, void* out,
+               hipStream_t st, const std::function<int()>& between);
+bool layer_full_step(const moeca_layer* L, int t);
+const Buffers& layer_buffers(const moeca_layer* L);
+
+// ---- DiT block kernels (block.hip, ffn.hip) -----------------------------
+constexpr int kFreqDim = 256;    // timestep embedding width
+constexpr int kMaxWidth = 2048;  // largest block width d
+constexpr int kProjTM = 128;     // projection GEMM tile: rows
+constexpr int kProjTN = 256;     // and output columns
+
+// Shared per-step activations of a block stack (device).
+struct BlockBufs {
+  int B;
+  float* x;        // [T][d] residual stream (the caller's)
+  float* x1;       // [T][d]
+  uint16_t* h;     // [T][d] attention input
+  uint16_t* u;     // [T][d] MoE routing input
+  uint16_t* u2;    // [T][d] rebuilt MoE input of synchronised tokens
+  uint16_t* q;     // [T][d]
+  uint16_t* kv;    // [T][2d]
+  uint16_t* o;     // [T][d]
+  uint16_t* y;     // [T][d]
+  int32_t* slist;  // [T] synchronised tokens by sample
+  int32_t* soff;   // [B+1]
+  int32_t* ident;  // [T] identity row list
+  int32_t* tab;    // [8] projection row offsets and tile counts (see launch_slist)
+};
+
+// dst[list[r]] = bf16(A[list[r]] . W^T + bias) for r < off[1]: one group of
+// listed rows (tables off[2], tiles[2] on the device), K inputs, Nout outputs.
+hipError_t launch_proj(const void* A, const void* W, const float* bias, const int32_t* off,
+                       const int32_t* tiles, const int32_t* list, int K, int Nout, void* dst,
+                       hipStream_t st);
+hipError_t launch_sinusoid(const float* t_values, int B, double* e, hipStream_t st);
+hipError_t launch_silu(const float* in, int n, double* out, hipStream_t st);
+// v[b][r] = W[r] . in[b] + bias[r] (+ table[labels[b]][r]) in fp64; out =
+// fp32(v), or out64 = silu(v) when out64 is set (then out is unused)
+hipError_t launch_gemv(const double* in, int B, int K, const void* W, const float* bias, int Nout,
+                       const void* table, const int32_t* labels, int n_classes, float* out,
+                       double* out64, hipStream_t st);
+// every token: [x = x1 + g_m(prev) y;] h = LN(x) mod_a; [cached: x1 = x + g_a a, u = LN(x1) mod_m]
+hipError_t launch_ln_attn(const BlockBufs& k, int T, int N, int d, const float* mod,
+                          const float* mod_prev, const uint16_t* a, bool cached, hipStream_t st);
+// listed tokens (slist, count soff[B]): x1 = x + g_a a, u_out = LN(x1) mod_m
+hipError_t launch_ln_mlp(const BlockBufs& k, int T, int N, int d, const float* mod,
+                         const uint16_t* a, uint16_t* u_out, hipStream_t st);
+// every token: x = x1 + g_m y
+hipError_t launch_ln_final(const BlockBufs& k, int T, int N, int d, const float* mod,
+                           hipStream_t st);
+// token lists from the sync flags (sync == NULL: every token) and the tables
+hipError_t launch_slist(const BlockBufs& k, const uint8_t* sync, int N, int d, hipStream_t st);
+hipError_t launch_attention(const BlockBufs& k, int N, int H, int dh, hipStream_t st);
 
 }  // namespace moeca

@@ -285,10 +285,29 @@ int moeca_bind_attention(moeca_layer* L, const void* attn_in, void* attn_cache) 
 }
 
 int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) {
+  return moeca::layer_step(L, x_t, x_t, t, out, static_cast<hipStream_t>(stream), {});
+}
+
+}  // extern "C"
+
+namespace moeca {
+
+int set_error(int code, const std::string& msg) { return fail(code, msg); }
+
+bool layer_full_step(const moeca_layer* L, int t) {
+  const moeca_policy& p = L->pol;
+  return p.mode == MOECA_MODE_FULL || !L->valid || (p.refresh_cycle > 0 && t % p.refresh_cycle == 0);
+}
+
+const Buffers& layer_buffers(const moeca_layer* L) { return L->buf; }
+
+int layer_step(moeca_layer* L, const void* x_t, const void* x_ffn, int t, void* out,
+               hipStream_t st, const std::function<int()>& between) {
   if (L == nullptr) return fail(MOECA_E_INVAL, "layer is NULL");
-  if (x_t == nullptr || out == nullptr) return fail(MOECA_E_INVAL, "x_t and out are required");
+  if (x_t == nullptr || x_ffn == nullptr || out == nullptr)
+    return fail(MOECA_E_INVAL, "x_t and out are required");
   if (t < 0) return fail(MOECA_E_INVAL, "t must be >= 0");
-  if (!aligned16(x_t) || !aligned16(out))
+  if (!aligned16(x_t) || !aligned16(x_ffn) || !aligned16(out))
     return fail(MOECA_E_INVAL, "x_t and out must be 16-byte aligned");
   if (L->W_r == nullptr) return fail(MOECA_E_STATE, "weights are not bound");
   if (L->ws == nullptr) return fail(MOECA_E_STATE, "workspace is not bound");
@@ -296,10 +315,8 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
     return fail(MOECA_E_STATE, "shared expert weights are not bound");
   const Shape& s = L->shape;
   const moeca_policy& p = L->pol;
-  hipStream_t st = static_cast<hipStream_t>(stream);
   const bool uncached = p.mode == MOECA_MODE_FULL;
-  const bool full =
-      uncached || !L->valid || (p.refresh_cycle > 0 && t % p.refresh_cycle == 0);
+  const bool full = layer_full_step(L, t);
 
   const bool timed = L->timing && L->timed_steps < kMaxTimedSteps;
   hipEvent_t* ev = timed ? &L->events[size_t(L->timed_steps) * kEventsPerStep] : nullptr;
@@ -351,8 +368,12 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
     return MOECA_E_HIP;
   arm();
   if (!check(moeca::launch_lists(s, moeca::ffn_plan(s), b, st), "lists")) return MOECA_E_HIP;
+  if (between) {
+    const int rc = between();
+    if (rc != MOECA_OK) return rc;
+  }
   arm();
-  if (!check(moeca::launch_ffn_up(s, x_t, L->W_up, L->W_up_sh, p.act, b, st), "ffn up"))
+  if (!check(moeca::launch_ffn_up(s, x_ffn, L->W_up, L->W_up_sh, p.act, b, st), "ffn up"))
     return MOECA_E_HIP;
   arm();
   if (!check(moeca::launch_ffn_down(s, L->W_down, L->W_down_sh, b, st), "ffn down"))
@@ -366,6 +387,10 @@ int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) 
   L->last_full = full;
   return MOECA_OK;
 }
+
+}  // namespace moeca
+
+extern "C" {
 
 int moeca_cache_reset(moeca_layer* L, void* stream) {
   if (L == nullptr) return fail(MOECA_E_INVAL, "layer is NULL");

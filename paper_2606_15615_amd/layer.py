@@ -64,6 +64,22 @@ class MoecaLayer:
         _lib.moeca_bind_workspace(self.h, base + self._ws_shift, nbytes)
         self._keep = []
 
+    @classmethod
+    def attach(cls, handle, workspace, d, E, k, d_ff, *, batch, tokens, dtype="bf16",
+               n_shared=0, device="cuda:0"):
+        """A non-owning view of a layer created elsewhere (a block of a
+        stack): ``workspace`` is the uint8 tensor slice the layer is bound to."""
+        torch = _torch()
+        self = cls.__new__(cls)
+        self.d, self.E, self.k, self.d_ff, self.B, self.N = d, E, k, d_ff, batch, tokens
+        self.n_shared, self.dtype = n_shared, dtype
+        self.act_np = np.uint16 if dtype == "bf16" else np.float32
+        self.device = torch.device(device)
+        self.h = handle
+        self.workspace = workspace
+        self._owned = False
+        return self
+
     # -- binding ---------------------------------------------------------
     def set_weights(self, W_r, b_r, W_up, W_down):
         self._keep = [W_r, b_r, W_up, W_down]
@@ -139,7 +155,7 @@ class MoecaLayer:
         torch.cuda.synchronize(self.device)
 
     def close(self):
-        if getattr(self, "h", None):
+        if getattr(self, "h", None) and getattr(self, "_owned", True):
             _lib.moeca_layer_destroy(self.h)
             self.h = None
 

@@ -195,3 +195,94 @@ def test_shared_experts_and_gated_ffn_host_paths(L):
     finally:
         L.moeca_layer_destroy(h)
         L.moeca_layer_destroy(plain)
+
+
+# ---- block stack ------------------------------------------------------------
+@pytest.mark.parametrize("args,kw", [
+    ((2, 1152, 16, 16, 2, 4608), {"dtype": 1}),          # fp32: the stack is bf16 only
+    ((2, 1152, 16, 16, 2, 4608), {"n_shared": 1}),
+    ((2, 4096, 32, 16, 2, 4608), {}),                    # d above 2048
+    ((2, 1152, 7, 16, 2, 4608), {}),                     # heads do not divide d
+    ((2, 1152, 12, 16, 2, 4608), {}),                    # head width 96 ok, see below
+    ((2, 576, 6, 16, 2, 4608), {}),                      # head width 96
+    ((2, 640, 5, 16, 2, 4608), {}),                      # head width 128
+    ((2, 1152, 144, 16, 2, 4608), {}),                   # head width 8
+    ((2, 1152, 96, 16, 2, 4608), {}),                    # head width 12
+    ((0, 1152, 16, 16, 2, 4608), {}),
+    ((2, 1152, 16, 16, 9, 4608), {}),                    # the layer's own limit on k
+])
+def test_stack_create_limits(L, args, kw):
+    ok = {(2, 1152, 12), (2, 576, 6), (2, 1152, 144)}
+    pol = _pol(L, batch=2, tokens=64)
+    for f, v in kw.items():
+        setattr(pol, f, v)
+    h = L.load().moeca_stack_create(*args, ctypes.byref(pol))
+    expect = not kw and args[:3] in ok
+    assert bool(h) == expect, (args, kw, L.moeca_last_error())
+    if h:
+        assert L.moeca_stack_workspace_bytes(h) > 0
+        L.moeca_stack_destroy(h)
+    else:
+        assert L.moeca_last_error() != ""
+
+
+def test_stack_host_error_paths(L):
+    lib = L.load()
+    B, N, d, E, k, dff = 2, 80, 576, 4, 2, 256
+    h = L.moeca_stack_create(3, d, 8, E, k, dff, _pol(L, batch=B, tokens=N))
+    try:
+        nbytes = L.moeca_stack_workspace_bytes(h)
+        lay = L.moeca_layer_create(d, E, k, dff, _pol(L, batch=B, tokens=N))
+        per_layer = L.moeca_workspace_bytes(lay)
+        L.moeca_layer_destroy(lay)
+        # three layers, three attention caches, the shared activations
+        assert nbytes >= 3 * (per_layer + B * N * d * 2) + B * N * d * (6 * 2 + 2 * 2 + 4)
+        fake = 1 << 40  # never dereferenced
+        W = L.moeca_block_weights(*([fake] * 10))
+        assert lib.moeca_stack_step(h, fake, fake, 0, None) == L.MOECA_E_STATE  # no workspace
+        assert lib.moeca_stack_cache_reset(h, None) == L.MOECA_E_STATE
+        assert lib.moeca_stack_set_block(h, 3, ctypes.byref(W)) == L.MOECA_E_INVAL
+        W.b_o = None
+        assert lib.moeca_stack_set_block(h, 0, ctypes.byref(W)) == L.MOECA_E_INVAL
+        W.b_o = fake + 2
+        assert lib.moeca_stack_set_block(h, 0, ctypes.byref(W)) == L.MOECA_E_INVAL
+        W.b_o, W.W_qkv = fake, fake + 8
+        assert lib.moeca_stack_set_block(h, 0, ctypes.byref(W)) == L.MOECA_E_INVAL
+        W.W_qkv, W.b_r = fake, None          # the router bias is optional
+        assert L.moeca_stack_set_block(h, 0, W) == L.MOECA_OK
+        assert lib.moeca_stack_bind_workspace(h, fake, nbytes - 1) == L.MOECA_E_INVAL
+        assert lib.moeca_stack_bind_workspace(h, fake + 16, nbytes) == L.MOECA_E_INVAL
+        assert L.moeca_stack_bind_workspace(h, fake, nbytes) == L.MOECA_OK
+        # block 1 has no weights: a run over it is refused, block 0 alone is not checked here
+        assert lib.moeca_stack_step(h, fake, fake, 0, None) == L.MOECA_E_STATE
+        assert "block 1" in L.moeca_last_error()
+        for first, count in ((-1, 1), (0, 0), (2, 2), (3, 1)):
+            assert lib.moeca_stack_step_blocks(h, fake, fake, 0, first, count, None) == \
+                L.MOECA_E_INVAL
+        assert lib.moeca_stack_step_blocks(h, fake, fake, -1, 0, 1, None) == L.MOECA_E_INVAL
+        assert lib.moeca_stack_step_blocks(h, fake + 4, fake, 0, 0, 1, None) == L.MOECA_E_INVAL
+        assert lib.moeca_stack_step_blocks(h, None, fake, 0, 0, 1, None) == L.MOECA_E_INVAL
+        assert lib.moeca_stack_embed(h, fake, fake, fake, fake, fake, fake, None, 0, fake,
+                                     None) == L.MOECA_E_INVAL          # labels without a table
+        assert lib.moeca_stack_embed(h, fake, None, fake + 8, fake, fake, fake, None, 0, fake,
+                                     None) == L.MOECA_E_INVAL          # misaligned W1
+        assert not lib.moeca_stack_layer(h, 3)
+        assert lib.moeca_stack_layer(h, 2)
+        # buffers: inside the workspace, aligned, disjoint, the right sizes
+        spans = [L.moeca_stack_debug_buffer(h, i) for i in range(L.SBUF["a"])]
+        spans += [L.moeca_stack_debug_buffer(h, L.SBUF[n], l) for n in ("a", "layer")
+                  for l in range(3)]
+        spans.sort()
+        for (o1, b1), (o2, _) in zip(spans, spans[1:]):
+            assert o1 % 256 == 0 and o1 + b1 <= o2
+        assert spans[-1][0] + spans[-1][1] <= nbytes
+        assert L.moeca_stack_debug_buffer(h, L.SBUF["kv"])[1] == B * N * 2 * d * 2
+        assert L.moeca_stack_debug_buffer(h, L.SBUF["layer"], 1)[1] == per_layer
+        with pytest.raises(L.MoecaError):
+            L.moeca_stack_debug_buffer(h, L.SBUF["a"], 3)
+        with pytest.raises(L.MoecaError):
+            L.moeca_stack_debug_buffer(h, 13)
+    finally:
+        L.moeca_stack_destroy(h)
+    lib.moeca_stack_destroy(None)
+    assert lib.moeca_stack_workspace_bytes(None) == 0
