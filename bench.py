@@ -251,12 +251,140 @@ def policy_study(args, shape, make_layer, xs, out, _lib):
     return rows
 
 
+def stack_bench(args):
+    """The DiT-MoE block stack: one sampling step = the timestep/class
+    embedding plus every block (attention, AdaLN, the branch-cached MoE
+    layer).  Cache steps (ratio mode, refresh cycle off after the first
+    full step) against the uncached comparator's full steps, both replayed
+    from HIP graphs of K steps."""
+    import torch
+    from paper_2606_15615_amd import _lib
+    from paper_2606_15615_amd.stack import MoecaStack
+    from paper_2606_15615_amd.synth import STACKS, StackSynth
+
+    _lib.load()  # fails loudly when the library is not built
+    sh = STACKS[args.workload]
+    ratio = 0.3 if args.ratio is None else args.ratio
+    dev = torch.device("cuda:0")
+    K, Wm = args.steps, args.warmup
+    T = Wm + K
+    log(f"[bench] stack {args.workload} {sh}; generating weights on the GPU")
+    syn = StackSynth(sh, args.seed)
+    weights = [syn.block_device(l, dev) for l in range(sh.L)]
+    emb = syn.embedder_device(dev)
+    labels = torch.from_numpy(syn.labels().astype(np.int32)).to(dev)
+    tv = syn.timestep_values(T)
+    t_rows = [torch.full((sh.B,), float(v), dtype=torch.float32, device=dev) for v in tv]
+    xs = syn.trajectory_device(T, dev)
+    x = torch.empty_like(xs[0])
+    c = torch.empty((sh.B, sh.d), dtype=torch.float32, device=dev)
+    stream = torch.cuda.current_stream()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+
+    def make(mode):
+        S = MoecaStack(sh.L, sh.d, sh.heads, sh.E, sh.k, sh.d_ff, batch=sh.B, tokens=sh.N,
+                       mode=mode, ratio=ratio, refresh_cycle=0)
+        for l, w in enumerate(weights):
+            S.set_block(l, w["W_ada"], w["b_ada"], w["W_qkv"], w["b_qkv"], w["W_o"], w["b_o"],
+                        w["W_r"], None, w["W_up"], w["W_down"])
+        S.reset()
+        return S
+
+    def one(S, t):
+        x.copy_(xs[t])
+        S.embed(t_rows[t], labels, emb["W1"], emb["b1"], emb["W2"], emb["b2"], emb["table"], c)
+        S.step(x, c, t)
+
+    def run(S, t0, t1):
+        for t in range(t0, t1):
+            one(S, t)
+
+    def measure(S, warm):
+        S.reset()
+        run(S, 0, warm)
+        torch.cuda.synchronize()
+        e0.record(stream)
+        run(S, warm, T)
+        e1.record(stream)
+        torch.cuda.synchronize()
+        ms_eager = e0.elapsed_time(e1) / K
+        ms_graph, graphed = ms_eager, False
+        if not args.no_graph:
+            S.reset()
+            run(S, 0, warm)
+            g = torch.cuda.CUDAGraph()
+            with torch.cuda.graph(g):
+                run(S, warm, T)
+            g.replay()
+            torch.cuda.synchronize()
+            S.reset()
+            run(S, 0, warm)
+            torch.cuda.synchronize()
+            e0.record(stream)
+            g.replay()
+            e1.record(stream)
+            torch.cuda.synchronize()
+            ms_graph, graphed = e0.elapsed_time(e1) / K, True
+            del g
+        # counts of the same steps
+        S.reset()
+        run(S, 0, warm)
+        rec = syn_n = 0
+        for t in range(warm, T):
+            one(S, t)
+            for l in range(sh.L):
+                st = S.layer(l).stats()
+                rec += st.n_recompute
+                syn_n += st.n_sync
+        return ms_eager, ms_graph, graphed, rec / K / sh.L, syn_n / K / sh.L
+
+    c_eager = c_graph = f_eager = f_graph = None
+    graphed, rec, syn_n = False, 0.0, 0.0
+    if args.phase in ("both", "cached"):
+        log("[bench] cache steps")
+        S = make(_lib.MOECA_MODE_RATIO)
+        c_eager, c_graph, graphed, rec, syn_n = measure(S, Wm)
+        S.close()
+        del S
+    if args.phase in ("both", "full"):
+        log("[bench] full steps (uncached comparator)")
+        S = make(_lib.MOECA_MODE_FULL)
+        f_eager, f_graph, g2, _, _ = measure(S, min(Wm, 2))
+        graphed = graphed or g2
+        S.close()
+
+    def r4(v):
+        return None if v is None else round(v, 4)
+    branches = sh.B * sh.N * sh.k
+    wl = (f"{args.workload}: {sh.L} DiT-MoE blocks d={sh.d}, {sh.heads} heads x {sh.d // sh.heads}, "
+          f"E={sh.E} top-{sh.k} d_ff={sh.d_ff} GELU, {sh.N} tokens x batch {sh.B}, "
+          f"timestep + class embedding, ratio mode rho={ratio}")
+    value = c_graph if c_graph is not None else f_graph
+    res = {"metric": "DiT-MoE stack sampling step (cache step)", "value": r4(value),
+           "unit": "ms/step", "n_gpus": 1, "steps": K, "warmup": Wm, "higher_is_better": False,
+           "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+           "ms_per_step": r4(value), "launch": "hip_graph" if graphed else "eager",
+           "eager_ms_per_step": r4(c_eager), "full_ms_per_step": r4(f_graph),
+           "eager_full_ms_per_step": r4(f_eager),
+           "cached_over_full": (round(c_graph / f_graph, 4)
+                                if c_graph is not None and f_graph is not None else None),
+           "refresh_ratio_actual": round(rec / branches, 4),
+           "synchronized_token_frac": round(syn_n / (sh.B * sh.N), 4),
+           "config": {"workload": wl, "batch": sh.B, "tokens": sh.N, "blocks": sh.L}}
+    print(json.dumps(res), flush=True)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
         print(f"bench.py runs on one GPU only (asked for --gpus {args.gpus}); "
               "the library has no multi-GPU path", file=sys.stderr)
         sys.exit(2)
+    from paper_2606_15615_amd.synth import STACKS
+    if args.workload in STACKS:
+        stack_bench(args)
+        return
     import torch
     from paper_2606_15615_amd import _lib
     from paper_2606_15615_amd.layer import MoecaLayer, np_to_device

@@ -25,11 +25,21 @@ __device__ __forceinline__ uint32_t pack2(float a, float b) {
 
 __device__ __forceinline__ double silu64(double z) { return z / (1.0 + exp(-z)); }
 
-// One correct rounding of an fp64 value to bf16 (nearest, ties to even):
-// rounding to odd into fp32 first (truncate, then set the last bit if
-// anything was dropped) keeps the second rounding from landing on a false
-// tie.
+// One correct rounding of an fp64 value to bf16 (nearest, ties to even).
+// In fp32's normal range the fp64 significand is rounded to 8 bits in
+// place (the carry may step the exponent) and the result converts to fp32
+// exactly.  Elsewhere (zero, subnormal, overflow, inf, NaN): rounding to
+// odd into fp32 first (truncate, then set the last bit if anything was
+// dropped) keeps the second rounding from landing on a false tie.
 __device__ __forceinline__ uint32_t f64_to_bf16(double v) {
+  const double av = fabs(v);
+  if (av >= 0x1p-126 && av < 0x1p127) {
+    uint64_t b = static_cast<uint64_t>(__double_as_longlong(v));
+    b += ((uint64_t(1) << 44) - 1) + ((b >> 45) & 1);
+    b &= ~((uint64_t(1) << 45) - 1);
+    return __float_as_uint(static_cast<float>(__longlong_as_double(static_cast<long long>(b)))) >>
+           16;
+  }
   uint32_t u = __float_as_uint(__double2float_rz(v));
   if ((u & 0x7fffffffu) > 0x7f800000u) return 0x7fc0u;
   if (static_cast<double>(__uint_as_float(u)) != v && (u & 0x7fffffffu) < 0x7f800000u) u |= 1u;
@@ -66,48 +76,67 @@ __global__ void silu_kernel(const float* __restrict__ in, int n, double* __restr
 
 // v[b][r] = (sum_k W[r][k] in[b][k] + bias[r]) (+ table[labels[b]][r]) in
 // fp64 (products and sums), then out = fp32(v), or out64 = silu(v) when
-// out64 is set; one wave per weight row r, every sample.  W rows are bf16
-// [Nout][K] (K a multiple of 8), in fp64 [B][K].  The AdaLN vectors feed the
-// routing input, so they take the decision path's arithmetic: one rounding.
+// out64 is set.  W rows are bf16 [Nout][K] (K a multiple of 8), in fp64
+// [B][K].  A wave takes kGemvRows weight rows and the samples four at a
+// time, so each input load serves four rows.  blockIdx.y picks one of up to
+// kGemvBatch matrices of the same shape (every block's AdaLN map in one
+// launch: enough waves in flight to stream the weights).  The AdaLN vectors
+// feed the routing input, so they take the decision path's arithmetic: one
+// rounding.
 constexpr int kGemvWaves = 4;
+constexpr int kGemvRows = 4;
 
 __global__ __launch_bounds__(kGemvWaves * kWave) void gemv_kernel(
-    const double* __restrict__ in, int B, int K, const uint16_t* __restrict__ W,
-    const float* __restrict__ bias, int Nout, const uint16_t* __restrict__ table,
-    const int32_t* __restrict__ labels, int n_classes, float* __restrict__ out,
+    const double* __restrict__ in, int B, int K, GemvBatch mats, int Nout,
+    const uint16_t* __restrict__ table, const int32_t* __restrict__ labels, int n_classes,
     double* __restrict__ out64) {
   const int lane = threadIdx.x & 63;
-  const int r = blockIdx.x * kGemvWaves + (threadIdx.x >> 6);
-  if (r >= Nout) return;
-  const uint16_t* wr = W + int64_t(r) * K;
+  const int r0 = (blockIdx.x * kGemvWaves + (threadIdx.x >> 6)) * kGemvRows;
+  if (r0 >= Nout) return;
+  const uint16_t* __restrict__ W = mats.W[blockIdx.y];
+  const float* __restrict__ bias = mats.bias[blockIdx.y];
+  float* __restrict__ out = mats.out[blockIdx.y];
   const int nc = K / 8;
-  for (int b0 = 0; b0 < B; b0 += 8) {
-    const int nb = min(8, B - b0);
-    double acc[8];
+  for (int b0 = 0; b0 < B; b0 += 4) {
+    const int nb = min(4, B - b0);
+    double acc[kGemvRows][4];
 #pragma unroll
-    for (int u = 0; u < 8; ++u) acc[u] = 0.0;
+    for (int q = 0; q < kGemvRows; ++q)
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[q][u] = 0.0;
     for (int c = lane; c < nc; c += kWave) {
-      const u32x4_t wv = *reinterpret_cast<const u32x4_t*>(wr + 8 * c);
-      double w[8];
+      double w[kGemvRows][8];
 #pragma unroll
-      for (int e = 0; e < 4; ++e) {
-        w[2 * e] = __uint_as_float(wv[e] << 16);
-        w[2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
+      for (int q = 0; q < kGemvRows; ++q) {
+        const int r = min(r0 + q, Nout - 1);
+        const u32x4_t wv = *reinterpret_cast<const u32x4_t*>(W + int64_t(r) * K + 8 * c);
+#pragma unroll
+        for (int e = 0; e < 4; ++e) {
+          w[q][2 * e] = __uint_as_float(wv[e] << 16);
+          w[q][2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
+        }
       }
 #pragma unroll
-      for (int u = 0; u < 8; ++u) {
+      for (int u = 0; u < 4; ++u) {
         if (u < nb) {
           const double* ip = in + int64_t(b0 + u) * K + 8 * c;
+          double iv[8];
 #pragma unroll
-          for (int e = 0; e < 8; ++e) acc[u] += w[e] * ip[e];
+          for (int e = 0; e < 8; ++e) iv[e] = ip[e];
+#pragma unroll
+          for (int q = 0; q < kGemvRows; ++q)
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc[q][u] += w[q][e] * iv[e];
         }
       }
     }
 #pragma unroll
-    for (int u = 0; u < 8; ++u) {
-      if (u < nb) {
-        const double s = wave_sum_f64(acc[u]);
-        if (lane == 0) {
+    for (int q = 0; q < kGemvRows; ++q) {
+      const int r = r0 + q;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        const double s = wave_sum_f64(acc[q][u]);
+        if (lane == 0 && u < nb && r < Nout) {
           const int b = b0 + u;
           double v = s + static_cast<double>(bias[r]);
           if (table != nullptr) {
@@ -262,6 +291,17 @@ __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
       }
     }
   }
+  // the attention feature, requested together with x (it is used after the
+  // first LayerNorm)
+  const bool with_a = MODE == kLnMlp || p.cached;
+  u32x2_t av[kLnChunks];
+  if (with_a) {
+#pragma unroll
+    for (int j = 0; j < kLnChunks; ++j) {
+      const int c = lane + kWave * j;
+      if (c < n4) av[j] = reinterpret_cast<const u32x2_t*>(p.a + o)[c];
+    }
+  }
   double mean, rstd;
   if (MODE == kLnAttn) {
     ln_stats(v, n4, lane, d, mean, rstd);
@@ -274,7 +314,7 @@ __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
   for (int j = 0; j < kLnChunks; ++j) {
     const int c = lane + kWave * j;
     if (c < n4) {
-      const u32x2_t aa = reinterpret_cast<const u32x2_t*>(p.a + o)[c];
+      const u32x2_t aa = av[j];
       const float4 gg = reinterpret_cast<const float4*>(ga)[c];
       v[j][0] = gated_add(v[j][0], gg.x, __uint_as_float(aa[0] << 16));
       v[j][1] = gated_add(v[j][1], gg.y, __uint_as_float(aa[0] & 0xffff0000u));
@@ -567,13 +607,14 @@ hipError_t launch_silu(const float* in, int n, double* out, hipStream_t st) {
   return hipGetLastError();
 }
 
-hipError_t launch_gemv(const double* in, int B, int K, const void* W, const float* bias, int Nout,
-                       const void* table, const int32_t* labels, int n_classes, float* out,
+hipError_t launch_gemv(const double* in, int B, int K, const GemvBatch& mats, int n_mats,
+                       int Nout, const void* table, const int32_t* labels, int n_classes,
                        double* out64, hipStream_t st) {
-  if (K % 8 != 0) return hipErrorInvalidValue;
-  launch_kernel(&gemv_kernel, dim3((Nout + kGemvWaves - 1) / kGemvWaves), dim3(kGemvWaves * kWave),
-                0, st, in, B, K, static_cast<const uint16_t*>(W), bias, Nout,
-                static_cast<const uint16_t*>(table), labels, n_classes, out, out64);
+  if (K % 8 != 0 || n_mats < 1 || n_mats > kGemvBatch) return hipErrorInvalidValue;
+  const int rows_per_block = kGemvWaves * kGemvRows;
+  launch_kernel(&gemv_kernel, dim3((Nout + rows_per_block - 1) / rows_per_block, n_mats),
+                dim3(kGemvWaves * kWave), 0, st, in, B, K, mats, Nout,
+                static_cast<const uint16_t*>(table), labels, n_classes, out64);
   return hipGetLastError();
 }
 

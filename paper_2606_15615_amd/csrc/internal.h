@@ -177,10 +177,18 @@ hipError_t launch_proj(const void* A, const void* W, const float* bias, const in
                        hipStream_t st);
 hipError_t launch_sinusoid(const float* t_values, int B, double* e, hipStream_t st);
 hipError_t launch_silu(const float* in, int n, double* out, hipStream_t st);
-// v[b][r] = W[r] . in[b] + bias[r] (+ table[labels[b]][r]) in fp64; out =
-// fp32(v), or out64 = silu(v) when out64 is set (then out is unused)
-hipError_t launch_gemv(const double* in, int B, int K, const void* W, const float* bias, int Nout,
-                       const void* table, const int32_t* labels, int n_classes, float* out,
+// Up to kGemvBatch matrices of one shape for one GEMV launch (by value).
+constexpr int kGemvBatch = 32;
+struct GemvBatch {
+  const uint16_t* W[kGemvBatch];
+  const float* bias[kGemvBatch];
+  float* out[kGemvBatch];
+};
+// for each matrix m < n_mats: v[b][r] = W_m[r] . in[b] + bias_m[r]
+// (+ table[labels[b]][r]) in fp64; out_m = fp32(v), or, with out64 set
+// (one matrix), out64 = silu(v)
+hipError_t launch_gemv(const double* in, int B, int K, const GemvBatch& mats, int n_mats,
+                       int Nout, const void* table, const int32_t* labels, int n_classes,
                        double* out64, hipStream_t st);
 // every token: [x = x1 + g_m(prev) y;] h = LN(x) mod_a; [cached: x1 = x + g_a a, u = LN(x1) mod_m]
 hipError_t launch_ln_attn(const BlockBufs& k, int T, int N, int d, const float* mod,

@@ -14,6 +14,7 @@
 // waits for the device or allocates device memory.
 #include <hip/hip_runtime.h>
 
+#include <algorithm>
 #include <cmath>
 #include <new>
 #include <string>
@@ -206,8 +207,21 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
     return fail(MOECA_E_HIP, std::string(what) + ": " + hipGetErrorString(e));
   };
   int rc;
-  // SiLU(c) for the AdaLN maps; the constant k/v row tables
+  // SiLU(c), then the AdaLN vectors of every block of the run (they depend
+  // on c only), kGemvBatch blocks per launch; the constant k/v row tables
   if ((rc = hip(moeca::launch_silu(c, S->B * d, sc, st), "silu")) != MOECA_OK) return rc;
+  for (int l0 = first; l0 < first + count; l0 += moeca::kGemvBatch) {
+    const int nm = std::min(moeca::kGemvBatch, first + count - l0);
+    moeca::GemvBatch mats{};
+    for (int i = 0; i < nm; ++i) {
+      mats.W[i] = static_cast<const uint16_t*>(S->w[l0 + i].W_ada);
+      mats.bias[i] = S->w[l0 + i].b_ada;
+      mats.out[i] = mod_all + size_t(l0 + i) * mod_stride;
+    }
+    if ((rc = hip(moeca::launch_gemv(sc, S->B, d, mats, nm, 6 * d, nullptr, nullptr, 0, nullptr,
+                                     st), "adaln")) != MOECA_OK)
+      return rc;
+  }
   if ((rc = hip(moeca::launch_slist(k, nullptr, N, d, st), "token list")) != MOECA_OK) return rc;
 
   for (int l = first; l < first + count; ++l) {
@@ -220,9 +234,6 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
     const uint16_t* Wkv = Wq + size_t(d) * d;
     const bool full = moeca::layer_full_step(lay, t);
 
-    if ((rc = hip(moeca::launch_gemv(sc, S->B, d, W.W_ada, W.b_ada, 6 * d, nullptr, nullptr, 0,
-                                     mod, nullptr, st), "adaln")) != MOECA_OK)
-      return rc;
     if ((rc = hip(moeca::launch_ln_attn(k, T, N, d, mod, mod_prev, a, !full, st), "ln1")) !=
         MOECA_OK)
       return rc;
@@ -298,13 +309,18 @@ int moeca_stack_embed(moeca_stack* S, const float* t_values, const int32_t* labe
   hipStream_t st = static_cast<hipStream_t>(stream);
   double* emb = reinterpret_cast<double*>(S->ws + S->off[S_EMB]);
   double* h1 = reinterpret_cast<double*>(S->ws + S->off[S_H1]);
+  moeca::GemvBatch m1{}, m2{};
+  m1.W[0] = static_cast<const uint16_t*>(W1);
+  m1.bias[0] = b1;
+  m2.W[0] = static_cast<const uint16_t*>(W2);
+  m2.bias[0] = b2;
+  m2.out[0] = c;
   hipError_t e = moeca::launch_sinusoid(t_values, S->B, emb, st);
   if (e == hipSuccess)
-    e = moeca::launch_gemv(emb, S->B, moeca::kFreqDim, W1, b1, S->d, nullptr, nullptr, 0,
-                           nullptr, h1, st);
+    e = moeca::launch_gemv(emb, S->B, moeca::kFreqDim, m1, 1, S->d, nullptr, nullptr, 0, h1, st);
   if (e == hipSuccess)
-    e = moeca::launch_gemv(h1, S->B, S->d, W2, b2, S->d, labels ? table : nullptr, labels,
-                           n_classes, c, nullptr, st);
+    e = moeca::launch_gemv(h1, S->B, S->d, m2, 1, S->d, labels ? table : nullptr, labels,
+                           n_classes, nullptr, st);
   if (e != hipSuccess) return fail(MOECA_E_HIP, std::string("embed: ") + hipGetErrorString(e));
   return MOECA_OK;
 }

@@ -301,10 +301,12 @@ class StackSynth:
         return self._rng(8).integers(0, self.shape.n_classes, size=self.shape.B)
 
     @staticmethod
-    def timestep_values(T: int, t_max: float = 999.0) -> np.ndarray:
-        """Diffusion timestep value of sampling step 0..T-1 (evenly spaced,
-        decreasing from t_max), float32."""
-        return (t_max * (1.0 - np.arange(T, dtype=np.float64) / T)).astype(np.float32)
+    def timestep_values(T: int, n_sampling: int = 250, t_max: float = 999.0) -> np.ndarray:
+        """Diffusion timestep value of the first T steps of an n_sampling-step
+        sampler (evenly spaced, decreasing from t_max; the paper's DiT-MoE
+        runs sample in 250 steps, Sec. 5.1), float32."""
+        i = np.arange(T, dtype=np.float64)
+        return (t_max * (1.0 - i / n_sampling)).astype(np.float32)
 
     def trajectory(self, T: int, drift: str = "loguniform"):
         """Yield ``T`` stack inputs x_t, shape (B, N, d), fp32."""
@@ -319,3 +321,60 @@ class StackSynth:
             if t > 0:
                 x = keep * x + mix * g.standard_normal((s.B, s.N, s.d), dtype=np.float32)
             yield x.copy()
+
+    # ---- device-side draws (benchmarks of the full-size stack) -----------
+    def _torch_gen(self, device, *key):
+        import torch
+        g = torch.Generator(device=device)
+        g.manual_seed(int(np.random.SeedSequence([self.seed, *key]).generate_state(1)[0]))
+        return g
+
+    def block_device(self, l: int, device) -> dict:
+        """Block l's weights drawn on the GPU by torch's seeded generator:
+        the distributions of ``block`` (not its values), bf16 matrices as
+        int16 bit patterns, fp32 biases."""
+        import torch
+        s = self.shape
+        g = self._torch_gen(device, 2000 + l)
+
+        def mat(*shape):
+            a = torch.randn(*shape, generator=g, device=device, dtype=torch.float32)
+            a *= 1.0 / math.sqrt(shape[-1])
+            return a.to(torch.bfloat16).view(torch.int16)
+
+        def bias(n):
+            return torch.randn(n, generator=g, device=device, dtype=torch.float32) * 0.02
+
+        d = s.d
+        return {"W_ada": mat(6 * d, d), "b_ada": bias(6 * d), "W_qkv": mat(3 * d, d),
+                "b_qkv": bias(3 * d), "W_o": mat(d, d), "b_o": bias(d), "W_r": mat(s.E, d),
+                "W_up": mat(s.E, s.d_ff, d), "W_down": mat(s.E, d, s.d_ff)}
+
+    def embedder_device(self, device) -> dict:
+        import torch
+        s = self.shape
+        g = self._torch_gen(device, 3000)
+
+        def mat(*shape, scale=None):
+            a = torch.randn(*shape, generator=g, device=device, dtype=torch.float32)
+            a *= scale if scale is not None else 1.0 / math.sqrt(shape[-1])
+            return a.to(torch.bfloat16).view(torch.int16)
+        return {"W1": mat(s.d, s.freq_dim),
+                "b1": torch.randn(s.d, generator=g, device=device) * 0.02,
+                "W2": mat(s.d, s.d), "b2": torch.randn(s.d, generator=g, device=device) * 0.02,
+                "table": mat(s.n_classes, s.d, scale=1.0)}
+
+    def trajectory_device(self, T: int, device, drift: str = "loguniform"):
+        """``T`` stack inputs (B, N, d) fp32 drawn on the GPU: x_0 ~ N(0, 1),
+        then the per-token drift model of ``trajectory``."""
+        import torch
+        s = self.shape
+        a = torch.from_numpy(self._layer.drift_rates(drift)[..., None].astype(np.float32)).to(device)
+        keep, mix = torch.sqrt(1.0 - a), torch.sqrt(a)
+        g = self._torch_gen(device, 4000)
+        x = torch.randn(s.B, s.N, s.d, generator=g, device=device)
+        out = [x.clone()]
+        for _ in range(1, T):
+            x = keep * x + mix * torch.randn(s.B, s.N, s.d, generator=g, device=device)
+            out.append(x.clone())
+        return out
