@@ -450,50 +450,65 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
 
   const int64_t row0 = int64_t(b) * N;
   const int nld = 2 * kAttnKeys * cpr;  // chunks of one K + V tile
-  u32x4_t ld[kMaxLd];
-  auto load_tile = [&](int kt) __attribute__((always_inline)) {
+  const int kch = kAttnKeys * cpr;      // chunks of the K half
+  // Chunk c of a tile: K chunks (c < kch) run along a key row (16 bytes of
+  // 8 head dims each, coalesced), V chunks key-fastest, so the 64 lanes of
+  // a wave hold 8 head dims of 64 consecutive keys (kch is a multiple of 64:
+  // whole waves take K or V) and write V^T as dwords after one lane-pair
+  // exchange.
+  auto load_tile = [&](int kt, u32x4_t (&dst)[kMaxLd]) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < kMaxLd; ++u) {
       const int c = tid + kAttnThreads * u;
       if (c < nld) {
-        const int which = c / (kAttnKeys * cpr);
-        const int r = c % (kAttnKeys * cpr);
-        const int key = min(kt * kAttnKeys + r / cpr, N - 1);
-        const int ch = r % cpr;
-        ld[u] = *reinterpret_cast<const u32x4_t*>(kv + (row0 + key) * (2 * d) + which * d +
-                                                   hh * dh + ch * 8);
+        int key, col;
+        if (c < kch) {
+          key = c / cpr;
+          col = hh * dh + (c % cpr) * 8;
+        } else {
+          key = (c - kch) % kAttnKeys;
+          col = d + hh * dh + ((c - kch) / kAttnKeys) * 8;
+        }
+        key = min(kt * kAttnKeys + key, N - 1);
+        dst[u] = *reinterpret_cast<const u32x4_t*>(kv + (row0 + key) * (2 * d) + col);
       }
     }
   };
-  auto store_tile = [&](int st) __attribute__((always_inline)) {
+  auto store_tile = [&](int st, const u32x4_t (&src)[kMaxLd]) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < kMaxLd; ++u) {
       const int c = tid + kAttnThreads * u;
       if (c < nld) {
-        const int which = c / (kAttnKeys * cpr);
-        const int r = c % (kAttnKeys * cpr);
-        const int key = r / cpr;
-        const int ch = r % cpr;
-        if (which == 0) {
-          *reinterpret_cast<u32x4_t*>(sk + st * KE + key * KP + ch * 8) = ld[u];
+        if (c < kch) {
+          *reinterpret_cast<u32x4_t*>(sk + st * KE + (c / cpr) * KP + (c % cpr) * 8) = src[u];
         } else {
-          uint16_t* vt = sv + st * VE + (ch * 8) * VP + key;
+          // lanes 2i, 2i + 1 hold keys 2i, 2i + 1: the even lane writes head
+          // dims 0-3 of both, the odd lane dims 4-7, one dword per dim
+          const int key = (c - kch) % kAttnKeys;
+          const int ch = (c - kch) / kAttnKeys;
+          const bool odd = key & 1;
+          u32x4_t other;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) {
-            vt[(2 * e) * VP] = static_cast<uint16_t>(ld[u][e] & 0xffffu);
-            vt[(2 * e + 1) * VP] = static_cast<uint16_t>(ld[u][e] >> 16);
+          for (int e = 0; e < 4; ++e) other[e] = static_cast<uint32_t>(dpp_i32<kDppRow[0]>(
+                                                     static_cast<int>(src[u][e])));
+          uint32_t* vt = reinterpret_cast<uint32_t*>(sv + st * VE + (ch * 8 + (odd ? 4 : 0)) * VP +
+                                                     (key & ~1));
+#pragma unroll
+          for (int e = 0; e < 2; ++e) {
+            // head dims 2e, 2e + 1 of this lane's half (dims 4 + ... for odd)
+            const uint32_t mine = odd ? src[u][2 + e] : src[u][e];
+            const uint32_t part = odd ? other[2 + e] : other[e];
+            const uint32_t lo_key = odd ? part : mine;  // the even key's pair of dims
+            const uint32_t hi_key = odd ? mine : part;
+            vt[(2 * e) * (VP / 2)] = (lo_key & 0xffffu) | (hi_key << 16);
+            vt[(2 * e + 1) * (VP / 2)] = (lo_key >> 16) | (hi_key & 0xffff0000u);
           }
         }
       }
     }
   };
 
-  const int nkt = (N + kAttnKeys - 1) / kAttnKeys;
-  load_tile(0);
-  __syncthreads();  // zeroing done before the first tile lands
-  store_tile(0);
-  __syncthreads();
-
+  // softmax state in log2 units of the scaled scores
   float m_run = -INFINITY, l_run = 0.0f;
   f32x16_t acc[OT];
 #pragma unroll
@@ -501,11 +516,9 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[t][v] = 0.0f;
 
-  for (int kt = 0; kt < nkt; ++kt) {
-    const int st = kt & 1;
-    if (kt + 1 < nkt) load_tile(kt + 1);
-    const uint16_t* ks = sk + st * KE;
-    const uint16_t* vs = sv + st * VE;
+  auto compute = [&](int kt) __attribute__((always_inline)) {
+    const uint16_t* ks = sk + (kt & 1) * KE;
+    const uint16_t* vs = sv + (kt & 1) * VE;
     // S^T for keys 32 t' + (0..31) of the tile
     f32x16_t sacc[2];
 #pragma unroll
@@ -513,41 +526,50 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
 #pragma unroll
       for (int v = 0; v < 16; ++v) sacc[t][v] = 0.0f;
 #pragma unroll
-      for (int s = 0; s < KS; ++s) {
+      for (int s2 = 0; s2 < KS; ++s2) {
         const bf16x8_t kf =
-            *reinterpret_cast<const bf16x8_t*>(ks + (32 * t + n) * KP + 16 * s + 8 * hf);
-        sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s], sacc[t], 0, 0, 0);
+            *reinterpret_cast<const bf16x8_t*>(ks + (32 * t + n) * KP + 16 * s2 + 8 * hf);
+        sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s2], sacc[t], 0, 0, 0);
       }
     }
-    // online softmax in log2 units; lane keys: 32 t + 8 (v / 4) + 4 hf + v % 4
+    // lane keys: 32 t + 8 (v / 4) + 4 hf + v % 4; only a ragged last tile
+    // has keys past N
+    if ((kt + 1) * kAttnKeys > N) {
+#pragma unroll
+      for (int t = 0; t < 2; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) {
+          const int key = kt * kAttnKeys + 32 * t + 8 * (v >> 2) + 4 * hf + (v & 3);
+          if (key >= N) sacc[t][v] = -INFINITY;
+        }
+    }
     float mx = -INFINITY;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int key = kt * kAttnKeys + 32 * t + 8 * (v >> 2) + 4 * hf + (v & 3);
-        const float sv2 = key < N ? sacc[t][v] * scale_log2 : -INFINITY;
-        sacc[t][v] = sv2;
-        mx = fmaxf(mx, sv2);
-      }
-    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave));
+      for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[t][v]);
+    mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale_log2;
     const float m_new = fmaxf(m_run, mx);
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
     float ps = 0.0f;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float pv = __builtin_amdgcn_exp2f(sacc[t][v] - m_new);
+        const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[t][v], scale_log2, -m_new));
         sacc[t][v] = pv;
         ps += pv;
       }
-    l_run = l_run * alpha + ps;
+    // rescale only when some query's running maximum moved
+    if (__ballot(m_new != m_run) != 0ull) {
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+      l_run *= alpha;
+#pragma unroll
+      for (int t = 0; t < OT; ++t)
+#pragma unroll
+        for (int v = 0; v < 16; ++v) acc[t][v] *= alpha;
+    }
+    l_run += ps;
     m_run = m_new;
-#pragma unroll
-    for (int t = 0; t < OT; ++t)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) acc[t][v] *= alpha;
     // O^T += V^T P^T, k-steps of 16 keys: registers v = 8 j .. 8 j + 7 of
     // half tile t are keys 32 t + 16 j + 4 hf + {0..3, 8..11}
 #pragma unroll
@@ -568,8 +590,29 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
           acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[ot], 0, 0, 0);
         }
       }
-    // the other stage was last read before the previous barrier
-    if (kt + 1 < nkt) store_tile(st ^ 1);
+  };
+
+  // Two tiles of loads in flight: during the compute of tile kt the
+  // registers hold tiles kt + 1 (stored to LDS after it) and kt + 2; a tile's
+  // loads are issued a whole iteration before they are stored.  A stage is
+  // refilled only after the barrier that follows the last compute reading it.
+  const int nkt = (N + kAttnKeys - 1) / kAttnKeys;
+  u32x4_t lda[kMaxLd], ldb[kMaxLd];
+  load_tile(0, lda);
+  __syncthreads();  // zeroing done before the first tile lands
+  store_tile(0, lda);
+  if (nkt > 1) load_tile(1, lda);
+  if (nkt > 2) load_tile(2, ldb);
+  __syncthreads();
+  for (int kt = 0; kt < nkt; kt += 2) {
+    compute(kt);
+    if (kt + 1 < nkt) store_tile((kt + 1) & 1, lda);
+    if (kt + 3 < nkt) load_tile(kt + 3, lda);
+    __syncthreads();
+    if (kt + 1 >= nkt) break;
+    compute(kt + 1);
+    if (kt + 2 < nkt) store_tile(kt & 1, ldb);
+    if (kt + 4 < nkt) load_tile(kt + 4, ldb);
     __syncthreads();
   }
 

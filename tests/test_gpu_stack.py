@@ -284,3 +284,13 @@ def test_stack_embed_matches_oracle():
         ref = D.cond_embed(tv, emb["W1"], emb["b1"], emb["W2"], emb["b2"], rows)
         got = c.cpu().numpy()
         np.testing.assert_allclose(got, ref, rtol=1e-5, atol=1e-6)
+
+
+def test_stack_full_width_forced():
+    """The dit28 block's attention shape (d = 1152, 16 heads of 72, 1024
+    tokens: 16 key tiles, 8 query tiles) with small experts, a full step and
+    two cache steps."""
+    sh = StackShape(L=1, d=1152, heads=16, E=4, k=2, d_ff=256, B=2, N=1024)
+    say("full width")
+    SS = StackSetup(sh, mode="ratio", seed=3, T=3, ratio=0.3)
+    run_forced(SS, 3)
