@@ -395,21 +395,25 @@ __global__ __launch_bounds__(kListThreads) void slist_kernel(
 // V tiles are double-buffered: the next tile's global loads are in flight
 // during the current tile's MFMAs.  KS = ceil(d_h / 16) k-steps for q.k,
 // OT = ceil(d_h / 32) output tiles of O^T; columns and rows past d_h are zero.
+// DH, when nonzero, fixes d_h at compile time (the chunk index arithmetic of
+// the tile loads then has constant divisors); 0 takes d_h from the argument.
 constexpr int kAttnQ = 128;
 constexpr int kAttnKeys = 64;
 constexpr int kAttnThreads = 256;
 
-template <int KS, int OT>
+template <int KS, int OT, int DH>
 __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kv,
     const int32_t* __restrict__ slist, const int32_t* __restrict__ soff, int B, int N, int H,
-    int dh, float scale_log2, uint16_t* __restrict__ o) {
+    int dh_arg, float scale_log2, uint16_t* __restrict__ o) {
+  const int dh = DH != 0 ? DH : dh_arg;
   constexpr int KP = 16 * KS + 8;     // K row in LDS (bf16), padded
   constexpr int VR = 32 * OT;         // V^T rows (head dims)
   constexpr int VP = kAttnKeys + 8;   // V^T row (keys), padded
   constexpr int KE = kAttnKeys * KP;  // elements of one K stage
   constexpr int VE = VR * VP;
-  constexpr int kMaxLd = (2 * kAttnKeys * (VR / 8) + kAttnThreads - 1) / kAttnThreads;
+  constexpr int kMaxLd = (2 * kAttnKeys * ((DH != 0 ? DH : VR) / 8) + kAttnThreads - 1) /
+                         kAttnThreads;  // 16-byte chunks per thread per tile
   __shared__ __attribute__((aligned(16))) uint16_t sk[2 * KE];
   __shared__ __attribute__((aligned(16))) uint16_t sv[2 * VE];
 
@@ -701,15 +705,16 @@ hipError_t launch_attention(const BlockBufs& k, int N, int H, int dh, hipStream_
   const dim3 grid(k.B * H * QT);
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(double(dh)));
   if (dh % 8 != 0 || dh > 96) return hipErrorInvalidValue;
-  if (dh <= 64)
-    launch_kernel(&attention_kernel<4, 2>, grid, dim3(kAttnThreads), 0, st, k.q, k.kv, k.slist,
-                  k.soff, k.B, N, H, dh, scale_log2, k.o);
-  else if (dh <= 80)
-    launch_kernel(&attention_kernel<5, 3>, grid, dim3(kAttnThreads), 0, st, k.q, k.kv, k.slist,
-                  k.soff, k.B, N, H, dh, scale_log2, k.o);
-  else
-    launch_kernel(&attention_kernel<6, 3>, grid, dim3(kAttnThreads), 0, st, k.q, k.kv, k.slist,
-                  k.soff, k.B, N, H, dh, scale_log2, k.o);
+#define MOECA_ATTN(KS, OT, DH)                                                                 \
+  launch_kernel(&attention_kernel<KS, OT, DH>, grid, dim3(kAttnThreads), 0, st, k.q, k.kv,    \
+                k.slist, k.soff, k.B, N, H, dh, scale_log2, k.o)
+  if (dh == 64) MOECA_ATTN(4, 2, 64);
+  else if (dh == 72) MOECA_ATTN(5, 3, 72);
+  else if (dh == 96) MOECA_ATTN(6, 3, 96);
+  else if (dh <= 64) MOECA_ATTN(4, 2, 0);
+  else if (dh <= 80) MOECA_ATTN(5, 3, 0);
+  else MOECA_ATTN(6, 3, 0);
+#undef MOECA_ATTN
   return hipGetLastError();
 }
 

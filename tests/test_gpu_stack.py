@@ -218,11 +218,13 @@ def test_stack_tiny_forced(mode, pol):
     run_forced(SS, 5)
 
 
-def test_stack_head64_ragged_forced():
-    """Head width 64 (the other attention tiling), 130 tokens: two query
-    tiles and three key tiles with a ragged tail."""
-    sh = StackShape(L=1, d=512, heads=8, E=8, k=2, d_ff=256, B=2, N=130)
-    say("head64 ragged")
+@pytest.mark.parametrize("d,heads", [(512, 8), (640, 8), (384, 8)])
+def test_stack_head_widths_ragged_forced(d, heads):
+    """Head widths 64 (the other fixed tiling), 80 and 48 (the tilings with a
+    run-time head width), 130 tokens: two query tiles and three key tiles
+    with a ragged tail."""
+    sh = StackShape(L=1, d=d, heads=heads, E=8, k=2, d_ff=256, B=2, N=130)
+    say(f"head width {d // heads}, ragged")
     SS = StackSetup(sh, mode="ratio", seed=1, T=3, ratio=0.5)
     run_forced(SS, 3)
 
