@@ -391,12 +391,15 @@ __global__ __launch_bounds__(kListThreads) void slist_kernel(
 // tile: the online softmax (running max and sum per query) needs one lane
 // exchange (l, l ^ 32) per tile.  The probabilities, rounded to bf16, are
 // the B operand of O^T += V^T P^T, whose k order (keys) follows the S^T
-// accumulator layout, so P never leaves registers; V^T sits in LDS.  K and
-// V tiles are double-buffered: the next tile's global loads are in flight
-// during the current tile's MFMAs.  KS = ceil(d_h / 16) k-steps for q.k,
+// accumulator layout, so P never leaves registers; V^T sits in LDS.  The
+// tiles are software-pipelined over a three-stage LDS ring: while tile kt's
+// P.V MFMAs run, tile kt + 1's q.k MFMAs and softmax proceed, tile kt + 2 is
+// stored and tile kt + 3's global loads are in flight (two dependent chains
+// per wave).  KS = ceil(d_h / 16) k-steps for q.k,
 // OT = ceil(d_h / 32) output tiles of O^T; columns and rows past d_h are zero.
-// DH, when nonzero, fixes d_h at compile time (the chunk index arithmetic of
-// the tile loads then has constant divisors); 0 takes d_h from the argument.
+// DH is d_h, a compile-time constant (every multiple of 8 up to 96 is
+// instantiated), so the chunk index arithmetic of the tile loads has
+// constant divisors and the register staging is sized to the width.
 constexpr int kAttnQ = 128;
 constexpr int kAttnKeys = 64;
 constexpr int kAttnThreads = 256;
@@ -406,16 +409,19 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kv,
     const int32_t* __restrict__ slist, const int32_t* __restrict__ soff, int B, int N, int H,
     int dh_arg, float scale_log2, uint16_t* __restrict__ o) {
-  const int dh = DH != 0 ? DH : dh_arg;
+  static_assert(DH % 8 == 0 && DH <= 96, "head width");
+  constexpr int dh = DH;
+  (void)dh_arg;
   constexpr int KP = 16 * KS + 8;     // K row in LDS (bf16), padded
   constexpr int VR = 32 * OT;         // V^T rows (head dims)
   constexpr int VP = kAttnKeys + 8;   // V^T row (keys), padded
   constexpr int KE = kAttnKeys * KP;  // elements of one K stage
   constexpr int VE = VR * VP;
-  constexpr int kMaxLd = (2 * kAttnKeys * ((DH != 0 ? DH : VR) / 8) + kAttnThreads - 1) /
-                         kAttnThreads;  // 16-byte chunks per thread per tile
-  __shared__ __attribute__((aligned(16))) uint16_t sk[2 * KE];
-  __shared__ __attribute__((aligned(16))) uint16_t sv[2 * VE];
+  constexpr int kMaxLd =
+      (2 * kAttnKeys * (DH / 8) + kAttnThreads - 1) / kAttnThreads;  // chunks per thread
+  constexpr int kStg = 3;             // LDS ring stages
+  __shared__ __attribute__((aligned(16))) uint16_t sk[kStg * KE];
+  __shared__ __attribute__((aligned(16))) uint16_t sv[kStg * VE];
 
   // (sample, head, query tile); the query tiles of one (sample, head) are
   // consecutive logical blocks on one XCD, so they share its L2 copy of K, V
@@ -434,10 +440,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
   const int d = H * dh;
   const int cpr = dh / 8;  // 16-byte chunks per head row
 
-  // zero both stages once: K columns and V^T rows past d_h stay zero
-  for (int i = tid; i < (2 * KE) / 8; i += kAttnThreads)
+  // zero every stage once: K columns and V^T rows past d_h stay zero
+  for (int i = tid; i < (kStg * KE) / 8; i += kAttnThreads)
     reinterpret_cast<u32x4_t*>(sk)[i] = u32x4_t{0, 0, 0, 0};
-  for (int i = tid; i < (2 * VE) / 8; i += kAttnThreads)
+  for (int i = tid; i < (kStg * VE) / 8; i += kAttnThreads)
     reinterpret_cast<u32x4_t*>(sv)[i] = u32x4_t{0, 0, 0, 0};
 
   // this lane's query and its fragments (B operand of S^T)
@@ -520,11 +526,9 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
 #pragma unroll
     for (int v = 0; v < 16; ++v) acc[t][v] = 0.0f;
 
-  auto compute = [&](int kt) __attribute__((always_inline)) {
-    const uint16_t* ks = sk + (kt & 1) * KE;
-    const uint16_t* vs = sv + (kt & 1) * VE;
-    // S^T for keys 32 t' + (0..31) of the tile
-    f32x16_t sacc[2];
+  // q.k of tile kt: S^T for keys 32 t + (0..31)
+  auto qk = [&](int kt, f32x16_t (&sacc)[2]) __attribute__((always_inline)) {
+    const uint16_t* ks = sk + (kt % kStg) * KE;
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
 #pragma unroll
@@ -536,8 +540,13 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
         sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s2], sacc[t], 0, 0, 0);
       }
     }
-    // lane keys: 32 t + 8 (v / 4) + 4 hf + v % 4; only a ragged last tile
-    // has keys past N
+  };
+  // softmax of tile kt: keys past N masked (only a ragged last tile has
+  // them), the running max and sum, O rescaled when some query's max moved,
+  // then P (bf16) as the B operand fragments of the tile's four 16-key
+  // k-steps; lane keys: 32 t + 8 (v / 4) + 4 hf + v % 4
+  auto softmax = [&](int kt, f32x16_t (&sacc)[2], bf16x8_t (&pf)[4])
+      __attribute__((always_inline)) {
     if ((kt + 1) * kAttnKeys > N) {
 #pragma unroll
       for (int t = 0; t < 2; ++t)
@@ -559,11 +568,10 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) {
-        const float pv = __builtin_amdgcn_exp2f(fmaf(sacc[t][v], scale_log2, -m_new));
-        sacc[t][v] = pv;
-        ps += pv;
+        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[t][v], scale_log2, -m_new));
+        sacc[t][v] = p;
+        ps += p;
       }
-    // rescale only when some query's running maximum moved
     if (__ballot(m_new != m_run) != 0ull) {
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
@@ -574,8 +582,6 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
     }
     l_run += ps;
     m_run = m_new;
-    // O^T += V^T P^T, k-steps of 16 keys: registers v = 8 j .. 8 j + 7 of
-    // half tile t are keys 32 t + 16 j + 4 hf + {0..3, 8..11}
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
@@ -584,39 +590,56 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
                          pack2(sacc[t][8 * j + 2], sacc[t][8 * j + 3]),
                          pack2(sacc[t][8 * j + 4], sacc[t][8 * j + 5]),
                          pack2(sacc[t][8 * j + 6], sacc[t][8 * j + 7])};
-        const bf16x8_t pf = __builtin_bit_cast(bf16x8_t, pw);
+        pf[2 * t + j] = __builtin_bit_cast(bf16x8_t, pw);
+      }
+  };
+  // O^T += V^T P^T for tile kt: fragment 2 t + j holds the keys
+  // 32 t + 16 j + 4 hf + {0..3, 8..11}
+  auto pv = [&](int kt, const bf16x8_t (&pf)[4]) __attribute__((always_inline)) {
+    const uint16_t* vs = sv + (kt % kStg) * VE;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int j = 0; j < 2; ++j)
 #pragma unroll
         for (int ot = 0; ot < OT; ++ot) {
           const uint16_t* vp = vs + (32 * ot + n) * VP + 32 * t + 16 * j + 4 * hf;
           const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vp);
           const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vp + 8);
           const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], hi[0], hi[1]});
-          acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf, acc[ot], 0, 0, 0);
+          acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[2 * t + j], acc[ot], 0, 0, 0);
         }
-      }
   };
 
-  // Two tiles of loads in flight: during the compute of tile kt the
-  // registers hold tiles kt + 1 (stored to LDS after it) and kt + 2; a tile's
-  // loads are issued a whole iteration before they are stored.  A stage is
-  // refilled only after the barrier that follows the last compute reading it.
+  // Prologue: tiles 0 and 1 stored, tile 2's loads in flight, tile 0's q.k
+  // and softmax done.  Iteration kt reads stage kt + 1 (q.k) and stage kt
+  // (p.v) and fills stage kt + 2, last read by the p.v of iteration kt - 1,
+  // before the previous barrier; the p.v of tile kt accumulates before the
+  // softmax of tile kt + 1 rescales O.
   const int nkt = (N + kAttnKeys - 1) / kAttnKeys;
-  u32x4_t lda[kMaxLd], ldb[kMaxLd];
-  load_tile(0, lda);
+  u32x4_t ld[kMaxLd];
+  load_tile(0, ld);
   __syncthreads();  // zeroing done before the first tile lands
-  store_tile(0, lda);
-  if (nkt > 1) load_tile(1, lda);
-  if (nkt > 2) load_tile(2, ldb);
+  store_tile(0, ld);
+  if (nkt > 1) {
+    load_tile(1, ld);
+    store_tile(1, ld);
+  }
+  if (nkt > 2) load_tile(2, ld);
   __syncthreads();
-  for (int kt = 0; kt < nkt; kt += 2) {
-    compute(kt);
-    if (kt + 1 < nkt) store_tile((kt + 1) & 1, lda);
-    if (kt + 3 < nkt) load_tile(kt + 3, lda);
-    __syncthreads();
-    if (kt + 1 >= nkt) break;
-    compute(kt + 1);
-    if (kt + 2 < nkt) store_tile(kt & 1, ldb);
-    if (kt + 4 < nkt) load_tile(kt + 4, ldb);
+  bf16x8_t pcur[4];
+  {
+    f32x16_t s0[2];
+    qk(0, s0);
+    softmax(0, s0, pcur);
+  }
+  for (int kt = 0; kt < nkt; ++kt) {
+    f32x16_t snext[2];
+    if (kt + 1 < nkt) qk(kt + 1, snext);
+    pv(kt, pcur);
+    if (kt + 2 < nkt) store_tile((kt + 2) % kStg, ld);
+    if (kt + 3 < nkt) load_tile(kt + 3, ld);
+    if (kt + 1 < nkt) softmax(kt + 1, snext, pcur);
     __syncthreads();
   }
 
@@ -705,15 +728,24 @@ hipError_t launch_attention(const BlockBufs& k, int N, int H, int dh, hipStream_
   const dim3 grid(k.B * H * QT);
   const float scale_log2 = static_cast<float>(1.4426950408889634 / std::sqrt(double(dh)));
   if (dh % 8 != 0 || dh > 96) return hipErrorInvalidValue;
-#define MOECA_ATTN(KS, OT, DH)                                                                 \
-  launch_kernel(&attention_kernel<KS, OT, DH>, grid, dim3(kAttnThreads), 0, st, k.q, k.kv,    \
-                k.slist, k.soff, k.B, N, H, dh, scale_log2, k.o)
-  if (dh == 64) MOECA_ATTN(4, 2, 64);
-  else if (dh == 72) MOECA_ATTN(5, 3, 72);
-  else if (dh == 96) MOECA_ATTN(6, 3, 96);
-  else if (dh <= 64) MOECA_ATTN(4, 2, 0);
-  else if (dh <= 80) MOECA_ATTN(5, 3, 0);
-  else MOECA_ATTN(6, 3, 0);
+#define MOECA_ATTN(DH)                                                                       \
+  launch_kernel(&attention_kernel<((DH) + 15) / 16, ((DH) + 31) / 32, DH>, grid,               \
+                dim3(kAttnThreads), 0, st, k.q, k.kv, k.slist, k.soff, k.B, N, H, dh,          \
+                scale_log2, k.o)
+  switch (dh / 8) {
+    case 1: MOECA_ATTN(8); break;
+    case 2: MOECA_ATTN(16); break;
+    case 3: MOECA_ATTN(24); break;
+    case 4: MOECA_ATTN(32); break;
+    case 5: MOECA_ATTN(40); break;
+    case 6: MOECA_ATTN(48); break;
+    case 7: MOECA_ATTN(56); break;
+    case 8: MOECA_ATTN(64); break;
+    case 9: MOECA_ATTN(72); break;
+    case 10: MOECA_ATTN(80); break;
+    case 11: MOECA_ATTN(88); break;
+    default: MOECA_ATTN(96); break;
+  }
 #undef MOECA_ATTN
   return hipGetLastError();
 }
