@@ -296,3 +296,54 @@ def test_stack_full_width_forced():
     say("full width")
     SS = StackSetup(sh, mode="ratio", seed=3, T=3, ratio=0.3)
     run_forced(SS, 3)
+
+
+def test_stack_nothing_to_refresh_is_bit_identical():
+    """A cache step whose input and conditioning equal the full step's, at
+    ratio 0: every branch is matched and reused, no token is synchronised
+    (the projections, attention and LN2 run over empty lists), and the
+    output equals the full step's bit for bit, on the GPU as in the oracle."""
+    import torch
+    sh = StackShape(L=2, d=576, heads=8, E=4, k=2, d_ff=256, B=2, N=80)
+    SS = StackSetup(sh, mode="ratio", seed=4, T=1, ratio=0.0)
+    outs = []
+    for t in range(2):
+        SS.x_dev.copy_(torch.from_numpy(SS.xs[0]))
+        SS.c_dev.copy_(torch.from_numpy(SS.cs[0]))
+        SS.S.step(SS.x_dev, SS.c_dev, t)
+        torch.cuda.synchronize()
+        outs.append(SS.x_dev.clone())
+        if t == 1:
+            assert int(SS.S.read("soff")[-1]) == 0
+            for l in range(sh.L):
+                st = SS.S.layer(l).stats()
+                assert st.n_recompute == 0 and st.n_sync == 0 and not st.full_step
+    assert torch.equal(outs[0], outs[1])
+    say("  nothing to refresh: cache step == full step")
+
+
+def test_stack_single_token_single_head_forced():
+    """One token per sample (attention over a single key: the output is
+    that key's value) and one 64-wide head."""
+    sh = StackShape(L=1, d=64, heads=1, E=4, k=2, d_ff=128, B=3, N=1)
+    say("single token, single head")
+    SS = StackSetup(sh, mode="ratio", seed=5, T=3, ratio=0.5)
+    run_forced(SS, 3)
+
+
+def test_stack_three_blocks_run_equals_block_by_block():
+    import torch
+    sh = StackShape(L=3, d=512, heads=8, E=8, k=2, d_ff=256, B=2, N=100)
+    A = StackSetup(sh, mode="threshold", seed=6, T=3)
+    Bs = StackSetup(sh, mode="threshold", seed=6, T=3)
+    xa, xb = torch.zeros_like(A.x_dev), torch.zeros_like(Bs.x_dev)
+    for t in range(3):
+        xa.copy_(torch.from_numpy(A.xs[t]))
+        xb.copy_(torch.from_numpy(Bs.xs[t]))
+        A.c_dev.copy_(torch.from_numpy(A.cs[t]))
+        Bs.c_dev.copy_(torch.from_numpy(Bs.cs[t]))
+        A.S.step(xa, A.c_dev, t)
+        Bs.S.step_blocks(xb, Bs.c_dev, t, 0, 2)   # blocks 0-1 in one call
+        Bs.S.step_blocks(xb, Bs.c_dev, t, 2, 1)   # then block 2
+        torch.cuda.synchronize()
+        assert torch.equal(xa, xb), f"t={t}"
