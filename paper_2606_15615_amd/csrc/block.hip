@@ -47,11 +47,11 @@ __device__ __forceinline__ uint32_t f64_to_bf16(double v) {
   return u >> 16;
 }
 
-// fp32(x + g f), the product exact in fp64, one rounding of the fp64 sum
-__device__ __forceinline__ float gated_add(float x, float g, float f) {
-  return static_cast<float>(static_cast<double>(x) +
-                            static_cast<double>(g) * static_cast<double>(f));
-}
+// fp32(x + g f) with one rounding of the exact value (a fused multiply-add;
+// g f is exact).  An fp64 evaluation rounded to fp32 gives the same value
+// except when its fp64 rounding lands exactly on an fp32 midpoint (about one
+// value in 2^29).
+__device__ __forceinline__ float gated_add(float x, float g, float f) { return fmaf(g, f, x); }
 
 // ---------------------------------------------------------------------------
 // conditioning
@@ -199,6 +199,27 @@ __device__ __forceinline__ void ln_stats(const float (&v)[kLnChunks][4], int n4,
   rstd = 1.0 / sqrt(var + 1e-6);
 }
 
+// bf16(LN(v) * (1 + scale) + shift) into row `dst` in fp32: the attention
+// input (off the decision path)
+__device__ __forceinline__ void ln_store_f32(const float (&v)[kLnChunks][4], int n4, int lane,
+                                             double mean, double rstd, const float* shift,
+                                             const float* scale, uint16_t* dst) {
+  const float mf = static_cast<float>(mean), rf = static_cast<float>(rstd);
+#pragma unroll
+  for (int j = 0; j < kLnChunks; ++j) {
+    const int c = lane + kWave * j;
+    if (c < n4) {
+      const float4 sh = reinterpret_cast<const float4*>(shift)[c];
+      const float4 sc = reinterpret_cast<const float4*>(scale)[c];
+      const float z0 = fmaf((v[j][0] - mf) * rf, 1.0f + sc.x, sh.x);
+      const float z1 = fmaf((v[j][1] - mf) * rf, 1.0f + sc.y, sh.y);
+      const float z2 = fmaf((v[j][2] - mf) * rf, 1.0f + sc.z, sh.z);
+      const float z3 = fmaf((v[j][3] - mf) * rf, 1.0f + sc.w, sh.w);
+      reinterpret_cast<u32x2_t*>(dst)[c] = u32x2_t{pack2(z0, z1), pack2(z2, z3)};
+    }
+  }
+}
+
 // bf16(LN(v) * (1 + scale) + shift) into row `dst`, in fp64 and rounded
 // once: this is the MoE routing input (decision-path arithmetic)
 __device__ __forceinline__ void ln_store(const float (&v)[kLnChunks][4], int n4, int lane,
@@ -305,7 +326,7 @@ __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
   double mean, rstd;
   if (MODE == kLnAttn) {
     ln_stats(v, n4, lane, d, mean, rstd);
-    ln_store(v, n4, lane, mean, rstd, m, m + d, p.h + o);
+    ln_store_f32(v, n4, lane, mean, rstd, m, m + d, p.h + o);
     if (!p.cached) return;
   }
   // x1 = x + g_a * a, then the MoE input from LN(x1)

@@ -5,10 +5,11 @@ Protocol (oracle-forced, per block): the oracle runs its own trajectory.
 Before each block step its state (the cached attention feature and the MoE
 layer's cache) is written into the GPU stack, the oracle's block input goes
 in, the GPU runs that one block, and:
-* the AdaLN vectors, the attention input h and, on cache steps, the routing
-  input u and x1 of the tokens outside S are bit-exact (decision-path
-  arithmetic on both sides), so every MoE decision of a cache step is
-  compared bit for bit (the layer checks of ``gpu_harness.check_step``);
+* the AdaLN vectors and, on cache steps, the routing input u and x1 of the
+  tokens outside S are bit-exact (decision-path arithmetic on both sides),
+  so every MoE decision of a cache step is compared bit for bit (the layer
+  checks of ``gpu_harness.check_step``); the attention input h is within one
+  bf16 ulp;
 * the attention path (k, v, q, attention output, a, x1, the rebuilt u), the
   MoE output y and the block output are within the bf16 tolerance (max
   relative error 2e-2 over the tensor);
@@ -136,8 +137,14 @@ def check_block(SS: StackSetup, l: int, t: int, st_o: D.BlockState, x: np.ndarra
     # decision-path arithmetic: bit-exact
     g_mod = SS.S.read("mod")[l]
     assert np.array_equal(g_mod, mod), f"{tag}: AdaLN vectors differ in {(g_mod != mod).sum()}"
+    # the attention input is computed in fp32 (off the decision path): within
+    # one bf16 ulp of the oracle's, or (where the modulation nearly cancels
+    # the shift) within fp32 rounding of the terms
     g_h = SS.S.read("h").reshape(B, N, d)
-    assert np.array_equal(g_h, rec["h"]), f"{tag}: h differs in {(g_h != rec['h']).sum()}"
+    hg, ho = O.to_f64(g_h, BF), O.to_f64(rec["h"], BF)
+    bound = np.abs(ho) * 2.0 ** -7 + 1e-5 * np.abs(ho).max()
+    assert np.all(np.abs(hg - ho) <= bound), \
+        f"{tag}: h off by {float(np.max(np.abs(hg - ho) - bound)):.3g} beyond the bound"
     g_u = SS.S.read("u").reshape(B, N, d)
     g_x1 = SS.S.read("x1").reshape(B, N, d)
     Sm = rec["sync"]
