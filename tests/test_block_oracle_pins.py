@@ -224,3 +224,46 @@ def test_stack_step_chains_blocks():
 def test_named_stacks_are_consistent():
     for sh in STACKS.values():
         assert sh.d % sh.heads == 0 and (sh.d // sh.heads) % 8 == 0 and sh.d % 64 == 0
+
+
+def test_adaln_matches_torch_modules():
+    syn, dims, blocks = make_blocks(TINY, seed=8)
+    W = blocks[0]
+    c = cond(syn, 321.0)
+    got = D.adaln(W.W_ada, W.b_ada, c)
+    lin = torch.nn.Linear(TINY.d, 6 * TINY.d, dtype=torch.float64)
+    with torch.no_grad():
+        lin.weight.copy_(torch.from_numpy(f64(W.W_ada)))
+        lin.bias.copy_(torch.from_numpy(W.b_ada.astype(np.float64)))
+        ref = lin(torch.nn.functional.silu(torch.from_numpy(c.astype(np.float64))))
+    np.testing.assert_array_equal(got, ref.numpy().astype(np.float32).reshape(TINY.B, 6, TINY.d))
+
+
+def test_full_refresh_cache_step_equals_full_step_for_refreshed_parts():
+    """At ratio 1 every token is synchronised and every branch recomputed: the
+    cache step's attention feature and rebuilt MoE input equal the full
+    step's on the same input, and for each token every expert selected in
+    both steps has the same cached row (the FFN of the rebuilt input)."""
+    syn, dims, blocks = make_blocks(TINY, seed=9)
+    traj = list(syn.trajectory(2))
+    W = blocks[0]
+    mod = D.adaln(W.W_ada, W.b_ada, cond(syn, 700.0))
+    pol = O.Policy(mode=O.MODE_RATIO, ratio=1.0)
+    _, st, _ = D.block_step(dims, pol, W, D.BlockState(dims), traj[0], mod, 0)
+    x = traj[1].copy()
+    x[:, :6] += 1.5          # a clearly changed input for some tokens
+    _, st_c, rc = D.block_step(dims, pol, W, st, x, mod, 1)
+    _, st_f, rf = D.block_step(dims, pol, W, D.BlockState(dims), x, mod, 0)
+    assert not rc["full"] and rf["full"] and rc["sync"].all()
+    np.testing.assert_array_equal(st_c.a, st_f.a)
+    np.testing.assert_array_equal(rc["u"], rf["u"])
+    np.testing.assert_array_equal(rc["x1"], rf["x1"])
+    same = 0
+    for b in range(dims.B):
+        for i in range(dims.N):
+            for e in set(st_c.moe.e_c[b, i]) & set(st_f.moe.e_c[b, i]):
+                qc = int(np.flatnonzero(st_c.moe.e_c[b, i] == e)[0])
+                qf = int(np.flatnonzero(st_f.moe.e_c[b, i] == e)[0])
+                np.testing.assert_array_equal(st_c.moe.h_c[b, i, qc], st_f.moe.h_c[b, i, qf])
+                same += 1
+    assert same > dims.B * dims.N   # most tokens keep at least one expert
