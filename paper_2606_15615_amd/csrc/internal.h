@@ -144,6 +144,14 @@ int set_error(int code, const std::string& msg);
 int layer_step(moeca_layer* L, const void* x_route, const void* x_ffn, int t, void* out,
                hipStream_t st, const std::function<int()>& between);
 bool layer_full_step(const moeca_layer* L, int t);
+// Bytes of the layer's FFN intermediate (sized for a full step).
+size_t layer_mid_bytes(const moeca_layer* L);
+// Lay the workspace out without the FFN intermediate (moeca_workspace_bytes
+// shrinks by layer_mid_bytes); layer_set_mid then gives its device address,
+// after every moeca_bind_workspace.  Layers that never step concurrently
+// (the blocks of a stack) share one intermediate.
+void layer_keep_mid_outside(moeca_layer* L);
+void layer_set_mid(moeca_layer* L, void* mid);
 const Buffers& layer_buffers(const moeca_layer* L);
 
 // ---- DiT block kernels (block.hip, ffn.hip) -----------------------------

@@ -56,7 +56,9 @@ struct Layout {
   size_t total;
 };
 
-Layout make_layout(const Shape& s) {
+// external_mid: the FFN intermediate lives outside this workspace (the
+// blocks of a stack run one after another and share one).
+Layout make_layout(const Shape& s, bool external_mid = false) {
   const size_t nbr = static_cast<size_t>(s.branches());
   const size_t ntok = static_cast<size_t>(s.tokens());
   const size_t act = s.act_bytes();
@@ -87,7 +89,7 @@ Layout make_layout(const Shape& s) {
   b[R_ENT] = size_t(s.B) * s.E * ((size_t(s.N) + 15) / 16) * 2 * 8;
   b[R_CNT_CH] = size_t(s.B) * ((size_t(s.N) * s.k + 1023) / 1024) * s.E * 4;
   b[R_WIDE] = size_t(s.B) * moeca::kWideWords * 4;
-  b[R_MID] = size_t(s.mid_rows()) * s.d_ff * act;
+  b[R_MID] = external_mid ? 0 : size_t(s.mid_rows()) * s.d_ff * act;
   b[R_H_SH] = size_t(s.S) * ntok * s.d * act;
   Layout L;
   size_t cur = 0;
@@ -119,6 +121,8 @@ struct moeca_layer {
   const void* attn_in = nullptr;
   void* attn_cache = nullptr;
   bool valid = false;
+  bool mid_outside = false;      // the FFN intermediate is not in ws
+  void* external_mid = nullptr;  // its address when mid_outside
   bool last_full = false;
   bool timing = false;
   std::vector<hipEvent_t> events;
@@ -266,7 +270,7 @@ int moeca_bind_workspace(moeca_layer* L, void* dev, size_t bytes) {
   b.rflags = reinterpret_cast<int32_t*>(w + o[R_RFLAGS]);
   b.tiles = reinterpret_cast<int32_t*>(w + o[R_TILES]);
   b.row_dst = reinterpret_cast<int32_t*>(w + o[R_ROW_DST]);
-  b.mid = w + o[R_MID];
+  b.mid = L->mid_outside ? L->external_mid : w + o[R_MID];
   b.h_sh = w + o[R_H_SH];
   L->ws = w;
   L->valid = false;
@@ -294,6 +298,22 @@ namespace moeca {
 
 int set_error(int code, const std::string& msg) { return fail(code, msg); }
 
+size_t layer_mid_bytes(const moeca_layer* L) {
+  const Shape& s = L->shape;
+  return size_t(s.mid_rows()) * s.d_ff * s.act_bytes();
+}
+
+void layer_keep_mid_outside(moeca_layer* L) {
+  L->mid_outside = true;
+  L->layout = make_layout(L->shape, true);
+  L->ws = nullptr;  // the layout changed: bind again
+}
+
+void layer_set_mid(moeca_layer* L, void* mid) {
+  L->external_mid = mid;
+  L->buf.mid = mid;
+}
+
 bool layer_full_step(const moeca_layer* L, int t) {
   const moeca_policy& p = L->pol;
   return p.mode == MOECA_MODE_FULL || !L->valid || (p.refresh_cycle > 0 && t % p.refresh_cycle == 0);
@@ -311,6 +331,8 @@ int layer_step(moeca_layer* L, const void* x_t, const void* x_ffn, int t, void* 
     return fail(MOECA_E_INVAL, "x_t and out must be 16-byte aligned");
   if (L->W_r == nullptr) return fail(MOECA_E_STATE, "weights are not bound");
   if (L->ws == nullptr) return fail(MOECA_E_STATE, "workspace is not bound");
+  if (L->mid_outside && L->external_mid == nullptr)
+    return fail(MOECA_E_STATE, "the FFN intermediate is not bound");
   if (L->shape.S > 0 && L->W_up_sh == nullptr)
     return fail(MOECA_E_STATE, "shared expert weights are not bound");
   const Shape& s = L->shape;

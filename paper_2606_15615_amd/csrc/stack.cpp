@@ -35,7 +35,7 @@ int fail(int code, const std::string& m) { return moeca::set_error(code, m); }
 // Shared regions, in MOECA_SBUF_* order for the public ones.
 enum Region {
   S_MOD, S_H, S_U, S_U2, S_Q, S_KV, S_O, S_X1, S_Y, S_SLIST, S_SOFF,
-  S_IDENT, S_TAB, S_SC, S_EMB, S_H1, S_COUNT
+  S_IDENT, S_TAB, S_SC, S_EMB, S_H1, S_MID, S_COUNT
 };
 
 }  // namespace
@@ -85,6 +85,8 @@ moeca_stack* moeca_stack_create(int n_blocks, int d, int heads, int E, int k, in
       moeca_stack_destroy(S);
       return bad(why);
     }
+    // the blocks step one after another: one FFN intermediate serves all
+    moeca::layer_keep_mid_outside(lay);
     S->layers.push_back(lay);
   }
   S->w.assign(n_blocks, moeca_block_weights{});
@@ -108,6 +110,7 @@ moeca_stack* moeca_stack_create(int n_blocks, int d, int heads, int E, int k, in
   b[S_SC] = size_t(S->B) * d * 8;
   b[S_EMB] = size_t(S->B) * moeca::kFreqDim * 8;
   b[S_H1] = size_t(S->B) * d * 8;
+  b[S_MID] = moeca::layer_mid_bytes(S->layers[0]);
   size_t cur = 0;
   for (int i = 0; i < S_COUNT; ++i) {
     S->off[i] = cur;
@@ -161,6 +164,7 @@ int moeca_stack_bind_workspace(moeca_stack* S, void* dev, size_t bytes) {
     const int rc = moeca_bind_workspace(S->layers[l], w + S->layer_off[l],
                                         moeca_workspace_bytes(S->layers[l]));
     if (rc != MOECA_OK) return rc;
+    moeca::layer_set_mid(S->layers[l], w + S->off[S_MID]);
   }
   moeca::BlockBufs& k = S->k;
   k.B = S->B;
