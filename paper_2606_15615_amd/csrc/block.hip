@@ -174,6 +174,7 @@ struct LnArgs {
   int T, N, d;
   int pending;              // x = x1 + g_m(prev) * y first (kLnAttn)
   int cached;               // kLnAttn on a cache step: also x1 and u from a
+  int routing;              // kLnMlp: u is the routing input (a full step)
 };
 
 __device__ __forceinline__ void ln_stats(const float (&v)[kLnChunks][4], int n4, int lane,
@@ -345,16 +346,24 @@ __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
     }
   }
   ln_stats(v, n4, lane, d, mean, rstd);
-  ln_store(v, n4, lane, mean, rstd, m + 3 * d, m + 4 * d, p.u + o);
+  // a routing input (LN1 of a cache step, LN2 of a full step) takes the
+  // decision-path arithmetic, so that the same input routes the same way on
+  // either kind of step; the rebuilt FFN input of a cache step takes fp32
+  if (MODE == kLnAttn || p.routing)
+    ln_store(v, n4, lane, mean, rstd, m + 3 * d, m + 4 * d, p.u + o);
+  else
+    ln_store_f32(v, n4, lane, mean, rstd, m + 3 * d, m + 4 * d, p.u + o);
 }
 
 // ---------------------------------------------------------------------------
 // synchronised tokens: per-sample ascending lists and the projection tables
 // ---------------------------------------------------------------------------
-// One 1024-thread block.  all: every token (full steps); else sync[t] != 0.
-// Writes slist (flat token ids, by sample), soff[B + 1], ident[t] = t and
-// tab = {0, nS, 0, tiles of nS rows x ntn_q, 0, T, 0, tiles of T rows x ntn_kv}
-// for the projections (128-row tiles).
+// One 1024-thread block per sample.  all: every token (full steps); else
+// sync[t] != 0.  Block b counts the flags of samples 0 .. b-1 (its base in
+// the list), then lists its own tokens in ascending order.  Writes slist
+// (flat token ids, by sample), soff[B + 1], ident[t] = t and, from the last
+// block, tab = {0, nS, 0, tiles of nS rows x ntn_q, 0, T, 0, tiles of T rows
+// x ntn_kv} for the projections (128-row tiles).
 constexpr int kListThreads = 1024;
 
 __global__ __launch_bounds__(kListThreads) void slist_kernel(
@@ -362,43 +371,54 @@ __global__ __launch_bounds__(kListThreads) void slist_kernel(
     int32_t* __restrict__ slist, int32_t* __restrict__ soff, int32_t* __restrict__ ident,
     int32_t* __restrict__ tab) {
   __shared__ int s_wave[kListThreads / kWave];
-  __shared__ int s_base;
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
+  const int b = blockIdx.x;
   const int T = B * N;
-  for (int i = tid; i < T; i += kListThreads) ident[i] = i;
-  if (tid == 0) s_base = 0;
-  __syncthreads();
-  for (int b = 0; b < B; ++b) {
-    if (tid == 0) soff[b] = s_base;
-    for (int i0 = 0; i0 < N; i0 += kListThreads) {
-      const int i = i0 + tid;
-      const bool f = i < N && (all || sync[int64_t(b) * N + i] != 0);
-      const uint64_t bal = __ballot(f);
-      if (lane == 0) s_wave[wv] = __popcll(bal);
-      __syncthreads();
-      int before = s_base;
-      for (int w = 0; w < wv; ++w) before += s_wave[w];
-      if (f) slist[before + __popcll(bal & ((1ull << lane) - 1ull))] = b * N + i;
-      __syncthreads();
-      if (tid == 0) {
-        int tot = 0;
-        for (int w = 0; w < kListThreads / kWave; ++w) tot += s_wave[w];
-        s_base += tot;
-      }
-      __syncthreads();
+  for (int i = tid; i < N; i += kListThreads) ident[b * N + i] = b * N + i;
+  // base: the listed tokens of the samples before this one
+  int base = 0;
+  if (all) {
+    base = b * N;
+  } else {
+    int mine = 0;
+    for (int i = tid; i < b * N; i += kListThreads) mine += sync[i] != 0;
+    // per-thread counts: sum over the block with a wave sum and the wave table
+    const int ws = wave_sum_i32(mine);
+    __syncthreads();
+    if (lane == 0) s_wave[wv] = ws;
+    __syncthreads();
+    for (int w = 0; w < kListThreads / kWave; ++w) base += s_wave[w];
+  }
+  int run = base;
+  for (int i0 = 0; i0 < N; i0 += kListThreads) {
+    const int i = i0 + tid;
+    const bool f = i < N && (all || sync[int64_t(b) * N + i] != 0);
+    const uint64_t bal = __ballot(f);
+    __syncthreads();
+    if (lane == 0) s_wave[wv] = __popcll(bal);
+    __syncthreads();
+    int before = run, tot = 0;
+    for (int w = 0; w < kListThreads / kWave; ++w) {
+      if (w < wv) before += s_wave[w];
+      tot += s_wave[w];
     }
+    if (f) slist[before + __popcll(bal & ((1ull << lane) - 1ull))] = b * N + i;
+    run += tot;
   }
   if (tid == 0) {
-    const int ns = s_base;
-    soff[B] = ns;
-    tab[0] = 0;
-    tab[1] = ns;
-    tab[2] = 0;
-    tab[3] = (ns + kProjTM - 1) / kProjTM * ntn_q;
-    tab[4] = 0;
-    tab[5] = T;
-    tab[6] = 0;
-    tab[7] = (T + kProjTM - 1) / kProjTM * ntn_kv;
+    soff[b] = base;
+    if (b == B - 1) {
+      const int ns = run;
+      soff[B] = ns;
+      tab[0] = 0;
+      tab[1] = ns;
+      tab[2] = 0;
+      tab[3] = (ns + kProjTM - 1) / kProjTM * ntn_q;
+      tab[4] = 0;
+      tab[5] = T;
+      tab[6] = 0;
+      tab[7] = (T + kProjTM - 1) / kProjTM * ntn_kv;
+    }
   }
 }
 
@@ -713,15 +733,16 @@ hipError_t launch_ln_attn(const BlockBufs& k, int T, int N, int d, const float* 
                           const float* mod_prev, const uint16_t* a, bool cached,
                           hipStream_t st) {
   LnArgs p{k.x, k.x1, k.y, a, k.h, k.u, mod, mod_prev, nullptr, nullptr, T, N, d,
-           mod_prev != nullptr ? 1 : 0, cached ? 1 : 0};
+           mod_prev != nullptr ? 1 : 0, cached ? 1 : 0, 0};
   launch_kernel(&ln_kernel<kLnAttn>, dim3((T + kLnWaves - 1) / kLnWaves), dim3(kLnWaves * kWave),
                 0, st, p);
   return hipGetLastError();
 }
 
 hipError_t launch_ln_mlp(const BlockBufs& k, int T, int N, int d, const float* mod,
-                         const uint16_t* a, uint16_t* u_out, hipStream_t st) {
-  LnArgs p{k.x, k.x1, k.y, a, k.h, u_out, mod, nullptr, k.slist, k.soff + k.B, T, N, d, 0, 1};
+                         const uint16_t* a, uint16_t* u_out, bool routing, hipStream_t st) {
+  LnArgs p{k.x, k.x1, k.y, a, k.h, u_out, mod, nullptr, k.slist, k.soff + k.B, T, N, d, 0, 1,
+           routing ? 1 : 0};
   launch_kernel(&ln_kernel<kLnMlp>, dim3((T + kLnWaves - 1) / kLnWaves), dim3(kLnWaves * kWave),
                 0, st, p);
   return hipGetLastError();
@@ -730,7 +751,7 @@ hipError_t launch_ln_mlp(const BlockBufs& k, int T, int N, int d, const float* m
 hipError_t launch_ln_final(const BlockBufs& k, int T, int N, int d, const float* mod,
                            hipStream_t st) {
   LnArgs p{k.x, k.x1, k.y, nullptr, nullptr, nullptr, mod, nullptr, nullptr, nullptr, T, N, d,
-           0, 0};
+           0, 0, 0};
   launch_kernel(&ln_kernel<kLnFinal>, dim3((T + kLnWaves - 1) / kLnWaves),
                 dim3(kLnWaves * kWave), 0, st, p);
   return hipGetLastError();
@@ -739,7 +760,7 @@ hipError_t launch_ln_final(const BlockBufs& k, int T, int N, int d, const float*
 hipError_t launch_slist(const BlockBufs& k, const uint8_t* sync, int N, int d, hipStream_t st) {
   const int ntn_q = (d + kProjTN - 1) / kProjTN;
   const int ntn_kv = (2 * d + kProjTN - 1) / kProjTN;
-  launch_kernel(&slist_kernel, dim3(1), dim3(kListThreads), 0, st, sync, sync == nullptr ? 1 : 0,
+  launch_kernel(&slist_kernel, dim3(k.B), dim3(kListThreads), 0, st, sync, sync == nullptr ? 1 : 0,
                 k.B, N, ntn_q, ntn_kv, k.slist, k.soff, k.ident, k.tab);
   return hipGetLastError();
 }

@@ -202,8 +202,9 @@ hipError_t launch_gemv(const double* in, int B, int K, const GemvBatch& mats, in
 hipError_t launch_ln_attn(const BlockBufs& k, int T, int N, int d, const float* mod,
                           const float* mod_prev, const uint16_t* a, bool cached, hipStream_t st);
 // listed tokens (slist, count soff[B]): x1 = x + g_a a, u_out = LN(x1) mod_m
+// (routing: u_out is a routing input and takes the decision-path arithmetic)
 hipError_t launch_ln_mlp(const BlockBufs& k, int T, int N, int d, const float* mod,
-                         const uint16_t* a, uint16_t* u_out, hipStream_t st);
+                         const uint16_t* a, uint16_t* u_out, bool routing, hipStream_t st);
 // every token: x = x1 + g_m y
 hipError_t launch_ln_final(const BlockBufs& k, int T, int N, int d, const float* mod,
                            hipStream_t st);

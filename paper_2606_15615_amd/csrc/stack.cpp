@@ -255,7 +255,7 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
       if ((r = hip(moeca::launch_proj(k.o, W.W_o, W.b_o, k.tab, k.tab + 2, k.slist, d, d, a, st),
                    "output projection")) != MOECA_OK)
         return r;
-      return hip(moeca::launch_ln_mlp(k, T, N, d, mod, a, u_out, st), "ln2");
+      return hip(moeca::launch_ln_mlp(k, T, N, d, mod, a, u_out, full, st), "ln2");
     };
     if (full) {
       if ((rc = hip(moeca::launch_slist(k, nullptr, N, d, st), "token list")) != MOECA_OK) return rc;
