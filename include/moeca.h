@@ -296,9 +296,10 @@ typedef struct moeca_block_weights {
   const void* W_down; /* [E][d][d_ff]                                          */
 } moeca_block_weights;
 
-/* Create a stack of n_blocks (>= 1) blocks of width d with `heads`
+/* Create a stack of n_blocks (1 to 4096) blocks of width d with `heads`
  * attention heads and the MoE layer (E, k, d_ff, policy) of
- * moeca_layer_create in each.  Host only; NULL on a bad argument. */
+ * moeca_layer_create in each.  Host only; NULL on a bad argument (the
+ * limits above, the layer's, or a non-bf16 policy or n_shared > 0). */
 moeca_stack* moeca_stack_create(int n_blocks, int d, int heads, int E, int k, int d_ff,
                                 const moeca_policy* policy);
 
