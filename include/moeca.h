@@ -328,7 +328,14 @@ int moeca_stack_bind_workspace(moeca_stack* stack, void* dev, size_t bytes);
  *   c [B][d] fp32, device: the conditioning vector of each sample.
  * Running all blocks is one model evaluation; a range lets a caller run
  * the stack in parts.  The step kind (full or cache) is decided per block
- * as in moeca_step.  Asynchronous on the stream; no allocation.
+ * as in moeca_step.  Asynchronous on the stream; no device allocation.
+ * On a cache step each block's k/v projection runs on a second stream
+ * owned by the stack (default priority, made on the first call that is not
+ * inside a graph capture, on the current device), forked from `stream`
+ * after the block's LayerNorm and joined back into it before the block's
+ * attention: work enqueued on `stream` after the call sees the whole step,
+ * and a graph captured from `stream` contains the fork.  Until that stream
+ * exists, or on another device, everything runs on `stream`.
  * MOECA_E_INVAL on a bad range, NULL or misaligned pointers; MOECA_E_STATE
  * if a block's weights or the workspace are unbound. */
 int moeca_stack_step_blocks(moeca_stack* stack, float* x, const float* c, int t, int first,

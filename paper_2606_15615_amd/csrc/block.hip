@@ -361,9 +361,10 @@ __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
 // One 1024-thread block per sample.  all: every token (full steps); else
 // sync[t] != 0.  Block b counts the flags of samples 0 .. b-1 (its base in
 // the list), then lists its own tokens in ascending order.  Writes slist
-// (flat token ids, by sample), soff[B + 1], ident[t] = t and, from the last
-// block, tab = {0, nS, 0, tiles of nS rows x ntn_q, 0, T, 0, tiles of T rows
-// x ntn_kv} for the projections (128-row tiles).
+// (flat token ids, by sample), soff[B + 1] and, from the last block,
+// tab[0..3] = {0, nS, 0, tiles of nS rows x ntn_q} for the projections
+// (128-row tiles); the full-list call also writes ident[t] = t and
+// tab[4..7] = {0, T, 0, tiles of T rows x ntn_kv}.
 constexpr int kListThreads = 1024;
 
 __global__ __launch_bounds__(kListThreads) void slist_kernel(
@@ -374,7 +375,11 @@ __global__ __launch_bounds__(kListThreads) void slist_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int b = blockIdx.x;
   const int T = B * N;
-  for (int i = tid; i < N; i += kListThreads) ident[b * N + i] = b * N + i;
+  // the whole-batch list and table entries never change: written by the
+  // full-list call only, so that a token-list call of a cache step writes
+  // nothing that a k/v projection running beside it reads
+  if (all)
+    for (int i = tid; i < N; i += kListThreads) ident[b * N + i] = b * N + i;
   // base: the listed tokens of the samples before this one
   int base = 0;
   if (all) {
@@ -414,10 +419,12 @@ __global__ __launch_bounds__(kListThreads) void slist_kernel(
       tab[1] = ns;
       tab[2] = 0;
       tab[3] = (ns + kProjTM - 1) / kProjTM * ntn_q;
-      tab[4] = 0;
-      tab[5] = T;
-      tab[6] = 0;
-      tab[7] = (T + kProjTM - 1) / kProjTM * ntn_kv;
+      if (all) {
+        tab[4] = 0;
+        tab[5] = T;
+        tab[6] = 0;
+        tab[7] = (T + kProjTM - 1) / kProjTM * ntn_kv;
+      }
     }
   }
 }

@@ -10,8 +10,11 @@
 // list from the layer's sync flags, their q projection, attention, output
 // projection (into the cached a) and LN2 of those tokens (the FFN input).
 // The gated residual x' = x1 + g_m y is folded into the next block's LN1 and,
-// after the last block of a run, applied by a final pass.  Nothing here
-// waits for the device or allocates device memory.
+// after the last block of a run, applied by a final pass.  On a cache step
+// the k/v projection runs on a second stream that the stack makes on its
+// first step outside a graph capture, forked after LN1 and joined before
+// the attention.  Nothing here waits for the device or allocates device
+// memory.
 #include <hip/hip_runtime.h>
 
 #include <algorithm>
@@ -52,7 +55,51 @@ struct moeca_stack {
   size_t total = 0;
   char* ws = nullptr;
   moeca::BlockBufs k{};
+  // a second stream for the k/v projection of cache steps, made on the
+  // first step that is not being captured, on that step's device
+  hipStream_t side = nullptr;
+  hipEvent_t ev_fork = nullptr, ev_kv = nullptr;
+  int side_dev = -1;
 };
+
+namespace {
+
+void release_side(moeca_stack* S) {
+  if (S->ev_kv) (void)hipEventDestroy(S->ev_kv);
+  if (S->ev_fork) (void)hipEventDestroy(S->ev_fork);
+  if (S->side) (void)hipStreamDestroy(S->side);
+  S->side = nullptr;
+  S->ev_fork = S->ev_kv = nullptr;
+  S->side_dev = -1;
+}
+
+// True when the k/v projection of a cache step may run on the side stream:
+// the side stream exists (or can be made now, outside a capture) on the
+// current device.  Any failure leaves the single-stream order.
+bool side_ready(moeca_stack* S, hipStream_t st) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return false;
+  }
+  if (S->side != nullptr) return S->side_dev == dev;
+  hipStreamCaptureStatus cs = hipStreamCaptureStatusNone;
+  if (hipStreamIsCapturing(st, &cs) != hipSuccess || cs != hipStreamCaptureStatusNone) {
+    (void)hipGetLastError();
+    return false;
+  }
+  if (hipStreamCreateWithFlags(&S->side, hipStreamNonBlocking) != hipSuccess ||
+      hipEventCreateWithFlags(&S->ev_fork, hipEventDisableTiming) != hipSuccess ||
+      hipEventCreateWithFlags(&S->ev_kv, hipEventDisableTiming) != hipSuccess) {
+    (void)hipGetLastError();
+    release_side(S);
+    return false;
+  }
+  S->side_dev = dev;
+  return true;
+}
+
+}  // namespace
 
 extern "C" {
 
@@ -130,6 +177,7 @@ moeca_stack* moeca_stack_create(int n_blocks, int d, int heads, int E, int k, in
 void moeca_stack_destroy(moeca_stack* S) {
   if (S == nullptr) return;
   for (moeca_layer* l : S->layers) moeca_layer_destroy(l);
+  release_side(S);
   delete S;
 }
 
@@ -227,6 +275,7 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
       return rc;
   }
   if ((rc = hip(moeca::launch_slist(k, nullptr, N, d, st), "token list")) != MOECA_OK) return rc;
+  const bool overlap = side_ready(S, st);
 
   for (int l = first; l < first + count; ++l) {
     const moeca_block_weights& W = S->w[l];
@@ -241,16 +290,32 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
     if ((rc = hip(moeca::launch_ln_attn(k, T, N, d, mod, mod_prev, a, !full, st), "ln1")) !=
         MOECA_OK)
       return rc;
-    // keys and values of every token (tables of the whole batch)
+    // keys and values of every token (tables of the whole batch).  On a
+    // cache step they go to the side stream: the layer's decision, the token
+    // list and the q projection (none reads k/v, none writes what the
+    // projection reads) fill the CUs its last partial round of tiles leaves
+    // idle; the attention waits for it.
+    const bool fork = !full && overlap;
+    if (fork) {
+      if ((rc = hip(hipEventRecord(S->ev_fork, st), "fork")) != MOECA_OK ||
+          (rc = hip(hipStreamWaitEvent(S->side, S->ev_fork, 0), "fork")) != MOECA_OK)
+        return rc;
+    }
     if ((rc = hip(moeca::launch_proj(k.h, Wkv, W.b_qkv + d, k.tab + 4, k.tab + 6, k.ident, d,
-                                     2 * d, k.kv, st), "kv projection")) != MOECA_OK)
+                                     2 * d, k.kv, fork ? S->side : st), "kv projection")) !=
+        MOECA_OK)
       return rc;
+    if (fork && (rc = hip(hipEventRecord(S->ev_kv, S->side), "fork")) != MOECA_OK) return rc;
+    auto join = [&]() -> int {
+      return fork ? hip(hipStreamWaitEvent(st, S->ev_kv, 0), "join") : MOECA_OK;
+    };
     // queries, attention, output projection and LN2 of the listed tokens
     auto refresh = [&](uint16_t* u_out) -> int {
       int r;
       if ((r = hip(moeca::launch_proj(k.h, Wq, W.b_qkv, k.tab, k.tab + 2, k.slist, d, d, k.q, st),
                    "q projection")) != MOECA_OK)
         return r;
+      if ((r = join()) != MOECA_OK) return r;
       if ((r = hip(moeca::launch_attention(k, N, H, dh, st), "attention")) != MOECA_OK) return r;
       if ((r = hip(moeca::launch_proj(k.o, W.W_o, W.b_o, k.tab, k.tab + 2, k.slist, d, d, a, st),
                    "output projection")) != MOECA_OK)
@@ -268,7 +333,10 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
         return r != MOECA_OK ? r : refresh(k.u2);
       });
     }
+    // the fork is joined on every path (a capture must end with it joined)
+    const int rj = join();
     if (rc != MOECA_OK) return rc;
+    if (rj != MOECA_OK) return rj;
   }
   const float* mod_last = mod_all + size_t(first + count - 1) * mod_stride;
   return hip(moeca::launch_ln_final(k, T, N, d, mod_last, st), "residual");
