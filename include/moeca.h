@@ -329,8 +329,7 @@ int moeca_stack_bind_workspace(moeca_stack* stack, void* dev, size_t bytes);
  * Running all blocks is one model evaluation; a range lets a caller run
  * the stack in parts.  The step kind (full or cache) is decided per block
  * as in moeca_step.  Asynchronous on the stream; no device allocation.
- * On a cache step each block's k/v projection runs on a second stream
- * owned by the stack (default priority, made on the first call that is not
+ * Each block's k/v projection runs on a second stream owned by the stack (default priority, made on the first call that is not
  * inside a graph capture, on the current device), forked from `stream`
  * after the block's LayerNorm and joined back into it before the block's
  * attention: work enqueued on `stream` after the call sees the whole step,

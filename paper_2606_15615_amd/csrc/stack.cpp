@@ -10,10 +10,10 @@
 // list from the layer's sync flags, their q projection, attention, output
 // projection (into the cached a) and LN2 of those tokens (the FFN input).
 // The gated residual x' = x1 + g_m y is folded into the next block's LN1 and,
-// after the last block of a run, applied by a final pass.  On a cache step
-// the k/v projection runs on a second stream that the stack makes on its
-// first step outside a graph capture, forked after LN1 and joined before
-// the attention.  Nothing here waits for the device or allocates device
+// after the last block of a run, applied by a final pass.  The k/v
+// projection runs on a second stream that the stack makes on its first step
+// outside a graph capture, forked after LN1 (and, on a full step, the token
+// list) and joined before the attention.  Nothing here waits for the device or allocates device
 // memory.
 #include <hip/hip_runtime.h>
 
@@ -290,12 +290,17 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
     if ((rc = hip(moeca::launch_ln_attn(k, T, N, d, mod, mod_prev, a, !full, st), "ln1")) !=
         MOECA_OK)
       return rc;
-    // keys and values of every token (tables of the whole batch).  On a
-    // cache step they go to the side stream: the layer's decision, the token
-    // list and the q projection (none reads k/v, none writes what the
-    // projection reads) fill the CUs its last partial round of tiles leaves
-    // idle; the attention waits for it.
-    const bool fork = !full && overlap;
+    // a full step lists every token first (the list call also rewrites the
+    // whole-batch table that the k/v projection reads)
+    if (full &&
+        (rc = hip(moeca::launch_slist(k, nullptr, N, d, st), "token list")) != MOECA_OK)
+      return rc;
+    // keys and values of every token (tables of the whole batch), on the
+    // side stream: what runs beside them on `stream` (a cache step's layer
+    // decision and token list, the q projection of either step) reads no
+    // k/v and writes nothing the projection reads, and fills the CUs its
+    // last partial round of tiles leaves idle; the attention waits for it.
+    const bool fork = overlap;
     if (fork) {
       if ((rc = hip(hipEventRecord(S->ev_fork, st), "fork")) != MOECA_OK ||
           (rc = hip(hipStreamWaitEvent(S->side, S->ev_fork, 0), "fork")) != MOECA_OK)
@@ -323,9 +328,8 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
       return hip(moeca::launch_ln_mlp(k, T, N, d, mod, a, u_out, full, st), "ln2");
     };
     if (full) {
-      if ((rc = hip(moeca::launch_slist(k, nullptr, N, d, st), "token list")) != MOECA_OK) return rc;
-      if ((rc = refresh(k.u)) != MOECA_OK) return rc;
-      rc = moeca::layer_step(lay, k.u, k.u, t, k.y, st, {});
+      rc = refresh(k.u);
+      if (rc == MOECA_OK) rc = moeca::layer_step(lay, k.u, k.u, t, k.y, st, {});
     } else {
       const uint8_t* sync = moeca::layer_buffers(lay).sync;
       rc = moeca::layer_step(lay, k.u, k.u2, t, k.y, st, [&]() -> int {
