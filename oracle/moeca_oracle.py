@@ -509,7 +509,7 @@ def combine(w_t: np.ndarray, hhat: np.ndarray, dtype: str, shared=()) -> np.ndar
 # ---------------------------------------------------------------------------
 def step(dims: Dims, policy: Policy, W: Weights, state: State, x_t: np.ndarray,
          t: int, attn_in: np.ndarray | None = None, tokens=None,
-         x_ffn: np.ndarray | None = None):
+         x_ffn: np.ndarray | None = None, forced: dict | None = None):
     """One layer step at sampling step ``t``.
 
     ``x_ffn`` (same shape and dtype as ``x_t``), when given, is the input of
@@ -522,6 +522,13 @@ def step(dims: Dims, policy: Policy, W: Weights, state: State, x_t: np.ndarray,
     tokens (the decision path always runs over the whole batch); outputs and
     rows of other tokens are then left unset (``rec['evaluated']``).
 
+    ``forced`` (test use only) replaces one rounded decision input by a value
+    computed elsewhere and runs every later step of the method on it
+    unchanged: ``"logits"`` (T, E) fp32 router logits, ``"Hbar"`` (B, E)
+    fp32 normalised entropies.  Where an fp64 result lies at an fp32
+    rounding tie either rounding is correct, so a checker adopts the other
+    side's value there and still compares everything that follows.
+
     Returns ``(out, new_state, rec)``: ``out`` (B, N, d) stored dtype;
     ``rec`` a dict of every intermediate of the step.
     """
@@ -533,8 +540,11 @@ def step(dims: Dims, policy: Policy, W: Weights, state: State, x_t: np.ndarray,
     rec = {"full": full}
 
     # 2. router
+    forced = forced or {}
     x64 = to_f64(x_t, dt).reshape(T, d)
     l64, logits = router_logits(x64, W.W_r64, W.b_r)
+    if "logits" in forced:
+        logits = np.asarray(forced["logits"], dtype=F32).reshape(T, E)
     e_flat, w_flat = route(logits, k, policy.norm_topk)
     e_t = e_flat.reshape(B, N, k)
     w_t = w_flat.reshape(B, N, k)
@@ -545,6 +555,8 @@ def step(dims: Dims, policy: Policy, W: Weights, state: State, x_t: np.ndarray,
         # 3-4. statistic and thresholds
         new.C = ema_update(state.C, e_t, policy.beta)
         Hbar = normalized_entropy(new.C)
+        if "Hbar" in forced:
+            Hbar = np.asarray(forced["Hbar"], dtype=F32).reshape(B, E)
         tau = adaptive_threshold(Hbar, policy.tau0, policy.alpha)
         rec.update(C=new.C, Hbar=Hbar, tau=tau)
 

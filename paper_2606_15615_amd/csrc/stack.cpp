@@ -306,14 +306,22 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
           (rc = hip(hipStreamWaitEvent(S->side, S->ev_fork, 0), "fork")) != MOECA_OK)
         return rc;
     }
-    if ((rc = hip(moeca::launch_proj(k.h, Wkv, W.b_qkv + d, k.tab + 4, k.tab + 6, k.ident, d,
-                                     2 * d, k.kv, fork ? S->side : st), "kv projection")) !=
-        MOECA_OK)
-      return rc;
-    if (fork && (rc = hip(hipEventRecord(S->ev_kv, S->side), "fork")) != MOECA_OK) return rc;
+    rc = hip(moeca::launch_proj(k.h, Wkv, W.b_qkv + d, k.tab + 4, k.tab + 6, k.ident, d, 2 * d,
+                                k.kv, fork ? S->side : st),
+             "kv projection");
+    if (fork) {
+      // the side stream's end is recorded even after a failed launch, so
+      // that the main stream joins it on every path below
+      const int rr = hip(hipEventRecord(S->ev_kv, S->side), "fork");
+      if (rc == MOECA_OK) rc = rr;
+    }
     auto join = [&]() -> int {
       return fork ? hip(hipStreamWaitEvent(st, S->ev_kv, 0), "join") : MOECA_OK;
     };
+    if (rc != MOECA_OK) {
+      join();
+      return rc;
+    }
     // queries, attention, output projection and LN2 of the listed tokens
     auto refresh = [&](uint16_t* u_out) -> int {
       int r;

@@ -15,7 +15,7 @@ pytestmark = pytest.mark.gpu
 from oracle import moeca_oracle as O
 from paper_2606_15615_amd.synth import LayerShape, WORKLOADS
 
-from gpu_harness import Setup, check_step, run_forced, say, rel_err
+from gpu_harness import Setup, check_step, oracle_rerun, run_forced, say, rel_err
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -124,9 +124,10 @@ def test_nothing_recomputed_is_bit_exact(mode):
     out0, st1, _ = O.step(S.dims, S.pol, S.W, st0, S.xs[0], 0, attn_in=S.attn[0])
     S.import_state(st1)
     out_g = S.gpu_step(S.xs[0], 1, S.attn[0])
-    out_o, st2, rec = O.step(S.dims, S.pol, S.W, st1, S.xs[0], 1, attn_in=S.attn[0])
+    rerun = oracle_rerun(S, st1, S.xs[0], 1, S.attn[0])
+    out_o, st2, rec = rerun(None)
     assert rec["mask"].sum() == 0
-    check_step(S, 1, rec, out_o, st1, st2, out_g, label="reuse-all")
+    check_step(S, 1, rec, out_o, st1, st2, out_g, label="reuse-all", rerun=rerun)
     assert np.array_equal(out_g, out_o)
     assert np.array_equal(out_o, out0)
 
@@ -146,11 +147,12 @@ def test_all_branches_tied(N, E, k):
     _, st1, _ = O.step(S.dims, S.pol, S.W, st0, x, 0, attn_in=S.attn[0])
     S.import_state(st1)
     out_g = S.gpu_step(x, 1, S.attn[0])
-    out_o, st2, rec = O.step(S.dims, S.pol, S.W, st1, x, 1, attn_in=S.attn[0])
+    rerun = oracle_rerun(S, st1, x, 1, S.attn[0])
+    out_o, st2, rec = rerun(None)
     assert rec["matched"].all()
     assert all(len(np.unique(rec["m"][b])) <= k for b in range(2))  # one margin per slot
     assert 0 < rec["mask"].sum() < rec["mask"].size
-    check_step(S, 1, rec, out_o, st1, st2, out_g, label=f"ties N={N} k={k}")
+    check_step(S, 1, rec, out_o, st1, st2, out_g, label=f"ties N={N} k={k}", rerun=rerun)
 
 
 def test_reset_mid_trajectory():
@@ -160,10 +162,11 @@ def test_reset_mid_trajectory():
     assert S.layer.stats().full_step == 0
     S.layer.reset()
     out_g = S.gpu_step(S.xs[3], 3, S.attn[3])
-    out_o, st_new, rec = O.step(S.dims, S.pol, S.W, O.State(S.dims, True), S.xs[3], 3,
-                                attn_in=S.attn[3])
+    st0 = O.State(S.dims, True)
+    rerun = oracle_rerun(S, st0, S.xs[3], 3, S.attn[3])
+    out_o, st_new, rec = rerun(None)
     assert rec["full"] and S.layer.stats().full_step == 1
-    check_step(S, 3, rec, out_o, O.State(S.dims, True), st_new, out_g, label="after reset")
+    check_step(S, 3, rec, out_o, st0, st_new, out_g, label="after reset", rerun=rerun)
 
 
 def test_determinism():
@@ -201,34 +204,61 @@ def test_xl256_trajectory(mode):
 
 
 # ---------------------------------------------------------------------------
-# The same layer at 1024 tokens x 8 (the benchmarked shape): decisions over
-# the whole batch, outputs and rows on sampled tokens.
+# Full-size layers at their benchmarked shapes: decisions over the whole
+# batch, outputs and rows on sampled tokens computed one by one by the
+# oracle.  Step 0 is a full-computation step (Sec. 4.1: the cache is
+# invalid), the later ones consecutive cache steps, each forced from the
+# oracle's state.  The rows of tokens the oracle does not evaluate are given
+# synthetic values and their norms after every step.
 # ---------------------------------------------------------------------------
-@pytest.mark.parametrize("mode", ["ratio", "threshold"])
-def test_xl1024_sampled(mode):
-    shape = WORKLOADS["xl1024"]
-    S = Setup(shape, mode=mode, seed=11, T=3, ratio=0.3, refresh_cycle=0)
-    dims = S.dims
-    rng = np.random.default_rng(12)
-    sample = np.sort(rng.choice(shape.tokens, size=48, replace=False))
+def sampled_tokens(shape, n, seed):
+    rng = np.random.default_rng(seed)
+    sample = np.sort(rng.choice(shape.tokens, size=n, replace=False))
     ev = np.zeros(shape.tokens, bool)
     ev[sample] = True
-    ev = ev.reshape(shape.B, shape.N)
-    # a valid cache: routing and statistic from the oracle's first two steps,
-    # rows of unsampled tokens filled with synthetic values and their norms
-    st = O.State(dims, attention=True)
-    for t in range(2):
-        _, st, _ = O.step(dims, S.pol, S.W, st, S.xs[t], t, attn_in=S.attn[t], tokens=sample)
-        fill = ~ev
-        rows = S.sy.rows((int(fill.sum()), shape.k, shape.d), scale=0.05)
-        st.h_c[fill] = rows
-        st.n_c[fill] = O.row_norms(rows, shape.dtype)
-    S.import_state(st)
-    out_g = S.gpu_step(S.xs[2], 2, S.attn[2])
-    out_o, st_new, rec = O.step(dims, S.pol, S.W, st, S.xs[2], 2, attn_in=S.attn[2],
-                                tokens=sample)
-    info = check_step(S, 2, rec, out_o, st, st_new, out_g, evaluated=ev, label=f"xl1024 {mode}")
-    say(f"  xl1024 {mode}: {info}")
+    return sample, ev.reshape(shape.B, shape.N)
+
+
+def fill_unsampled(S, st, ev):
+    fill = ~ev
+    rows = S.sy.rows((int(fill.sum()), S.shape.k, S.shape.d), scale=0.05)
+    st.h_c[fill] = rows
+    st.n_c[fill] = O.row_norms(rows, S.shape.dtype)
+
+
+def run_sampled(S, T, sample, ev, label):
+    st = O.State(S.dims, attention=S.attention)
+    infos = []
+    for t in range(T):
+        say(f"  [{label}] step {t}")
+        S.import_state(st)
+        a = None if S.attn is None else S.attn[t]
+        out_g = S.gpu_step(S.xs[t], t, a)
+        rerun = oracle_rerun(S, st, S.xs[t], t, a, tokens=sample)
+        out_o, st_new, rec = rerun(None)
+        assert rec["full"] == (t == 0)
+        info = check_step(S, t, rec, out_o, st, st_new, out_g, evaluated=ev,
+                          label=f"{label} t={t}", rerun=rerun)
+        st = info.pop("state")
+        fill_unsampled(S, st, ev)
+        infos.append(info)
+        say(f"  {label} t={t}: {info}")
+    return infos
+
+
+@pytest.mark.timeout(600)
+@pytest.mark.parametrize("mode", ["ratio", "threshold"])
+def test_xl1024_sampled(mode):
+    """The benchmarked layer (d=1152, 16 experts, top-2, 4608 hidden, 1024
+    tokens x 8, 30 % refresh): a refresh step over all 16384 branches (about
+    1024 GEMM rows per expert), then three consecutive cache steps."""
+    shape = WORKLOADS["xl1024"]
+    S = Setup(shape, mode=mode, seed=11, T=4, ratio=0.3, refresh_cycle=0)
+    sample, ev = sampled_tokens(shape, 48, 12)
+    infos = run_sampled(S, 4, sample, ev, f"xl1024 {mode}")
+    if mode == "ratio":
+        for info in infos[1:]:
+            assert abs(info["recompute_frac"] - 0.3) < 0.02
 
 
 # ---------------------------------------------------------------------------
@@ -246,6 +276,24 @@ def test_skewed_ratio_sweep(ratio):
               bias="zipf", drift="bimodal")
     infos = run_forced(S, 4, label=f"skewed rho={ratio}")
     say(f"  skewed rho={ratio}: {infos}")
+
+
+@pytest.mark.timeout(900)
+def test_skewed_full_size_sampled():
+    """The skewed-routing layer at its benchmarked size (d=3072, 32 experts,
+    top-2, 8192 hidden, 4096 tokens x 2, Zipf(1.2) router prior, bimodal
+    drift) at refresh ratios 0.1, 0.5 and 0.9: a refresh step and two cache
+    steps each, outputs and rows on sampled tokens."""
+    base = Setup(WORKLOADS["skewed"], mode="ratio", seed=22, T=3, ratio=0.1, refresh_cycle=0,
+                 bias="zipf", drift="bimodal")
+    sample, ev = sampled_tokens(base.shape, 24, 23)
+    for ratio in (0.1, 0.5, 0.9):
+        S = base if ratio == 0.1 else base.with_policy(ratio=ratio)
+        infos = run_sampled(S, 3, sample, ev, f"skewed full rho={ratio}")
+        for info in infos[1:]:
+            assert info["recompute_frac"] >= ratio - 0.02
+        if S is not base:
+            S.release()
 
 
 def test_skewed_threshold():
@@ -318,35 +366,64 @@ def test_fine_nothing_recomputed_still_runs_shared_experts():
     _, st1, _ = O.step(S.dims, S.pol, S.W, st0, S.xs[0], 0, attn_in=S.attn[0])
     S.import_state(st1)
     out_g = S.gpu_step(S.xs[1], 1, S.attn[1])
-    out_o, st2, rec = O.step(S.dims, S.pol, S.W, st1, S.xs[1], 1, attn_in=S.attn[1])
+    rerun = oracle_rerun(S, st1, S.xs[1], 1, S.attn[1])
+    out_o, st2, rec = rerun(None)
     assert rec["mask"].sum() == (~rec["matched"]).sum()
-    info = check_step(S, 1, rec, out_o, st1, st2, out_g, label="fine reuse")
+    info = check_step(S, 1, rec, out_o, st1, st2, out_g, label="fine reuse", rerun=rerun)
     say(f"  fine reuse: {info}")
 
 
 @pytest.mark.timeout(600)
 def test_fine_sampled():
     """The benchmarked fine-grained layer (d=2048, 64 experts, top-8, 1408
-    hidden SwiGLU, 2 shared experts, 4096 tokens x 4, 25 % refresh):
-    decisions over the whole batch, outputs and rows on sampled tokens."""
+    hidden SwiGLU, 2 shared experts, 4096 tokens x 4, 25 % refresh): a
+    refresh step and two cache steps, outputs and rows on sampled tokens."""
     shape = WORKLOADS["fine"]
     S = Setup(shape, mode="ratio", seed=20, T=3, ratio=0.25, refresh_cycle=0, norm_topk=False)
-    dims = S.dims
-    rng = np.random.default_rng(21)
-    sample = np.sort(rng.choice(shape.tokens, size=24, replace=False))
-    ev = np.zeros(shape.tokens, bool)
-    ev[sample] = True
-    ev = ev.reshape(shape.B, shape.N)
-    st = O.State(dims, attention=True)
-    for t in range(2):
-        _, st, _ = O.step(dims, S.pol, S.W, st, S.xs[t], t, attn_in=S.attn[t], tokens=sample)
-        fill = ~ev
-        rows = S.sy.rows((int(fill.sum()), shape.k, shape.d), scale=0.05)
-        st.h_c[fill] = rows
-        st.n_c[fill] = O.row_norms(rows, shape.dtype)
+    sample, ev = sampled_tokens(shape, 24, 21)
+    run_sampled(S, 3, sample, ev, "fine sampled")
+
+
+# ---------------------------------------------------------------------------
+# Steps replayed from a HIP graph (the launch mode of the benchmark) against
+# the oracle: one cache step captured once, then replayed from successive
+# oracle states and inputs, with eager work between the replays.
+# ---------------------------------------------------------------------------
+@pytest.mark.parametrize("wl,mode", [("ragged", "ratio"), ("ragged", "threshold"),
+                                     ("xl1024", "ratio")])
+def test_graph_replayed_steps(wl, mode):
+    import torch
+    from paper_2606_15615_amd.layer import device_to_np, np_to_device
+    shape = RAGGED if wl == "ragged" else WORKLOADS["xl1024"]
+    T = 5
+    S = Setup(shape, mode=mode, seed=24, T=T, ratio=0.3, refresh_cycle=0)
+    sampled = wl != "ragged"
+    sample, ev = sampled_tokens(shape, 32, 25) if sampled else (None, None)
+    st = O.State(S.dims, attention=True)
+    _, st, _ = O.step(S.dims, S.pol, S.W, st, S.xs[0], 0, attn_in=S.attn[0], tokens=sample)
+    if sampled:
+        fill_unsampled(S, st, ev)
+    L = S.layer
+    x_static = np_to_device(S.xs[1], L.device)
     S.import_state(st)
-    out_g = S.gpu_step(S.xs[2], 2, S.attn[2])
-    out_o, st_new, rec = O.step(dims, S.pol, S.W, st, S.xs[2], 2, attn_in=S.attn[2],
-                                tokens=sample)
-    info = check_step(S, 2, rec, out_o, st, st_new, out_g, evaluated=ev, label="fine sampled")
-    say(f"  fine sampled: {info}")
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        L.step(x_static, 1, S.out)
+    for t in range(1, T):
+        say(f"  [graph {wl} {mode}] replay for step {t}")
+        S.import_state(st)
+        S.attn_in.copy_(np_to_device(S.attn[t], L.device))
+        x_static.copy_(np_to_device(S.xs[t], L.device))
+        S.out.zero_()
+        g.replay()
+        torch.cuda.synchronize()
+        out_g = device_to_np(S.out, S.act_np)
+        rerun = oracle_rerun(S, st, S.xs[t], t, S.attn[t], tokens=sample)
+        out_o, st_new, rec = rerun(None)
+        assert not rec["full"]
+        info = check_step(S, t, rec, out_o, st, st_new, out_g, evaluated=ev,
+                          label=f"graph {wl} {mode} t={t}", rerun=rerun)
+        st = info.pop("state")
+        if sampled:
+            fill_unsampled(S, st, ev)
+        say(f"  graph {wl} {mode} t={t}: {info}")

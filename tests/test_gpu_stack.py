@@ -185,8 +185,10 @@ def check_block(SS: StackSetup, l: int, t: int, st_o: D.BlockState, x: np.ndarra
     mrec = rec["moe"]
     if not full:
         view = _LayerView(lay, dims.layer())
+        rerun = lambda forced: O.step(dims.layer(), SS.pol, W.moe, st_o.moe, rec["u_route"], t,
+                                      x_ffn=rec["u"], forced=forced)
         check_step(view, t, mrec, rec["y"], st_o.moe, st_new.moe, g_y,
-                   uncached=SS.pol.mode == O.MODE_FULL, label=tag)
+                   uncached=SS.pol.mode == O.MODE_FULL, label=tag, rerun=rerun)
     else:
         lg = lay.read("logits")
         err = float(np.abs(lg.astype(np.float64) - mrec["logits64"]).max())

@@ -109,7 +109,7 @@ def _torch_expert(X, up, dn, act):
         # the up-projection rows alternate gate / up
         hid = F.silu(F.linear(X, up[0::2])) * F.linear(X, up[1::2])
     else:
-        hid = F.gelu(F.linear(X, up), approximate="tanh")
+        hid = F.gelu(F.linear(X, up), approximate="none" if act == "gelu_erf" else "tanh")
     return F.linear(hid, dn)
 
 
@@ -798,3 +798,154 @@ def test_brute_force_cache_norms():
         for s in range(2):
             v = math.sqrt(math.fsum(float(a) ** 2 for a in st.h_c[0, i, s]))
             assert st.n_c[0, i, s] == F32(v)
+
+
+# ---------------------------------------------------------------------------
+# decision rules at exact equality, with hand-derived expectations
+# ---------------------------------------------------------------------------
+def _hand_layer(d, E, k, N, W_r_rows, tokens_x):
+    """fp32 layer whose router rows and inputs are given exactly (no draws):
+    expert weights are small integers, so only the decision path matters."""
+    dims = O.Dims(d=d, E=E, k=k, d_ff=4, B=1, N=N, dtype="fp32")
+    W_r = np.array(W_r_rows, F32)
+    W_up = np.ones((E, 4, d), F32)
+    W_down = np.ones((E, d, 4), F32)
+    W = O.Weights(dims, W_r, None, W_up, W_down)
+    x = np.array(tokens_x, F32).reshape(1, N, d)
+    return dims, W, x
+
+
+def _valid_state(dims, e_c, w_c, n_c):
+    st = O.State(dims, attention=False)
+    st.e_c[...] = np.array(e_c, np.int32).reshape(st.e_c.shape)
+    st.w_c[...] = np.array(w_c, F32).reshape(st.w_c.shape)
+    st.n_c[...] = np.array(n_c, F32).reshape(st.n_c.shape)
+    st.h_c[...] = F32(0.25)
+    st.valid = True
+    return st
+
+
+def test_threshold_rule_is_strict_at_equality():
+    """Sec. 4.2 threshold rule: a matched branch is recomputed iff s > tau.
+
+    Hand values.  Router rows (1, 0), (1, 0), (0, 1).  Token 0 has x = (1, 0):
+    logits (1, 1, 0), experts (0, 1) (equal logits: lower id first), gate
+    weights exp(0) / (exp(0) + exp(0)) = (1/2, 1/2) exactly.  Token 1 has
+    x = (0, 1): logits (0, 0, 1), experts (2, 0), weights
+    (1 / (1 + e^-1), e^-1 / (1 + e^-1)) = (0.731..., 0.268...).
+    With lambda1 = lambda2 = 0 the score is s = w; with alpha = 0 the
+    threshold is tau0 whatever the entropy.  tau0 = 1/2: token 0 has
+    s == tau exactly on both branches, so both are reused; token 1 recomputes
+    only its first branch.  tau0 one fp32 step below 1/2: token 0 recomputes
+    both."""
+    dims, W, x = _hand_layer(2, 3, 2, 2, [[1, 0], [1, 0], [0, 1]], [[1, 0], [0, 1]])
+    st = _valid_state(dims, [[0, 1], [2, 0]], [[0.3, 0.9], [0.1, 0.2]], [[1, 2], [3, 4]])
+    base = dict(mode=O.MODE_THRESHOLD, alpha=0.0, lambda1=0.0, lambda2=0.0, refresh_cycle=0)
+    _, _, rec = O.step(dims, O.Policy(tau0=0.5, **base), W, st, x, 1)
+    assert rec["e_t"][0].tolist() == [[0, 1], [2, 0]]
+    assert rec["w_t"][0, 0].tolist() == [0.5, 0.5]
+    e1 = math.exp(-1.0)
+    assert rec["w_t"][0, 1].tolist() == [float(F32(1 / (1 + e1))), float(F32(e1 / (1 + e1)))]
+    assert rec["tau"].tolist() == [[0.5, 0.5, 0.5]]
+    assert rec["matched"].all()
+    assert rec["m"][0, 0].tolist() == [0.0, 0.0]
+    assert rec["mask"][0].tolist() == [[False, False], [True, False]]
+    assert rec["S"][0].tolist() == [False, True]
+    below = float(np.nextafter(F32(0.5), F32(0.0)))
+    _, _, rec = O.step(dims, O.Policy(tau0=below, **base), W, st, x, 1)
+    assert rec["mask"][0].tolist() == [[True, True], [True, False]]
+
+
+@pytest.mark.parametrize("ratio,chosen", [(0.25, [0, 1]), (0.375, [0, 1, 2]),
+                                          (0.75, [0, 1, 2, 3, 4, 5])])
+def test_ratio_budget_ties_take_lowest_flat_ids(ratio, chosen):
+    """Ratio mode (reading R-14 with the tie rule R-16): among equal margins
+    at the budget boundary the lower flat ids (b N + i) k + p win.
+
+    Hand values.  Two experts with equal router rows, every token x = (1, 0):
+    logits (1, 1), experts (0, 1), weights (1/2, 1/2).  The cache holds the
+    same experts with w_c = 1/2 and equal norms, so Delta = 0 and o = 1/2 on
+    every branch and every margin is equal.  N = 4, k = 2: 8 branches and
+    K_b = floor(8 rho + 1/2) = 2, 3, 6."""
+    dims, W, x = _hand_layer(2, 2, 2, 4, [[1, 0], [1, 0]], [[1, 0]] * 4)
+    st = _valid_state(dims, [[0, 1]] * 4, [[0.5, 0.5]] * 4, [[1, 1]] * 4)
+    pol = O.Policy(mode=O.MODE_RATIO, ratio=ratio, refresh_cycle=0)
+    _, _, rec = O.step(dims, pol, W, st, x, 1)
+    assert rec["matched"].all()
+    assert len(set(rec["m"].reshape(-1).tolist())) == 1
+    want = np.zeros(8, bool)
+    want[chosen] = True
+    assert rec["mask"].reshape(-1).tolist() == want.tolist()
+
+
+def test_ratio_budget_boundary_ties_behind_a_larger_margin():
+    """The same layer with one token's weights changed so that its two
+    branches carry larger margins: they come first; the remaining budget
+    goes to the lowest flat ids among the tied rest.  Token 2 is routed with
+    x = (2, 0) to experts (0, 1) again (equal logits 2, 2: weights 1/2) but
+    its cache has w_c = 0 on both slots, so Delta = 1/2 and its margins
+    exceed the others' by 1/2.  K_b = 3: flat ids 4, 5 (token 2), then 0."""
+    dims, W, x = _hand_layer(2, 2, 2, 4, [[1, 0], [1, 0]], [[1, 0], [1, 0], [2, 0], [1, 0]])
+    st = _valid_state(dims, [[0, 1]] * 4, [[0.5, 0.5], [0.5, 0.5], [0, 0], [0.5, 0.5]],
+                      [[1, 1]] * 4)
+    pol = O.Policy(mode=O.MODE_RATIO, ratio=0.375, refresh_cycle=0)
+    _, _, rec = O.step(dims, pol, W, st, x, 1)
+    m = rec["m"].reshape(-1)
+    assert m[4] == m[5] and float(m[4]) == float(m[0]) + 0.5
+    assert rec["mask"].reshape(-1).tolist() == [True, False, False, False, True, True,
+                                                False, False]
+
+
+def test_gelu_forms_match_library():
+    """Both GELU forms (reading R-17) against torch's fp64 GELU and against
+    math.erf / math.tanh evaluated point by point."""
+    z = np.concatenate([np.linspace(-8, 8, 4001), [-30.0, -1e-3, 0.0, 1e-3, 30.0]])
+    zt = torch.from_numpy(z)
+    exact = torch.nn.functional.gelu(zt, approximate="none").numpy()
+    tanh_form = torch.nn.functional.gelu(zt, approximate="tanh").numpy()
+    np.testing.assert_allclose(O.gelu(z, "gelu_erf"), exact, rtol=1e-14, atol=1e-15)
+    np.testing.assert_allclose(O.gelu(z, "gelu_tanh"), tanh_form, rtol=1e-14, atol=1e-15)
+    for v in (-2.5, -0.7, 0.3, 1.0, 4.2):
+        assert abs(O.gelu(np.array([v]), "gelu_erf")[0]
+                   - 0.5 * v * (1 + math.erf(v / math.sqrt(2)))) <= 1e-15
+        c = math.sqrt(2 / math.pi) * (v + 0.044715 * v ** 3)
+        assert abs(O.gelu(np.array([v]), "gelu_tanh")[0] - 0.5 * v * (1 + math.tanh(c))) <= 1e-15
+    # the two forms differ (the erf one is not the tanh one under another name)
+    assert np.abs(O.gelu(z, "gelu_erf") - O.gelu(z, "gelu_tanh")).max() > 1e-4
+
+
+def test_erf_gelu_layer_matches_torch_fp64():
+    """The uncached layer with erf GELU against torch.nn.functional in fp64."""
+    sy, dims, W = build(SMALL32, seed=31)
+    x = next(sy.trajectory(1))
+    got = O.uncached_layer(dims, W, x, act="gelu_erf").reshape(-1, dims.d).astype(np.float64)
+    want, _, _ = _torch_moe(dims, W, x, act="gelu_erf")
+    assert np.abs(got - want).max() / np.abs(want).max() < 1e-6
+    tanh_ref, _, _ = _torch_moe(dims, W, x, act="gelu_tanh")
+    assert np.abs(got - tanh_ref).max() / np.abs(want).max() > 1e-5
+
+
+@pytest.mark.parametrize("shape", [LayerShape(d=256, E=8, k=2, d_ff=512, B=2, N=96, dtype="fp32"),
+                                   LayerShape(d=256, E=8, k=2, d_ff=512, B=2, N=96, dtype="bf16")])
+def test_oracle_independent_of_thread_count(shape):
+    """Every result of a trajectory (refresh and cache steps) is bit-identical
+    with the BLAS limited to one thread and with all threads."""
+    from threadpoolctl import threadpool_limits
+    sy, dims, W = build(shape, seed=33)
+    xs = list(sy.trajectory(3))
+    pol = O.Policy(mode=O.MODE_RATIO, ratio=0.3, refresh_cycle=0)
+
+    def run(threads):
+        with threadpool_limits(limits=threads):
+            W1 = O.Weights(dims, W.W_r, W.b_r, W.W_up, W.W_down)
+            return run_traj(dims, pol, W1, xs)
+
+    a_out, a_rec, _, a_st = run(1)
+    b_out, b_rec, _, b_st = run(None)
+    for oa, ob in zip(a_out, b_out):
+        assert np.array_equal(oa, ob)
+    for ra, rb in zip(a_rec, b_rec):
+        for key in ("logits64", "logits", "e_t", "w_t", "Hbar", "tau", "m", "mask", "lst", "h_new"):
+            assert np.array_equal(ra[key], rb[key]), key
+    for f in ("e_c", "w_c", "n_c", "h_c", "C"):
+        assert np.array_equal(getattr(a_st, f), getattr(b_st, f)), f
