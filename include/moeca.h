@@ -166,6 +166,29 @@ int moeca_bind_attention(moeca_layer* layer, const void* attn_in, void* attn_cac
  * weights are unbound. */
 int moeca_step(moeca_layer* layer, const void* x_t, int t, void* out, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): the
+ * uncached routed MoE layer, i.e. what moeca_step computes for a
+ * MOECA_MODE_FULL layer (router, top-k gates, every branch through its
+ * expert FFN, combine), over the first `samples` samples of N tokens.
+ *   x   [samples][N][d]  device, policy dtype
+ *   out [samples][N][d]  device, policy dtype
+ * Needs only the bound weights (and shared weights when n_shared > 0): no
+ * workspace, whatever the layer's mode, and the layer's cache and statistic
+ * are neither read nor written.  Every intermediate lives in one
+ * library-owned device array of 64 MiB per GPU, held from the library's
+ * first use on that GPU until the process ends; this call allocates no
+ * device or host memory and never synchronises.  A call whose intermediates
+ * exceed that array (about samples * N * (k + n_shared) * (d + d_ff) * 2
+ * bytes in bf16) is MOECA_E_INVAL with the sizes in moeca_last_error().
+ * Every call on one GPU shares its array: calls that overlap on one GPU
+ * (other streams, other threads) race and must be ordered by the caller.
+ * MOECA_E_INVAL: NULL layer, x or out, unaligned x or out (16 bytes),
+ * samples outside [1, B]; MOECA_E_STATE: weights unbound; MOECA_E_HIP: the
+ * array's address could not be obtained or a launch failed. */
+int moeca_forward_noalloc(const moeca_layer* layer, const void* x, int samples, void* out,
+                          void* stream);
+
 /* Enqueue a cache reset on the stream: every cached branch becomes empty,
  * the EMA statistic becomes zero, and the next step is a full step. */
 int moeca_cache_reset(moeca_layer* layer, void* stream);

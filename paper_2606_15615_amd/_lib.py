@@ -73,6 +73,8 @@ _SIGS = {
     "moeca_bind_attention": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_void_p]),
     "moeca_step": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
                                   ctypes.c_void_p, ctypes.c_void_p]),
+    "moeca_forward_noalloc": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p, ctypes.c_int,
+                                             ctypes.c_void_p, ctypes.c_void_p]),
     "moeca_cache_reset": (ctypes.c_int, [ctypes.c_void_p, ctypes.c_void_p]),
     "moeca_get_stats": (ctypes.c_int, [ctypes.c_void_p, ctypes.POINTER(moeca_stats),
                                        ctypes.c_void_p]),
@@ -174,6 +176,10 @@ def moeca_bind_attention(h, attn_in, attn_cache) -> int:
 
 def moeca_step(h, x_t, t, out, stream) -> int:
     return _check(load().moeca_step(h, x_t, t, out, stream))
+
+
+def moeca_forward_noalloc(h, x, samples, out, stream) -> int:
+    return _check(load().moeca_forward_noalloc(h, x, samples, out, stream))
 
 
 def moeca_cache_reset(h, stream) -> int:

@@ -34,6 +34,7 @@ SOURCES = {
     "combine.hip": ["-ffp-contract=off"],
     "ffn.hip": [],
     "block.hip": ["-ffp-contract=off"],
+    "noalloc.hip": [],
     "moeca.cpp": ["-ffp-contract=off"],
     "stack.cpp": [],
 }

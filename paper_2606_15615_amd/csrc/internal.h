@@ -133,6 +133,14 @@ hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void
                           void* attn_cache, const Buffers& b, hipStream_t st);
 hipError_t launch_reset(const Shape& s, const Buffers& b, hipStream_t st);
 
+// ---- the entry point that allocates nothing (noalloc.hip) --------------
+// Bytes of the library-owned device array every call of
+// moeca_forward_noalloc on a GPU shares.
+constexpr size_t kNoallocScratchBytes = size_t(64) << 20;
+// The array's device address on the current device (looked up once per
+// device with hipGetSymbolAddress).
+hipError_t noalloc_scratch(void** out);
+
 // ---- the MoE layer step, as used by a block (moeca.cpp) ----------------
 // The step of moeca_step with the router reading x_route and the expert FFN
 // reading x_ffn; `between`, when set, is called after the decision and the

@@ -104,6 +104,42 @@ Layout make_layout(const Shape& s, bool external_mid = false) {
   return L;
 }
 
+// Device views of the regions of a workspace at w laid out as lay; the FFN
+// intermediate at mid when it lives outside the workspace.
+Buffers map_buffers(char* w, const Layout& lay, void* mid) {
+  const size_t* o = lay.off;
+  Buffers b{};
+  b.e_c = reinterpret_cast<int32_t*>(w + o[R_E_C]);
+  b.w_c = reinterpret_cast<float*>(w + o[R_W_C]);
+  b.n_c = reinterpret_cast<float*>(w + o[R_N_C]);
+  b.h_c = w + o[R_H_C];
+  b.stat = reinterpret_cast<float*>(w + o[R_STAT]);
+  b.ent = reinterpret_cast<double*>(w + o[R_ENT]);
+  b.logits = reinterpret_cast<float*>(w + o[R_LOGITS]);
+  b.e_t = reinterpret_cast<int32_t*>(w + o[R_E_T]);
+  b.w_t = reinterpret_cast<float*>(w + o[R_W_T]);
+  b.hbar = reinterpret_cast<float*>(w + o[R_HBAR]);
+  b.tau = reinterpret_cast<float*>(w + o[R_TAU]);
+  b.margin = reinterpret_cast<float*>(w + o[R_MARGIN]);
+  b.q = reinterpret_cast<int32_t*>(w + o[R_Q]);
+  b.mask = reinterpret_cast<uint8_t*>(w + o[R_MASK]);
+  b.sigma = reinterpret_cast<int32_t*>(w + o[R_SIGMA]);
+  b.sync = reinterpret_cast<uint8_t*>(w + o[R_SYNC]);
+  b.off = reinterpret_cast<int32_t*>(w + o[R_OFF]);
+  b.list = reinterpret_cast<int32_t*>(w + o[R_LIST]);
+  b.pos = reinterpret_cast<int32_t*>(w + o[R_POS]);
+  b.cnt_bs = reinterpret_cast<int32_t*>(w + o[R_CNT_BS]);
+  b.cnt_ch = reinterpret_cast<int32_t*>(w + o[R_CNT_CH]);
+  b.wide = reinterpret_cast<int32_t*>(w + o[R_WIDE]);
+  b.stats_bs = reinterpret_cast<int32_t*>(w + o[R_STATS_BS]);
+  b.rflags = reinterpret_cast<int32_t*>(w + o[R_RFLAGS]);
+  b.tiles = reinterpret_cast<int32_t*>(w + o[R_TILES]);
+  b.row_dst = reinterpret_cast<int32_t*>(w + o[R_ROW_DST]);
+  b.mid = mid != nullptr ? mid : w + o[R_MID];
+  b.h_sh = w + o[R_H_SH];
+  return b;
+}
+
 }  // namespace
 
 struct moeca_layer {
@@ -242,36 +278,7 @@ int moeca_bind_workspace(moeca_layer* L, void* dev, size_t bytes) {
     return fail(MOECA_E_INVAL, "workspace too small: need " + std::to_string(L->layout.total) +
                                    " bytes, got " + std::to_string(bytes));
   char* w = static_cast<char*>(dev);
-  const size_t* o = L->layout.off;
-  Buffers& b = L->buf;
-  b.e_c = reinterpret_cast<int32_t*>(w + o[R_E_C]);
-  b.w_c = reinterpret_cast<float*>(w + o[R_W_C]);
-  b.n_c = reinterpret_cast<float*>(w + o[R_N_C]);
-  b.h_c = w + o[R_H_C];
-  b.stat = reinterpret_cast<float*>(w + o[R_STAT]);
-  b.ent = reinterpret_cast<double*>(w + o[R_ENT]);
-  b.logits = reinterpret_cast<float*>(w + o[R_LOGITS]);
-  b.e_t = reinterpret_cast<int32_t*>(w + o[R_E_T]);
-  b.w_t = reinterpret_cast<float*>(w + o[R_W_T]);
-  b.hbar = reinterpret_cast<float*>(w + o[R_HBAR]);
-  b.tau = reinterpret_cast<float*>(w + o[R_TAU]);
-  b.margin = reinterpret_cast<float*>(w + o[R_MARGIN]);
-  b.q = reinterpret_cast<int32_t*>(w + o[R_Q]);
-  b.mask = reinterpret_cast<uint8_t*>(w + o[R_MASK]);
-  b.sigma = reinterpret_cast<int32_t*>(w + o[R_SIGMA]);
-  b.sync = reinterpret_cast<uint8_t*>(w + o[R_SYNC]);
-  b.off = reinterpret_cast<int32_t*>(w + o[R_OFF]);
-  b.list = reinterpret_cast<int32_t*>(w + o[R_LIST]);
-  b.pos = reinterpret_cast<int32_t*>(w + o[R_POS]);
-  b.cnt_bs = reinterpret_cast<int32_t*>(w + o[R_CNT_BS]);
-  b.cnt_ch = reinterpret_cast<int32_t*>(w + o[R_CNT_CH]);
-  b.wide = reinterpret_cast<int32_t*>(w + o[R_WIDE]);
-  b.stats_bs = reinterpret_cast<int32_t*>(w + o[R_STATS_BS]);
-  b.rflags = reinterpret_cast<int32_t*>(w + o[R_RFLAGS]);
-  b.tiles = reinterpret_cast<int32_t*>(w + o[R_TILES]);
-  b.row_dst = reinterpret_cast<int32_t*>(w + o[R_ROW_DST]);
-  b.mid = L->mid_outside ? L->external_mid : w + o[R_MID];
-  b.h_sh = w + o[R_H_SH];
+  L->buf = map_buffers(w, L->layout, L->mid_outside ? L->external_mid : nullptr);
   L->ws = w;
   L->valid = false;
   return MOECA_OK;
@@ -290,6 +297,45 @@ int moeca_bind_attention(moeca_layer* L, const void* attn_in, void* attn_cache) 
 
 int moeca_step(moeca_layer* L, const void* x_t, int t, void* out, void* stream) {
   return moeca::layer_step(L, x_t, x_t, t, out, static_cast<hipStream_t>(stream), {});
+}
+
+int moeca_forward_noalloc(const moeca_layer* L, const void* x, int samples, void* out,
+                          void* stream) {
+  if (L == nullptr) return fail(MOECA_E_INVAL, "layer is NULL");
+  if (x == nullptr || out == nullptr) return fail(MOECA_E_INVAL, "x and out are required");
+  if (!aligned16(x) || !aligned16(out)) return fail(MOECA_E_INVAL, "x and out must be 16-byte aligned");
+  if (samples < 1 || samples > L->shape.B)
+    return fail(MOECA_E_INVAL, "samples must be in [1, " + std::to_string(L->shape.B) + "]");
+  Shape s = L->shape;
+  s.B = samples;
+  const Layout lay = make_layout(s);
+  if (lay.total > moeca::kNoallocScratchBytes)
+    return fail(MOECA_E_INVAL, "this call needs " + std::to_string(lay.total) +
+                                   " bytes of scratch; the library's array holds " +
+                                   std::to_string(moeca::kNoallocScratchBytes) +
+                                   " (use fewer samples per call, or moeca_step)");
+  if (L->W_r == nullptr) return fail(MOECA_E_STATE, "weights are not bound");
+  if (s.S > 0 && L->W_up_sh == nullptr)
+    return fail(MOECA_E_STATE, "shared expert weights are not bound");
+  void* base = nullptr;
+  hipError_t e = moeca::noalloc_scratch(&base);
+  if (e != hipSuccess)
+    return fail(MOECA_E_HIP, std::string("scratch address: ") + hipGetErrorString(e));
+  const Buffers b = map_buffers(static_cast<char*>(base), lay, nullptr);
+  const moeca_policy& p = L->pol;
+  const auto st = static_cast<hipStream_t>(stream);
+  // the uncached layer: every branch recomputed, no statistic, no cache
+  // metadata and no attention path (the MOECA_MODE_FULL step)
+  if ((e = moeca::launch_router(s, x, L->W_r, L->b_r, p.norm_topk, p.beta, false, b, st)) ==
+          hipSuccess &&
+      (e = moeca::launch_decide(s, moeca::kSelFull, 0, p.lambda0, p.lambda1, p.lambda2, false,
+                                p.tau0, p.alpha, b, st)) == hipSuccess &&
+      (e = moeca::launch_lists(s, moeca::ffn_plan(s), b, st)) == hipSuccess &&
+      (e = moeca::launch_ffn_up(s, x, L->W_up, L->W_up_sh, p.act, b, st)) == hipSuccess &&
+      (e = moeca::launch_ffn_down(s, L->W_down, L->W_down_sh, b, st)) == hipSuccess)
+    e = moeca::launch_combine(s, 0, out, nullptr, nullptr, b, st);
+  if (e != hipSuccess) return fail(MOECA_E_HIP, std::string("launch: ") + hipGetErrorString(e));
+  return MOECA_OK;
 }
 
 }  // extern "C"

@@ -147,6 +147,32 @@ def test_host_error_paths(L):
     assert lib.moeca_debug_set_valid(None, 1) == L.MOECA_E_INVAL
 
 
+def test_noalloc_forward_host_error_paths(L):
+    """moeca_forward_noalloc refuses, on the host and before any device call:
+    a NULL layer or buffer, misaligned buffers, sample counts outside
+    [1, B], work whose intermediates exceed the library's 64 MiB array, and
+    unbound weights."""
+    lib = L.load()
+    fake = 1 << 40  # never dereferenced
+    assert lib.moeca_forward_noalloc(None, fake, 1, fake, None) == L.MOECA_E_INVAL
+    big = L.moeca_layer_create(1152, 16, 2, 4608, _pol(L, batch=8, tokens=1024))
+    try:
+        assert lib.moeca_forward_noalloc(big, None, 1, fake, None) == L.MOECA_E_INVAL
+        assert lib.moeca_forward_noalloc(big, fake, 1, fake + 8, None) == L.MOECA_E_INVAL
+        assert lib.moeca_forward_noalloc(big, fake, 0, fake, None) == L.MOECA_E_INVAL
+        assert lib.moeca_forward_noalloc(big, fake, 9, fake, None) == L.MOECA_E_INVAL
+        assert "samples must be in [1, 8]" in L.moeca_last_error()
+        # 8 and 3 samples of 1024 tokens exceed the array, 2 fit (then the
+        # unbound weights are the next refusal)
+        for n in (8, 3):
+            assert lib.moeca_forward_noalloc(big, fake, n, fake, None) == L.MOECA_E_INVAL
+            assert "bytes of scratch" in L.moeca_last_error()
+        assert lib.moeca_forward_noalloc(big, fake, 2, fake, None) == L.MOECA_E_STATE
+        assert "weights are not bound" in L.moeca_last_error()
+    finally:
+        L.moeca_layer_destroy(big)
+
+
 def test_workspace_grows_with_the_layer(L):
     a = L.moeca_layer_create(1152, 16, 2, 4608, _pol(L, batch=8, tokens=256))
     b = L.moeca_layer_create(1152, 16, 2, 4608, _pol(L, batch=8, tokens=1024))
