@@ -1139,7 +1139,8 @@ hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda0
 hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st) {
   const int nb = s.N * s.k;
   const int nt_up = (s.up_rows() + plan.tn_up - 1) / plan.tn_up;
-  const int nt_down = (s.d + plan.tn_down - 1) / plan.tn_down;
+  // units of the down projection per M tile: N tiles times K pieces
+  const int nt_down = (s.d + plan.tn_down - 1) / plan.tn_down * plan.split_down;
   const int rc_n = (nb + kSelThreads - 1) / kSelThreads;
   if (s.E > 64) return hipErrorInvalidValue;
   launch_kernel(&lists_kernel, dim3(s.B * rc_n), dim3(kSelThreads), 0, st, b.mask, b.e_t,

@@ -704,6 +704,280 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
 }
 
 // ---------------------------------------------------------------------------
+// bf16 MFMA grouped GEMM for weight-streaming steps: few rows per expert, so
+// every weight byte is used by one tile and the step is bound by how fast
+// the CUs pull the weights in.  The tile is 128 rows x 288 columns, so that
+// an expert's up-projection rows split into equal tiles that give every CU
+// about one (16 experts x 4608 rows: 256 tiles); the down projection splits
+// K into SPLIT equal pieces (units), each writing its fp32 partial sums to
+// part[piece][row][column], which reduce_partials_kernel adds in piece
+// order.  8 waves (two per SIMD) of 32 rows x 144 columns, each 2 x 9
+// v_mfma_f32_16x16x32_bf16 tiles (weights the A operand, token rows the B
+// operand: a lane holds four consecutive output columns of one row), on the
+// large kernel's three-stage direct-to-LDS ring of 64-wide k-tiles with the
+// same XOR-swizzled 16-byte chunks.  A stage holds 128 token rows and 288
+// weight rows (52 KB): 36 DMA instructions of 8 weight rows, so waves 0-3
+// issue five and waves 4-7 four.  Units are numbered expert-major, then k
+// piece, then N tile, then M tile, and walked like the large kernel's
+// tiles (contiguous ranges per XCD): the units that share a k piece of an
+// expert's rows run together on one XCD.
+// ---------------------------------------------------------------------------
+constexpr int kThinTM = 128;
+constexpr int kThinTN = 288;
+constexpr int kThinWaves = 8;
+constexpr int kThinThreads = kThinWaves * kWave;
+constexpr int kThinTileA = kThinTM * kTK;            // 16 KB
+constexpr int kThinTileB = kThinTN * kTK;            // 36 KB
+constexpr int kThinStage = kThinTileA + kThinTileB;  // 52 KB
+constexpr int kThinLoadsA = kThinTM / 8 / kThinWaves;                     // 2 per wave
+constexpr int kThinInstB = kThinTN / 8;                                   // 36
+constexpr int kThinLoadsB = (kThinInstB + kThinWaves - 1) / kThinWaves;   // 5 (waves 0-3), 4
+static_assert(kThinInstB % kThinWaves == kThinWaves / 2, "waves 0-3 issue one more weight load");
+
+typedef __attribute__((ext_vector_type(4))) float f32x4_t;
+
+template <int N>
+__device__ __forceinline__ void s_waitcnt_vm_n() {
+  // gfx9 encoding, vmcnt N < 16: expcnt and lgkmcnt left at their maxima
+  static_assert(N >= 0 && N < 16, "vmcnt");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
+template <int KIND, int ACT, int SPLIT>
+__global__ __launch_bounds__(kThinThreads, 1) void gemm_bf16_thin_kernel(
+    const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
+    const int32_t* __restrict__ off, const int32_t* __restrict__ tile_off,
+    const int32_t* __restrict__ list, const int32_t* __restrict__ row_dst, int E, int k, int K,
+    int Nout, int64_t part_rows, uint16_t* __restrict__ dst, float* __restrict__ part) {
+  constexpr int TM = kThinTM, TN = kThinTN;
+  constexpr int FM = 2, FN = 9;  // 16 x 16 accumulator tiles of a wave
+  static_assert(KIND != kDown || ACT == kActNone, "the down projection has no activation");
+  static_assert(SPLIT == 1 || KIND == kDown, "only the down projection splits K");
+  __shared__ __attribute__((aligned(16))) uint16_t lds[kStages * kThinStage];
+  __shared__ int s_src[TM];
+  __shared__ int s_dst[TM];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int wv = tid >> 6;
+  const int wm = wv >> 1, wn = wv & 1;  // 4 x 2 waves
+  const int G = E;
+  const int total = tile_off[G];
+  const int per = (total + kXcds - 1) / kXcds;
+  const int lo = (blockIdx.x % kXcds) * per;
+  const int hi = min(total, lo + per);
+  const int stride = gridDim.x / kXcds;
+  const int toff0 = lane < G ? tile_off[lane] : 0x7fffffff;
+  const int toff1 = lane + 64 < G ? tile_off[lane + 64] : 0x7fffffff;
+  const int KT = K / kTK;
+  const int NT = (Nout + TN - 1) / TN;
+  // waves issuing kThinLoadsB weight loads (wave-uniform: from readfirstlane)
+  const bool five = __builtin_amdgcn_readfirstlane(wv) < kThinInstB % kThinWaves;
+  // stored chunk position: chunk ^ ((row >> 1) & 7) with row = 8 i + lane / 8
+  // and i = wv + 8 u (the parity of wv), as in the large kernel
+  const int chunk = (lane & 7) ^ (4 * (wv & 1) + (lane >> 4));
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(lds) + wv * 1024);
+
+  struct Unit {
+    int e, r0, rows, n0, ks, kt0, kt1;
+  };
+  auto unit = [&](int L) __attribute__((always_inline)) {
+    Unit u;
+    int e_base;
+    u.e = tile_group(L, toff0, toff1, e_base);
+    const int o0 = off[u.e];
+    const int cnt = off[u.e + 1] - o0;
+    const int mt = (cnt + TM - 1) / TM;
+    const int local = L - e_base;
+    const int m = local % mt;
+    const int rest = local / mt;
+    u.ks = rest / NT;
+    u.r0 = o0 + m * TM;
+    u.rows = min(TM, cnt - m * TM);
+    u.n0 = (rest % NT) * TN;
+    u.kt0 = u.ks * KT / SPLIT;
+    u.kt1 = (u.ks + 1) * KT / SPLIT;
+    // the unit is the same for every lane (the group comes from a ballot):
+    // say so, so that the k-loop and the stage addresses stay scalar
+    u.e = __builtin_amdgcn_readfirstlane(u.e);
+    u.r0 = __builtin_amdgcn_readfirstlane(u.r0);
+    u.rows = __builtin_amdgcn_readfirstlane(u.rows);
+    u.n0 = __builtin_amdgcn_readfirstlane(u.n0);
+    u.ks = __builtin_amdgcn_readfirstlane(u.ks);
+    u.kt0 = __builtin_amdgcn_readfirstlane(u.kt0);
+    u.kt1 = __builtin_amdgcn_readfirstlane(u.kt1);
+    return u;
+  };
+
+  const uint16_t* ga[kThinLoadsA];
+  const uint16_t* gb[kThinLoadsB];
+  auto start_unit = [&](const Unit& t, int src, int dstr) __attribute__((always_inline)) {
+    if (tid < TM) {
+      s_src[tid] = src;
+      s_dst[tid] = dstr;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int u = 0; u < kThinLoadsA; ++u) {
+      const int r = 8 * (wv + kThinWaves * u) + (lane >> 3);
+      ga[u] = A + int64_t(s_src[r]) * K + chunk * 8;
+    }
+    const uint16_t* Wg = W + int64_t(t.e) * Nout * K;
+#pragma unroll
+    for (int u = 0; u < kThinLoadsB; ++u) {
+      const int r = 8 * (wv + kThinWaves * u) + (lane >> 3);
+      const int n = min(t.n0 + min(r, TN - 1), Nout - 1);  // rows past the tile or N: clamped
+      gb[u] = Wg + int64_t(n) * K + chunk * 8;
+    }
+  };
+  auto issue = [&](int kt, int st) __attribute__((always_inline)) {
+    const uint32_t base = lds0 + st * (kThinStage * 2);
+#pragma unroll
+    for (int u = 0; u < kThinLoadsA; ++u) dma16(ga[u] + kt * kTK, base + u * kThinWaves * 1024);
+#pragma unroll
+    for (int u = 0; u < kThinLoadsB; ++u)
+      if (u + 1 < kThinLoadsB || five)
+        dma16(gb[u] + kt * kTK, base + kThinTileA * 2 + u * kThinWaves * 1024);
+  };
+  // this wave's loads of the oldest stage in flight have landed once at most
+  // one later stage's loads are outstanding
+  auto wait_stage = [&](bool last) __attribute__((always_inline)) {
+    if (last) s_waitcnt_vm_n<0>();
+    else if (five) s_waitcnt_vm_n<kThinLoadsA + kThinLoadsB>();
+    else s_waitcnt_vm_n<kThinLoadsA + kThinLoadsB - 1>();
+  };
+
+  int L = lo + static_cast<int>(blockIdx.x) / kXcds;
+  if (L >= hi) return;
+  Unit cur = unit(L);
+  {
+    int src = 0, dstr = -1;
+    if (tid < TM) group_row<KIND>(cur.e, E, cur.r0, cur.rows, tid, k, off, list, row_dst, src, dstr);
+    start_unit(cur, src, dstr);
+  }
+  if (cur.kt0 < cur.kt1) issue(cur.kt0, 0);
+  if (cur.kt0 + 1 < cur.kt1) issue(cur.kt0 + 1, 1);
+
+  for (;;) {
+    const int Ln = L + stride;
+    const bool has_next = Ln < hi;
+    Unit nxt = cur;
+    int nsrc = 0, ndst = -1;
+    if (has_next) {
+      nxt = unit(Ln);
+      if (tid < TM) group_row<KIND>(nxt.e, E, nxt.r0, nxt.rows, tid, k, off, list, row_dst, nsrc, ndst);
+    }
+
+    f32x4_t acc[FN][FM];
+#pragma unroll
+    for (int j = 0; j < FN; ++j)
+#pragma unroll
+      for (int i = 0; i < FM; ++i) acc[j][i] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+
+    // a wave whose rows lie wholly past the unit's rows, or whose columns
+    // past N, skips its MFMAs (it still loads its share and syncs)
+    const bool active = wm * 32 < cur.rows && cur.n0 + wn * 144 < Nout;
+    int st = 0;
+    for (int kt = cur.kt0; kt < cur.kt1; ++kt) {
+      wait_stage(kt + 1 >= cur.kt1);
+      __builtin_amdgcn_s_barrier();
+      if (kt + 2 < cur.kt1) issue(kt + 2, st == 0 ? 2 : st - 1);
+      const uint16_t* xs = lds + st * kThinStage;
+      const uint16_t* ws = xs + kThinTileA;
+      if (active) {
+#pragma unroll
+        for (int s2 = 0; s2 < kTK / 32; ++s2) {
+          const int c = 4 * s2 + (lane >> 4);  // logical 16-byte chunk of this lane
+          bf16x8_t xa[FM], wb[FN];
+#pragma unroll
+          for (int i = 0; i < FM; ++i) {
+            const int row = wm * 32 + i * 16 + (lane & 15);
+            xa[i] = *reinterpret_cast<const bf16x8_t*>(xs + (row * 8 + (c ^ ((row >> 1) & 7))) * 8);
+          }
+#pragma unroll
+          for (int j = 0; j < FN; ++j) {
+            const int row = wn * 144 + j * 16 + (lane & 15);
+            wb[j] = *reinterpret_cast<const bf16x8_t*>(ws + (row * 8 + (c ^ ((row >> 1) & 7))) * 8);
+          }
+#pragma unroll
+          for (int j = 0; j < FN; ++j)
+#pragma unroll
+            for (int i = 0; i < FM; ++i)
+              acc[j][i] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb[j], xa[i], acc[j][i], 0, 0, 0);
+        }
+      }
+      st = st == 2 ? 0 : st + 1;
+    }
+
+    // destination rows of this wave's accumulators; then the LDS goes to the
+    // next unit, whose first loads start before this unit's epilogue
+    int drow[FM];
+#pragma unroll
+    for (int i = 0; i < FM; ++i) drow[i] = s_dst[wm * 32 + i * 16 + (lane & 15)];
+    __syncthreads();
+    if (has_next) {
+      start_unit(nxt, nsrc, ndst);
+      if (nxt.kt0 < nxt.kt1) issue(nxt.kt0, 0);
+      if (nxt.kt0 + 1 < nxt.kt1) issue(nxt.kt0 + 1, 1);
+    }
+
+    // epilogue: lane holds columns c .. c + 3 of row (lane & 15) of each
+    // 16 x 16 tile, c = n0 + 144 wn + 16 j + 4 (lane >> 4)
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      const int r = wm * 32 + i * 16 + (lane & 15);
+#pragma unroll
+      for (int j = 0; j < FN; ++j) {
+        const int c = cur.n0 + wn * 144 + j * 16 + 4 * (lane >> 4);
+        if (c >= Nout || r >= cur.rows) continue;
+        const f32x4_t& a = acc[j][i];
+        if constexpr (SPLIT > 1) {
+          *reinterpret_cast<f32x4_t*>(part + (int64_t(cur.ks) * part_rows + cur.r0 + r) * Nout + c) = a;
+        } else {
+          const u32x2_t v{pack2_bf16(act_fn<ACT>(a[0]), act_fn<ACT>(a[1])),
+                          pack2_bf16(act_fn<ACT>(a[2]), act_fn<ACT>(a[3]))};
+          *reinterpret_cast<u32x2_t*>(dst + int64_t(drow[i]) * Nout + c) = v;
+        }
+      }
+    }
+    if (!has_next) break;
+    L = Ln;
+    cur = nxt;
+  }
+}
+
+// h_c[row_dst[r]] = bf16(((part[0][r] + part[1][r]) + ...) + part[S-1][r])
+// for the listed rows r < off[E] (the down projection's K pieces, added in
+// piece order); one wave per row, 16 bytes of bf16 per lane and step.
+template <int SPLIT>
+__global__ __launch_bounds__(256) void reduce_partials_kernel(
+    const float* __restrict__ part, int64_t part_rows, const int32_t* __restrict__ off,
+    const int32_t* __restrict__ row_dst, int E, int d, uint16_t* __restrict__ h_c) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int r = static_cast<int>(blockIdx.x) * 4 + static_cast<int>(threadIdx.x) / kWave;
+  if (r >= off[E]) return;
+  const int64_t drow = row_dst[r];
+  for (int g = lane; g < d / 8; g += kWave) {
+    f32x4_t s0 = *reinterpret_cast<const f32x4_t*>(part + int64_t(r) * d + g * 8);
+    f32x4_t s1 = *reinterpret_cast<const f32x4_t*>(part + int64_t(r) * d + g * 8 + 4);
+#pragma unroll
+    for (int p = 1; p < SPLIT; ++p) {
+      const float* q = part + (int64_t(p) * part_rows + r) * d + g * 8;
+      const f32x4_t a0 = *reinterpret_cast<const f32x4_t*>(q);
+      const f32x4_t a1 = *reinterpret_cast<const f32x4_t*>(q + 4);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        s0[u] = __fadd_rn(s0[u], a0[u]);
+        s1[u] = __fadd_rn(s1[u], a1[u]);
+      }
+    }
+    *reinterpret_cast<u32x4_t*>(h_c + drow * d + g * 8) =
+        u32x4_t{pack2_bf16(s0[0], s0[1]), pack2_bf16(s0[2], s0[3]), pack2_bf16(s1[0], s1[1]),
+                pack2_bf16(s1[2], s1[3])};
+  }
+}
+
+// ---------------------------------------------------------------------------
 // fp32 grouped GEMM (fp32 layers): 64x64 block tile, 4x4 per thread, FMA.
 // ---------------------------------------------------------------------------
 constexpr int kF32T = 64;
@@ -796,11 +1070,47 @@ constexpr int kBlocksPerCu = 2;
 // shared groups (weights Wsh, outputs dst_sh) with Nout weight rows and K
 // inputs per group.
 template <int KIND, int ACT>
-hipError_t launch_gemm(const Shape& s, const void* A, const void* W, const void* Wsh, int K,
-                       int Nout, const Buffers& b, void* dst, void* dst_sh, hipStream_t st) {
+hipError_t launch_gemm(const Shape& s, const FfnPlan& plan, const void* A, const void* W,
+                       const void* Wsh, int K, int Nout, const Buffers& b, void* dst, void* dst_sh,
+                       hipStream_t st) {
   const int G = s.groups();
+  if (plan.thin) {
+    // bf16, ungated, no shared experts (thin_capable)
+    if constexpr (ACT == kActSwiglu || ACT == kActBias) {
+      return hipErrorInvalidValue;
+    } else {
+      const int32_t* toff = b.tiles + (KIND == kUp ? 0 : G + 1);
+      const auto* a = static_cast<const uint16_t*>(A);
+      const auto* w = static_cast<const uint16_t*>(W);
+      const int64_t rows = s.mid_rows();
+      if (KIND == kDown && plan.split_down == kThinSplit && b.part != nullptr) {
+        // the stage's start event goes with the GEMM, its stop event with
+        // the addition of the partial sums
+        const LaunchEvents ev = launch_events();
+        launch_events() = LaunchEvents{};
+        launch_kernel_ev(&gemm_bf16_thin_kernel<kDown, kActNone, kThinSplit>, dim3(device_cus()),
+                         dim3(kThinThreads), 0, st, ev.start, nullptr, a, w, b.off, toff, b.list,
+                         b.row_dst, s.E, s.k, K, Nout, rows, static_cast<uint16_t*>(nullptr),
+                         b.part);
+        const hipError_t e = hipGetLastError();
+        if (e != hipSuccess) return e;
+        launch_kernel_ev(&reduce_partials_kernel<kThinSplit>,
+                         dim3(static_cast<unsigned>((rows + 3) / 4)), dim3(256), 0, st, nullptr,
+                         ev.stop, static_cast<const float*>(b.part), rows, b.off, b.row_dst, s.E,
+                         s.d, static_cast<uint16_t*>(b.h_c));
+      } else if (KIND == kDown) {
+        launch_kernel(&gemm_bf16_thin_kernel<kDown, kActNone, 1>, dim3(device_cus()),
+                      dim3(kThinThreads), 0, st, a, w, b.off, toff, b.list, b.row_dst, s.E, s.k,
+                      K, Nout, rows, static_cast<uint16_t*>(dst), static_cast<float*>(nullptr));
+      } else {
+        launch_kernel(&gemm_bf16_thin_kernel<kUp, ACT, 1>, dim3(device_cus()),
+                      dim3(kThinThreads), 0, st, a, w, b.off, toff, b.list, b.row_dst, s.E, s.k,
+                      K, Nout, rows, static_cast<uint16_t*>(dst), static_cast<float*>(nullptr));
+      }
+      return hipGetLastError();
+    }
+  }
   if (s.bf16) {
-    const FfnPlan plan = ffn_plan(s);
     const int tn = KIND == kUp ? plan.tn_up : plan.tn_down;
     const int32_t* toff = b.tiles + (KIND == kUp ? 0 : G + 1);
     const int grid = device_cus() * kBlocksPerCu;  // multiple of 8
@@ -833,14 +1143,26 @@ hipError_t launch_gemm(const Shape& s, const void* A, const void* W, const void*
 
 // Weight-row counts of at least 512 take the large 128 x 256 tile (a
 // partial last N tile is masked); smaller ones the 128 x 128 / 128 x 64
-// tiles.
-FfnPlan ffn_plan(const Shape& s) {
+// tiles; the thin plan the 128 x 288 tile.
+FfnPlan ffn_plan(const Shape& s, bool thin) {
   auto tn = [](int n) { return n >= 512 ? kBigTN : (n % 128 == 0 ? 128 : 64); };
   FfnPlan p;
   p.tm = 128;
+  if (thin && thin_capable(s)) {
+    p.thin = true;
+    p.tn_up = p.tn_down = kThinTN;
+    p.split_down = kThinSplit;
+    return p;
+  }
   p.tn_up = tn(s.up_rows());
   p.tn_down = tn(s.d);
   return p;
+}
+
+bool thin_capable(const Shape& s) {
+  const int nt = (s.up_rows() + kThinTN - 1) / kThinTN;
+  return s.bf16 && s.S == 0 && !s.swiglu && s.E <= 64 && s.branches() <= int64_t(256) * s.E &&
+         2 * s.E * nt >= device_cus();
 }
 
 int device_cus() {
@@ -858,19 +1180,19 @@ int device_cus() {
 }
 
 hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, const void* W_up_sh,
-                         int act, const Buffers& b, hipStream_t st) {
+                         int act, const FfnPlan& plan, const Buffers& b, hipStream_t st) {
   const int n = s.up_rows();
   if (act == MOECA_ACT_SWIGLU)
-    return launch_gemm<kUp, kActSwiglu>(s, x, W_up, W_up_sh, s.d, n, b, b.mid, b.mid, st);
+    return launch_gemm<kUp, kActSwiglu>(s, plan, x, W_up, W_up_sh, s.d, n, b, b.mid, b.mid, st);
   if (act == MOECA_ACT_GELU_ERF)
-    return launch_gemm<kUp, kActGeluErf>(s, x, W_up, W_up_sh, s.d, n, b, b.mid, b.mid, st);
-  return launch_gemm<kUp, kActGeluTanh>(s, x, W_up, W_up_sh, s.d, n, b, b.mid, b.mid, st);
+    return launch_gemm<kUp, kActGeluErf>(s, plan, x, W_up, W_up_sh, s.d, n, b, b.mid, b.mid, st);
+  return launch_gemm<kUp, kActGeluTanh>(s, plan, x, W_up, W_up_sh, s.d, n, b, b.mid, b.mid, st);
 }
 
 hipError_t launch_ffn_down(const Shape& s, const void* W_down, const void* W_down_sh,
-                           const Buffers& b, hipStream_t st) {
-  return launch_gemm<kDown, kActNone>(s, b.mid, W_down, W_down_sh, s.d_ff, s.d, b, b.h_c, b.h_sh,
-                                      st);
+                           const FfnPlan& plan, const Buffers& b, hipStream_t st) {
+  return launch_gemm<kDown, kActNone>(s, plan, b.mid, W_down, W_down_sh, s.d_ff, s.d, b, b.h_c,
+                                      b.h_sh, st);
 }
 
 hipError_t launch_proj(const void* A, const void* W, const float* bias, const int32_t* off,

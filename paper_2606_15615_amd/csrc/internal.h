@@ -98,17 +98,32 @@ struct Buffers {
   int32_t* wide;    // [B][kWideWords] per-sample scratch of the multi-block decision path
   void* mid;        // [B*N*k + S*T][d_ff] FFN activation of listed and shared rows
   void* h_sh;       // [S][T][d] shared experts' outputs
+  float* part;      // [kThinSplit][B*N*k][d] fp32 partial sums of the down projection's
+                    // K pieces (layers that may take the weight-streaming plan)
 };
 
-// Tiling of the grouped expert FFN: M tile (rows of one expert) and N tile
-// of the up and down projections.  The lists kernel turns the per-expert row
-// counts into tile prefixes with the same plan.
+// Tiling of the grouped expert FFN: M tile (rows of one expert), N tile of
+// the up and down projections, and the number of K pieces of the down
+// projection.  The lists kernel turns the per-expert row counts into tile
+// (unit) prefixes with the same plan.  thin: the weight-streaming kernel
+// (128 x 288 tiles) for both projections, the down projection in
+// kThinSplit K pieces whose fp32 partial sums are added in piece order.
 struct FfnPlan {
   int tm;
   int tn_up;
   int tn_down;
+  int split_down = 1;
+  bool thin = false;
 };
-FfnPlan ffn_plan(const Shape& s);
+constexpr int kThinSplit = 4;
+// A ratio-mode cache step takes the thin plan when its budget leaves at most
+// this many rows per expert on average (unmatched branches come on top).
+constexpr int kThinRows = 112;
+FfnPlan ffn_plan(const Shape& s, bool thin = false);
+// Layers that may take the thin plan: bf16, no shared experts, ungated, at
+// most 256 rows per expert on a full step, and enough 288-wide
+// up-projection tiles for half the CUs.  Their workspace holds `part`.
+bool thin_capable(const Shape& s);
 int device_cus();
 
 enum SelectMode { kSelFull = 0, kSelThreshold = 1, kSelRatio = 2 };
@@ -126,9 +141,10 @@ hipError_t launch_decide(const Shape& s, int sel_mode, int budget, float lambda0
 hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, hipStream_t st);
 // act: MOECA_ACT_* of the policy.  W_*_sh: the shared experts (S > 0).
 hipError_t launch_ffn_up(const Shape& s, const void* x, const void* W_up, const void* W_up_sh,
-                         int act, const Buffers& b, hipStream_t st);
+                         int act, const FfnPlan& plan, const Buffers& b, hipStream_t st);
+// With plan.split_down > 1 this also adds the partial sums into the cache rows.
 hipError_t launch_ffn_down(const Shape& s, const void* W_down, const void* W_down_sh,
-                           const Buffers& b, hipStream_t st);
+                           const FfnPlan& plan, const Buffers& b, hipStream_t st);
 hipError_t launch_combine(const Shape& s, int write_cache, void* out, const void* attn_in,
                           void* attn_cache, const Buffers& b, hipStream_t st);
 hipError_t launch_reset(const Shape& s, const Buffers& b, hipStream_t st);

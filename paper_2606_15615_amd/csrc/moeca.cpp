@@ -47,7 +47,8 @@ size_t align_up(size_t v) { return (v + kAlign - 1) / kAlign * kAlign; }
 enum Region {
   R_E_C, R_W_C, R_N_C, R_H_C, R_STAT, R_LOGITS, R_E_T, R_W_T, R_HBAR, R_TAU, R_MARGIN, R_Q,
   R_MASK, R_SIGMA, R_SYNC, R_OFF, R_LIST, R_POS,
-  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_ENT, R_CNT_CH, R_WIDE, R_MID, R_H_SH, R_COUNT
+  R_CNT_BS, R_STATS_BS, R_RFLAGS, R_TILES, R_ROW_DST, R_ENT, R_CNT_CH, R_WIDE, R_MID, R_H_SH,
+  R_PART, R_COUNT
 };
 
 struct Layout {
@@ -57,8 +58,11 @@ struct Layout {
 };
 
 // external_mid: the FFN intermediate lives outside this workspace (the
-// blocks of a stack run one after another and share one).
-Layout make_layout(const Shape& s, bool external_mid = false) {
+// blocks of a stack run one after another and share one).  partials: room
+// for the down projection's partial sums of the weight-streaming plan
+// (layers that can take it; not for the uncached forward of
+// moeca_forward_noalloc, which never does).
+Layout make_layout(const Shape& s, bool external_mid = false, bool partials = true) {
   const size_t nbr = static_cast<size_t>(s.branches());
   const size_t ntok = static_cast<size_t>(s.tokens());
   const size_t act = s.act_bytes();
@@ -91,6 +95,9 @@ Layout make_layout(const Shape& s, bool external_mid = false) {
   b[R_WIDE] = size_t(s.B) * moeca::kWideWords * 4;
   b[R_MID] = external_mid ? 0 : size_t(s.mid_rows()) * s.d_ff * act;
   b[R_H_SH] = size_t(s.S) * ntok * s.d * act;
+  b[R_PART] = partials && moeca::thin_capable(s)
+                  ? size_t(moeca::kThinSplit) * size_t(s.mid_rows()) * s.d * 4
+                  : 0;
   Layout L;
   size_t cur = 0;
   for (int i = 0; i < R_COUNT; ++i) {
@@ -137,6 +144,7 @@ Buffers map_buffers(char* w, const Layout& lay, void* mid) {
   b.row_dst = reinterpret_cast<int32_t*>(w + o[R_ROW_DST]);
   b.mid = mid != nullptr ? mid : w + o[R_MID];
   b.h_sh = w + o[R_H_SH];
+  b.part = lay.bytes[R_PART] != 0 ? reinterpret_cast<float*>(w + o[R_PART]) : nullptr;
   return b;
 }
 
@@ -160,6 +168,7 @@ struct moeca_layer {
   bool mid_outside = false;      // the FFN intermediate is not in ws
   void* external_mid = nullptr;  // its address when mid_outside
   bool last_full = false;
+  bool last_thin = false;
   bool timing = false;
   std::vector<hipEvent_t> events;
   int timed_steps = 0;
@@ -308,7 +317,7 @@ int moeca_forward_noalloc(const moeca_layer* L, const void* x, int samples, void
     return fail(MOECA_E_INVAL, "samples must be in [1, " + std::to_string(L->shape.B) + "]");
   Shape s = L->shape;
   s.B = samples;
-  const Layout lay = make_layout(s);
+  const Layout lay = make_layout(s, false, false);
   if (lay.total > moeca::kNoallocScratchBytes)
     return fail(MOECA_E_INVAL, "this call needs " + std::to_string(lay.total) +
                                    " bytes of scratch; the library's array holds " +
@@ -331,8 +340,10 @@ int moeca_forward_noalloc(const moeca_layer* L, const void* x, int samples, void
       (e = moeca::launch_decide(s, moeca::kSelFull, 0, p.lambda0, p.lambda1, p.lambda2, false,
                                 p.tau0, p.alpha, b, st)) == hipSuccess &&
       (e = moeca::launch_lists(s, moeca::ffn_plan(s), b, st)) == hipSuccess &&
-      (e = moeca::launch_ffn_up(s, x, L->W_up, L->W_up_sh, p.act, b, st)) == hipSuccess &&
-      (e = moeca::launch_ffn_down(s, L->W_down, L->W_down_sh, b, st)) == hipSuccess)
+      (e = moeca::launch_ffn_up(s, x, L->W_up, L->W_up_sh, p.act, moeca::ffn_plan(s), b, st)) ==
+          hipSuccess &&
+      (e = moeca::launch_ffn_down(s, L->W_down, L->W_down_sh, moeca::ffn_plan(s), b, st)) ==
+          hipSuccess)
     e = moeca::launch_combine(s, 0, out, nullptr, nullptr, b, st);
   if (e != hipSuccess) return fail(MOECA_E_HIP, std::string("launch: ") + hipGetErrorString(e));
   return MOECA_OK;
@@ -434,17 +445,23 @@ int layer_step(moeca_layer* L, const void* x_t, const void* x_ffn, int t, void* 
                                   p.alpha, b, st),
              "decide"))
     return MOECA_E_HIP;
+  // ratio-mode cache steps whose budget leaves few rows per expert stream
+  // the weights with the thin plan
+  const bool thin = !full && p.mode == MOECA_MODE_RATIO &&
+                    int64_t(budget) * s.B <= int64_t(moeca::kThinRows) * s.E &&
+                    L->buf.part != nullptr;
+  const moeca::FfnPlan plan = moeca::ffn_plan(s, thin);
   arm();
-  if (!check(moeca::launch_lists(s, moeca::ffn_plan(s), b, st), "lists")) return MOECA_E_HIP;
+  if (!check(moeca::launch_lists(s, plan, b, st), "lists")) return MOECA_E_HIP;
   if (between) {
     const int rc = between();
     if (rc != MOECA_OK) return rc;
   }
   arm();
-  if (!check(moeca::launch_ffn_up(s, x_ffn, L->W_up, L->W_up_sh, p.act, b, st), "ffn up"))
+  if (!check(moeca::launch_ffn_up(s, x_ffn, L->W_up, L->W_up_sh, p.act, plan, b, st), "ffn up"))
     return MOECA_E_HIP;
   arm();
-  if (!check(moeca::launch_ffn_down(s, L->W_down, L->W_down_sh, b, st), "ffn down"))
+  if (!check(moeca::launch_ffn_down(s, L->W_down, L->W_down_sh, plan, b, st), "ffn down"))
     return MOECA_E_HIP;
   arm();
   if (!check(moeca::launch_combine(s, uncached ? 0 : 1, out, L->attn_in, L->attn_cache, b, st),
@@ -453,6 +470,7 @@ int layer_step(moeca_layer* L, const void* x_t, const void* x_ffn, int t, void* 
   if (timed) ++L->timed_steps;
   if (!uncached) L->valid = true;
   L->last_full = full;
+  L->last_thin = plan.thin;
   return MOECA_OK;
 }
 
@@ -497,6 +515,7 @@ int moeca_get_stats(moeca_layer* L, moeca_stats* out, void* stream) {
   out->reuse_over_match =
       out->n_matched > 0 ? double(out->n_reused) / double(out->n_matched) : 0.0;
   out->full_step = L->last_full ? 1 : 0;
+  out->thin_ffn = L->last_thin ? 1 : 0;
   for (int32_t v : rf) out->nonfinite |= v;
   return MOECA_OK;
 }

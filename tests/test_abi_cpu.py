@@ -179,7 +179,12 @@ def test_workspace_grows_with_the_layer(L):
     c = L.moeca_layer_create(1152, 16, 2, 4608, _pol(L, batch=8, tokens=1024, dtype=1))
     try:
         wa, wb, wc = (L.moeca_workspace_bytes(h) for h in (a, b, c))
-        assert wb > 3.9 * wa and wc > 1.9 * wb
+        # the 256-token layer (256 rows per expert on a full step) may stream
+        # the weights with the thin plan: its workspace also holds the fp32
+        # partial sums of the down projection's four K pieces
+        part = 4 * (8 * 256 * 2) * 1152 * 4
+        assert wa > part
+        assert wb > 3.9 * (wa - part) and wc > 1.9 * wb
         # cache rows + FFN activation rows dominate: 16384 * (1152 + 4608) * 2 bytes
         assert wb >= 16384 * (1152 + 4608) * 2
     finally:

@@ -261,6 +261,38 @@ def test_xl1024_sampled(mode):
             assert abs(info["recompute_frac"] - 0.3) < 0.02
 
 
+@pytest.mark.timeout(600)
+def test_xl256_sampled():
+    """The layer at 256 tokens x 8 (d=1152, 16 experts, top-2, 4608 hidden,
+    30 % refresh): its cache steps leave about 77 rows per expert and take
+    the weight-streaming plan (128 x 288 tiles, the down projection in four
+    K pieces added in order); a refresh step, then three cache steps."""
+    shape = WORKLOADS["xl256"]
+    S = Setup(shape, mode="ratio", seed=12, T=4, ratio=0.3, refresh_cycle=0)
+    sample, ev = sampled_tokens(shape, 48, 13)
+    infos = run_sampled(S, 4, sample, ev, "xl256 ratio")
+    assert [i["thin_ffn"] for i in infos] == [0, 1, 1, 1]
+
+
+# ---------------------------------------------------------------------------
+# The weight-streaming plan at sizes the oracle evaluates whole: tiles that
+# are exactly 288 wide, ragged N tiles and K pieces (37 k-tiles: 9, 9, 9,
+# 10), and experts with more than one 128-row tile.
+# ---------------------------------------------------------------------------
+THIN_SHAPES = [
+    (LayerShape(d=576, E=16, k=2, d_ff=2304, B=2, N=128, dtype="bf16"), 0.3),
+    (LayerShape(d=640, E=16, k=2, d_ff=2368, B=2, N=100, dtype="bf16"), 0.3),
+    (LayerShape(d=576, E=8, k=2, d_ff=4608, B=4, N=256, dtype="bf16"), 0.4),
+]
+
+
+@pytest.mark.parametrize("shape,ratio", THIN_SHAPES)
+def test_thin_plan_trajectory(shape, ratio):
+    S = Setup(shape, mode="ratio", seed=31, T=4, ratio=ratio, refresh_cycle=0)
+    infos = run_forced(S, 4, label=f"thin {shape}")
+    assert [i["thin_ffn"] for i in infos] == [0, 1, 1, 1]
+
+
 # ---------------------------------------------------------------------------
 # Skewed routing: 32 experts with a Zipf(1.2) router prior, bimodal token
 # drift (90 % slow, 10 % fast), swept over refresh ratios.  Width reduced
