@@ -529,7 +529,7 @@ def main():
         L.reset()
         run(L, 0, warm)
         torch.cuda.synchronize()
-        rec, syn, flushed = [], [], []
+        rec, syn, flushed, thin = [], [], [], []
         for t in range(Wm, T):
             if flush is not None:
                 flush.fill_(t & 0xff)
@@ -542,8 +542,9 @@ def main():
                 flushed.append(e0.elapsed_time(e1))
             rec.append(st.n_recompute)
             syn.append(st.n_sync)
+            thin.append(st.thin_ffn)
         ms_flushed = float(np.mean(flushed)) if flushed else None
-        return ms_eager, ms_graph, graphed, stage, (rec, syn, ms_flushed)
+        return ms_eager, ms_graph, graphed, stage, (rec, syn, ms_flushed, thin)
 
     flush = (torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev)
              if args.flush_mib > 0 else None)
@@ -563,7 +564,7 @@ def main():
     for rho in [float(v) for v in args.sweep.split(",") if v.strip()]:
         log(f"[bench] sweep: cache steps at ratio {rho}")
         Ls = make(_lib.MOECA_MODE_RATIO, ratio=rho)
-        ms_e, ms_g, graphed_s, stage_s, (rec_s, _, _) = phase(Ls, Wm)
+        ms_e, ms_g, graphed_s, stage_s, (rec_s, _, _, _) = phase(Ls, Wm)
         Ls.close()
         sweep.append({"ratio": rho, "ms_per_step": round(ms_g, 4),
                       "refresh_ratio_actual": round(float(np.mean(rec_s)) / (shape.tokens * shape.k), 4),
@@ -595,7 +596,7 @@ def main():
            "dtype": shape.dtype, "data": "synthetic",
            "config": {"workload": wl, "batch": shape.B, "tokens": shape.N, "phase": args.phase}}
     if res_c is not None:
-        ms_eager, ms_graph, graphed, stage, (rec, syn, ms_flushed) = res_c
+        ms_eager, ms_graph, graphed, stage, (rec, syn, ms_flushed, thin) = res_c
         mean_rec = float(np.mean(rec))
         up_ms = stage["ffn_up"]
         ffn_ms = stage["ffn_up"] + stage["ffn_down"]
@@ -614,6 +615,8 @@ def main():
             traffic = None
         up_kernel = ("gemm_bf16_big_kernel<0,3> (expert FFN up-projection + SwiGLU)"
                      if act == "swiglu" else
+                     "gemm_bf16_thin_kernel<0,0,1> (expert FFN up-projection + GELU, "
+                     "weight-streaming tiles)" if np.mean(thin) > 0.5 else
                      "gemm_bf16_big_kernel<0,0> (expert FFN up-projection + GELU)")
         res.update({
             "value": round(ms_graph, 4),
@@ -626,6 +629,9 @@ def main():
             "recomputed_branches": round(mean_rec, 1),
             "shared_expert_rows": shared_rows,
             "synchronized_tokens": round(float(np.mean(syn)), 1),
+            # share of the timed steps whose expert FFN took the
+            # weight-streaming (few rows per expert) tiling
+            "thin_ffn_steps": round(float(np.mean(thin)), 3),
             "stage_ms": {k: round(v, 4) for k, v in stage.items()},
             "step_hbm_frac": round(step_bytes / (ms_graph * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             "roofline": {
@@ -641,7 +647,7 @@ def main():
             },
         })
     if res_f is not None:
-        ms_eager_f, ms_graph_f, _, stage_f, (_, _, ms_flushed_f) = res_f
+        ms_eager_f, ms_graph_f, _, stage_f, (_, _, ms_flushed_f, _) = res_f
         res.update({"full_ms_per_step": round(ms_graph_f, 4),
                     "full_flushed_ms_per_step": None if ms_flushed_f is None else round(ms_flushed_f, 4),
                     "eager_full_ms_per_step": round(ms_eager_f, 4),
