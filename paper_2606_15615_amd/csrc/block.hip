@@ -439,11 +439,12 @@ __global__ __launch_bounds__(kListThreads) void slist_kernel(
 // tile: the online softmax (running max and sum per query) needs one lane
 // exchange (l, l ^ 32) per tile.  The probabilities, rounded to bf16, are
 // the B operand of O^T += V^T P^T, whose k order (keys) follows the S^T
-// accumulator layout, so P never leaves registers; V^T sits in LDS.  The
-// tiles are software-pipelined over a three-stage LDS ring: while tile kt's
-// P.V MFMAs run, tile kt + 1's q.k MFMAs and softmax proceed, tile kt + 2 is
-// stored and tile kt + 3's global loads are in flight (two dependent chains
-// per wave).  KS = ceil(d_h / 16) k-steps for q.k,
+// accumulator layout, so P never leaves registers; V^T sits in LDS.  The K
+// and V tiles go through a two-stage LDS ring (50 KB at d_h = 72), so three
+// blocks share a CU (twelve waves): on a cache step the query tiles of the
+// synchronised tokens then run in one round instead of two.  Tile kt + 2's
+// global loads are issued before tile kt's math and stored into tile kt's
+// stage after the barrier that ends it.  KS = ceil(d_h / 16) k-steps for q.k,
 // OT = ceil(d_h / 32) output tiles of O^T; columns and rows past d_h are zero.
 // DH is d_h, a compile-time constant (every multiple of 8 up to 96 is
 // instantiated), so the chunk index arithmetic of the tile loads has
@@ -453,21 +454,26 @@ constexpr int kAttnKeys = 64;
 constexpr int kAttnThreads = 256;
 
 template <int KS, int OT, int DH>
-__global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
+__global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
     const uint16_t* __restrict__ q, const uint16_t* __restrict__ kv,
     const int32_t* __restrict__ slist, const int32_t* __restrict__ soff, int B, int N, int H,
     int dh_arg, float scale_log2, uint16_t* __restrict__ o) {
   static_assert(DH % 8 == 0 && DH <= 96, "head width");
   constexpr int dh = DH;
   (void)dh_arg;
-  constexpr int KP = 16 * KS + 8;     // K row in LDS (bf16), padded
-  constexpr int VR = 32 * OT;         // V^T rows (head dims)
-  constexpr int VP = kAttnKeys + 8;   // V^T row (keys), padded
-  constexpr int KE = kAttnKeys * KP;  // elements of one K stage
+  constexpr int CPR = DH / 8;              // 16-byte chunks per head row
+  // K rows in LDS: KC chunks, an odd count, so that the 16 rows a
+  // ds_read_b128 phase serves start on distinct 4-bank groups; the chunks
+  // past d_h hold whatever the loads put there and are never read
+  constexpr int KC = CPR | 1;
+  constexpr int KE = kAttnKeys * KC * 8;   // elements of one K stage
+  constexpr int KI = KC;                   // DMA instructions per K tile (64 chunks each)
+  constexpr int KIW = (KI + 3) / 4;        // per wave, at most
+  constexpr int VR = 32 * OT;              // V^T rows (head dims)
+  constexpr int VP = kAttnKeys + 8;        // V^T row (keys), padded
   constexpr int VE = VR * VP;
-  constexpr int kMaxLd =
-      (2 * kAttnKeys * (DH / 8) + kAttnThreads - 1) / kAttnThreads;  // chunks per thread
-  constexpr int kStg = 3;             // LDS ring stages
+  constexpr int kLd = (kAttnKeys * CPR + kAttnThreads - 1) / kAttnThreads;  // V chunks per thread
+  constexpr int kStg = 2;                  // LDS ring stages
   __shared__ __attribute__((aligned(16))) uint16_t sk[kStg * KE];
   __shared__ __attribute__((aligned(16))) uint16_t sv[kStg * VE];
 
@@ -486,11 +492,8 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
   const int tid = threadIdx.x, lane = tid & 63, wv = tid >> 6;
   const int n = lane & 31, hf = lane >> 5;
   const int d = H * dh;
-  const int cpr = dh / 8;  // 16-byte chunks per head row
 
-  // zero every stage once: K columns and V^T rows past d_h stay zero
-  for (int i = tid; i < (kStg * KE) / 8; i += kAttnThreads)
-    reinterpret_cast<u32x4_t*>(sk)[i] = u32x4_t{0, 0, 0, 0};
+  // zero the V stages once: V^T rows past d_h stay zero
   for (int i = tid; i < (kStg * VE) / 8; i += kAttnThreads)
     reinterpret_cast<u32x4_t*>(sv)[i] = u32x4_t{0, 0, 0, 0};
 
@@ -507,60 +510,66 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
   }
 
   const int64_t row0 = int64_t(b) * N;
-  const int nld = 2 * kAttnKeys * cpr;  // chunks of one K + V tile
-  const int kch = kAttnKeys * cpr;      // chunks of the K half
-  // Chunk c of a tile: K chunks (c < kch) run along a key row (16 bytes of
-  // 8 head dims each, coalesced), V chunks key-fastest, so the 64 lanes of
-  // a wave hold 8 head dims of 64 consecutive keys (kch is a multiple of 64:
-  // whole waves take K or V) and write V^T as dwords after one lane-pair
-  // exchange.
-  auto load_tile = [&](int kt, u32x4_t (&dst)[kMaxLd]) __attribute__((always_inline)) {
+  // K: direct global -> LDS loads.  DMA instruction i of a tile (wave i % 4)
+  // covers chunks 64 i .. 64 i + 63 of the stage, chunk q holding chunk
+  // q % KC of key q / KC (padding chunks load the key's first chunk).
+  const uint32_t sk0 = __builtin_amdgcn_readfirstlane(lds_addr(sk));
+  const int kwv = __builtin_amdgcn_readfirstlane(wv);
+  auto load_k = [&](int kt, int st) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < kMaxLd; ++u) {
-      const int c = tid + kAttnThreads * u;
-      if (c < nld) {
-        int key, col;
-        if (c < kch) {
-          key = c / cpr;
-          col = hh * dh + (c % cpr) * 8;
-        } else {
-          key = (c - kch) % kAttnKeys;
-          col = d + hh * dh + ((c - kch) / kAttnKeys) * 8;
-        }
-        key = min(kt * kAttnKeys + key, N - 1);
-        dst[u] = *reinterpret_cast<const u32x4_t*>(kv + (row0 + key) * (2 * d) + col);
+    for (int u = 0; u < KIW; ++u) {
+      const int i = kwv + 4 * u;
+      if (i < KI) {
+        const int qc = 64 * i + lane;
+        const int key = min(kt * kAttnKeys + qc / KC, N - 1);
+        const int c = qc % KC;
+        const uint16_t* g = kv + (row0 + key) * (2 * d) + hh * dh + (c < CPR ? c : 0) * 8;
+        dma16(g, sk0 + (st * KE + i * 512) * 2);
       }
     }
   };
-  auto store_tile = [&](int st, const u32x4_t (&src)[kMaxLd]) __attribute__((always_inline)) {
+  // V: through registers (it is stored transposed).  Chunk c of a tile:
+  // key c % 64, head dims 8 (c / 64) .. + 7, so the 64 lanes of a wave hold
+  // 8 head dims of 64 consecutive keys and write V^T as dwords after one
+  // lane-pair exchange.  Every thread issues kLd loads (chunks past the
+  // tile re-read its last chunk and are not stored), so that the count of
+  // loads in flight after a tile's K loads is known.
+  constexpr int nch = kAttnKeys * CPR;
+  auto load_v = [&](int kt, u32x4_t (&dst)[kLd]) __attribute__((always_inline)) {
 #pragma unroll
-    for (int u = 0; u < kMaxLd; ++u) {
+    for (int u = 0; u < kLd; ++u) {
+      const int c = min(tid + kAttnThreads * u, nch - 1);
+      const int key = min(kt * kAttnKeys + c % kAttnKeys, N - 1);
+      const int col = d + hh * dh + (c / kAttnKeys) * 8;
+      dst[u] = *reinterpret_cast<const u32x4_t*>(kv + (row0 + key) * (2 * d) + col);
+    }
+  };
+  auto store_v = [&](int st, const u32x4_t (&src)[kLd]) __attribute__((always_inline)) {
+#pragma unroll
+    for (int u = 0; u < kLd; ++u) {
       const int c = tid + kAttnThreads * u;
-      if (c < nld) {
-        if (c < kch) {
-          *reinterpret_cast<u32x4_t*>(sk + st * KE + (c / cpr) * KP + (c % cpr) * 8) = src[u];
-        } else {
-          // lanes 2i, 2i + 1 hold keys 2i, 2i + 1: the even lane writes head
-          // dims 0-3 of both, the odd lane dims 4-7, one dword per dim
-          const int key = (c - kch) % kAttnKeys;
-          const int ch = (c - kch) / kAttnKeys;
-          const bool odd = key & 1;
-          u32x4_t other;
+      // wave-uniform: nch is a multiple of 64
+      if (c < nch) {
+        // lanes 2i, 2i + 1 hold keys 2i, 2i + 1: the even lane writes head
+        // dims 0-3 of both, the odd lane dims 4-7, one dword per dim
+        const int key = c % kAttnKeys;
+        const int ch = c / kAttnKeys;
+        const bool odd = key & 1;
+        u32x4_t other;
 #pragma unroll
-          for (int e = 0; e < 4; ++e) other[e] = static_cast<uint32_t>(dpp_i32<kDppRow[0]>(
-                                                     static_cast<int>(src[u][e])));
-          uint32_t* vt = reinterpret_cast<uint32_t*>(sv + st * VE + (ch * 8 + (odd ? 4 : 0)) * VP +
-                                                     (key & ~1));
+        for (int e = 0; e < 4; ++e) other[e] = static_cast<uint32_t>(dpp_i32<kDppRow[0]>(
+                                                   static_cast<int>(src[u][e])));
+        uint32_t* vt = reinterpret_cast<uint32_t*>(sv + st * VE + (ch * 8 + (odd ? 4 : 0)) * VP +
+                                                   (key & ~1));
 #pragma unroll
-          for (int e = 0; e < 2; ++e) {
-            // head dims 2e, 2e + 1 of this lane's half (dims 4 + ... for odd)
-            const uint32_t mine = odd ? src[u][2 + e] : src[u][e];
-            const uint32_t part = odd ? other[2 + e] : other[e];
-            const uint32_t lo_key = odd ? part : mine;  // the even key's pair of dims
-            const uint32_t hi_key = odd ? mine : part;
-            vt[(2 * e) * (VP / 2)] = (lo_key & 0xffffu) | (hi_key << 16);
-            vt[(2 * e + 1) * (VP / 2)] = (lo_key >> 16) | (hi_key & 0xffff0000u);
-          }
+        for (int e = 0; e < 2; ++e) {
+          // head dims 2e, 2e + 1 of this lane's half (dims 4 + ... for odd)
+          const uint32_t mine = odd ? src[u][2 + e] : src[u][e];
+          const uint32_t part = odd ? other[2 + e] : other[e];
+          const uint32_t lo_key = odd ? part : mine;  // the even key's pair of dims
+          const uint32_t hi_key = odd ? mine : part;
+          vt[(2 * e) * (VP / 2)] = (lo_key & 0xffffu) | (hi_key << 16);
+          vt[(2 * e + 1) * (VP / 2)] = (lo_key >> 16) | (hi_key & 0xffff0000u);
         }
       }
     }
@@ -583,8 +592,11 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
       for (int v = 0; v < 16; ++v) sacc[t][v] = 0.0f;
 #pragma unroll
       for (int s2 = 0; s2 < KS; ++s2) {
+        // head dims past d_h (chunk CPR and above) are zero, as in q
+        const int cc = 2 * s2 + hf;
         const bf16x8_t kf =
-            *reinterpret_cast<const bf16x8_t*>(ks + (32 * t + n) * KP + 16 * s2 + 8 * hf);
+            cc < CPR ? *reinterpret_cast<const bf16x8_t*>(ks + ((32 * t + n) * KC + cc) * 8)
+                     : bf16x8_t{};
         sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s2], sacc[t], 0, 0, 0);
       }
     }
@@ -659,36 +671,40 @@ __global__ __launch_bounds__(kAttnThreads, 2) void attention_kernel(
         }
   };
 
-  // Prologue: tiles 0 and 1 stored, tile 2's loads in flight, tile 0's q.k
-  // and softmax done.  Iteration kt reads stage kt + 1 (q.k) and stage kt
-  // (p.v) and fills stage kt + 2, last read by the p.v of iteration kt - 1,
-  // before the previous barrier; the p.v of tile kt accumulates before the
-  // softmax of tile kt + 1 rescales O.
+  // Prologue: tiles 0 and 1 in their stages.  Iteration kt runs tile kt's
+  // q.k and softmax, issues tile kt + 2's V loads, runs the p.v on stage
+  // kt % 2, waits for tile kt + 1's K loads (issued in the previous
+  // iteration, before this one's V loads: at most kLd loads may remain),
+  // and after the barrier (every wave done with stage kt % 2) stores tile
+  // kt + 2's V there and starts its K loads into it.
   const int nkt = (N + kAttnKeys - 1) / kAttnKeys;
-  u32x4_t ld[kMaxLd];
-  load_tile(0, ld);
-  __syncthreads();  // zeroing done before the first tile lands
-  store_tile(0, ld);
+  u32x4_t ld[kLd];
+  __syncthreads();  // V zeroing done before the first tile lands
+  load_k(0, 0);
+  load_v(0, ld);
+  store_v(0, ld);
   if (nkt > 1) {
-    load_tile(1, ld);
-    store_tile(1, ld);
+    load_k(1, 1);
+    load_v(1, ld);
+    store_v(1, ld);
   }
-  if (nkt > 2) load_tile(2, ld);
+  wait_vmcnt<0>();
   __syncthreads();
-  bf16x8_t pcur[4];
-  {
-    f32x16_t s0[2];
-    qk(0, s0);
-    softmax(0, s0, pcur);
-  }
   for (int kt = 0; kt < nkt; ++kt) {
-    f32x16_t snext[2];
-    if (kt + 1 < nkt) qk(kt + 1, snext);
-    pv(kt, pcur);
-    if (kt + 2 < nkt) store_tile((kt + 2) % kStg, ld);
-    if (kt + 3 < nkt) load_tile(kt + 3, ld);
-    if (kt + 1 < nkt) softmax(kt + 1, snext, pcur);
+    f32x16_t sacc[2];
+    bf16x8_t pf[4];
+    qk(kt, sacc);
+    softmax(kt, sacc, pf);
+    const bool more = kt + 2 < nkt;  // block-uniform
+    if (more) load_v(kt + 2, ld);
+    pv(kt, pf);
+    if (more) wait_vmcnt<kLd>();
+    else wait_vmcnt<0>();
     __syncthreads();
+    if (more) {
+      store_v(kt % kStg, ld);
+      load_k(kt + 2, kt % kStg);
+    }
   }
 
   // normalise and store: lane holds head dims 32 ot + 8 g + 4 hf + (0..3)

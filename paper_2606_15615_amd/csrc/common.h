@@ -30,6 +30,39 @@ template <> struct Act<float> {
   static __device__ __forceinline__ float from_f32(float v) { return v; }
 };
 
+// ---- direct global -> LDS loads ---------------------------------------------
+// 16 bytes per lane, global -> LDS at the wave-uniform LDS byte address
+// `lds` (lane l lands at lds + 16 l).  Issued as inline assembly so that the
+// compiler does not treat it as an LDS store: it would otherwise wait for
+// every outstanding DMA before each LDS read.  The kernel orders the
+// accesses itself with s_waitcnt vmcnt and s_barrier (loads complete in
+// order, so the compiler's own vmcnt waits stay conservative).  m0 is
+// reserved by the compiler, which may not preserve it around the statement:
+// this is safe because no kernel here has other m0 uses (the generated code
+// contains no m0 access besides these statements).
+__device__ __forceinline__ void dma16(const uint16_t* g, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off"
+      :
+      : "s"(lds), "v"(g)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ uint32_t lds_addr(const void* p) {
+  return static_cast<uint32_t>(
+      reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)p));
+}
+
+// Wait until at most N vector memory operations of this wave are in flight
+// (gfx9 encoding of s_waitcnt, N < 16; expcnt and lgkmcnt not waited for).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 16, "vmcnt");
+  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
+}
+
 // ---- lane exchange within 16-lane rows (DPP) -------------------------------
 // Row permutations: xor 1, xor 2, half-row mirror, row mirror.  Applied in
 // this order, a commutative reduction leaves every lane of the row with the

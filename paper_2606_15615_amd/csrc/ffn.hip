@@ -386,29 +386,6 @@ __device__ __forceinline__ void s_waitcnt_vm(int n) {
   else __builtin_amdgcn_s_waitcnt(0x0F70 | kLoadsPerStage);
 }
 
-// 16 bytes per lane, global -> LDS at the wave-uniform LDS byte address
-// `lds` (lane l lands at lds + 16 l).  Issued as inline assembly so that the
-// compiler does not treat it as an LDS store: it would otherwise wait for
-// every outstanding DMA before each LDS read.  The kernel orders the
-// accesses itself with s_waitcnt vmcnt and s_barrier (loads complete in
-// order, so the compiler's own vmcnt waits stay conservative).  m0 is
-// reserved by the compiler, which may not preserve it around the statement:
-// this is safe because no kernel here has other m0 uses (the generated code
-// contains no m0 access besides these statements).
-__device__ __forceinline__ void dma16(const uint16_t* g, uint32_t lds) {
-  asm volatile(
-      "s_mov_b32 m0, %0\n\t"
-      "s_nop 0\n\t"
-      "global_load_lds_dwordx4 %1, off"
-      :
-      : "s"(lds), "v"(g)
-      : "memory", "m0");
-}
-
-__device__ __forceinline__ uint32_t lds_addr(const void* p) {
-  return static_cast<uint32_t>(
-      reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)p));
-}
 
 // MFMA operand fragments of one 16-wide k-step: weights are the A operand
 // (32 output columns x 16 k), token rows the B operand (16 k x 32 rows), so
@@ -736,12 +713,6 @@ static_assert(kThinInstB % kThinWaves == kThinWaves / 2, "waves 0-3 issue one mo
 
 typedef __attribute__((ext_vector_type(4))) float f32x4_t;
 
-template <int N>
-__device__ __forceinline__ void s_waitcnt_vm_n() {
-  // gfx9 encoding, vmcnt N < 16: expcnt and lgkmcnt left at their maxima
-  static_assert(N >= 0 && N < 16, "vmcnt");
-  __builtin_amdgcn_s_waitcnt(0x0F70 | N);
-}
 
 template <int KIND, int ACT, int SPLIT>
 __global__ __launch_bounds__(kThinThreads, 1) void gemm_bf16_thin_kernel(
@@ -842,9 +813,9 @@ __global__ __launch_bounds__(kThinThreads, 1) void gemm_bf16_thin_kernel(
   // this wave's loads of the oldest stage in flight have landed once at most
   // one later stage's loads are outstanding
   auto wait_stage = [&](bool last) __attribute__((always_inline)) {
-    if (last) s_waitcnt_vm_n<0>();
-    else if (five) s_waitcnt_vm_n<kThinLoadsA + kThinLoadsB>();
-    else s_waitcnt_vm_n<kThinLoadsA + kThinLoadsB - 1>();
+    if (last) wait_vmcnt<0>();
+    else if (five) wait_vmcnt<kThinLoadsA + kThinLoadsB>();
+    else wait_vmcnt<kThinLoadsA + kThinLoadsB - 1>();
   };
 
   int L = lo + static_cast<int>(blockIdx.x) / kXcds;
