@@ -493,9 +493,16 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
   const int n = lane & 31, hf = lane >> 5;
   const int d = H * dh;
 
-  // zero the V stages once: V^T rows past d_h stay zero
-  for (int i = tid; i < (kStg * VE) / 8; i += kAttnThreads)
-    reinterpret_cast<u32x4_t*>(sv)[i] = u32x4_t{0, 0, 0, 0};
+  // V^T rows past d_h, set once: zero, except that when d_h is not a
+  // multiple of 32 the first of them holds ones, so that its row of O^T
+  // accumulates the softmax denominator sum_k p_k (of the bf16 p the p.v
+  // MFMAs use) with the same rescaling as O, and the VALU adds none
+  constexpr bool kSumRow = DH % 32 != 0;
+  for (int i = tid; i < (kStg * VE) / 8; i += kAttnThreads) {
+    const bool ones = kSumRow && (i % (VE / 8)) / (VP / 8) == DH;
+    const uint32_t v = ones ? 0x3F803F80u : 0u;  // two bf16 1.0
+    reinterpret_cast<u32x4_t*>(sv)[i] = u32x4_t{v, v, v, v};
+  }
 
   // this lane's query and its fragments (B operand of S^T)
   const int qi = qt * kAttnQ + wv * 32 + n;
@@ -630,17 +637,17 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
       for (int v = 0; v < 16; ++v) {
         const float p = __builtin_amdgcn_exp2f(fmaf(sacc[t][v], scale_log2, -m_new));
         sacc[t][v] = p;
-        ps += p;
+        if constexpr (!kSumRow) ps += p;
       }
     if (__ballot(m_new != m_run) != 0ull) {
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
+      if constexpr (!kSumRow) l_run *= alpha;
 #pragma unroll
       for (int t = 0; t < OT; ++t)
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[t][v] *= alpha;
     }
-    l_run += ps;
+    if constexpr (!kSumRow) l_run += ps;
     m_run = m_new;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
@@ -707,8 +714,19 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
     }
   }
 
-  // normalise and store: lane holds head dims 32 ot + 8 g + 4 hf + (0..3)
-  const float l_tot = l_run + __shfl_xor(l_run, 32, kWave);
+  // normalise and store: lane holds head dims 32 ot + 8 g + 4 hf + (0..3);
+  // the denominator: the ones row d_h of O^T (held by the lanes of half
+  // (d_h % 8) / 4, register 4 ((d_h % 32) / 8) + d_h % 4 of tile d_h / 32),
+  // or the two halves' running sums
+  float l_tot;
+  if constexpr (kSumRow) {
+    constexpr int so = DH / 32, sr = 4 * ((DH % 32) / 8) + DH % 4, sh = (DH % 8) / 4;
+    const float mine = acc[so][sr];
+    const float other = __shfl_xor(mine, 32, kWave);
+    l_tot = hf == sh ? mine : other;
+  } else {
+    l_tot = l_run + __shfl_xor(l_run, 32, kWave);
+  }
   const float inv = 1.0f / l_tot;
   if (qi < nq) {
     uint16_t* orow = o + int64_t(tok) * d + hh * dh;
