@@ -529,7 +529,7 @@ def main():
         L.reset()
         run(L, 0, warm)
         torch.cuda.synchronize()
-        rec, syn, flushed, thin = [], [], [], []
+        rec, syn, flushed, plan = [], [], [], []
         for t in range(Wm, T):
             if flush is not None:
                 flush.fill_(t & 0xff)
@@ -542,9 +542,9 @@ def main():
                 flushed.append(e0.elapsed_time(e1))
             rec.append(st.n_recompute)
             syn.append(st.n_sync)
-            thin.append(st.thin_ffn)
+            plan.append(st.ffn_plan)
         ms_flushed = float(np.mean(flushed)) if flushed else None
-        return ms_eager, ms_graph, graphed, stage, (rec, syn, ms_flushed, thin)
+        return ms_eager, ms_graph, graphed, stage, (rec, syn, ms_flushed, plan)
 
     flush = (torch.empty(args.flush_mib << 20, dtype=torch.uint8, device=dev)
              if args.flush_mib > 0 else None)
@@ -596,7 +596,7 @@ def main():
            "dtype": shape.dtype, "data": "synthetic",
            "config": {"workload": wl, "batch": shape.B, "tokens": shape.N, "phase": args.phase}}
     if res_c is not None:
-        ms_eager, ms_graph, graphed, stage, (rec, syn, ms_flushed, thin) = res_c
+        ms_eager, ms_graph, graphed, stage, (rec, syn, ms_flushed, plan) = res_c
         mean_rec = float(np.mean(rec))
         up_ms = stage["ffn_up"]
         ffn_ms = stage["ffn_up"] + stage["ffn_down"]
@@ -616,7 +616,7 @@ def main():
         up_kernel = ("gemm_bf16_big_kernel<0,3> (expert FFN up-projection + SwiGLU)"
                      if act == "swiglu" else
                      "gemm_bf16_thin_kernel<0,0,1> (expert FFN up-projection + GELU, "
-                     "weight-streaming tiles)" if np.mean(thin) > 0.5 else
+                     "weight-streaming tiles)" if np.mean(np.array(plan) == 1) > 0.5 else
                      "gemm_bf16_big_kernel<0,0> (expert FFN up-projection + GELU)")
         res.update({
             "value": round(ms_graph, 4),
@@ -629,9 +629,9 @@ def main():
             "recomputed_branches": round(mean_rec, 1),
             "shared_expert_rows": shared_rows,
             "synchronized_tokens": round(float(np.mean(syn)), 1),
-            # share of the timed steps whose expert FFN took the
-            # weight-streaming (few rows per expert) tiling
-            "thin_ffn_steps": round(float(np.mean(thin)), 3),
+            # tiling of the expert FFN on the counted steps: 0 the 128 x 256
+            # tiles, 1 the weight-streaming tiles
+            "ffn_plan_steps": {str(v): int(c) for v, c in zip(*np.unique(plan, return_counts=True))},
             "stage_ms": {k: round(v, 4) for k, v in stage.items()},
             "step_hbm_frac": round(step_bytes / (ms_graph * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
             "roofline": {

@@ -205,8 +205,9 @@ typedef struct moeca_stats {
   int32_t nonfinite;       /* 1 if a router logit was NaN or infinite          */
   double reuse_over_match; /* n_reused / n_matched (Sec. 5.4, Fig. 8); 0 if none */
   int32_t expert_count[64];/* recomputed branches per expert                  */
-  int32_t thin_ffn;        /* 1 if the expert FFN of the last step streamed the
-                              weights with the few-rows-per-expert tiling    */
+  int32_t ffn_plan;        /* tiling of the last step's expert FFN: 0 the
+                              128 x 256 tiles, 1 the weight-streaming tiles
+                              (few rows per expert)                          */
 } moeca_stats;
 
 /* Copy the last step's statistics to *out.  Synchronises the stream. */

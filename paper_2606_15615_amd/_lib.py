@@ -49,7 +49,7 @@ class moeca_stats(ctypes.Structure):
         ("n_reused", ctypes.c_int64), ("n_sync", ctypes.c_int64),
         ("full_step", ctypes.c_int32), ("nonfinite", ctypes.c_int32),
         ("reuse_over_match", ctypes.c_double), ("expert_count", ctypes.c_int32 * 64),
-        ("thin_ffn", ctypes.c_int32),
+        ("ffn_plan", ctypes.c_int32),
     ]
 
 

@@ -168,7 +168,7 @@ struct moeca_layer {
   bool mid_outside = false;      // the FFN intermediate is not in ws
   void* external_mid = nullptr;  // its address when mid_outside
   bool last_full = false;
-  bool last_thin = false;
+  int last_plan = 0;
   bool timing = false;
   std::vector<hipEvent_t> events;
   int timed_steps = 0;
@@ -470,7 +470,7 @@ int layer_step(moeca_layer* L, const void* x_t, const void* x_ffn, int t, void* 
   if (timed) ++L->timed_steps;
   if (!uncached) L->valid = true;
   L->last_full = full;
-  L->last_thin = plan.thin;
+  L->last_plan = plan.thin ? 1 : 0;
   return MOECA_OK;
 }
 
@@ -515,7 +515,7 @@ int moeca_get_stats(moeca_layer* L, moeca_stats* out, void* stream) {
   out->reuse_over_match =
       out->n_matched > 0 ? double(out->n_reused) / double(out->n_matched) : 0.0;
   out->full_step = L->last_full ? 1 : 0;
-  out->thin_ffn = L->last_thin ? 1 : 0;
+  out->ffn_plan = L->last_plan;
   for (int32_t v : rf) out->nonfinite |= v;
   return MOECA_OK;
 }

@@ -184,7 +184,7 @@ def check_step(S: Setup, t: int, rec: dict, out_o, st_old: O.State, st_new: O.St
     dims, dt = S.dims, S.shape.dtype
     B, N, k, E, d = dims.B, dims.N, dims.k, dims.E, dims.d
     tol = TOL[dt]
-    info = {"label": label, "t": t, "thin_ffn": int(L.stats().thin_ffn)}
+    info = {"label": label, "t": t, "ffn_plan": int(L.stats().ffn_plan)}
     forced = {}
 
     # router: logits bit-exact unless the oracle's fp64 sum is a near-tie

@@ -271,7 +271,7 @@ def test_xl256_sampled():
     S = Setup(shape, mode="ratio", seed=12, T=4, ratio=0.3, refresh_cycle=0)
     sample, ev = sampled_tokens(shape, 48, 13)
     infos = run_sampled(S, 4, sample, ev, "xl256 ratio")
-    assert [i["thin_ffn"] for i in infos] == [0, 1, 1, 1]
+    assert [i["ffn_plan"] for i in infos] == [0, 1, 1, 1]
 
 
 # ---------------------------------------------------------------------------
@@ -290,7 +290,7 @@ THIN_SHAPES = [
 def test_thin_plan_trajectory(shape, ratio):
     S = Setup(shape, mode="ratio", seed=31, T=4, ratio=ratio, refresh_cycle=0)
     infos = run_forced(S, 4, label=f"thin {shape}")
-    assert [i["thin_ffn"] for i in infos] == [0, 1, 1, 1]
+    assert [i["ffn_plan"] for i in infos] == [0, 1, 1, 1]
 
 
 # ---------------------------------------------------------------------------
