@@ -18,6 +18,8 @@ typedef __attribute__((ext_vector_type(4))) unsigned int u32x4_t;
 typedef __attribute__((ext_vector_type(2))) unsigned int u32x2_t;
 typedef __attribute__((ext_vector_type(2))) float f32x2_t;
 typedef __attribute__((ext_vector_type(2))) __bf16 bf16x2_t;
+typedef __attribute__((ext_vector_type(4))) short v4i16_t;
+typedef __attribute__((ext_vector_type(8))) short v8i16_t;
 
 __device__ __forceinline__ uint32_t pack2(float a, float b) {
   return __builtin_bit_cast(uint32_t, __builtin_convertvector(f32x2_t{a, b}, bf16x2_t));
@@ -439,16 +441,18 @@ __global__ __launch_bounds__(kListThreads) void slist_kernel(
 // tile: the online softmax (running max and sum per query) needs one lane
 // exchange (l, l ^ 32) per tile.  The probabilities, rounded to bf16, are
 // the B operand of O^T += V^T P^T, whose k order (keys) follows the S^T
-// accumulator layout, so P never leaves registers; V^T sits in LDS.  The K
-// and V tiles go through a two-stage LDS ring (50 KB at d_h = 72), so three
+// accumulator layout, so P never leaves registers.  K and V tiles land in
+// LDS key-major, as they sit in memory, through direct global -> LDS loads
+// (no register staging), in a two-stage ring (36 KB at d_h = 72), so three
 // blocks share a CU (twelve waves): on a cache step the query tiles of the
-// synchronised tokens then run in one round instead of two.  Tile kt + 2's
-// global loads are issued before tile kt's math and stored into tile kt's
-// stage after the barrier that ends it.  KS = ceil(d_h / 16) k-steps for q.k,
-// OT = ceil(d_h / 32) output tiles of O^T; columns and rows past d_h are zero.
-// DH is d_h, a compile-time constant (every multiple of 8 up to 96 is
-// instantiated), so the chunk index arithmetic of the tile loads has
-// constant divisors and the register staging is sized to the width.
+// synchronised tokens then run in one round instead of two.  The V^T
+// operand of p.v is read from the key-major V tile with the transposing
+// LDS read.  Tile kt + 2's loads start after the barrier that ends tile
+// kt's math and run under tile kt + 1's.  KS = ceil(d_h / 16) k-steps for
+// q.k, OT = ceil(d_h / 32) output tiles of O^T; columns and rows past d_h
+// are zero.  DH is d_h, a compile-time constant (every multiple of 8 up to
+// 96 is instantiated), so the chunk index arithmetic of the tile loads has
+// constant divisors.
 constexpr int kAttnQ = 128;
 constexpr int kAttnKeys = 64;
 constexpr int kAttnThreads = 256;
@@ -462,20 +466,16 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
   constexpr int dh = DH;
   (void)dh_arg;
   constexpr int CPR = DH / 8;              // 16-byte chunks per head row
-  // K rows in LDS: KC chunks, an odd count, so that the 16 rows a
-  // ds_read_b128 phase serves start on distinct 4-bank groups; the chunks
-  // past d_h hold whatever the loads put there and are never read
+  // K and V rows in LDS (key-major, as in memory): KC chunks, an odd count,
+  // so that the rows a read phase serves start on distinct bank groups; the
+  // chunks past d_h hold whatever the loads put there and are never used
   constexpr int KC = CPR | 1;
-  constexpr int KE = kAttnKeys * KC * 8;   // elements of one K stage
-  constexpr int KI = KC;                   // DMA instructions per K tile (64 chunks each)
-  constexpr int KIW = (KI + 3) / 4;        // per wave, at most
-  constexpr int VR = 32 * OT;              // V^T rows (head dims)
-  constexpr int VP = kAttnKeys + 8;        // V^T row (keys), padded
-  constexpr int VE = VR * VP;
-  constexpr int kLd = (kAttnKeys * CPR + kAttnThreads - 1) / kAttnThreads;  // V chunks per thread
+  constexpr int KE = kAttnKeys * KC * 8;   // elements of one K (or V) stage
+  constexpr int KI = KC;                   // DMA instructions per tile of K or V (64 chunks each)
+  constexpr int KIW = (2 * KI + 3) / 4;    // per wave and tile, at most
   constexpr int kStg = 2;                  // LDS ring stages
   __shared__ __attribute__((aligned(16))) uint16_t sk[kStg * KE];
-  __shared__ __attribute__((aligned(16))) uint16_t sv[kStg * VE];
+  __shared__ __attribute__((aligned(16))) uint16_t sv[kStg * KE];
 
   // (sample, head, query tile); the query tiles of one (sample, head) are
   // consecutive logical blocks on one XCD, so they share its L2 copy of K, V
@@ -493,16 +493,11 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
   const int n = lane & 31, hf = lane >> 5;
   const int d = H * dh;
 
-  // V^T rows past d_h, set once: zero, except that when d_h is not a
-  // multiple of 32 the first of them holds ones, so that its row of O^T
-  // accumulates the softmax denominator sum_k p_k (of the bf16 p the p.v
-  // MFMAs use) with the same rescaling as O, and the VALU adds none
+  // the V^T rows past d_h of the p.v operand are zero, except that when
+  // d_h is not a multiple of 32 the first of them is all ones, so that its
+  // row of O^T accumulates the softmax denominator sum_k p_k (of the bf16 p
+  // the p.v MFMAs use) with the same rescaling as O, and the VALU adds none
   constexpr bool kSumRow = DH % 32 != 0;
-  for (int i = tid; i < (kStg * VE) / 8; i += kAttnThreads) {
-    const bool ones = kSumRow && (i % (VE / 8)) / (VP / 8) == DH;
-    const uint32_t v = ones ? 0x3F803F80u : 0u;  // two bf16 1.0
-    reinterpret_cast<u32x4_t*>(sv)[i] = u32x4_t{v, v, v, v};
-  }
 
   // this lane's query and its fragments (B operand of S^T)
   const int qi = qt * kAttnQ + wv * 32 + n;
@@ -517,67 +512,27 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
   }
 
   const int64_t row0 = int64_t(b) * N;
-  // K: direct global -> LDS loads.  DMA instruction i of a tile (wave i % 4)
-  // covers chunks 64 i .. 64 i + 63 of the stage, chunk q holding chunk
-  // q % KC of key q / KC (padding chunks load the key's first chunk).
+  // K and V: direct global -> LDS loads, key-major rows of KC chunks.  DMA
+  // instruction i (wave i % 4) of a tile covers chunks 64 ii .. 64 ii + 63
+  // of the K stage (i < KI, ii = i) or of the V stage (ii = i - KI), chunk
+  // qc holding chunk qc % KC of key qc / KC (padding chunks load the key's
+  // first chunk).
   const uint32_t sk0 = __builtin_amdgcn_readfirstlane(lds_addr(sk));
+  const uint32_t sv0 = __builtin_amdgcn_readfirstlane(lds_addr(sv));
   const int kwv = __builtin_amdgcn_readfirstlane(wv);
-  auto load_k = [&](int kt, int st) __attribute__((always_inline)) {
+  auto load_kv = [&](int kt, int st) __attribute__((always_inline)) {
 #pragma unroll
     for (int u = 0; u < KIW; ++u) {
       const int i = kwv + 4 * u;
-      if (i < KI) {
-        const int qc = 64 * i + lane;
+      if (i < 2 * KI) {
+        const bool isv = i >= KI;
+        const int ii = isv ? i - KI : i;
+        const int qc = 64 * ii + lane;
         const int key = min(kt * kAttnKeys + qc / KC, N - 1);
         const int c = qc % KC;
-        const uint16_t* g = kv + (row0 + key) * (2 * d) + hh * dh + (c < CPR ? c : 0) * 8;
-        dma16(g, sk0 + (st * KE + i * 512) * 2);
-      }
-    }
-  };
-  // V: through registers (it is stored transposed).  Chunk c of a tile:
-  // key c % 64, head dims 8 (c / 64) .. + 7, so the 64 lanes of a wave hold
-  // 8 head dims of 64 consecutive keys and write V^T as dwords after one
-  // lane-pair exchange.  Every thread issues kLd loads (chunks past the
-  // tile re-read its last chunk and are not stored), so that the count of
-  // loads in flight after a tile's K loads is known.
-  constexpr int nch = kAttnKeys * CPR;
-  auto load_v = [&](int kt, u32x4_t (&dst)[kLd]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int u = 0; u < kLd; ++u) {
-      const int c = min(tid + kAttnThreads * u, nch - 1);
-      const int key = min(kt * kAttnKeys + c % kAttnKeys, N - 1);
-      const int col = d + hh * dh + (c / kAttnKeys) * 8;
-      dst[u] = *reinterpret_cast<const u32x4_t*>(kv + (row0 + key) * (2 * d) + col);
-    }
-  };
-  auto store_v = [&](int st, const u32x4_t (&src)[kLd]) __attribute__((always_inline)) {
-#pragma unroll
-    for (int u = 0; u < kLd; ++u) {
-      const int c = tid + kAttnThreads * u;
-      // wave-uniform: nch is a multiple of 64
-      if (c < nch) {
-        // lanes 2i, 2i + 1 hold keys 2i, 2i + 1: the even lane writes head
-        // dims 0-3 of both, the odd lane dims 4-7, one dword per dim
-        const int key = c % kAttnKeys;
-        const int ch = c / kAttnKeys;
-        const bool odd = key & 1;
-        u32x4_t other;
-#pragma unroll
-        for (int e = 0; e < 4; ++e) other[e] = static_cast<uint32_t>(dpp_i32<kDppRow[0]>(
-                                                   static_cast<int>(src[u][e])));
-        uint32_t* vt = reinterpret_cast<uint32_t*>(sv + st * VE + (ch * 8 + (odd ? 4 : 0)) * VP +
-                                                   (key & ~1));
-#pragma unroll
-        for (int e = 0; e < 2; ++e) {
-          // head dims 2e, 2e + 1 of this lane's half (dims 4 + ... for odd)
-          const uint32_t mine = odd ? src[u][2 + e] : src[u][e];
-          const uint32_t part = odd ? other[2 + e] : other[e];
-          const uint32_t lo_key = odd ? part : mine;  // the even key's pair of dims
-          const uint32_t hi_key = odd ? mine : part;
-          vt[(2 * e) * (VP / 2)] = (lo_key & 0xffffu) | (hi_key << 16);
-          vt[(2 * e + 1) * (VP / 2)] = (lo_key >> 16) | (hi_key & 0xffff0000u);
-        }
+        const uint16_t* g =
+            kv + (row0 + key) * (2 * d) + (isv ? d : 0) + hh * dh + (c < CPR ? c : 0) * 8;
+        dma16(g, (isv ? sv0 : sk0) + (st * KE + ii * 512) * 2);
       }
     }
   };
@@ -661,40 +616,51 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
       }
   };
   // O^T += V^T P^T for tile kt: fragment 2 t + j holds the keys
-  // 32 t + 16 j + 4 hf + {0..3, 8..11}
+  // 32 t + 16 j + 4 hf + {0..3, 8..11}.  The V^T operand (lane: head dim
+  // 32 ot + (lane & 31), those 8 keys) comes from the key-major V stage
+  // through ds_read_b64_tr_b16: within a group of 16 lanes, lane i receives
+  // element i % 4 of the 8-byte chunks that lanes 4 m + i / 4 (m = 0..3)
+  // point at.  So lane 4 m + a of the group points at head dims
+  // d0 + 4 a .. + 3 of key kb + m, and lane i (head dim d0 + i) receives
+  // keys kb .. kb + 3, then kb + 8 .. kb + 11 from a second read.  Head dims
+  // past d_h are replaced after the reads (their addresses are clamped).
+  const int i16 = lane & 15;
+  const int dl = 16 * ((lane >> 4) & 1);          // the group's first head dim in a tile
+  typedef __attribute__((address_space(3))) v4i16_t* lp;
   auto pv = [&](int kt, const bf16x8_t (&pf)[4]) __attribute__((always_inline)) {
-    const uint16_t* vs = sv + (kt % kStg) * VE;
+    const uint16_t* vs = sv + (kt % kStg) * KE;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
-      for (int j = 0; j < 2; ++j)
+      for (int j = 0; j < 2; ++j) {
+        const int kb = 32 * t + 16 * j + 4 * hf + (i16 >> 2);  // key this lane points at
 #pragma unroll
         for (int ot = 0; ot < OT; ++ot) {
-          const uint16_t* vp = vs + (32 * ot + n) * VP + 32 * t + 16 * j + 4 * hf;
-          const u32x2_t lo = *reinterpret_cast<const u32x2_t*>(vp);
-          const u32x2_t hi = *reinterpret_cast<const u32x2_t*>(vp + 8);
-          const bf16x8_t vf = __builtin_bit_cast(bf16x8_t, u32x4_t{lo[0], lo[1], hi[0], hi[1]});
+          const int col = 32 * ot + dl + 4 * (i16 & 3);
+          const uint16_t* vp = vs + kb * (KC * 8) + (col < DH ? col : 0);
+          const v4i16_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lp)(vp));
+          const v4i16_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lp)(vp + 8 * KC * 8));
+          bf16x8_t vf = __builtin_bit_cast(
+              bf16x8_t, v8i16_t{lo[0], lo[1], lo[2], lo[3], hi[0], hi[1], hi[2], hi[3]});
+          if (32 * ot + 32 > DH) {
+            const int dim = 32 * ot + dl + i16;  // this lane's head dim
+            if (dim >= DH) {
+              const uint32_t w = kSumRow && dim == DH ? 0x3F803F80u : 0u;  // bf16 ones or zeros
+              vf = __builtin_bit_cast(bf16x8_t, u32x4_t{w, w, w, w});
+            }
+          }
           acc[ot] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(vf, pf[2 * t + j], acc[ot], 0, 0, 0);
         }
+      }
   };
 
   // Prologue: tiles 0 and 1 in their stages.  Iteration kt runs tile kt's
-  // q.k and softmax, issues tile kt + 2's V loads, runs the p.v on stage
-  // kt % 2, waits for tile kt + 1's K loads (issued in the previous
-  // iteration, before this one's V loads: at most kLd loads may remain),
-  // and after the barrier (every wave done with stage kt % 2) stores tile
-  // kt + 2's V there and starts its K loads into it.
+  // q.k, softmax and p.v on stage kt % 2, waits for tile kt + 1's loads
+  // (issued in the previous iteration), and after the barrier (every wave
+  // done with stage kt % 2) starts tile kt + 2's loads into it.
   const int nkt = (N + kAttnKeys - 1) / kAttnKeys;
-  u32x4_t ld[kLd];
-  __syncthreads();  // V zeroing done before the first tile lands
-  load_k(0, 0);
-  load_v(0, ld);
-  store_v(0, ld);
-  if (nkt > 1) {
-    load_k(1, 1);
-    load_v(1, ld);
-    store_v(1, ld);
-  }
+  load_kv(0, 0);
+  if (nkt > 1) load_kv(1, 1);
   wait_vmcnt<0>();
   __syncthreads();
   for (int kt = 0; kt < nkt; ++kt) {
@@ -702,16 +668,10 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
     bf16x8_t pf[4];
     qk(kt, sacc);
     softmax(kt, sacc, pf);
-    const bool more = kt + 2 < nkt;  // block-uniform
-    if (more) load_v(kt + 2, ld);
     pv(kt, pf);
-    if (more) wait_vmcnt<kLd>();
-    else wait_vmcnt<0>();
+    wait_vmcnt<0>();
     __syncthreads();
-    if (more) {
-      store_v(kt % kStg, ld);
-      load_k(kt + 2, kt % kStg);
-    }
+    if (kt + 2 < nkt) load_kv(kt + 2, kt % kStg);
   }
 
   // normalise and store: lane holds head dims 32 ot + 8 g + 4 hf + (0..3);
