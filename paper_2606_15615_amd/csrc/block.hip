@@ -537,7 +537,12 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
     }
   };
 
-  // softmax state in log2 units of the scaled scores
+  // softmax state in log2 units of the scaled scores.  m_run is the shift of
+  // the exponentials, not always the running max: it moves only when a tile
+  // brings a score more than kLazy above it, so p = 2^(s - m_run) stays
+  // below 2^kLazy, and O (with the sum) is rescaled on few tiles instead of
+  // nearly every one.  The normalised result is the same up to rounding.
+  constexpr float kLazy = 8.0f;
   float m_run = -INFINITY, l_run = 0.0f;
   f32x16_t acc[OT];
 #pragma unroll
@@ -549,11 +554,14 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
   auto qk = [&](int kt, f32x16_t (&sacc)[2]) __attribute__((always_inline)) {
     const uint16_t* ks = sk + (kt % kStg) * KE;
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
+    for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int v = 0; v < 16; ++v) sacc[t][v] = 0.0f;
+    // the two key halves alternate, so consecutive MFMAs are independent
 #pragma unroll
-      for (int s2 = 0; s2 < KS; ++s2) {
+    for (int s2 = 0; s2 < KS; ++s2)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
         // head dims past d_h (chunk CPR and above) are zero, as in q
         const int cc = 2 * s2 + hf;
         const bf16x8_t kf =
@@ -561,7 +569,6 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
                      : bf16x8_t{};
         sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(kf, qf[s2], sacc[t], 0, 0, 0);
       }
-    }
   };
   // softmax of tile kt: keys past N masked (only a ragged last tile has
   // them), the running max and sum, O rescaled when some query's max moved,
@@ -584,26 +591,27 @@ __global__ __launch_bounds__(kAttnThreads, 3) void attention_kernel(
 #pragma unroll
       for (int v = 0; v < 16; ++v) mx = fmaxf(mx, sacc[t][v]);
     mx = fmaxf(mx, __shfl_xor(mx, 32, kWave)) * scale_log2;
-    const float m_new = fmaxf(m_run, mx);
-    float ps = 0.0f;
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[t][v], scale_log2, -m_new));
-        sacc[t][v] = p;
-        if constexpr (!kSumRow) ps += p;
-      }
-    if (__ballot(m_new != m_run) != 0ull) {
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    const bool up = mx > m_run + kLazy;  // always on the first tile
+    if (__ballot(up) != 0ull) {
+      const float m_new = up ? mx : m_run;
+      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);  // 0 on the first tile
       if constexpr (!kSumRow) l_run *= alpha;
 #pragma unroll
       for (int t = 0; t < OT; ++t)
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[t][v] *= alpha;
+      m_run = m_new;
     }
+    float ps = 0.0f;
+#pragma unroll
+    for (int t = 0; t < 2; ++t)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const float p = __builtin_amdgcn_exp2f(fmaf(sacc[t][v], scale_log2, -m_run));
+        sacc[t][v] = p;
+        if constexpr (!kSumRow) ps += p;
+      }
     if constexpr (!kSumRow) l_run += ps;
-    m_run = m_new;
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
