@@ -617,6 +617,8 @@ def main():
                      if act == "swiglu" else
                      "gemm_bf16_thin_kernel<0,0,1> (expert FFN up-projection + GELU, "
                      "weight-streaming tiles)" if np.mean(np.array(plan) == 1) > 0.5 else
+                     "gemm_bf16_wide_kernel<0> (expert FFN up-projection + GELU, "
+                     "expert-wide tiles)" if np.mean(np.array(plan) == 2) > 0.5 else
                      "gemm_bf16_big_kernel<0,0> (expert FFN up-projection + GELU)")
         res.update({
             "value": round(ms_graph, 4),
@@ -630,7 +632,8 @@ def main():
             "shared_expert_rows": shared_rows,
             "synchronized_tokens": round(float(np.mean(syn)), 1),
             # tiling of the expert FFN on the counted steps: 0 the 128 x 256
-            # tiles, 1 the weight-streaming tiles
+            # tiles, 1 the weight-streaming tiles, 2 the expert-wide
+            # up-projection tiles
             "ffn_plan_steps": {str(v): int(c) for v, c in zip(*np.unique(plan, return_counts=True))},
             "stage_ms": {k: round(v, 4) for k, v in stage.items()},
             "step_hbm_frac": round(step_bytes / (ms_graph * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),

@@ -207,7 +207,9 @@ typedef struct moeca_stats {
   int32_t expert_count[64];/* recomputed branches per expert                  */
   int32_t ffn_plan;        /* tiling of the last step's expert FFN: 0 the
                               128 x 256 tiles, 1 the weight-streaming tiles
-                              (few rows per expert)                          */
+                              (few rows per expert), 2 the expert-wide
+                              up-projection tiles (a few hundred rows per
+                              expert) with the 128 x 256 down projection     */
 } moeca_stats;
 
 /* Copy the last step's statistics to *out.  Synchronises the stream. */

@@ -50,6 +50,18 @@ __device__ __forceinline__ void dma16(const uint16_t* g, uint32_t lds) {
       : "memory", "m0");
 }
 
+// The same load with a wave-uniform 64-bit base (SGPRs) and a per-lane
+// 32-bit byte offset: the lane reads base + voff.
+__device__ __forceinline__ void dma16_s(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2"
+      :
+      : "s"(lds), "v"(voff), "s"(base)
+      : "memory", "m0");
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return static_cast<uint32_t>(
       reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)p));

@@ -567,12 +567,13 @@ __global__ __launch_bounds__(kSelThreads) void decide_kernel(
 // down at [E+S+1, 2(E+S)+1].
 __device__ __forceinline__ void write_shared_groups(int32_t* __restrict__ off,
                                                     int32_t* __restrict__ tiles, int E, int S,
-                                                    int T, int tm, int nt_up, int nt_down, int o,
-                                                    int tu, int td) {
+                                                    int T, int tm_up, int tm, int nt_up,
+                                                    int nt_down, int o, int tu, int td) {
+  const int mts_up = (T + tm_up - 1) / tm_up;
   const int mts = (T + tm - 1) / tm;
   for (int s2 = 0; s2 <= S; ++s2) {
     off[E + s2] = o + s2 * T;
-    tiles[E + s2] = tu + s2 * mts * nt_up;
+    tiles[E + s2] = tu + s2 * mts_up * nt_up;
     tiles[E + S + 1 + E + s2] = td + s2 * mts * nt_down;
   }
 }
@@ -590,8 +591,8 @@ __device__ __forceinline__ void write_shared_groups(int32_t* __restrict__ off,
 // ---------------------------------------------------------------------------
 __global__ __launch_bounds__(kSelThreads) void lists_kernel(
     const uint8_t* __restrict__ mask, const int32_t* __restrict__ e_t,
-    const int32_t* __restrict__ cnt_ch, int B, int N, int E, int S, int k, int tm, int nt_up,
-    int nt_down, const int32_t* __restrict__ sigma, int32_t* __restrict__ off,
+    const int32_t* __restrict__ cnt_ch, int B, int N, int E, int S, int k, int tm_up, int tm,
+    int nt_up, int nt_down, const int32_t* __restrict__ sigma, int32_t* __restrict__ off,
     int32_t* __restrict__ tiles, int32_t* __restrict__ list, int32_t* __restrict__ pos,
     int32_t* __restrict__ row_dst) {
   __shared__ int s_part_tot[kSelThreads];
@@ -640,19 +641,21 @@ __global__ __launch_bounds__(kSelThreads) void lists_kernel(
         bf += s_part_bef[pp * E + lane];
       }
     }
+    const int mt_up = (t + tm_up - 1) / tm_up;
     const int mt = (t + tm - 1) / tm;
     // inclusive scans over experts
     const int o = wave_incl_scan_i32(t);
-    const int tu = wave_incl_scan_i32(mt * nt_up);
+    const int tu = wave_incl_scan_i32(mt_up * nt_up);
     const int td = wave_incl_scan_i32(mt * nt_down);
     if (lane < E) s_base[lane] = o - t + bf;
     if (my == 0 && lane < E) {
       // exclusive prefixes per expert; the last expert also writes the
       // prefixes of the shared experts and the totals
       off[lane] = o - t;
-      tiles[lane] = tu - mt * nt_up;
+      tiles[lane] = tu - mt_up * nt_up;
       tiles[E + S + 1 + lane] = td - mt * nt_down;
-      if (lane == E - 1) write_shared_groups(off, tiles, E, S, B * N, tm, nt_up, nt_down, o, tu, td);
+      if (lane == E - 1)
+        write_shared_groups(off, tiles, E, S, B * N, tm_up, tm, nt_up, nt_down, o, tu, td);
     }
   }
   int rk = 0;
@@ -1144,7 +1147,7 @@ hipError_t launch_lists(const Shape& s, const FfnPlan& plan, const Buffers& b, h
   const int rc_n = (nb + kSelThreads - 1) / kSelThreads;
   if (s.E > 64) return hipErrorInvalidValue;
   launch_kernel(&lists_kernel, dim3(s.B * rc_n), dim3(kSelThreads), 0, st, b.mask, b.e_t,
-                b.cnt_ch, s.B, s.N, s.E, s.S, s.k, plan.tm, nt_up, nt_down, b.sigma, b.off,
+                b.cnt_ch, s.B, s.N, s.E, s.S, s.k, plan.tm_up, plan.tm, nt_up, nt_down, b.sigma, b.off,
                 b.tiles, b.list, b.pos, b.row_dst);
   return hipGetLastError();
 }

@@ -28,6 +28,8 @@
 // and consecutive logical tiles sit on the same XCD, so the M tiles sharing a
 // weight slice run together and the expert's gathered rows stay in that
 // XCD's L2.
+#include <type_traits>
+
 #include "common.h"
 #include "internal.h"
 #include "moeca.h"
@@ -421,11 +423,12 @@ __device__ __forceinline__ void mfma_step(f32x16_t (&acc)[FN][FM], const Frags<F
 }
 
 // One k-tile (four k-steps) on a swizzled stage, the next step's fragment
-// reads interleaved with the current step's MFMAs.
-template <int FN, int FM>
+// reads interleaved with the current step's MFMAs; hook(ks) runs after
+// k-step ks's MFMAs are issued.
+template <int FN, int FM, typename Hook>
 __device__ __forceinline__ void mfma_ktile_pipe(f32x16_t (&acc)[FN][FM], const uint16_t* xs,
                                                 const uint16_t* ws, int xrow0, int wrow0,
-                                                int lane) {
+                                                int lane, Hook&& hook) {
   constexpr int KS = kTK / 16;
   Frags<FN, FM> cur, nxt;
   read_frags(cur, xs, ws, xrow0, wrow0, 0, lane);
@@ -433,6 +436,7 @@ __device__ __forceinline__ void mfma_ktile_pipe(f32x16_t (&acc)[FN][FM], const u
   for (int ks = 0; ks < KS; ++ks) {
     if (ks + 1 < KS) read_frags(nxt, xs, ws, xrow0, wrow0, ks + 1, lane);
     mfma_step(acc, cur);
+    hook(ks);
     if (ks + 1 < KS) cur = nxt;
   }
   // schedule: first step's reads, then per step one MFMA per read of the
@@ -550,13 +554,20 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
       gb[u] = Wg + int64_t(n) * K + chunk * 8;
     }
   };
-  auto issue = [&](int kt, int st) __attribute__((always_inline)) {
+  // this wave's loads p0 .. p1 - 1 of k-tile kt into stage st (token rows
+  // first, then weight rows)
+  auto issue_part = [&](int kt, int st, int p0, int p1) __attribute__((always_inline)) {
     const uint32_t base = lds0 + st * (kStageElems * 2);
 #pragma unroll
-    for (int u = 0; u < kLoadsA; ++u) dma16(ga[u] + kt * kTK, base + u * kBigWaves * 1024);
+    for (int u = 0; u < kLoadsA; ++u)
+      if (u >= p0 && u < p1) dma16(ga[u] + kt * kTK, base + u * kBigWaves * 1024);
 #pragma unroll
     for (int u = 0; u < kLoadsB; ++u)
-      dma16(gb[u] + kt * kTK, base + kTileA * 2 + u * kBigWaves * 1024);
+      if (kLoadsA + u >= p0 && kLoadsA + u < p1)
+        dma16(gb[u] + kt * kTK, base + kTileA * 2 + u * kBigWaves * 1024);
+  };
+  auto issue = [&](int kt, int st) __attribute__((always_inline)) {
+    issue_part(kt, st, 0, kLoadsPerStage);
   };
 
   int L = lo + static_cast<int>(blockIdx.x) / kXcds;
@@ -602,10 +613,13 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
       if (kt + 1 < KT) s_waitcnt_vm(kLoadsPerStage);
       else s_waitcnt_vm(0);
       __builtin_amdgcn_s_barrier();
-      if (kt + 2 < KT) issue(kt + 2, st == 0 ? 2 : st - 1);
+      const bool more = kt + 2 < KT;
+      const int nst = st == 0 ? 2 : st - 1;
       const uint16_t* base = lds + st * kStageElems;
+      if (more) issue(kt + 2, nst);
       if (active)
-        mfma_ktile_pipe<FN, FM>(acc, base, base + kTileA, wm * FM * 32, wn * FN * 32, lane);
+        mfma_ktile_pipe<FN, FM>(acc, base, base + kTileA, wm * FM * 32, wn * FN * 32, lane,
+                                [](int) {});
       st = st == 2 ? 0 : st + 1;
     }
 
@@ -917,6 +931,212 @@ __global__ __launch_bounds__(kThinThreads, 1) void gemm_bf16_thin_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// bf16 MFMA up-projection for cache steps with a few hundred rows per
+// expert: a tile takes all of an expert's listed rows (up to 384; more are
+// split into equal parts) by 144 output columns.  On such a step every
+// weight byte is loaded by one tile only, each CU gets about two tiles (16
+// experts x 4608 columns: 512 tiles), and the token rows an expert's 32
+// tiles share are read from L2.  8 waves (two per SIMD), wave w taking the
+// 16-row tiles w, w + 8, w + 16 (a tile with fewer rows stays balanced: the
+// waves of a SIMD, w and w + 4, interleave) and all 144 columns, as up to
+// 3 x 9 v_mfma_f32_16x16x32_bf16 tiles (weights the A operand, token rows
+// the B operand: a lane holds four consecutive output columns of one row).
+// Two-stage ring of 64-wide k-tiles (2 x 66 KB) filled by direct global ->
+// LDS loads with the large kernel's XOR-swizzled 16-byte chunks; the next
+// k-tile's loads go out one between each weight fragment's MFMAs (issued
+// in one burst they hold the wave at the load queue, away from its MFMAs),
+// and loads of row groups wholly past the tile's rows are skipped.
+// ---------------------------------------------------------------------------
+constexpr int kWideTM = 384;
+constexpr int kWideTN = 144;
+constexpr int kWideWaves = 8;
+constexpr int kWideThreads = kWideWaves * kWave;
+constexpr int kWideTileA = kWideTM * kTK;                                // 48 KB
+constexpr int kWideTileB = kWideTN * kTK;                                // 18 KB
+constexpr int kWideStage = kWideTileA + kWideTileB;                      // 66 KB
+constexpr int kWideInstA = kWideTM / 8;                                  // 48 DMA instructions
+constexpr int kWideInstB = kWideTN / 8;                                  // 18
+constexpr int kWideLoadsA = (kWideInstA + kWideWaves - 1) / kWideWaves;  // 6
+constexpr int kWideLoadsB = (kWideInstB + kWideWaves - 1) / kWideWaves;  // 3 (waves 0-1), 2
+static_assert(2 * kWideStage * 2 <= 163840, "two stages within the LDS");
+
+// One 64-wide k-tile of a wide-kernel wave: its NR row tiles with rows
+// (16 rows: w + 8 r) against the FN column tiles, the token-row fragments of
+// a 32-wide k step held, the weight fragments read one at a time; hook(q)
+// runs after the q-th weight fragment's MFMAs (q = 0 .. 2 FN - 1), so that
+// the caller can spread work over the k-tile.
+template <int NR, int FN, typename Hook>
+__device__ __forceinline__ void wide_ktile(f32x4_t (&acc)[FN][NR], const uint16_t* xs,
+                                           const uint16_t* ws, int wv, int lane, Hook&& hook) {
+#pragma unroll
+  for (int s2 = 0; s2 < kTK / 32; ++s2) {
+    const int c = 4 * s2 + (lane >> 4);  // logical 16-byte chunk of this lane
+    bf16x8_t xa[NR];
+#pragma unroll
+    for (int r = 0; r < NR; ++r) {
+      const int row = 16 * (wv + kWideWaves * r) + (lane & 15);
+      xa[r] = *reinterpret_cast<const bf16x8_t*>(xs + (row * 8 + (c ^ ((row >> 1) & 7))) * 8);
+    }
+#pragma unroll
+    for (int j = 0; j < FN; ++j) {
+      const int row = j * 16 + (lane & 15);
+      const bf16x8_t wb =
+          *reinterpret_cast<const bf16x8_t*>(ws + (row * 8 + (c ^ ((row >> 1) & 7))) * 8);
+#pragma unroll
+      for (int r = 0; r < NR; ++r)
+        acc[j][r] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(wb, xa[r], acc[j][r], 0, 0, 0);
+      hook(s2 * FN + j);
+    }
+  }
+}
+
+template <int ACT>
+__global__ __launch_bounds__(kWideThreads, 1) void gemm_bf16_wide_kernel(
+    const uint16_t* __restrict__ A, const uint16_t* __restrict__ W,
+    const int32_t* __restrict__ off, const int32_t* __restrict__ tile_off,
+    const int32_t* __restrict__ list, int E, int k, int K, int Nout,
+    uint16_t* __restrict__ dst) {
+  constexpr int FR = kWideTM / 16 / kWideWaves;  // 16-row tiles per wave (3)
+  constexpr int FN = kWideTN / 16;               // 16-column tiles (9)
+  static_assert(FR == 3, "the row-tile dispatch below covers zero to three");
+  static_assert(kWideLoadsA + kWideLoadsB <= 2 * FN, "one load per weight fragment");
+  __shared__ __attribute__((aligned(16))) uint16_t lds[2 * kWideStage];
+
+  const int tid = threadIdx.x;
+  const int lane = tid & 63;
+  const int kwv = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int total = tile_off[E];
+  const int per = (total + kXcds - 1) / kXcds;
+  const int lo = (blockIdx.x % kXcds) * per;
+  const int hi = min(total, lo + per);
+  const int stride = gridDim.x / kXcds;
+  const int toff0 = lane < E ? tile_off[lane] : 0x7fffffff;
+  const int toff1 = lane + 64 < E ? tile_off[lane + 64] : 0x7fffffff;
+  const int KT = K / kTK;
+  // stored chunk position: chunk ^ ((row >> 1) & 7) with row = 8 i + lane / 8
+  // and i = wv + 8 u (the parity of wv), as in the large kernel
+  const int chunk = (lane & 7) ^ (4 * (kwv & 1) + (lane >> 4));
+  const uint32_t lds0 = __builtin_amdgcn_readfirstlane(lds_addr(lds) + kwv * 1024);
+
+  for (int L = lo + static_cast<int>(blockIdx.x) / kXcds; L < hi; L += stride) {
+    int e_base;
+    const int e = __builtin_amdgcn_readfirstlane(tile_group(L, toff0, toff1, e_base));
+    const int o0 = off[e];
+    const int cnt = off[e + 1] - o0;
+    const int mt = (cnt + kWideTM - 1) / kWideTM;
+    const int local = __builtin_amdgcn_readfirstlane(L - e_base);
+    const int m = local % mt;
+    // part m of mt equal parts of the expert's rows (at most kWideTM each)
+    const int r0 = __builtin_amdgcn_readfirstlane(o0 + m * cnt / mt);
+    const int rows = __builtin_amdgcn_readfirstlane(o0 + (m + 1) * cnt / mt - r0);
+    const int n0 = __builtin_amdgcn_readfirstlane((local / mt) * kWideTN);
+
+    // byte offset of each of this lane's A loads (its token row); rows past
+    // the tile re-read its first row and are never stored.  Loads take a
+    // wave-uniform base and these 32-bit offsets, so few registers hold them.
+    uint32_t aoff[kWideLoadsA];
+#pragma unroll
+    for (int u = 0; u < kWideLoadsA; ++u) {
+      const int r = 8 * (kwv + kWideWaves * u) + (lane >> 3);
+      aoff[u] = static_cast<uint32_t>(((list[r0 + (r < rows ? r : 0)] / k) * K + chunk * 8) * 2);
+    }
+    const uint16_t* wg = W + (int64_t(e) * Nout + n0) * K;  // wave-uniform
+    const uint32_t woff = static_cast<uint32_t>(((8 * kwv + (lane >> 3)) * K + chunk * 8) * 2);
+    // the p-th of this wave's loads of k-tile kt into stage st (p <
+    // kWideLoadsA: token rows, then weight rows)
+    auto issue_one = [&](int kt, int st, int p) __attribute__((always_inline)) {
+      const uint32_t base = lds0 + st * (kWideStage * 2);
+      if (p < kWideLoadsA) {
+        const int i = kwv + kWideWaves * p;
+        if (8 * i < rows) dma16_s(A + kt * kTK, aoff[p], base + p * kWideWaves * 1024);
+      } else {
+        const int u = p - kWideLoadsA;
+        if (kwv + kWideWaves * u < kWideInstB)
+          dma16_s(wg + int64_t(u) * (8 * kWideWaves) * K + kt * kTK, woff,
+                  base + kWideTileA * 2 + u * kWideWaves * 1024);
+      }
+    };
+    auto issue = [&](int kt, int st) __attribute__((always_inline)) {
+#pragma unroll
+      for (int p = 0; p < kWideLoadsA + kWideLoadsB; ++p) issue_one(kt, st, p);
+    };
+
+    // The tile for a wave with NR row tiles that hold rows (w + 8 r, r < NR):
+    // k-loop and epilogue, one instantiation per NR so that each has its
+    // accumulators in fixed registers and straight-line MFMAs.  Every wave
+    // issues its loads and meets every barrier, NR = 0 included.
+    auto run = [&](auto nr_c) __attribute__((always_inline)) {
+      constexpr int NR = decltype(nr_c)::value;
+      constexpr int NA = NR > 0 ? NR : 1;
+      f32x4_t acc[FN][NA];
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+#pragma unroll
+        for (int r = 0; r < NA; ++r) acc[j][r] = f32x4_t{0.0f, 0.0f, 0.0f, 0.0f};
+      issue(0, 0);
+      for (int kt = 0; kt < KT; ++kt) {
+        // this wave's loads of stage kt & 1 have landed; after the barrier so
+        // have every wave's, and every wave is done with the other stage
+        wait_vmcnt<0>();
+        __builtin_amdgcn_s_barrier();
+        const bool more = kt + 1 < KT;
+        if constexpr (NR > 0) {
+          const uint16_t* xs = lds + (kt & 1) * kWideStage;
+          wide_ktile<NR, FN>(acc, xs, xs + kWideTileA, kwv, lane, [&](int q) {
+            if (more && q < kWideLoadsA + kWideLoadsB) issue_one(kt + 1, (kt + 1) & 1, q);
+          });
+        } else {
+          if (more) issue(kt + 1, (kt + 1) & 1);
+        }
+      }
+      __syncthreads();  // every wave done with the LDS before a next tile's loads
+
+      // epilogue: the lane holds columns 16 j + 4 g .. + 3 (g = lane >> 4) of
+      // row (lane & 15) of each 16 x 16 tile.  Activation and bf16 rounding;
+      // then lanes l and l ^ 16 exchange runs so that for each pair of column
+      // tiles (2 p, 2 p + 1) lane g writes 16 bytes: columns 8 (g / 2) .. + 7
+      // of tile 2 p + (g & 1).  The ninth tile is written in 8-byte runs.
+      const int g = lane >> 4, h = g & 1;
+#pragma unroll
+      for (int r = 0; r < NR; ++r) {
+        const int row = 16 * (kwv + kWideWaves * r) + (lane & 15);
+        const bool ok = row < rows;
+        uint16_t* orow = dst + int64_t(r0 + row) * Nout + n0;
+        u32x2_t pk[FN];
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const f32x4_t& a = acc[j][r];
+          pk[j] = u32x2_t{pack2_bf16(act_fn<ACT>(a[0]), act_fn<ACT>(a[1])),
+                          pack2_bf16(act_fn<ACT>(a[2]), act_fn<ACT>(a[3]))};
+        }
+#pragma unroll
+        for (int p = 0; p < FN / 2; ++p) {
+          const u32x2_t keep = h ? pk[2 * p + 1] : pk[2 * p];
+          const u32x2_t send = h ? pk[2 * p] : pk[2 * p + 1];
+          const uint32_t q0 = __shfl_xor(send[0], 16, kWave);
+          const uint32_t q1 = __shfl_xor(send[1], 16, kWave);
+          const int col = 16 * (2 * p + h) + 4 * (g - h);
+          if (ok)
+            *reinterpret_cast<u32x4_t*>(orow + col) =
+                h ? u32x4_t{q0, q1, keep[0], keep[1]} : u32x4_t{keep[0], keep[1], q0, q1};
+        }
+        if constexpr (FN % 2 == 1) {
+          if (ok) *reinterpret_cast<u32x2_t*>(orow + 16 * (FN - 1) + 4 * g) = pk[FN - 1];
+        }
+      }
+    };
+    // this wave's row tiles with rows (wave-uniform)
+    const int nr = __builtin_amdgcn_readfirstlane(((rows + 15) / 16 - kwv + kWideWaves - 1) / kWideWaves);
+    switch (nr) {
+      case 3: run(std::integral_constant<int, 3>{}); break;
+      case 2: run(std::integral_constant<int, 2>{}); break;
+      case 1: run(std::integral_constant<int, 1>{}); break;
+      default: run(std::integral_constant<int, 0>{}); break;
+    }
+  }
+}
+
 // h_c[row_dst[r]] = bf16(((part[0][r] + part[1][r]) + ...) + part[S-1][r])
 // for the listed rows r < off[E] (the down projection's K pieces, added in
 // piece order); one wave per row, 16 bytes of bf16 per lane and step.
@@ -1045,6 +1265,17 @@ hipError_t launch_gemm(const Shape& s, const FfnPlan& plan, const void* A, const
                        const void* Wsh, int K, int Nout, const Buffers& b, void* dst, void* dst_sh,
                        hipStream_t st) {
   const int G = s.groups();
+  if (KIND == kUp && plan.wide_up) {
+    // bf16, ungated, no shared experts (wide_capable)
+    if constexpr (ACT == kActSwiglu || ACT == kActBias || KIND != kUp) {
+      return hipErrorInvalidValue;
+    } else {
+      launch_kernel(&gemm_bf16_wide_kernel<ACT>, dim3(device_cus()), dim3(kWideThreads), 0, st,
+                    static_cast<const uint16_t*>(A), static_cast<const uint16_t*>(W), b.off,
+                    b.tiles, b.list, s.E, s.k, K, Nout, static_cast<uint16_t*>(dst));
+      return hipGetLastError();
+    }
+  }
   if (plan.thin) {
     // bf16, ungated, no shared experts (thin_capable)
     if constexpr (ACT == kActSwiglu || ACT == kActBias) {
@@ -1114,11 +1345,12 @@ hipError_t launch_gemm(const Shape& s, const FfnPlan& plan, const void* A, const
 
 // Weight-row counts of at least 512 take the large 128 x 256 tile (a
 // partial last N tile is masked); smaller ones the 128 x 128 / 128 x 64
-// tiles; the thin plan the 128 x 288 tile.
-FfnPlan ffn_plan(const Shape& s, bool thin) {
+// tiles; the thin plan the 128 x 288 tile; the wide plan the expert-wide
+// 384 x 144 up-projection tile (the down projection keeps the large tile).
+FfnPlan ffn_plan(const Shape& s, bool thin, bool wide) {
   auto tn = [](int n) { return n >= 512 ? kBigTN : (n % 128 == 0 ? 128 : 64); };
   FfnPlan p;
-  p.tm = 128;
+  p.tm = p.tm_up = 128;
   if (thin && thin_capable(s)) {
     p.thin = true;
     p.tn_up = p.tn_down = kThinTN;
@@ -1127,7 +1359,17 @@ FfnPlan ffn_plan(const Shape& s, bool thin) {
   }
   p.tn_up = tn(s.up_rows());
   p.tn_down = tn(s.d);
+  if (wide && wide_capable(s)) {
+    p.wide_up = true;
+    p.tm_up = kWideTM;
+    p.tn_up = kWideTN;
+  }
   return p;
+}
+
+bool wide_capable(const Shape& s) {
+  return s.bf16 && s.S == 0 && !s.swiglu && s.E <= 64 && s.up_rows() % kWideTN == 0 &&
+         s.d % kTK == 0 && s.tokens() * s.d < (int64_t(1) << 31);
 }
 
 bool thin_capable(const Shape& s) {

@@ -114,12 +114,21 @@ struct FfnPlan {
   int tn_down;
   int split_down = 1;
   bool thin = false;
+  bool wide_up = false;  // the up projection takes the expert-wide kernel
+  int tm_up = 128;       // M tile of the up projection's tile table
 };
 constexpr int kThinSplit = 4;
 // A ratio-mode cache step takes the thin plan when its budget leaves at most
 // this many rows per expert on average (unmatched branches come on top).
 constexpr int kThinRows = 112;
-FfnPlan ffn_plan(const Shape& s, bool thin = false);
+// A ratio-mode cache step with more rows per expert than that, and at most
+// this many on average, takes the expert-wide up-projection tiles (all of
+// an expert's rows, up to 384, by 144 columns).
+constexpr int kWideRows = 320;
+FfnPlan ffn_plan(const Shape& s, bool thin = false, bool wide = false);
+// Layers that may take the wide up projection: bf16, no shared experts,
+// ungated, d_ff a multiple of 144.
+bool wide_capable(const Shape& s);
 // Layers that may take the thin plan: bf16, no shared experts, ungated, at
 // most 256 rows per expert on a full step, and enough 288-wide
 // up-projection tiles for half the CUs.  Their workspace holds `part`.

@@ -450,7 +450,10 @@ int layer_step(moeca_layer* L, const void* x_t, const void* x_ffn, int t, void* 
   const bool thin = !full && p.mode == MOECA_MODE_RATIO &&
                     int64_t(budget) * s.B <= int64_t(moeca::kThinRows) * s.E &&
                     L->buf.part != nullptr;
-  const moeca::FfnPlan plan = moeca::ffn_plan(s, thin);
+  // and those that leave a few hundred take the expert-wide up projection
+  const bool wide = !full && p.mode == MOECA_MODE_RATIO &&
+                    int64_t(budget) * s.B <= int64_t(moeca::kWideRows) * s.E;
+  const moeca::FfnPlan plan = moeca::ffn_plan(s, thin, wide);
   arm();
   if (!check(moeca::launch_lists(s, plan, b, st), "lists")) return MOECA_E_HIP;
   if (between) {
@@ -470,7 +473,7 @@ int layer_step(moeca_layer* L, const void* x_t, const void* x_ffn, int t, void* 
   if (timed) ++L->timed_steps;
   if (!uncached) L->valid = true;
   L->last_full = full;
-  L->last_plan = plan.thin ? 1 : 0;
+  L->last_plan = plan.thin ? 1 : plan.wide_up ? 2 : 0;
   return MOECA_OK;
 }
 

@@ -259,6 +259,8 @@ def test_xl1024_sampled(mode):
     if mode == "ratio":
         for info in infos[1:]:
             assert abs(info["recompute_frac"] - 0.3) < 0.02
+        # cache steps: about 307 rows per expert, the expert-wide up projection
+        assert [i["ffn_plan"] for i in infos] == [0, 2, 2, 2]
 
 
 @pytest.mark.timeout(600)
@@ -291,6 +293,29 @@ def test_thin_plan_trajectory(shape, ratio):
     S = Setup(shape, mode="ratio", seed=31, T=4, ratio=ratio, refresh_cycle=0)
     infos = run_forced(S, 4, label=f"thin {shape}")
     assert [i["ffn_plan"] for i in infos] == [0, 1, 1, 1]
+
+
+# ---------------------------------------------------------------------------
+# The expert-wide up projection at sizes the oracle evaluates whole: up to
+# 384 rows of an expert in one tile by 144 columns; experts past 384 rows
+# split into equal parts (the skewed shape has experts of a few rows and
+# experts split in several parts), row counts that are not multiples of
+# 16, and zero to three row tiles per wave.
+# ---------------------------------------------------------------------------
+WIDE_SHAPES = [
+    (LayerShape(d=576, E=8, k=2, d_ff=1152, B=4, N=512, dtype="bf16"), 0.3, None),
+    (LayerShape(d=512, E=8, k=2, d_ff=576, B=4, N=1024, dtype="bf16"), 0.29, None),
+    (LayerShape(d=640, E=16, k=2, d_ff=1728, B=2, N=1000, dtype="bf16"), 0.6, None),
+    (LayerShape(d=512, E=16, k=2, d_ff=576, B=2, N=1024, dtype="bf16"), 0.7, "zipf"),
+]
+
+
+@pytest.mark.parametrize("shape,ratio,bias", WIDE_SHAPES)
+def test_wide_plan_trajectory(shape, ratio, bias):
+    S = Setup(shape, mode="ratio", seed=41, T=4, ratio=ratio, refresh_cycle=0,
+              **({} if bias is None else {"bias": bias, "drift": "bimodal"}))
+    infos = run_forced(S, 4, label=f"wide {shape} {bias}")
+    assert [i["ffn_plan"] for i in infos] == [0, 2, 2, 2]
 
 
 # ---------------------------------------------------------------------------
