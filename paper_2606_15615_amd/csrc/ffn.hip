@@ -1169,7 +1169,9 @@ __global__ __launch_bounds__(256) void reduce_partials_kernel(
 }
 
 // ---------------------------------------------------------------------------
-// fp32 grouped GEMM (fp32 layers): 64x64 block tile, 4x4 per thread, FMA.
+// fp32 grouped GEMM (fp32 layers): 64 x 64 block tile (token rows by output
+// columns), 16-wide k-steps through LDS, four waves of 32 x 32 on the fp32
+// matrix cores (v_mfma_f32_32x32x2_f32, fp32 products accumulated in fp32).
 // ---------------------------------------------------------------------------
 constexpr int kF32T = 64;
 constexpr int kF32K = 16;
@@ -1181,8 +1183,8 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(
     const int32_t* __restrict__ row_dst, int E, int G, int k, int K, int Nout,
     float* __restrict__ dst, float* __restrict__ dst_sh) {
   constexpr bool kGated = ACT == kActSwiglu;
-  __shared__ float As[kF32K][kF32T + 4];
-  __shared__ float Bs[kF32K][kF32T + 4];
+  __shared__ float As[kF32K][kF32T + 4];  // token rows, k-major
+  __shared__ float Bs[kF32K][kF32T + 4];  // weight rows, k-major
   __shared__ int s_src[kF32T];
   __shared__ int s_dst[kF32T];
   __shared__ int s_tile[4];
@@ -1200,13 +1202,24 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(
   const int r0 = s_tile[1], rows = s_tile[2], n0 = s_tile[3];
   if (tid < kF32T) group_row<KIND>(e, E, r0, rows, tid, k, off, list, row_dst, s_src[tid], s_dst[tid]);
   __syncthreads();
+  // tile loads: thread -> row lr, k columns lk .. lk + 3 of the 16-wide k-step
   const int lr = tid >> 2, lk = (tid & 3) * 4;
   const float* Wg = e < E ? W + int64_t(e) * Nout * K : Wsh + int64_t(e - E) * Nout * K;
   float* const og = e < E ? dst : dst_sh;
   const float* ap = A + int64_t(s_src[lr]) * K + lk;
   const float* bp = Wg + int64_t(n0 + lr) * K + lk;
-  const int tx = tid & 15, ty = tid >> 4;
-  float acc[4][4] = {};
+  // MFMA: wave w computes outputs 32 (w & 1) .. + 31 (weights, the A operand)
+  // by tokens 32 (w >> 1) .. + 31 (the B operand) with v_mfma_f32_32x32x2_f32;
+  // lane l supplies output / token (l & 31) at k-row l >> 5 of each 2-wide
+  // k-step and holds D[8 (v / 4) + 4 (l >> 5) + v % 4][l & 31] in acc[v]:
+  // four consecutive outputs of one token per group v / 4
+  const int lane = tid & 63, wv = tid >> 6;
+  const int wo = (wv & 1) * 32, wt = (wv >> 1) * 32;
+  const int lc = lane & 31, lh = lane >> 5;
+  typedef __attribute__((ext_vector_type(16))) float f32x16_v;
+  f32x16_v acc;
+#pragma unroll
+  for (int v = 0; v < 16; ++v) acc[v] = 0.0f;
   for (int k0 = 0; k0 < K; k0 += kF32K) {
     const float4 va = *reinterpret_cast<const float4*>(ap + k0);
     const float4 vb = *reinterpret_cast<const float4*>(bp + k0);
@@ -1220,31 +1233,23 @@ __global__ __launch_bounds__(256) void gemm_f32_kernel(
     Bs[lk + 3][lr] = vb.w;
     __syncthreads();
 #pragma unroll
-    for (int kk = 0; kk < kF32K; ++kk) {
-      float a[4], b[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i) a[i] = As[kk][ty * 4 + i];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) b[j] = Bs[kk][tx * 4 + j];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) acc[i][j] = fmaf(a[i], b[j], acc[i][j]);
-    }
+    for (int kk = 0; kk < kF32K; kk += 2)
+      acc = __builtin_amdgcn_mfma_f32_32x32x2f32(Bs[kk + lh][wo + lc], As[kk + lh][wt + lc], acc,
+                                                 0, 0, 0);
     __syncthreads();
   }
+  const int drow = s_dst[wt + lc];
+  if (drow < 0) return;
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int drow = s_dst[ty * 4 + i];
-    if (drow < 0) continue;
+  for (int q = 0; q < 4; ++q) {
+    const int c = n0 + wo + 8 * q + 4 * lh;  // outputs c .. c + 3
     if constexpr (kGated) {  // columns (gate, up, gate, up) -> two outputs
-      float* out = og + int64_t(drow) * (Nout / 2) + (n0 + tx * 4) / 2;
-      out[0] = silu_f(acc[i][0]) * acc[i][1];
-      out[1] = silu_f(acc[i][2]) * acc[i][3];
+      *reinterpret_cast<float2*>(og + int64_t(drow) * (Nout / 2) + c / 2) =
+          make_float2(silu_f(acc[4 * q]) * acc[4 * q + 1], silu_f(acc[4 * q + 2]) * acc[4 * q + 3]);
     } else {
-      float* out = og + int64_t(drow) * Nout + n0 + tx * 4;
-#pragma unroll
-      for (int j = 0; j < 4; ++j) out[j] = act_fn<ACT>(acc[i][j]);
+      *reinterpret_cast<float4*>(og + int64_t(drow) * Nout + c) =
+          make_float4(act_fn<ACT>(acc[4 * q]), act_fn<ACT>(acc[4 * q + 1]),
+                      act_fn<ACT>(acc[4 * q + 2]), act_fn<ACT>(acc[4 * q + 3]));
     }
   }
 }
