@@ -156,9 +156,11 @@ __global__ __launch_bounds__(kGemvWaves * kWave) void gemv_kernel(
 // ---------------------------------------------------------------------------
 // LayerNorm + AdaLN modulation and the gated residuals, one wave per row
 // ---------------------------------------------------------------------------
-// d <= kMaxWidth: a lane holds float4 chunks lane + 64 j of the row.
+// d <= kMaxWidth: a lane holds float4 chunks lane + 64 j (j < NC) of the
+// row; NC = ceil(d / 256) is a template parameter, so the registers held
+// per lane (and the waves a CU keeps in flight) follow the width.
 constexpr int kLnWaves = 4;
-constexpr int kLnChunks = kMaxWidth / 4 / kWave;  // 8
+constexpr int kLnChunks = kMaxWidth / 4 / kWave;  // 8, the most
 
 enum { kLnAttn = 0, kLnMlp = 1, kLnFinal = 2 };
 
@@ -179,18 +181,19 @@ struct LnArgs {
   int routing;              // kLnMlp: u is the routing input (a full step)
 };
 
-__device__ __forceinline__ void ln_stats(const float (&v)[kLnChunks][4], int n4, int lane,
-                                         int d, double& mean, double& rstd) {
+template <int NC>
+__device__ __forceinline__ void ln_stats(const float (&v)[NC][4], int n4, int lane, int d,
+                                         double& mean, double& rstd) {
   double s = 0.0;
 #pragma unroll
-  for (int j = 0; j < kLnChunks; ++j)
+  for (int j = 0; j < NC; ++j)
     if (lane + kWave * j < n4)
 #pragma unroll
       for (int e = 0; e < 4; ++e) s += v[j][e];
   const double mu = wave_sum_f64(s) / d;
   double q = 0.0;
 #pragma unroll
-  for (int j = 0; j < kLnChunks; ++j)
+  for (int j = 0; j < NC; ++j)
     if (lane + kWave * j < n4)
 #pragma unroll
       for (int e = 0; e < 4; ++e) {
@@ -204,12 +207,13 @@ __device__ __forceinline__ void ln_stats(const float (&v)[kLnChunks][4], int n4,
 
 // bf16(LN(v) * (1 + scale) + shift) into row `dst` in fp32: the attention
 // input (off the decision path)
-__device__ __forceinline__ void ln_store_f32(const float (&v)[kLnChunks][4], int n4, int lane,
+template <int NC>
+__device__ __forceinline__ void ln_store_f32(const float (&v)[NC][4], int n4, int lane,
                                              double mean, double rstd, const float* shift,
                                              const float* scale, uint16_t* dst) {
   const float mf = static_cast<float>(mean), rf = static_cast<float>(rstd);
 #pragma unroll
-  for (int j = 0; j < kLnChunks; ++j) {
+  for (int j = 0; j < NC; ++j) {
     const int c = lane + kWave * j;
     if (c < n4) {
       const float4 sh = reinterpret_cast<const float4*>(shift)[c];
@@ -225,11 +229,12 @@ __device__ __forceinline__ void ln_store_f32(const float (&v)[kLnChunks][4], int
 
 // bf16(LN(v) * (1 + scale) + shift) into row `dst`, in fp64 and rounded
 // once: this is the MoE routing input (decision-path arithmetic)
-__device__ __forceinline__ void ln_store(const float (&v)[kLnChunks][4], int n4, int lane,
+template <int NC>
+__device__ __forceinline__ void ln_store(const float (&v)[NC][4], int n4, int lane,
                                          double mean, double rstd, const float* shift,
                                          const float* scale, uint16_t* dst) {
 #pragma unroll
-  for (int j = 0; j < kLnChunks; ++j) {
+  for (int j = 0; j < NC; ++j) {
     const int c = lane + kWave * j;
     if (c < n4) {
       const float4 sh = reinterpret_cast<const float4*>(shift)[c];
@@ -247,7 +252,7 @@ __device__ __forceinline__ void ln_store(const float (&v)[kLnChunks][4], int n4,
   }
 }
 
-template <int MODE>
+template <int MODE, int NC>
 __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
   const int lane = threadIdx.x & 63;
   const int r = blockIdx.x * kLnWaves + (threadIdx.x >> 6);
@@ -263,12 +268,12 @@ __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
   const int b = row / p.N;
   const int64_t o = int64_t(row) * d;
   const float* m = p.mod + int64_t(b) * 6 * d;  // sh_a, sc_a, g_a, sh_m, sc_m, g_m
-  float v[kLnChunks][4];
+  float v[NC][4];
 
   if constexpr (MODE == kLnFinal) {
     const float* g = m + 5 * d;
 #pragma unroll
-    for (int j = 0; j < kLnChunks; ++j) {
+    for (int j = 0; j < NC; ++j) {
       const int c = lane + kWave * j;
       if (c < n4) {
         const float4 x1 = reinterpret_cast<const float4*>(p.x1 + o)[c];
@@ -289,7 +294,7 @@ __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
   if (MODE == kLnAttn && p.pending) {
     const float* gp = p.mod_prev + int64_t(b) * 6 * d + 5 * d;
 #pragma unroll
-    for (int j = 0; j < kLnChunks; ++j) {
+    for (int j = 0; j < NC; ++j) {
       const int c = lane + kWave * j;
       if (c < n4) {
         const float4 x1 = reinterpret_cast<const float4*>(p.x1 + o)[c];
@@ -304,7 +309,7 @@ __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
     }
   } else {
 #pragma unroll
-    for (int j = 0; j < kLnChunks; ++j) {
+    for (int j = 0; j < NC; ++j) {
       const int c = lane + kWave * j;
       if (c < n4) {
         const float4 xx = reinterpret_cast<const float4*>(p.x + o)[c];
@@ -318,10 +323,10 @@ __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
   // the attention feature, requested together with x (it is used after the
   // first LayerNorm)
   const bool with_a = MODE == kLnMlp || p.cached;
-  u32x2_t av[kLnChunks];
+  u32x2_t av[NC];
   if (with_a) {
 #pragma unroll
-    for (int j = 0; j < kLnChunks; ++j) {
+    for (int j = 0; j < NC; ++j) {
       const int c = lane + kWave * j;
       if (c < n4) av[j] = reinterpret_cast<const u32x2_t*>(p.a + o)[c];
     }
@@ -335,7 +340,7 @@ __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
   // x1 = x + g_a * a, then the MoE input from LN(x1)
   const float* ga = m + 2 * d;
 #pragma unroll
-  for (int j = 0; j < kLnChunks; ++j) {
+  for (int j = 0; j < NC; ++j) {
     const int c = lane + kWave * j;
     if (c < n4) {
       const u32x2_t aa = av[j];
@@ -738,32 +743,45 @@ hipError_t launch_gemv(const double* in, int B, int K, const GemvBatch& mats, in
   return hipGetLastError();
 }
 
+// one wave per row; the instantiation holding ceil(d / 256) float4 chunks
+// per lane
+template <int MODE>
+hipError_t launch_ln(const LnArgs& p, int T, int d, hipStream_t st) {
+  const dim3 grid((T + kLnWaves - 1) / kLnWaves), block(kLnWaves * kWave);
+  switch ((d / 4 + kWave - 1) / kWave) {
+    case 1: launch_kernel(&ln_kernel<MODE, 1>, grid, block, 0, st, p); break;
+    case 2: launch_kernel(&ln_kernel<MODE, 2>, grid, block, 0, st, p); break;
+    case 3: launch_kernel(&ln_kernel<MODE, 3>, grid, block, 0, st, p); break;
+    case 4: launch_kernel(&ln_kernel<MODE, 4>, grid, block, 0, st, p); break;
+    case 5: launch_kernel(&ln_kernel<MODE, 5>, grid, block, 0, st, p); break;
+    case 6: launch_kernel(&ln_kernel<MODE, 6>, grid, block, 0, st, p); break;
+    case 7: launch_kernel(&ln_kernel<MODE, 7>, grid, block, 0, st, p); break;
+    case 8: launch_kernel(&ln_kernel<MODE, 8>, grid, block, 0, st, p); break;
+    default: return hipErrorInvalidValue;
+  }
+  return hipGetLastError();
+}
+
 hipError_t launch_ln_attn(const BlockBufs& k, int T, int N, int d, const float* mod,
                           const float* mod_prev, const uint16_t* a, bool cached,
                           hipStream_t st) {
   LnArgs p{k.x, k.x1, k.y, a, k.h, k.u, mod, mod_prev, nullptr, nullptr, T, N, d,
            mod_prev != nullptr ? 1 : 0, cached ? 1 : 0, 0};
-  launch_kernel(&ln_kernel<kLnAttn>, dim3((T + kLnWaves - 1) / kLnWaves), dim3(kLnWaves * kWave),
-                0, st, p);
-  return hipGetLastError();
+  return launch_ln<kLnAttn>(p, T, d, st);
 }
 
 hipError_t launch_ln_mlp(const BlockBufs& k, int T, int N, int d, const float* mod,
                          const uint16_t* a, uint16_t* u_out, bool routing, hipStream_t st) {
   LnArgs p{k.x, k.x1, k.y, a, k.h, u_out, mod, nullptr, k.slist, k.soff + k.B, T, N, d, 0, 1,
            routing ? 1 : 0};
-  launch_kernel(&ln_kernel<kLnMlp>, dim3((T + kLnWaves - 1) / kLnWaves), dim3(kLnWaves * kWave),
-                0, st, p);
-  return hipGetLastError();
+  return launch_ln<kLnMlp>(p, T, d, st);
 }
 
 hipError_t launch_ln_final(const BlockBufs& k, int T, int N, int d, const float* mod,
                            hipStream_t st) {
   LnArgs p{k.x, k.x1, k.y, nullptr, nullptr, nullptr, mod, nullptr, nullptr, nullptr, T, N, d,
            0, 0, 0};
-  launch_kernel(&ln_kernel<kLnFinal>, dim3((T + kLnWaves - 1) / kLnWaves),
-                dim3(kLnWaves * kWave), 0, st, p);
-  return hipGetLastError();
+  return launch_ln<kLnFinal>(p, T, d, st);
 }
 
 hipError_t launch_slist(const BlockBufs& k, const uint8_t* sync, int N, int d, hipStream_t st) {
