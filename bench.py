@@ -8,9 +8,11 @@ per-sample branch budget; the full-recompute comparator (the uncached layer
 through the same kernels) is timed on the same inputs.  Each phase runs
 its K steps eagerly with HIP events between kernels (per-kernel times), then
 replays the same K steps from one HIP graph (the headline time).  The
-roofline object is for the FFN up-projection launch; its HBM traffic comes
-from the committed rocprofv3 counter summary, and is null when the kernel
-source no longer matches the one the counters were taken on.
+roofline object is for the longer of the two expert-FFN GEMM launches,
+against the lower of its two roofs (MFMA peak, or arithmetic intensity x HBM
+peak); its HBM traffic comes from the committed rocprofv3 counter summary,
+and is null when the kernel source no longer matches the one the counters
+were taken on.
 
     python bench.py [--steps K] [--warmup W] [--workload xl1024]
                     [--phase both|cached|full] [--no-cpu] [--no-graph]
@@ -163,11 +165,12 @@ def blas_reference(shape, args):
     return res
 
 
-def kernel_traffic(kernel_src: str, summary: str):
-    """HBM bytes per launch of the FFN-up kernel from the committed counter
-    summary (FETCH_SIZE and WRITE_SIZE, scaled by the copy-kernel factors;
-    keys ``ffn_up.kernel_source_sha256`` and ``ffn_up.hbm_bytes_per_launch``),
-    or None when the kernel source changed since the counters were taken."""
+def kernel_traffic(kernel_src: str, summary: str, stage: str = "ffn_up"):
+    """HBM bytes per launch of a GEMM stage (``ffn_up`` or ``ffn_down``) from
+    the committed counter summary (FETCH_SIZE and WRITE_SIZE, scaled by the
+    copy-kernel factors; keys ``<stage>.kernel_source_sha256`` and
+    ``<stage>.hbm_bytes_per_launch``), or None when the kernel source changed
+    since the counters were taken."""
     import hashlib
     try:
         vals = {}
@@ -178,9 +181,9 @@ def kernel_traffic(kernel_src: str, summary: str):
                     vals[k.strip()] = v.strip()
         with open(kernel_src, "rb") as f:
             digest = hashlib.sha256(f.read()).hexdigest()
-        if vals.get("ffn_up.kernel_source_sha256") != digest:
+        if vals.get(f"{stage}.kernel_source_sha256") != digest:
             return None
-        return float(vals["ffn_up.hbm_bytes_per_launch"])
+        return float(vals[f"{stage}.hbm_bytes_per_launch"])
     except (OSError, KeyError, ValueError):
         return None
 
@@ -599,9 +602,9 @@ def main():
         ms_eager, ms_graph, graphed, stage, (rec, syn, ms_flushed, plan) = res_c
         mean_rec = float(np.mean(rec))
         up_ms = stage["ffn_up"]
-        ffn_ms = stage["ffn_up"] + stage["ffn_down"]
+        down_ms = stage["ffn_down"]
+        ffn_ms = up_ms + down_ms
         rows = mean_rec + shared_rows
-        up_tf = rows * up_flop / (up_ms * 1e-3) / 1e12
         ffn_tf = rows * (up_flop + down_flop) / (ffn_ms * 1e-3) / 1e12
         # algorithmic HBM bytes of a cache step: expert weights (routed and
         # shared), inputs, cached rows, recomputed rows written, shared
@@ -609,17 +612,63 @@ def main():
         wbytes = (shape.E + shape.n_shared) * (shape.up_rows + shape.d_ff) * shape.d * abytes
         step_bytes = (wbytes + shape.tokens * shape.d * abytes * 2 + branches * shape.d * abytes
                       + 2 * shared_rows * shape.d * abytes)
+        # per GEMM launch: flop (2 d d_ff per row) and algorithmic bytes (the
+        # weights of every expert, which a cache step at these ratios reads
+        # whole, and per row its input row read and its output row written)
+        up_w = (shape.E + shape.n_shared) * shape.up_rows * shape.d * abytes
+        down_w = (shape.E + shape.n_shared) * shape.d_ff * shape.d * abytes
+        gemms = {
+            "ffn_up": {"ms": up_ms, "flop": rows * up_flop,
+                       "bytes": up_w + rows * (shape.d + shape.d_ff) * abytes},
+            "ffn_down": {"ms": down_ms, "flop": rows * down_flop,
+                         "bytes": down_w + rows * (shape.d_ff + shape.d) * abytes},
+        }
+        for g in gemms.values():
+            g["tflops"] = g["flop"] / (g["ms"] * 1e-3) / 1e12
+            g["gbs"] = g["bytes"] / (g["ms"] * 1e-3) / 1e9
+            g["intensity"] = g["flop"] / g["bytes"]
+        # the dominant kernel: the longer of the two GEMM launches; its roof
+        # is the lower of the MFMA peak and intensity x HBM peak
+        dom = max(gemms, key=lambda n: gemms[n]["ms"])
+        g = gemms[dom]
+        hbm_bound = g["intensity"] * PEAK_HBM_GBS / 1e3 < peak
         traffic = kernel_traffic(os.path.join(ROOT, "paper_2606_15615_amd", "csrc", "ffn.hip"),
-                                 os.path.join(ROOT, "profiles", "xl1024_cached_counters.txt"))
+                                 os.path.join(ROOT, "profiles", "xl1024_cached_counters.txt"),
+                                 dom)
         if args.workload != "xl1024":
             traffic = None
-        up_kernel = ("gemm_bf16_big_kernel<0,3> (expert FFN up-projection + SwiGLU)"
-                     if act == "swiglu" else
-                     "gemm_bf16_thin_kernel<0,0,1> (expert FFN up-projection + GELU, "
-                     "weight-streaming tiles)" if np.mean(np.array(plan) == 1) > 0.5 else
-                     "gemm_bf16_wide_kernel<0> (expert FFN up-projection + GELU, "
-                     "expert-wide tiles)" if np.mean(np.array(plan) == 2) > 0.5 else
-                     "gemm_bf16_big_kernel<0,0> (expert FFN up-projection + GELU)")
+        swiglu = act == "swiglu"
+        thin = np.mean(np.array(plan) == 1) > 0.5
+        wide = np.mean(np.array(plan) == 2) > 0.5
+        kernel_names = {
+            "ffn_up": ("gemm_bf16_big_kernel<0,3> (expert FFN up-projection + SwiGLU)" if swiglu
+                       else "gemm_bf16_thin_kernel<0,0,1> (expert FFN up-projection + GELU, "
+                            "weight-streaming tiles)" if thin
+                       else "gemm_bf16_wide_kernel<0> (expert FFN up-projection + GELU, "
+                            "expert-wide tiles)" if wide
+                       else "gemm_bf16_big_kernel<0,0> (expert FFN up-projection + GELU)"),
+            "ffn_down": ("gemm_bf16_thin_kernel<1,2,4> + reduce_partials_kernel<4> (expert FFN "
+                         "down-projection, weight-streaming tiles in four K pieces)" if thin
+                         else "gemm_bf16_big_kernel<1,2> (expert FFN down-projection, "
+                              "scattered into the cache slots)"),
+        }
+        roof = {
+            "bound": "hbm" if hbm_bound else "mfma",
+            "kernel": kernel_names[dom],
+            "achieved": round(g["gbs"] if hbm_bound else g["tflops"], 2),
+            "peak": PEAK_HBM_GBS if hbm_bound else peak,
+            "unit": "GB/s" if hbm_bound else "TFLOP/s",
+            "frac": round(g["gbs"] / PEAK_HBM_GBS if hbm_bound else g["tflops"] / peak, 4),
+            "traffic": None if traffic is None else int(traffic),
+            "launch_ms": round(g["ms"], 4),
+            "flop_per_launch": g["flop"],
+            "bytes_per_launch": g["bytes"],
+            "intensity_flop_per_byte": round(g["intensity"], 1),
+            "ridge_flop_per_byte": round(peak * 1e3 / PEAK_HBM_GBS, 1),
+            # the same launch against the MFMA peak
+            "mfma_tflops": round(g["tflops"], 2),
+            "mfma_frac": round(g["tflops"] / peak, 4),
+        }
         res.update({
             "value": round(ms_graph, 4),
             "ms_per_step": round(ms_graph, 4),
@@ -637,17 +686,12 @@ def main():
             "ffn_plan_steps": {str(v): int(c) for v, c in zip(*np.unique(plan, return_counts=True))},
             "stage_ms": {k: round(v, 4) for k, v in stage.items()},
             "step_hbm_frac": round(step_bytes / (ms_graph * 1e-3) / 1e9 / PEAK_HBM_GBS, 4),
-            "roofline": {
-                "bound": "mfma",
-                "kernel": up_kernel,
-                "achieved": round(up_tf, 2),
-                "peak": peak,
-                "unit": "TFLOP/s",
-                "frac": round(up_tf / peak, 4),
-                "traffic": None if traffic is None else int(traffic),
-                "launch_ms": round(up_ms, 4),
-                "flop_per_launch": rows * up_flop,
-            },
+            "gemm_launches": {n: {"ms": round(v["ms"], 4), "tflops": round(v["tflops"], 1),
+                                  "mfma_frac": round(v["tflops"] / peak, 4),
+                                  "gbs": round(v["gbs"], 1),
+                                  "hbm_frac": round(v["gbs"] / PEAK_HBM_GBS, 4)}
+                              for n, v in gemms.items()},
+            "roofline": roof,
         })
     if res_f is not None:
         ms_eager_f, ms_graph_f, _, stage_f, (_, _, ms_flushed_f, _) = res_f
