@@ -387,6 +387,21 @@ def test_score_signal_ablations_are_exact():
     assert np.array_equal(O.score(w, w_c, n_c, e_c, q, matched, 0.0, 0.0, 1.0)[2], w)
 
 
+def test_score_share_counts_only_cached_branches():
+    """o (Sec. 4.2 score eq.) is the matched cached branch's norm over the
+    norms of the token's cached branches: a slot holding no branch (e_c = -1,
+    with a stale norm left in it) is not part of the sum.  Token 0 has one
+    cached branch, so its o is 1; token 1 has two, with norms 1 and 3."""
+    e_t = np.array([[2, 5], [2, 5]], np.int32)
+    e_c = np.array([[2, -1], [5, 2]], np.int32)
+    n_c = np.array([[2.0, 7.0], [3.0, 1.0]], F32)
+    w = np.array([[0.5, 0.5], [0.5, 0.5]], F32)
+    matched, q = O.match(e_t, e_c)
+    assert matched.tolist() == [[True, False], [True, True]]
+    _, o, _ = O.score(w, w, n_c, e_c, q, matched, 0.0, 1.0)
+    assert o.tolist() == [[1.0, 0.0], [0.25, 0.75]]
+
+
 def test_score_reduces_to_weight_threshold_without_lambdas():
     rng = np.random.default_rng(11)
     T, k = 200, 2
