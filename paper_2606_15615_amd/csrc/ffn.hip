@@ -28,6 +28,7 @@
 // and consecutive logical tiles sit on the same XCD, so the M tiles sharing a
 // weight slice run together and the expert's gathered rows stay in that
 // XCD's L2.
+#include <algorithm>
 #include <type_traits>
 
 #include "common.h"
@@ -1383,6 +1384,8 @@ bool thin_capable(const Shape& s) {
          2 * s.E * nt >= device_cus();
 }
 
+int cus_per_xcd() { return device_cus() / kXcds; }
+
 int device_cus() {
   static int cus = 0;
   if (cus == 0) {
@@ -1415,10 +1418,13 @@ hipError_t launch_ffn_down(const Shape& s, const void* W_down, const void* W_dow
 
 hipError_t launch_proj(const void* A, const void* W, const float* bias, const int32_t* off,
                        const int32_t* tiles, const int32_t* list, int K, int Nout, void* dst,
-                       hipStream_t st) {
-  if (K % kTK != 0 || Nout < 1) return hipErrorInvalidValue;
+                       hipStream_t st, int blocks_per_xcd) {
+  if (K % kTK != 0 || Nout < 1 || blocks_per_xcd < 0) return hipErrorInvalidValue;
+  // the grid stays a multiple of the XCD count (block b runs on XCD b % 8)
+  const int grid = blocks_per_xcd > 0 ? kXcds * std::min(blocks_per_xcd, cus_per_xcd())
+                                      : device_cus();
   const auto* w = static_cast<const uint16_t*>(W);
-  launch_kernel(&gemm_bf16_big_kernel<kProj, kActBias>, dim3(device_cus()), dim3(kBigThreads), 0,
+  launch_kernel(&gemm_bf16_big_kernel<kProj, kActBias>, dim3(grid), dim3(kBigThreads), 0,
                 st, static_cast<const uint16_t*>(A), w, w, off, tiles, list,
                 static_cast<const int32_t*>(nullptr), 1, 1, 1, K, Nout, bias,
                 static_cast<uint16_t*>(dst), static_cast<uint16_t*>(dst));

@@ -213,9 +213,14 @@ struct BlockBufs {
 
 // dst[list[r]] = bf16(A[list[r]] . W^T + bias) for r < off[1]: one group of
 // listed rows (tables off[2], tiles[2] on the device), K inputs, Nout outputs.
+// blocks_per_xcd > 0 gives the persistent grid that many blocks per XCD
+// instead of one per CU (the rest of the CUs stay free for kernels on another
+// stream that run beside it).
 hipError_t launch_proj(const void* A, const void* W, const float* bias, const int32_t* off,
                        const int32_t* tiles, const int32_t* list, int K, int Nout, void* dst,
-                       hipStream_t st);
+                       hipStream_t st, int blocks_per_xcd = 0);
+// CUs per XCD (the device's CU count over 8).
+int cus_per_xcd();
 hipError_t launch_sinusoid(const float* t_values, int B, double* e, hipStream_t st);
 hipError_t launch_silu(const float* in, int n, double* out, hipStream_t st);
 // Up to kGemvBatch matrices of one shape for one GEMV launch (by value).

@@ -306,8 +306,22 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
           (rc = hip(hipStreamWaitEvent(S->side, S->ev_fork, 0), "fork")) != MOECA_OK)
         return rc;
     }
+    // On a cache step its persistent grid takes only as many blocks per XCD
+    // as it needs to finish in the rounds of tiles it takes on every CU
+    // (1024 x 8 tokens: 576 tiles, 72 per XCD, three rounds: 24 of an
+    // XCD's 32 CUs), so that the decision kernels beside it find free CUs
+    // (the one-block-per-sample decide kernel, 1024 threads, cannot share a
+    // CU with a GEMM block) and the q projection starts on them.
+    int kv_share = 0;
+    if (fork && !full) {
+      const int per_xcd =
+          ((T + moeca::kProjTM - 1) / moeca::kProjTM * ((2 * d + moeca::kProjTN - 1) / moeca::kProjTN) +
+           7) / 8;
+      const int rounds = (per_xcd + moeca::cus_per_xcd() - 1) / moeca::cus_per_xcd();
+      kv_share = std::max(1, (per_xcd + rounds - 1) / std::max(1, rounds));
+    }
     rc = hip(moeca::launch_proj(k.h, Wkv, W.b_qkv + d, k.tab + 4, k.tab + 6, k.ident, d, 2 * d,
-                                k.kv, fork ? S->side : st),
+                                k.kv, fork ? S->side : st, kv_share),
              "kv projection");
     if (fork) {
       // the side stream's end is recorded even after a failed launch, so
@@ -315,8 +329,13 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
       const int rr = hip(hipEventRecord(S->ev_kv, S->side), "fork");
       if (rc == MOECA_OK) rc = rr;
     }
+    // the main stream waits for the side stream once per block (every wait
+    // is a barrier packet in the queue, which costs microseconds)
+    bool joined = !fork;
     auto join = [&]() -> int {
-      return fork ? hip(hipStreamWaitEvent(st, S->ev_kv, 0), "join") : MOECA_OK;
+      if (joined) return MOECA_OK;
+      joined = true;
+      return hip(hipStreamWaitEvent(st, S->ev_kv, 0), "join");
     };
     if (rc != MOECA_OK) {
       join();
@@ -345,7 +364,8 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
         return r != MOECA_OK ? r : refresh(k.u2);
       });
     }
-    // the fork is joined on every path (a capture must end with it joined)
+    // the fork is joined on every path (a capture must end with it joined);
+    // after the attention's wait this adds nothing
     const int rj = join();
     if (rc != MOECA_OK) return rc;
     if (rj != MOECA_OK) return rj;
