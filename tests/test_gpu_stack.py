@@ -334,6 +334,19 @@ def test_stack_full_width_forced():
     run_forced(SS, 3)
 
 
+@pytest.mark.timeout(600)
+def test_stack_full_width_batch8_forced():
+    """The benchmarked block's attention path at its full batch (d = 1152,
+    16 heads of 72, 1024 tokens x 8, with small experts): the launch
+    configuration of the timed stack, where a cache step's k/v projection
+    (576 tiles) runs on the side stream with 24 blocks per XCD beside the
+    decision kernels; a full step and two cache steps."""
+    sh = StackShape(L=1, d=1152, heads=16, E=4, k=2, d_ff=256, B=8, N=1024)
+    say("full width, batch 8")
+    SS = StackSetup(sh, mode="ratio", seed=7, T=3, ratio=0.3)
+    run_forced(SS, 3)
+
+
 def test_stack_nothing_to_refresh_is_bit_identical():
     """A cache step whose input and conditioning equal the full step's, at
     ratio 0: every branch is matched and reused, no token is synchronised
