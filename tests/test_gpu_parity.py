@@ -264,6 +264,23 @@ def test_xl1024_sampled(mode):
 
 
 @pytest.mark.timeout(600)
+@pytest.mark.parametrize("ratio,plan", [(0.05, 2), (0.6, 0)])
+def test_xl1024_sampled_other_ratios(ratio, plan):
+    """The benchmarked layer at a low and a high refresh ratio: the cache
+    steps leave about 50 rows per expert plus the unmatched branches (the
+    expert-wide up projection with few rows per tile) and about 600 (the
+    128 x 256 tiles for both projections); a refresh step, then two cache
+    steps."""
+    shape = WORKLOADS["xl1024"]
+    S = Setup(shape, mode="ratio", seed=13, T=3, ratio=ratio, refresh_cycle=0)
+    sample, ev = sampled_tokens(shape, 32, 14)
+    infos = run_sampled(S, 3, sample, ev, f"xl1024 rho={ratio}")
+    for info in infos[1:]:
+        assert info["recompute_frac"] >= ratio - 0.02
+    assert [i["ffn_plan"] for i in infos] == [0, plan, plan]
+
+
+@pytest.mark.timeout(600)
 def test_xl256_sampled():
     """The layer at 256 tokens x 8 (d=1152, 16 experts, top-2, 4608 hidden,
     30 % refresh): its cache steps leave about 77 rows per expert and take
