@@ -501,3 +501,33 @@ def test_graph_replayed_steps(wl, mode):
         if sampled:
             fill_unsampled(S, st, ev)
         say(f"  graph {wl} {mode} t={t}: {info}")
+
+
+# ---------------------------------------------------------------------------
+# A seeded sweep over layer configurations: shapes (widths, expert counts,
+# top-k including 3 and 6, shared experts, SwiGLU, fp32), every mode and the
+# controller settings drawn at random inside the documented limits
+# ---------------------------------------------------------------------------
+import random_cases
+
+
+@pytest.mark.parametrize("i", range(random_cases.N_CASES))
+def test_random_configuration(i):
+    shape, mode, pol, T, bias = random_cases.case(i)
+    say(f"  case {i}: {shape} {mode} {pol} T={T} bias={bias}")
+    S = Setup(shape, mode=mode, seed=1000 + i, T=T, bias=bias, **pol)
+    infos = run_forced(S, T, label=f"random {i}")
+    say(f"  case {i}: {infos}")
+
+
+@pytest.mark.parametrize("j", range(random_cases.N_PLAN_CASES))
+def test_random_plan_configuration(j):
+    """Seeded ratio-mode cases drawn to take the weight-streaming plan or the
+    expert-wide up projection on every cache step (one multi-block decision
+    among them: over 8192 branches per sample)."""
+    shape, pol, T, plan = random_cases.plan_case(j)
+    say(f"  plan case {j}: {shape} {pol} T={T} plan={plan}")
+    S = Setup(shape, mode="ratio", seed=2000 + j, T=T, **pol)
+    infos = run_forced(S, T, label=f"random plan {j}")
+    say(f"  plan case {j}: {infos}")
+    assert [i["ffn_plan"] for i in infos] == [0] + [plan] * (T - 1)
