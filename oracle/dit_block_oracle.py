@@ -113,12 +113,18 @@ def cond_embed(t: np.ndarray, W1, b1, W2, b2, y_rows=None) -> np.ndarray:
     return c.astype(F32)
 
 
-def adaln(W_ada, b_ada, c: np.ndarray) -> np.ndarray:
-    """The six modulation vectors per sample: (B, 6, d) fp32 from
-    W_ada (6d, d) bf16 and b_ada (6d,) fp32 applied to SiLU(c)."""
+def adaln_f64(W_ada, b_ada, c: np.ndarray) -> np.ndarray:
+    """The six modulation vectors per sample before their one rounding:
+    (B, 6, d) fp64 from W_ada (6d, d) bf16 and b_ada (6d,) fp32 applied to
+    SiLU(c)."""
     B, d = c.shape
     m = mo.silu(np.asarray(c, F64)) @ bf16_f64(W_ada).T + np.asarray(b_ada, F64)
-    return m.astype(F32).reshape(B, 6, d)
+    return m.reshape(B, 6, d)
+
+
+def adaln(W_ada, b_ada, c: np.ndarray) -> np.ndarray:
+    """The six modulation vectors per sample, rounded once to fp32: (B, 6, d)."""
+    return adaln_f64(W_ada, b_ada, c).astype(F32)
 
 
 # ---------------------------------------------------------------------------

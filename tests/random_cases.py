@@ -9,6 +9,8 @@ number, so a failing case is reproduced by its number alone.
 """
 from __future__ import annotations
 
+import math
+
 import numpy as np
 
 from paper_2606_15615_amd.synth import LayerShape
@@ -88,3 +90,32 @@ def plan_case(j: int):
     steps = int(g.integers(3, 5))
     shape = LayerShape(d=d, E=E, k=k, d_ff=d_ff, B=B, N=N, dtype="bf16")
     return shape, pol, steps, plan
+
+
+N_STACK_CASES = 12
+
+
+def stack_case(i: int):
+    """(stack shape, mode, policy kwargs, steps) of a small block stack: the
+    head widths 8-96 in steps of 8 (d = heads x head width a multiple of 64,
+    at most 1152), one or two blocks, ragged token counts."""
+    from paper_2606_15615_amd.synth import StackShape
+    g = np.random.Generator(np.random.PCG64(np.random.SeedSequence([20263, i])))
+    dh = 8 * (1 + (5 * i) % 12)                      # every head width once per 12 cases
+    step = 64 // math.gcd(dh, 64)                     # heads: d = heads dh a multiple of 64
+    heads = step * int(g.integers(1, max(1, 1152 // (dh * step)) + 1))
+    d = dh * heads
+    E = int(g.choice([2, 3, 4, 8, 12, 16]))
+    k = int(g.choice([kk for kk in (1, 2, 4) if kk <= E]))
+    d_ff = 64 * int(g.integers(1, 9))
+    L = int(g.integers(1, 3))
+    B = int(g.integers(1, 4))
+    N = int(g.integers(1, 300))
+    mode = str(g.choice(["ratio", "threshold", "full"], p=[0.5, 0.35, 0.15]))
+    pol = dict(ratio=float(np.float32(g.uniform(0.0, 1.0))),
+               tau0=float(np.float32(g.uniform(0.2, 1.0))),
+               alpha=float(np.float32(g.uniform(0.0, 0.9))),
+               beta=float(np.float32(g.uniform(0.0, 0.9))),
+               refresh_cycle=int(g.choice([0, 2, 3])))
+    steps = int(g.integers(2, 5))
+    return StackShape(L=L, d=d, heads=heads, E=E, k=k, d_ff=d_ff, B=B, N=N), mode, pol, steps

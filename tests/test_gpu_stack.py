@@ -25,7 +25,7 @@ import pytest
 from oracle import dit_block_oracle as D
 from oracle import moeca_oracle as O
 from paper_2606_15615_amd.synth import STACKS, StackShape, StackSynth
-from gpu_harness import TOL, check_step, rel_err, say
+from gpu_harness import TOL, check_step, near_f32_tie, rel_err, say
 
 pytestmark = pytest.mark.gpu
 
@@ -115,6 +115,10 @@ def topk_safe(logits64: np.ndarray, k: int, err: float) -> np.ndarray:
     return np.all(s[:, :-1] - s[:, 1:] > 2 * err, axis=1)
 
 
+def tag0(l: int, t: int) -> str:
+    return f"block {l} t={t}"
+
+
 def check_block(SS: StackSetup, l: int, t: int, st_o: D.BlockState, x: np.ndarray):
     """Run block l of step t on the GPU from the oracle's state and input and
     compare; returns the oracle's (x_out, new state)."""
@@ -128,15 +132,27 @@ def check_block(SS: StackSetup, l: int, t: int, st_o: D.BlockState, x: np.ndarra
     SS.S.step_blocks(SS.x_dev, SS.c_dev, t, l, 1)
     torch.cuda.synchronize()
     W = SS.blocks[l]
-    mod = D.adaln(W.W_ada, W.b_ada, SS.cs[t])
+    # decision-path arithmetic: bit-exact.  The AdaLN vectors are fp64 sums
+    # rounded once to fp32; where the oracle's fp64 value sits within fp64
+    # rounding noise of an fp32 midpoint the other neighbour is as correct,
+    # and both sides then go on from the GPU's vectors
+    m64 = D.adaln_f64(W.W_ada, W.b_ada, SS.cs[t])
+    mod = m64.astype(np.float32)
+    g_mod = SS.S.read("mod")[l]
+    off = g_mod != mod
+    if off.any():
+        tie = near_f32_tie(m64)
+        assert np.all(tie[off]), f"{tag0(l, t)}: AdaLN vectors differ in {int(off.sum())} " \
+            f"values, {int((off & ~tie).sum())} of them away from an fp32 rounding tie"
+        nb = (g_mod[off] == np.nextafter(mod[off], np.float32(np.inf))) | \
+             (g_mod[off] == np.nextafter(mod[off], np.float32(-np.inf)))
+        assert np.all(nb), f"{tag0(l, t)}: an AdaLN value at a tie is not a neighbour"
+        say(f"  {tag0(l, t)}: {int(off.sum())} AdaLN value(s) at an fp32 rounding tie")
+        mod = g_mod
     x_out, st_new, rec = D.block_step(dims, SS.pol, W, st_o, x, mod, t)
     full = rec["full"]
     tag = f"block {l} t={t} {'full' if full else 'cache'}"
     say(f"  {tag}: |S| = {int(rec['sync'].sum())} of {T}")
-
-    # decision-path arithmetic: bit-exact
-    g_mod = SS.S.read("mod")[l]
-    assert np.array_equal(g_mod, mod), f"{tag}: AdaLN vectors differ in {(g_mod != mod).sum()}"
     # the attention input is computed in fp32 (off the decision path): within
     # one bf16 ulp of the oracle's, or (where the modulation nearly cancels
     # the shift) within fp32 rounding of the terms
@@ -396,3 +412,16 @@ def test_stack_three_blocks_run_equals_block_by_block():
         Bs.S.step_blocks(xb, Bs.c_dev, t, 2, 1)   # then block 2
         torch.cuda.synchronize()
         assert torch.equal(xa, xb), f"t={t}"
+
+
+import random_cases
+
+
+@pytest.mark.parametrize("i", range(random_cases.N_STACK_CASES))
+def test_stack_random_configuration(i):
+    """Seeded small stacks over every head width 8-96, one or two blocks,
+    ragged token counts, every mode and drawn controller settings."""
+    sh, mode, pol, T = random_cases.stack_case(i)
+    say(f"stack case {i}: {sh} {mode} {pol} T={T}")
+    SS = StackSetup(sh, mode=mode, seed=3000 + i, T=T, **pol)
+    run_forced(SS, T)
