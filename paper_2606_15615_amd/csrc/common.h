@@ -62,6 +62,32 @@ __device__ __forceinline__ void dma16_s(const void* base, uint32_t voff, uint32_
       : "memory", "m0");
 }
 
+// The same two loads with the non-temporal hint, for a stream whose every
+// byte feeds one tile (the expert weights of the weight-streaming and
+// expert-wide tilings): its lines are not kept for reuse, so the stream
+// neither displaces the step's other data from the caches nor, on a miss in
+// the last-level cache, forces that cache's dirty lines out to HBM before
+// it can be served.  Not for operands that several tiles share through L2.
+__device__ __forceinline__ void dma16_nt(const uint16_t* g, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, off nt"
+      :
+      : "s"(lds), "v"(g)
+      : "memory", "m0");
+}
+
+__device__ __forceinline__ void dma16_s_nt(const void* base, uint32_t voff, uint32_t lds) {
+  asm volatile(
+      "s_mov_b32 m0, %0\n\t"
+      "s_nop 0\n\t"
+      "global_load_lds_dwordx4 %1, %2 nt"
+      :
+      : "s"(lds), "v"(voff), "s"(base)
+      : "memory", "m0");
+}
+
 __device__ __forceinline__ uint32_t lds_addr(const void* p) {
   return static_cast<uint32_t>(
       reinterpret_cast<uintptr_t>((__attribute__((address_space(3))) const void*)p));

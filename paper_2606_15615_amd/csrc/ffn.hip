@@ -712,7 +712,9 @@ __global__ __launch_bounds__(kBigThreads, 1) void gemm_bf16_big_kernel(
 // issue five and waves 4-7 four.  Units are numbered expert-major, then k
 // piece, then N tile, then M tile, and walked like the large kernel's
 // tiles (contiguous ranges per XCD): the units that share a k piece of an
-// expert's rows run together on one XCD.
+// expert's rows run together on one XCD.  The weight rows, used by one unit
+// each, are loaded with the non-temporal hint (the token rows, shared by an
+// expert's N tiles, are not).
 // ---------------------------------------------------------------------------
 constexpr int kThinTM = 128;
 constexpr int kThinTN = 288;
@@ -823,7 +825,7 @@ __global__ __launch_bounds__(kThinThreads, 1) void gemm_bf16_thin_kernel(
 #pragma unroll
     for (int u = 0; u < kThinLoadsB; ++u)
       if (u + 1 < kThinLoadsB || five)
-        dma16(gb[u] + kt * kTK, base + kThinTileA * 2 + u * kThinWaves * 1024);
+        dma16_nt(gb[u] + kt * kTK, base + kThinTileA * 2 + u * kThinWaves * 1024);
   };
   // this wave's loads of the oldest stage in flight have landed once at most
   // one later stage's loads are outstanding
@@ -947,7 +949,8 @@ __global__ __launch_bounds__(kThinThreads, 1) void gemm_bf16_thin_kernel(
 // LDS loads with the large kernel's XOR-swizzled 16-byte chunks; the next
 // k-tile's loads go out one between each weight fragment's MFMAs (issued
 // in one burst they hold the wave at the load queue, away from its MFMAs),
-// and loads of row groups wholly past the tile's rows are skipped.
+// and loads of row groups wholly past the tile's rows are skipped.  The
+// weight rows (one tile each) are loaded with the non-temporal hint.
 // ---------------------------------------------------------------------------
 constexpr int kWideTM = 384;
 constexpr int kWideTN = 144;
@@ -1054,7 +1057,7 @@ __global__ __launch_bounds__(kWideThreads, 1) void gemm_bf16_wide_kernel(
       } else {
         const int u = p - kWideLoadsA;
         if (kwv + kWideWaves * u < kWideInstB)
-          dma16_s(wg + int64_t(u) * (8 * kWideWaves) * K + kt * kTK, woff,
+          dma16_s_nt(wg + int64_t(u) * (8 * kWideWaves) * K + kt * kTK, woff,
                   base + kWideTileA * 2 + u * kWideWaves * 1024);
       }
     };
