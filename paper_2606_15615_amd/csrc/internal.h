@@ -123,7 +123,8 @@ constexpr int kThinSplit = 4;
 constexpr int kThinRows = 112;
 // A ratio-mode cache step with more rows per expert than that, and at most
 // this many on average, takes the expert-wide up-projection tiles (all of
-// an expert's rows, up to 384, by 144 columns).
+// an expert's rows, up to 384, by 144 columns); so does a full step with at
+// most this many branches per expert on average.
 constexpr int kWideRows = 320;
 FfnPlan ffn_plan(const Shape& s, bool thin = false, bool wide = false);
 // Layers that may take the wide up projection: bf16, no shared experts,

@@ -450,9 +450,11 @@ int layer_step(moeca_layer* L, const void* x_t, const void* x_ffn, int t, void* 
   const bool thin = !full && p.mode == MOECA_MODE_RATIO &&
                     int64_t(budget) * s.B <= int64_t(moeca::kThinRows) * s.E &&
                     L->buf.part != nullptr;
-  // and those that leave a few hundred take the expert-wide up projection
-  const bool wide = !full && p.mode == MOECA_MODE_RATIO &&
-                    int64_t(budget) * s.B <= int64_t(moeca::kWideRows) * s.E;
+  // and those that leave a few hundred take the expert-wide up projection,
+  // as do full steps of that many rows per expert (every branch)
+  const bool wide = (full ? int64_t(s.B) * s.N * s.k <= int64_t(moeca::kWideRows) * s.E
+                          : p.mode == MOECA_MODE_RATIO &&
+                                int64_t(budget) * s.B <= int64_t(moeca::kWideRows) * s.E);
   const moeca::FfnPlan plan = moeca::ffn_plan(s, thin, wide);
   arm();
   if (!check(moeca::launch_lists(s, plan, b, st), "lists")) return MOECA_E_HIP;

@@ -28,6 +28,17 @@ def say(msg):
     print(msg, flush=True)
 
 
+def full_step_plan(shape: LayerShape) -> int:
+    """FFN tiling the library takes on a full step of this layer: the
+    expert-wide up projection (2) when every branch leaves at most 320 rows
+    per expert on average and the layer can take it (bf16, ungated, no
+    shared experts, hidden width a multiple of 144), else the 128-row tiles
+    (0)."""
+    wide_capable = (shape.dtype == "bf16" and shape.n_shared == 0 and shape.ffn == "gelu"
+                    and shape.d_ff % 144 == 0 and shape.tokens * shape.d < 2 ** 31)
+    return 2 if wide_capable and shape.branches <= 320 * shape.E else 0
+
+
 class Setup:
     """Seeded weights + trajectory, the oracle objects and a GPU layer."""
 

@@ -15,7 +15,8 @@ pytestmark = pytest.mark.gpu
 from oracle import moeca_oracle as O
 from paper_2606_15615_amd.synth import LayerShape, WORKLOADS
 
-from gpu_harness import Setup, check_step, oracle_rerun, run_forced, say, rel_err
+from gpu_harness import (Setup, check_step, full_step_plan, oracle_rerun, run_forced, say,
+                         rel_err)
 
 
 @pytest.fixture(scope="module", autouse=True)
@@ -260,7 +261,7 @@ def test_xl1024_sampled(mode):
         for info in infos[1:]:
             assert abs(info["recompute_frac"] - 0.3) < 0.02
         # cache steps: about 307 rows per expert, the expert-wide up projection
-        assert [i["ffn_plan"] for i in infos] == [0, 2, 2, 2]
+        assert [i["ffn_plan"] for i in infos] == [full_step_plan(shape), 2, 2, 2]
 
 
 @pytest.mark.timeout(600)
@@ -277,7 +278,7 @@ def test_xl1024_sampled_other_ratios(ratio, plan):
     infos = run_sampled(S, 3, sample, ev, f"xl1024 rho={ratio}")
     for info in infos[1:]:
         assert info["recompute_frac"] >= ratio - 0.02
-    assert [i["ffn_plan"] for i in infos] == [0, plan, plan]
+    assert [i["ffn_plan"] for i in infos] == [full_step_plan(S.shape), plan, plan]
 
 
 @pytest.mark.timeout(600)
@@ -290,7 +291,7 @@ def test_xl256_sampled():
     S = Setup(shape, mode="ratio", seed=12, T=4, ratio=0.3, refresh_cycle=0)
     sample, ev = sampled_tokens(shape, 48, 13)
     infos = run_sampled(S, 4, sample, ev, "xl256 ratio")
-    assert [i["ffn_plan"] for i in infos] == [0, 1, 1, 1]
+    assert [i["ffn_plan"] for i in infos] == [full_step_plan(S.shape), 1, 1, 1]
 
 
 # ---------------------------------------------------------------------------
@@ -309,7 +310,7 @@ THIN_SHAPES = [
 def test_thin_plan_trajectory(shape, ratio):
     S = Setup(shape, mode="ratio", seed=31, T=4, ratio=ratio, refresh_cycle=0)
     infos = run_forced(S, 4, label=f"thin {shape}")
-    assert [i["ffn_plan"] for i in infos] == [0, 1, 1, 1]
+    assert [i["ffn_plan"] for i in infos] == [full_step_plan(S.shape), 1, 1, 1]
 
 
 # ---------------------------------------------------------------------------
@@ -332,7 +333,7 @@ def test_wide_plan_trajectory(shape, ratio, bias):
     S = Setup(shape, mode="ratio", seed=41, T=4, ratio=ratio, refresh_cycle=0,
               **({} if bias is None else {"bias": bias, "drift": "bimodal"}))
     infos = run_forced(S, 4, label=f"wide {shape} {bias}")
-    assert [i["ffn_plan"] for i in infos] == [0, 2, 2, 2]
+    assert [i["ffn_plan"] for i in infos] == [full_step_plan(S.shape), 2, 2, 2]
 
 
 # ---------------------------------------------------------------------------
@@ -530,4 +531,4 @@ def test_random_plan_configuration(j):
     S = Setup(shape, mode="ratio", seed=2000 + j, T=T, **pol)
     infos = run_forced(S, T, label=f"random plan {j}")
     say(f"  plan case {j}: {infos}")
-    assert [i["ffn_plan"] for i in infos] == [0] + [plan] * (T - 1)
+    assert [i["ffn_plan"] for i in infos] == [full_step_plan(S.shape)] + [plan] * (T - 1)
