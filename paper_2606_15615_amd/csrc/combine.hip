@@ -138,8 +138,10 @@ __global__ __launch_bounds__(kCombWaves * kWave) void combine_kernel(
 template <typename T> struct Raw8;
 template <> struct Raw8<uint16_t> {
   typedef __attribute__((ext_vector_type(4))) unsigned int v;
+  // the combine reads each cached row and attention row once per step:
+  // non-temporal loads, so that they do not displace the step's other data
   static __device__ __forceinline__ v load(const uint16_t* p) {
-    return *reinterpret_cast<const v*>(p);
+    return __builtin_nontemporal_load(reinterpret_cast<const v*>(p));
   }
   static __device__ __forceinline__ void store(uint16_t* p, v x) { *reinterpret_cast<v*>(p) = x; }
   static __device__ __forceinline__ void widen(v x, float* f) {
