@@ -4,6 +4,7 @@
 // (Sec. 4.1, synchronised update) and multi-head self-attention of those
 // tokens' queries over every token of the sample.  The q/k/v and output
 // projections are the grouped GEMM's projection instantiation (ffn.hip).
+#include <algorithm>
 #include <cmath>
 
 #include "common.h"
@@ -77,76 +78,103 @@ __global__ void silu_kernel(const float* __restrict__ in, int n, double* __restr
 }
 
 // v[b][r] = (sum_k W[r][k] in[b][k] + bias[r]) (+ table[labels[b]][r]) in
-// fp64 (products and sums), then out = fp32(v), or out64 = silu(v) when
-// out64 is set.  W rows are bf16 [Nout][K] (K a multiple of 8), in fp64
-// [B][K].  A wave takes kGemvRows weight rows and the samples four at a
-// time, so each input load serves four rows.  blockIdx.y picks one of up to
-// kGemvBatch matrices of the same shape (every block's AdaLN map in one
-// launch: enough waves in flight to stream the weights).  The AdaLN vectors
-// feed the routing input, so they take the decision path's arithmetic: one
-// rounding.
-constexpr int kGemvWaves = 4;
-constexpr int kGemvRows = 4;
+// fp64, then out = fp32(v), or out64 = silu(v) when out64 is set.  W rows
+// are bf16 [Nout][K] (K a multiple of 32, at most kMaxWidth), in fp64
+// [B][K].  One launch covers up to kGemvBatch matrices of the same shape
+// (every block's AdaLN map at once).
+//
+// The products run on the fp64 matrix cores (v_mfma_f64_16x16x4f64), which
+// here deliver several times the fp64 rate of the vector units: a wave
+// takes 16 weight rows (the A operand) against up to kGemvSamples samples
+// (the B operand; the other columns of the 16 are zero and discarded).
+// Lane l loads 8 consecutive bf16 of weight row l % 16 at columns
+// c + 8 (l / 16) of each 32-column block c and feeds them to 8 MFMAs in turn,
+// MFMA u taking column c + 8 (l / 16) + u for k-row l / 16 in both operands,
+// so that one 16-byte load serves 8 MFMAs, and kGemvDepth such loads are in
+// flight per lane.  The samples' inputs are staged in LDS once per block
+// (persistent blocks walk the 16-row tiles of all the matrices).  Four
+// accumulator chains rotate over the MFMAs and are added in a fixed order
+// (eight were slower).  The AdaLN vectors feed the routing input, so they
+// take the decision path's arithmetic: an fp64 evaluation with one rounding.
+constexpr int kGemvWaves = 8;
+constexpr int kGemvSamples = 8;
+constexpr int kGemvDepth = 8;  // 32-column blocks of weights in flight per wave
+
+typedef __attribute__((ext_vector_type(4))) double f64x4_g;
 
 __global__ __launch_bounds__(kGemvWaves * kWave) void gemv_kernel(
-    const double* __restrict__ in, int B, int K, GemvBatch mats, int Nout,
+    const double* __restrict__ in, int B, int K, GemvBatch mats, int n_mats, int Nout,
     const uint16_t* __restrict__ table, const int32_t* __restrict__ labels, int n_classes,
     double* __restrict__ out64) {
+  __shared__ __attribute__((aligned(16))) double s_in[kGemvSamples * kMaxWidth];  // 128 KB
   const int lane = threadIdx.x & 63;
-  const int r0 = (blockIdx.x * kGemvWaves + (threadIdx.x >> 6)) * kGemvRows;
-  if (r0 >= Nout) return;
-  const uint16_t* __restrict__ W = mats.W[blockIdx.y];
-  const float* __restrict__ bias = mats.bias[blockIdx.y];
-  float* __restrict__ out = mats.out[blockIdx.y];
-  const int nc = K / 8;
-  for (int b0 = 0; b0 < B; b0 += 4) {
-    const int nb = min(4, B - b0);
-    double acc[kGemvRows][4];
+  const int wv = threadIdx.x >> 6;
+  const int n = lane & 15, g = lane >> 4;
+  const int per_mat = (Nout + 15) / 16;
+  const int tiles = per_mat * n_mats;
+  const int nblk = K / 32;
+  for (int b0 = 0; b0 < B; b0 += kGemvSamples) {
+    const int nb = min(kGemvSamples, B - b0);
+    __syncthreads();  // every wave is done with the previous samples' inputs
+    for (int i = threadIdx.x; i < nb * K; i += kGemvWaves * kWave)
+      s_in[i] = in[int64_t(b0) * K + i];
+    __syncthreads();
+    const bool has_col = n < nb;  // B column n is a staged sample
+    const double* __restrict__ xin = s_in + (has_col ? n : 0) * K + 8 * g;
+    for (int tt = blockIdx.x + gridDim.x * wv; tt < tiles; tt += gridDim.x * kGemvWaves) {
+      const int m = tt / per_mat;
+      const int r0 = (tt % per_mat) * 16;
+      const uint16_t* __restrict__ wrow =
+          mats.W[m] + int64_t(min(r0 + n, Nout - 1)) * K + 8 * g;
+      f64x4_g acc[4];
 #pragma unroll
-    for (int q = 0; q < kGemvRows; ++q)
+      for (int c = 0; c < 4; ++c) acc[c] = f64x4_g{0.0, 0.0, 0.0, 0.0};
+      u32x4_t raw[kGemvDepth];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) acc[q][u] = 0.0;
-    for (int c = lane; c < nc; c += kWave) {
-      double w[kGemvRows][8];
+      for (int d0 = 0; d0 < kGemvDepth; ++d0)
+        if (d0 < nblk) raw[d0] = *reinterpret_cast<const u32x4_t*>(wrow + 32 * d0);
+      for (int c0 = 0; c0 < nblk; c0 += kGemvDepth) {
 #pragma unroll
-      for (int q = 0; q < kGemvRows; ++q) {
-        const int r = min(r0 + q, Nout - 1);
-        const u32x4_t wv = *reinterpret_cast<const u32x4_t*>(W + int64_t(r) * K + 8 * c);
+        for (int d0 = 0; d0 < kGemvDepth; ++d0) {
+          const int c = c0 + d0;
+          if (c < nblk) {
+            double wv8[8], xv[8];
 #pragma unroll
-        for (int e = 0; e < 4; ++e) {
-          w[q][2 * e] = __uint_as_float(wv[e] << 16);
-          w[q][2 * e + 1] = __uint_as_float(wv[e] & 0xffff0000u);
+            for (int e = 0; e < 4; ++e) {
+              wv8[2 * e] = __uint_as_float(raw[d0][e] << 16);
+              wv8[2 * e + 1] = __uint_as_float(raw[d0][e] & 0xffff0000u);
+            }
+            // the block kGemvDepth ahead reuses this register set
+            if (c + kGemvDepth < nblk)
+              raw[d0] = *reinterpret_cast<const u32x4_t*>(wrow + 32 * (c + kGemvDepth));
+#pragma unroll
+            for (int e = 0; e < 8; e += 2) {
+              const double2 t2 = *reinterpret_cast<const double2*>(xin + 32 * c + e);
+              xv[e] = has_col ? t2.x : 0.0;
+              xv[e + 1] = has_col ? t2.y : 0.0;
+            }
+#pragma unroll
+            for (int u = 0; u < 8; ++u)
+              acc[u & 3] = __builtin_amdgcn_mfma_f64_16x16x4f64(wv8[u], xv[u], acc[u & 3], 0, 0, 0);
+          }
         }
       }
+      // lane l, register r: weight row r0 + 4 r + l / 16, sample l % 16
+      const float* __restrict__ bias = mats.bias[m];
+      float* __restrict__ out = mats.out[m];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        if (u < nb) {
-          const double* ip = in + int64_t(b0 + u) * K + 8 * c;
-          double iv[8];
-#pragma unroll
-          for (int e = 0; e < 8; ++e) iv[e] = ip[e];
-#pragma unroll
-          for (int q = 0; q < kGemvRows; ++q)
-#pragma unroll
-            for (int e = 0; e < 8; ++e) acc[q][u] += w[q][e] * iv[e];
-        }
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < kGemvRows; ++q) {
-      const int r = r0 + q;
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        const double s = wave_sum_f64(acc[q][u]);
-        if (lane == 0 && u < nb && r < Nout) {
-          const int b = b0 + u;
-          double v = s + static_cast<double>(bias[r]);
+      for (int r = 0; r < 4; ++r) {
+        const int row = r0 + 4 * r + g;
+        if (has_col && row < Nout) {
+          const int b = b0 + n;
+          double v = ((acc[0][r] + acc[1][r]) + (acc[2][r] + acc[3][r])) +
+                     static_cast<double>(bias[row]);
           if (table != nullptr) {
             const int lab = labels[b];
-            if (lab >= 0 && lab < n_classes) v += bf16_to_f32(table[int64_t(lab) * Nout + r]);
+            if (lab >= 0 && lab < n_classes) v += bf16_to_f32(table[int64_t(lab) * Nout + row]);
           }
-          if (out64 != nullptr) out64[int64_t(b) * Nout + r] = silu64(v);
-          else out[int64_t(b) * Nout + r] = static_cast<float>(v);
+          if (out64 != nullptr) out64[int64_t(b) * Nout + row] = silu64(v);
+          else out[int64_t(b) * Nout + row] = static_cast<float>(v);
         }
       }
     }
@@ -735,11 +763,15 @@ hipError_t launch_silu(const float* in, int n, double* out, hipStream_t st) {
 hipError_t launch_gemv(const double* in, int B, int K, const GemvBatch& mats, int n_mats,
                        int Nout, const void* table, const int32_t* labels, int n_classes,
                        double* out64, hipStream_t st) {
-  if (K % 8 != 0 || n_mats < 1 || n_mats > kGemvBatch) return hipErrorInvalidValue;
-  const int rows_per_block = kGemvWaves * kGemvRows;
-  launch_kernel(&gemv_kernel, dim3((Nout + rows_per_block - 1) / rows_per_block, n_mats),
-                dim3(kGemvWaves * kWave), 0, st, in, B, K, mats, Nout,
-                static_cast<const uint16_t*>(table), labels, n_classes, out64);
+  if (K % 32 != 0 || K > kMaxWidth || n_mats < 1 || n_mats > kGemvBatch)
+    return hipErrorInvalidValue;
+  // a small launch spreads its tiles over up to one block per CU (tile t
+  // goes to block t mod blocks, wave t / blocks mod kGemvWaves)
+  const int tiles = (Nout + 15) / 16 * n_mats;
+  const int blocks = std::min(tiles, device_cus());
+  launch_kernel(&gemv_kernel, dim3(blocks), dim3(kGemvWaves * kWave), 0,
+                st, in, B, K, mats, n_mats, Nout, static_cast<const uint16_t*>(table), labels,
+                n_classes, out64);
   return hipGetLastError();
 }
 

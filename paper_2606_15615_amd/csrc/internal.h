@@ -233,7 +233,8 @@ struct GemvBatch {
 };
 // for each matrix m < n_mats: v[b][r] = W_m[r] . in[b] + bias_m[r]
 // (+ table[labels[b]][r]) in fp64; out_m = fp32(v), or, with out64 set
-// (one matrix), out64 = silu(v)
+// (one matrix), out64 = silu(v).  K a multiple of 32, at most kMaxWidth
+// (hipErrorInvalidValue otherwise)
 hipError_t launch_gemv(const double* in, int B, int K, const GemvBatch& mats, int n_mats,
                        int Nout, const void* table, const int32_t* labels, int n_classes,
                        double* out64, hipStream_t st);
