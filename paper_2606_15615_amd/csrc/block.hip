@@ -207,6 +207,7 @@ struct LnArgs {
   int pending;              // x = x1 + g_m(prev) * y first (kLnAttn)
   int cached;               // kLnAttn on a cache step: also x1 and u from a
   int routing;              // kLnMlp: u is the routing input (a full step)
+  const float* x1p;         // [T][d] the previous block's x1 (with pending)
 };
 
 template <int NC>
@@ -318,21 +319,24 @@ __global__ __launch_bounds__(kLnWaves * kWave) void ln_kernel(LnArgs p) {
     return;
   }
 
-  // the row's x: the block input, or the previous block's x1 + g_m y
-  if (MODE == kLnAttn && p.pending) {
+  // the row's x: the block input, or the previous block's x1 + g_m y.  A
+  // cache step does not store that x: LN2 rebuilds it for the listed
+  // tokens from the same operands (a full step stores it for LN2)
+  if (p.pending) {
     const float* gp = p.mod_prev + int64_t(b) * 6 * d + 5 * d;
 #pragma unroll
     for (int j = 0; j < NC; ++j) {
       const int c = lane + kWave * j;
       if (c < n4) {
-        const float4 x1 = reinterpret_cast<const float4*>(p.x1 + o)[c];
+        const float4 x1 = reinterpret_cast<const float4*>(p.x1p + o)[c];
         const u32x2_t yy = reinterpret_cast<const u32x2_t*>(p.y + o)[c];
         const float4 gg = reinterpret_cast<const float4*>(gp)[c];
         v[j][0] = gated_add(x1.x, gg.x, __uint_as_float(yy[0] << 16));
         v[j][1] = gated_add(x1.y, gg.y, __uint_as_float(yy[0] & 0xffff0000u));
         v[j][2] = gated_add(x1.z, gg.z, __uint_as_float(yy[1] << 16));
         v[j][3] = gated_add(x1.w, gg.w, __uint_as_float(yy[1] & 0xffff0000u));
-        reinterpret_cast<float4*>(p.x + o)[c] = float4{v[j][0], v[j][1], v[j][2], v[j][3]};
+        if (MODE == kLnAttn && !p.cached)
+          reinterpret_cast<float4*>(p.x + o)[c] = float4{v[j][0], v[j][1], v[j][2], v[j][3]};
       }
     }
   } else {
@@ -798,21 +802,22 @@ hipError_t launch_ln_attn(const BlockBufs& k, int T, int N, int d, const float* 
                           const float* mod_prev, const uint16_t* a, bool cached,
                           hipStream_t st) {
   LnArgs p{k.x, k.x1, k.y, a, k.h, k.u, mod, mod_prev, nullptr, nullptr, T, N, d,
-           mod_prev != nullptr ? 1 : 0, cached ? 1 : 0, 0};
+           mod_prev != nullptr ? 1 : 0, cached ? 1 : 0, 0, k.x1p};
   return launch_ln<kLnAttn>(p, T, d, st);
 }
 
 hipError_t launch_ln_mlp(const BlockBufs& k, int T, int N, int d, const float* mod,
-                         const uint16_t* a, uint16_t* u_out, bool routing, hipStream_t st) {
-  LnArgs p{k.x, k.x1, k.y, a, k.h, u_out, mod, nullptr, k.slist, k.soff + k.B, T, N, d, 0, 1,
-           routing ? 1 : 0};
+                         const float* mod_prev, const uint16_t* a, uint16_t* u_out, bool routing,
+                         hipStream_t st) {
+  LnArgs p{k.x, k.x1, k.y, a, k.h, u_out, mod, mod_prev, k.slist, k.soff + k.B, T, N, d,
+           mod_prev != nullptr ? 1 : 0, 1, routing ? 1 : 0, k.x1p};
   return launch_ln<kLnMlp>(p, T, d, st);
 }
 
 hipError_t launch_ln_final(const BlockBufs& k, int T, int N, int d, const float* mod,
                            hipStream_t st) {
   LnArgs p{k.x, k.x1, k.y, nullptr, nullptr, nullptr, mod, nullptr, nullptr, nullptr, T, N, d,
-           0, 0, 0};
+           0, 0, 0, nullptr};
   return launch_ln<kLnFinal>(p, T, d, st);
 }
 

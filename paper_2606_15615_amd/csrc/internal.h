@@ -198,7 +198,9 @@ constexpr int kProjTN = 256;     // and output columns
 struct BlockBufs {
   int B;
   float* x;        // [T][d] residual stream (the caller's)
-  float* x1;       // [T][d]
+  float* x1;       // [T][d] this block's x1 (one of two buffers, alternating by block)
+  float* x1b;      // [T][d] the other buffer
+  const float* x1p;  // [T][d] the previous block's x1 in a multi-block run
   uint16_t* h;     // [T][d] attention input
   uint16_t* u;     // [T][d] MoE routing input
   uint16_t* u2;    // [T][d] rebuilt MoE input of synchronised tokens
@@ -238,13 +240,16 @@ struct GemvBatch {
 hipError_t launch_gemv(const double* in, int B, int K, const GemvBatch& mats, int n_mats,
                        int Nout, const void* table, const int32_t* labels, int n_classes,
                        double* out64, hipStream_t st);
-// every token: [x = x1 + g_m(prev) y;] h = LN(x) mod_a; [cached: x1 = x + g_a a, u = LN(x1) mod_m]
+// every token: [x = x1p + g_m(prev) y, stored on full steps;] h = LN(x) mod_a;
+// [cached: x1 = x + g_a a, u = LN(x1) mod_m]
 hipError_t launch_ln_attn(const BlockBufs& k, int T, int N, int d, const float* mod,
                           const float* mod_prev, const uint16_t* a, bool cached, hipStream_t st);
-// listed tokens (slist, count soff[B]): x1 = x + g_a a, u_out = LN(x1) mod_m
-// (routing: u_out is a routing input and takes the decision-path arithmetic)
+// listed tokens (slist, count soff[B]): [x = x1p + g_m(prev) y when mod_prev
+// is set;] x1 = x + g_a a, u_out = LN(x1) mod_m (routing: u_out is a routing
+// input and takes the decision-path arithmetic)
 hipError_t launch_ln_mlp(const BlockBufs& k, int T, int N, int d, const float* mod,
-                         const uint16_t* a, uint16_t* u_out, bool routing, hipStream_t st);
+                         const float* mod_prev, const uint16_t* a, uint16_t* u_out, bool routing,
+                         hipStream_t st);
 // every token: x = x1 + g_m y
 hipError_t launch_ln_final(const BlockBufs& k, int T, int N, int d, const float* mod,
                            hipStream_t st);

@@ -38,7 +38,7 @@ int fail(int code, const std::string& m) { return moeca::set_error(code, m); }
 // Shared regions, in MOECA_SBUF_* order for the public ones.
 enum Region {
   S_MOD, S_H, S_U, S_U2, S_Q, S_KV, S_O, S_X1, S_Y, S_SLIST, S_SOFF,
-  S_IDENT, S_TAB, S_SC, S_EMB, S_H1, S_MID, S_COUNT
+  S_IDENT, S_TAB, S_SC, S_EMB, S_H1, S_MID, S_X1B, S_COUNT
 };
 
 }  // namespace
@@ -149,6 +149,7 @@ moeca_stack* moeca_stack_create(int n_blocks, int d, int heads, int E, int k, in
   b[S_KV] = T * 2 * d * 2;
   b[S_O] = T * d * 2;
   b[S_X1] = T * d * 4;
+  b[S_X1B] = T * d * 4;  // x1 of every other block of a run
   b[S_Y] = T * d * 2;
   b[S_SLIST] = T * 4;
   b[S_SOFF] = size_t(S->B + 1) * 4;
@@ -218,6 +219,8 @@ int moeca_stack_bind_workspace(moeca_stack* S, void* dev, size_t bytes) {
   k.B = S->B;
   k.x = nullptr;
   k.x1 = reinterpret_cast<float*>(w + S->off[S_X1]);
+  k.x1b = reinterpret_cast<float*>(w + S->off[S_X1B]);
+  k.x1p = nullptr;
   k.h = reinterpret_cast<uint16_t*>(w + S->off[S_H]);
   k.u = reinterpret_cast<uint16_t*>(w + S->off[S_U]);
   k.u2 = reinterpret_cast<uint16_t*>(w + S->off[S_U2]);
@@ -286,6 +289,13 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
     const auto* Wq = static_cast<const uint16_t*>(W.W_qkv);
     const uint16_t* Wkv = Wq + size_t(d) * d;
     const bool full = moeca::layer_full_step(lay, t);
+    // x1 alternates between two buffers from block to block, so that a cache
+    // step's LN2 can rebuild the listed tokens' x from the previous block's
+    // x1 instead of LN1 storing x for every token
+    float* const xa = reinterpret_cast<float*>(S->ws + S->off[S_X1]);
+    float* const xb = reinterpret_cast<float*>(S->ws + S->off[S_X1B]);
+    k.x1 = ((l - first) & 1) ? xb : xa;
+    k.x1p = l > first ? (((l - first) & 1) ? xa : xb) : nullptr;
 
     if ((rc = hip(moeca::launch_ln_attn(k, T, N, d, mod, mod_prev, a, !full, st), "ln1")) !=
         MOECA_OK)
@@ -352,7 +362,9 @@ int moeca_stack_step_blocks(moeca_stack* S, float* x, const float* c, int t, int
       if ((r = hip(moeca::launch_proj(k.o, W.W_o, W.b_o, k.tab, k.tab + 2, k.slist, d, d, a, st),
                    "output projection")) != MOECA_OK)
         return r;
-      return hip(moeca::launch_ln_mlp(k, T, N, d, mod, a, u_out, full, st), "ln2");
+      return hip(moeca::launch_ln_mlp(k, T, N, d, mod, full ? nullptr : mod_prev, a, u_out, full,
+                                      st),
+                 "ln2");
     };
     if (full) {
       rc = refresh(k.u);
